@@ -1,0 +1,181 @@
+"""CPU oracle for the UltraQuant FP4 KV-cache path (test infrastructure).
+
+Only the test suite, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg
+of ``bench.py`` may import this package.  The product library never does.
+The arithmetic lives in ``uq_oracle.c`` (plain C, fp64 attention); this
+module only marshals numpy arrays through ctypes.  See the header of
+``uq_oracle.c`` for what each function follows in the paper and for the
+readings taken where the paper is silent.
+"""
+import ctypes
+import os
+
+import numpy as np
+
+from . import build as _build
+
+HEAD_DIM = 128
+PAGE_SIZE = 16
+TILE_CODES = 1024
+TILE_SCALES = 64
+C_DEFAULT = 0.156
+
+_lib = None
+
+
+def lib():
+    """Load ``liboracle.so``, compiling it first if it is not there."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_build.LIB):
+            _build.build()
+        L = ctypes.CDLL(_build.LIB)
+        vp, i64, i32, f32, f64 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float, ctypes.c_double
+        L.uqo_wht128_f32.argtypes = [vp, i64]
+        L.uqo_wht128_f64.argtypes = [vp, vp]
+        L.uqo_scale_exponent.argtypes = [f32, f32]
+        L.uqo_scale_exponent.restype = i32
+        L.uqo_e2m1_encode.argtypes = [f32, i32]
+        L.uqo_e2m1_encode.restype = ctypes.c_uint8
+        L.uqo_e2m1_value.argtypes = [ctypes.c_uint8, i32]
+        L.uqo_e2m1_value.restype = f64
+        L.uqo_e4m3_encode.argtypes = [f32]
+        L.uqo_e4m3_encode.restype = ctypes.c_uint8
+        L.uqo_e4m3_value.argtypes = [ctypes.c_uint8]
+        L.uqo_e4m3_value.restype = f64
+        L.uqo_prepare_query.argtypes = [vp, i64, vp]
+        L.uqo_quantize_vector.argtypes = [vp, f32, i32, vp, vp]
+        L.uqo_quantize_vectors.argtypes = [vp, i64, f32, i32, vp, vp]
+        L.uqo_quantize_kv.argtypes = [vp, vp, i64, i32, i64, vp, i64, f32, i32, vp, vp]
+        L.uqo_quantize_kv.restype = i64
+        L.uqo_load_vector.argtypes = [vp, vp, i32, i64, i32, i32, i32, vp, vp]
+        L.uqo_dequant_vector.argtypes = [vp, vp, i32, i64, i32, i32, i32, vp]
+        L.uqo_decode_attention.argtypes = [vp, i32, i32, i32, vp, vp, vp, i32, vp, f64, i32, vp]
+        _lib = L
+    return _lib
+
+
+def _ptr(a):
+    return ctypes.c_void_p(a.ctypes.data)
+
+
+def _f32(x):
+    return np.ascontiguousarray(x, dtype=np.float32)
+
+
+def wht128_f32(x):
+    """fp32 butterfly rotation R x of each 128-vector (reading R1)."""
+    y = _f32(x).copy()
+    assert y.shape[-1] == HEAD_DIM
+    lib().uqo_wht128_f32(_ptr(y), y.size // HEAD_DIM)
+    return y
+
+
+def wht128_f64(x):
+    """Exact fp64 rotation H x / sqrt(128) of one 128-vector."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    y = np.empty(HEAD_DIM, np.float64)
+    lib().uqo_wht128_f64(_ptr(x), _ptr(y))
+    return y
+
+
+def scale_exponent(m, c=C_DEFAULT):
+    return int(lib().uqo_scale_exponent(float(np.float32(m)), float(np.float32(c))))
+
+
+def e2m1_encode(x, E):
+    return int(lib().uqo_e2m1_encode(float(np.float32(x)), int(E)))
+
+
+def e2m1_value(code, scale_byte):
+    return float(lib().uqo_e2m1_value(int(code), int(scale_byte)))
+
+
+def e4m3_encode(x):
+    return int(lib().uqo_e4m3_encode(float(np.float32(x))))
+
+
+def e4m3_value(b):
+    return float(lib().uqo_e4m3_value(int(b)))
+
+
+def prepare_query(q):
+    """q [..., 128] -> FP8 E4M3 bytes of the rotated query (Algorithm 1, Decode)."""
+    q = _f32(q)
+    out = np.empty(q.shape, np.uint8)
+    lib().uqo_prepare_query(_ptr(q), q.size // HEAD_DIM, _ptr(out))
+    return out
+
+
+def quantize_vector(x, c=C_DEFAULT, rotate=True):
+    """One 128-vector -> (codes[128] one per byte, scale_bytes[4])."""
+    x = _f32(x).reshape(HEAD_DIM)
+    codes = np.empty(HEAD_DIM, np.uint8)
+    sb = np.empty(4, np.uint8)
+    lib().uqo_quantize_vector(_ptr(x), float(np.float32(c)), int(bool(rotate)), _ptr(codes), _ptr(sb))
+    return codes, sb
+
+
+def quantize_vectors(x, c=C_DEFAULT, rotate=True):
+    """[..., 128] -> (codes [..., 128] one per byte, scale_bytes [..., 4])."""
+    x = _f32(x)
+    n = x.size // HEAD_DIM
+    codes = np.empty(x.shape, np.uint8)
+    sb = np.empty(x.shape[:-1] + (4,), np.uint8)
+    lib().uqo_quantize_vectors(_ptr(x), n, float(np.float32(c)), int(bool(rotate)), _ptr(codes), _ptr(sb))
+    return codes, sb
+
+
+def alloc_pools(num_pages, num_kv_heads, fill=0):
+    codes = np.full(num_pages * num_kv_heads * 2 * TILE_CODES, fill, np.uint8)
+    scales = np.full(num_pages * num_kv_heads * 2 * TILE_SCALES, fill, np.uint8)
+    return codes, scales
+
+
+def quantize_kv(k, v, slot_mapping, num_pages, c=C_DEFAULT, rotate_v=True, pools=None):
+    """k, v: [T, Hkv, 128] (any float dtype, converted exactly to fp32).
+
+    Writes into ``pools`` (codes, scales) if given, else into zero-filled new
+    pools, and returns them.
+    """
+    k = _f32(k)
+    v = _f32(v)
+    T, Hkv, D = k.shape
+    assert D == HEAD_DIM and v.shape == k.shape
+    slots = np.ascontiguousarray(slot_mapping, dtype=np.int64)
+    assert slots.shape == (T,)
+    if pools is None:
+        pools = alloc_pools(num_pages, Hkv)
+    codes, scales = pools
+    lib().uqo_quantize_kv(_ptr(k), _ptr(v), T, Hkv, Hkv * HEAD_DIM, _ptr(slots), int(num_pages),
+                          float(np.float32(c)), int(bool(rotate_v)), _ptr(codes), _ptr(scales))
+    return codes, scales
+
+
+def load_vector(pools, num_kv_heads, page, head, kv, t):
+    codes = np.empty(HEAD_DIM, np.uint8)
+    sb = np.empty(4, np.uint8)
+    lib().uqo_load_vector(_ptr(pools[0]), _ptr(pools[1]), num_kv_heads, page, head, kv, t, _ptr(codes), _ptr(sb))
+    return codes, sb
+
+
+def dequant_vector(pools, num_kv_heads, page, head, kv, t):
+    out = np.empty(HEAD_DIM, np.float64)
+    lib().uqo_dequant_vector(_ptr(pools[0]), _ptr(pools[1]), num_kv_heads, page, head, kv, t, _ptr(out))
+    return out
+
+
+def decode_attention(q, pools, page_table, context_lens, num_kv_heads, softmax_scale=None, rotate_v=True):
+    """q [B, Hq, 128] -> fp64 attention output [B, Hq, 128] (Algorithm 1, Decode)."""
+    q = _f32(q)
+    B, Hq, D = q.shape
+    assert D == HEAD_DIM and Hq % num_kv_heads == 0
+    pt = np.ascontiguousarray(page_table, dtype=np.int32)
+    ctx = np.ascontiguousarray(context_lens, dtype=np.int32)
+    assert pt.shape[0] == B and ctx.shape == (B,)
+    if softmax_scale is None:
+        softmax_scale = 1.0 / np.sqrt(HEAD_DIM)
+    out = np.empty((B, Hq, HEAD_DIM), np.float64)
+    lib().uqo_decode_attention(_ptr(q), B, Hq, num_kv_heads, _ptr(pools[0]), _ptr(pools[1]), _ptr(pt),
+                               pt.shape[1], _ptr(ctx), float(softmax_scale), int(bool(rotate_v)), _ptr(out))
+    return out

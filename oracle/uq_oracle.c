@@ -1,0 +1,338 @@
+/*
+ * uq_oracle.c -- plain, slow CPU oracle for the UltraQuant FP4 KV-cache path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may link, load or
+ * call this file; only the test suite, the smoke check and the benchmark's
+ * CPU-baseline leg use it.  It shares no code, header, table or constant
+ * generator with the HIP library: every rule below is written out from the
+ * paper (arXiv 2606.20474, "UltraQuant") and from the cache-format
+ * specification in include/uq.h.
+ *
+ * What it computes (each function cites the passage it follows):
+ *   - the fixed Walsh-Hadamard rotation R = H_128 / sqrt(128)
+ *       (section "Ultra-TurboQuant": a fixed WHT spreads outliers;
+ *        Algorithm 1, Write: K <- R.K; Decode: Q <- R.Q),
+ *   - per-32-channel UE8M0 exponent E = round(log2(c * m)), m = max|x|
+ *       (section "Constant-Optimized Scaling"; Algorithm 1, Write),
+ *   - FP4 E2M1 nearest-level rounding q(x / 2^E) onto
+ *       F = {0, +-0.5, +-1, +-1.5, +-2, +-3, +-4, +-6}
+ *       (section "Constant-Optimized Scaling", the definition of q),
+ *   - packing 2 codes per byte + 1 scale byte per group
+ *       (section "Cache Layout": 17 bytes per 32 elements),
+ *   - dequantisation value = code * 2^(byte - 127)
+ *       (section "Dequantization", its single equation),
+ *   - the FP8 E4M3 query cast (Algorithm 1, Decode),
+ *   - softmax attention over the dequantised cache, in fp64.
+ *
+ * Readings where the paper is silent (the same list is kept with the design
+ * notes of the repository):
+ *   R1 the rotation is Sylvester H_128 with no sign diagonal, evaluated in
+ *      fp32 as an in-place butterfly with stage widths 1,2,4,...,64, pair
+ *      (i, i+h) -> (x_i + x_{i+h}, x_i - x_{i+h}), then one fp32 multiply by
+ *      fl32(1/sqrt(128)).  Codes are integers decided from these fp32 values,
+ *      so the order is part of the format.
+ *   R2 "round(log2(y))" is nearest-integer rounding in the log domain
+ *      (threshold at significand sqrt(2)); y = fl32(c * m) is one fp32
+ *      multiply.  m = 0 gives E = -127.  E is clamped to [-127, 127], so the
+ *      byte E + 127 is never the UE8M0 NaN byte 255.
+ *   R3 ties in q go to the level with an even E2M1 code; values beyond 6
+ *      saturate to 6; the sign bit of x is kept even when |code| = 0.
+ *   R4 FP8 E4M3 is the OCP "fn" variant (bias 7, no infinities, max 448),
+ *      round-to-nearest-even, saturating; no query scale.
+ *   R5 K is always rotated; V is rotated iff rotate_v (Algorithm 1 rotates
+ *      keys only; rotate_v = 0 is that mode).  With rotate_v the attention
+ *      output is mapped back by R (R is symmetric and orthonormal).
+ *
+ * Built with: gcc -O2 -std=c11 -fopenmp -ffp-contract=off -shared -fPIC
+ * (no -ffast-math: fp32 results must follow IEEE round-to-nearest-even).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define UQO_D 128          /* head dimension */
+#define UQO_GROUP 32       /* channels per scale group */
+#define UQO_NGROUP 4       /* groups per head vector */
+#define UQO_PAGE 16        /* tokens per page */
+#define UQO_TILE_CODES 1024   /* bytes of codes per (page, head, K|V) tile */
+#define UQO_TILE_SCALES 64    /* bytes of scales per (page, head, K|V) tile */
+
+/* The E2M1 magnitudes, indexed by the low 3 bits of a code (section
+ * "Constant-Optimized Scaling", the set F). */
+static const double kE2M1Mag[8] = {0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0};
+
+/* ---------------------------------------------------------------------- */
+/* Rotation (section "Ultra-TurboQuant"; Algorithm 1), reading R1.          */
+/* ---------------------------------------------------------------------- */
+void uqo_wht128_f32(float *x, int64_t n_vec) {
+    const float inv_sqrt = (float)(1.0 / sqrt(128.0));
+    for (int64_t v = 0; v < n_vec; ++v) {
+        float *p = x + v * UQO_D;
+        for (int h = 1; h < UQO_D; h <<= 1) {
+            for (int i = 0; i < UQO_D; ++i) {
+                if (i & h) continue;
+                float a = p[i], b = p[i + h];
+                p[i] = a + b;
+                p[i + h] = a - b;
+            }
+        }
+        for (int i = 0; i < UQO_D; ++i) p[i] = p[i] * inv_sqrt;
+    }
+}
+
+/* Exact rotation in fp64: y = H_128 x / sqrt(128), H[i][j] = (-1)^popcount(i&j). */
+void uqo_wht128_f64(const double *x, double *y) {
+    const double inv_sqrt = 1.0 / sqrt(128.0);
+    for (int i = 0; i < UQO_D; ++i) {
+        double s = 0.0;
+        for (int j = 0; j < UQO_D; ++j)
+            s += (__builtin_popcount((unsigned)(i & j)) & 1) ? -x[j] : x[j];
+        y[i] = s * inv_sqrt;
+    }
+}
+
+/* ---------------------------------------------------------------------- */
+/* Scale exponent (section "Constant-Optimized Scaling"), reading R2.       */
+/* ---------------------------------------------------------------------- */
+int uqo_scale_exponent(float m, float c) {
+    float y = c * m;                 /* one fp32 multiply */
+    if (!(y > 0.0f)) return -127;    /* m = 0 (all-zero group) */
+    int e;
+    double f = frexp((double)y, &e); /* y = f * 2^e, f in [0.5, 1) */
+    /* log2(y) = (e - 1) + log2(2f); round to nearest: +1 iff 2f >= sqrt(2).
+     * 2f has 24 significant bits, so it never equals sqrt(2); the double
+     * nearest to sqrt(2) separates the same fp32 neighbours. */
+    int E = (e - 1) + ((2.0 * f >= sqrt(2.0)) ? 1 : 0);
+    if (E < -127) E = -127;
+    if (E > 127) E = 127;
+    return E;
+}
+
+/* ---------------------------------------------------------------------- */
+/* E2M1 rounding q(.) (section "Constant-Optimized Scaling"), reading R3.  */
+/* Returns the 4-bit code: bit 3 = sign, bits 0-2 = index into F.           */
+/* ---------------------------------------------------------------------- */
+uint8_t uqo_e2m1_encode(float x, int E) {
+    double t = ldexp((double)x, -E);   /* x / 2^E, exact in fp64 */
+    double a = fabs(t);
+    int best = 0;
+    double best_d = fabs(a - kE2M1Mag[0]);
+    for (int k = 1; k < 8; ++k) {
+        double d = fabs(a - kE2M1Mag[k]);
+        if (d < best_d || (d == best_d && (k % 2) == 0)) {
+            best = k;
+            best_d = d;
+        }
+    }
+    return (uint8_t)((signbit(x) ? 8 : 0) | best);
+}
+
+/* Dequantisation (section "Dequantization"): code * 2^(byte - 127). */
+double uqo_e2m1_value(uint8_t code, int scale_byte) {
+    double mag = kE2M1Mag[code & 7];
+    double v = ldexp(mag, scale_byte - 127);
+    return (code & 8) ? -v : v;
+}
+
+/* ---------------------------------------------------------------------- */
+/* FP8 E4M3 (OCP fn) encode / decode (Algorithm 1, Decode), reading R4.     */
+/* ---------------------------------------------------------------------- */
+double uqo_e4m3_value(uint8_t b) {
+    int s = b >> 7, e = (b >> 3) & 15, m = b & 7;
+    if (e == 15 && m == 7) return NAN;
+    double v = (e == 0) ? ldexp((double)m / 8.0, -6) : ldexp(1.0 + (double)m / 8.0, e - 7);
+    return s ? -v : v;
+}
+
+uint8_t uqo_e4m3_encode(float x) {
+    if (isnan(x)) return 0x7F;
+    if (isinf(x)) return (uint8_t)((signbit(x) ? 0x80 : 0) | 0x7E);
+    double a = fabs((double)x);
+    /* nearest among the 127 finite non-negative encodings 0x00..0x7E; the
+     * byte order is the numeric order, ties go to the even byte (even
+     * mantissa); anything above 448 lands on 448 (saturation). */
+    int best = 0;
+    double best_d = fabs(a - uqo_e4m3_value(0));
+    for (int k = 1; k <= 0x7E; ++k) {
+        double d = fabs(a - uqo_e4m3_value((uint8_t)k));
+        if (d < best_d || (d == best_d && (k % 2) == 0)) {
+            best = k;
+            best_d = d;
+        }
+    }
+    return (uint8_t)((signbit(x) ? 0x80 : 0) | best);
+}
+
+/* Query preparation (Algorithm 1, Decode): q8 = e4m3(R q), per 128-vector. */
+static void prepare_query_row(const float *q, uint8_t *q8) {
+    float tmp[UQO_D];
+    memcpy(tmp, q, sizeof(tmp));
+    uqo_wht128_f32(tmp, 1);
+    for (int i = 0; i < UQO_D; ++i) q8[i] = uqo_e4m3_encode(tmp[i]);
+}
+
+void uqo_prepare_query(const float *q, int64_t rows, uint8_t *q8) {
+#pragma omp parallel for schedule(static)
+    for (int64_t r = 0; r < rows; ++r) prepare_query_row(q + r * UQO_D, q8 + r * UQO_D);
+}
+
+/* ---------------------------------------------------------------------- */
+/* Quantise one head vector (Algorithm 1, Write): optional rotation, per-   */
+/* group exponent, per-element code.  codes[128] holds one code per byte.   */
+/* ---------------------------------------------------------------------- */
+void uqo_quantize_vector(const float *x_in, float c, int rotate, uint8_t *codes, uint8_t *scale_bytes) {
+    float x[UQO_D];
+    memcpy(x, x_in, sizeof(x));
+    if (rotate) uqo_wht128_f32(x, 1);
+    for (int g = 0; g < UQO_NGROUP; ++g) {
+        float m = 0.0f;
+        for (int i = 0; i < UQO_GROUP; ++i) {
+            float a = fabsf(x[g * UQO_GROUP + i]);
+            if (a > m) m = a;
+        }
+        int E = uqo_scale_exponent(m, c);
+        scale_bytes[g] = (uint8_t)(E + 127);
+        for (int i = 0; i < UQO_GROUP; ++i) codes[g * UQO_GROUP + i] = uqo_e2m1_encode(x[g * UQO_GROUP + i], E);
+    }
+}
+
+/* Batch form of uqo_quantize_vector over n_vec contiguous 128-vectors. */
+void uqo_quantize_vectors(const float *x, int64_t n_vec, float c, int rotate, uint8_t *codes, uint8_t *scale_bytes) {
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n_vec; ++i)
+        uqo_quantize_vector(x + i * UQO_D, c, rotate, codes + i * UQO_D, scale_bytes + i * UQO_NGROUP);
+}
+
+/* ---------------------------------------------------------------------- */
+/* Page layout (the cache format of include/uq.h).  Written out here from   */
+/* that specification, independently of the library.                       */
+/*   codes  pool: [num_pages][num_kv_heads][2 = K,V][1024 B]                */
+/*   scales pool: [num_pages][num_kv_heads][2 = K,V][4 groups][16 tokens]   */
+/*   K tile byte of (token t, channel c): ((c/32)*16 + t)*16 + (c%32)/2     */
+/*   V tile byte of (token t, channel c):                                   */
+/*        ((t/4)*16 + c/8)*16 + (t%4)*4 + (c%8)/2                           */
+/*   even channel in the low nibble, odd channel in the high nibble.         */
+/* ---------------------------------------------------------------------- */
+static inline int64_t tile_index(int64_t page, int num_kv_heads, int head, int kv) {
+    return (page * num_kv_heads + head) * 2 + kv;
+}
+static inline int code_byte_offset(int kv, int t, int ch) {
+    if (kv == 0) return ((ch / 32) * 16 + t) * 16 + (ch % 32) / 2;
+    return ((t / 4) * 16 + ch / 8) * 16 + (t % 4) * 4 + (ch % 8) / 2;
+}
+
+void uqo_store_vector(uint8_t *codes_pool, uint8_t *scales_pool, int num_kv_heads, int64_t page, int head,
+                      int kv, int t, const uint8_t *codes, const uint8_t *scale_bytes) {
+    int64_t ti = tile_index(page, num_kv_heads, head, kv);
+    uint8_t *ct = codes_pool + ti * UQO_TILE_CODES;
+    uint8_t *st = scales_pool + ti * UQO_TILE_SCALES;
+    for (int ch = 0; ch < UQO_D; ++ch) {
+        int off = code_byte_offset(kv, t, ch);
+        if (ch % 2 == 0) ct[off] = (uint8_t)((ct[off] & 0xF0) | (codes[ch] & 0x0F));
+        else ct[off] = (uint8_t)((ct[off] & 0x0F) | ((codes[ch] & 0x0F) << 4));
+    }
+    for (int g = 0; g < UQO_NGROUP; ++g) st[g * UQO_PAGE + t] = scale_bytes[g];
+}
+
+void uqo_load_vector(const uint8_t *codes_pool, const uint8_t *scales_pool, int num_kv_heads, int64_t page,
+                     int head, int kv, int t, uint8_t *codes, uint8_t *scale_bytes) {
+    int64_t ti = tile_index(page, num_kv_heads, head, kv);
+    const uint8_t *ct = codes_pool + ti * UQO_TILE_CODES;
+    const uint8_t *st = scales_pool + ti * UQO_TILE_SCALES;
+    for (int ch = 0; ch < UQO_D; ++ch) {
+        uint8_t b = ct[code_byte_offset(kv, t, ch)];
+        codes[ch] = (ch % 2 == 0) ? (b & 0x0F) : (b >> 4);
+    }
+    for (int g = 0; g < UQO_NGROUP; ++g) scale_bytes[g] = st[g * UQO_PAGE + t];
+}
+
+/* ---------------------------------------------------------------------- */
+/* Quantize-on-write (Algorithm 1, Write) into the paged pools.             */
+/* k, v: [num_tokens][num_kv_heads][128] fp32 with a token stride in floats; */
+/* slot_mapping[t] = page * 16 + offset, negative = skip.  Returns the      */
+/* number of tokens written.                                                 */
+/* ---------------------------------------------------------------------- */
+int64_t uqo_quantize_kv(const float *k, const float *v, int64_t num_tokens, int num_kv_heads,
+                        int64_t token_stride, const int64_t *slot_mapping, int64_t num_pages, float c,
+                        int rotate_v, uint8_t *codes_pool, uint8_t *scales_pool) {
+    int64_t written = 0;
+#pragma omp parallel for schedule(static) reduction(+ : written)
+    for (int64_t t = 0; t < num_tokens; ++t) {
+        int64_t slot = slot_mapping[t];
+        if (slot < 0 || slot >= num_pages * UQO_PAGE) continue;
+        int64_t page = slot / UQO_PAGE;
+        int off = (int)(slot % UQO_PAGE);
+        for (int h = 0; h < num_kv_heads; ++h) {
+            uint8_t codes[UQO_D], sb[UQO_NGROUP];
+            uqo_quantize_vector(k + t * token_stride + (int64_t)h * UQO_D, c, 1, codes, sb);
+            uqo_store_vector(codes_pool, scales_pool, num_kv_heads, page, h, 0, off, codes, sb);
+            uqo_quantize_vector(v + t * token_stride + (int64_t)h * UQO_D, c, rotate_v, codes, sb);
+            uqo_store_vector(codes_pool, scales_pool, num_kv_heads, page, h, 1, off, codes, sb);
+        }
+        written += 1;
+    }
+    return written;
+}
+
+/* Dequantise one stored vector to fp64 (section "Dequantization"). */
+void uqo_dequant_vector(const uint8_t *codes_pool, const uint8_t *scales_pool, int num_kv_heads, int64_t page,
+                        int head, int kv, int t, double *out) {
+    uint8_t codes[UQO_D], sb[UQO_NGROUP];
+    uqo_load_vector(codes_pool, scales_pool, num_kv_heads, page, head, kv, t, codes, sb);
+    for (int ch = 0; ch < UQO_D; ++ch) out[ch] = uqo_e2m1_value(codes[ch], sb[ch / UQO_GROUP]);
+}
+
+/* ---------------------------------------------------------------------- */
+/* Decode attention over the paged cache, fp64 (Algorithm 1, Decode).       */
+/*   q: [batch][num_q_heads][128] fp32 (rotated and cast to FP8 here),      */
+/*   page_table: [batch][max_pages_per_seq], context_lens: [batch].         */
+/*   Query head h reads KV head h / (num_q_heads / num_kv_heads).           */
+/*   out: [batch][num_q_heads][128] fp64; an empty context gives zeros.     */
+/* Plain definition: s_j = scale * <q8, k_j>, p = softmax(s), o = sum p_j v_j */
+/* then o <- R o when V was stored rotated.                                  */
+/* ---------------------------------------------------------------------- */
+void uqo_decode_attention(const float *q, int batch, int num_q_heads, int num_kv_heads, const uint8_t *codes_pool,
+                          const uint8_t *scales_pool, const int32_t *page_table, int max_pages_per_seq,
+                          const int32_t *context_lens, double softmax_scale, int rotate_v, double *out) {
+    const int G = num_q_heads / num_kv_heads;
+#pragma omp parallel for schedule(dynamic) collapse(2)
+    for (int b = 0; b < batch; ++b) {
+        for (int hq = 0; hq < num_q_heads; ++hq) {
+            const int hk = hq / G;
+            const int ctx = context_lens[b];
+            double *o = out + ((int64_t)b * num_q_heads + hq) * UQO_D;
+            for (int i = 0; i < UQO_D; ++i) o[i] = 0.0;
+            if (ctx <= 0) continue;
+            uint8_t q8[UQO_D];
+            prepare_query_row(q + ((int64_t)b * num_q_heads + hq) * UQO_D, q8);
+            double qd[UQO_D];
+            for (int i = 0; i < UQO_D; ++i) qd[i] = uqo_e4m3_value(q8[i]);
+            double *s = (double *)malloc(sizeof(double) * (size_t)ctx);
+            double kv[UQO_D];
+            double smax = -INFINITY;
+            for (int j = 0; j < ctx; ++j) {
+                int64_t page = page_table[(int64_t)b * max_pages_per_seq + j / UQO_PAGE];
+                uqo_dequant_vector(codes_pool, scales_pool, num_kv_heads, page, hk, 0, j % UQO_PAGE, kv);
+                double dot = 0.0;
+                for (int i = 0; i < UQO_D; ++i) dot += qd[i] * kv[i];
+                s[j] = softmax_scale * dot;
+                if (s[j] > smax) smax = s[j];
+            }
+            double denom = 0.0;
+            double acc[UQO_D];
+            for (int i = 0; i < UQO_D; ++i) acc[i] = 0.0;
+            for (int j = 0; j < ctx; ++j) {
+                double p = exp(s[j] - smax);
+                denom += p;
+                int64_t page = page_table[(int64_t)b * max_pages_per_seq + j / UQO_PAGE];
+                uqo_dequant_vector(codes_pool, scales_pool, num_kv_heads, page, hk, 1, j % UQO_PAGE, kv);
+                for (int i = 0; i < UQO_D; ++i) acc[i] += p * kv[i];
+            }
+            free(s);
+            for (int i = 0; i < UQO_D; ++i) acc[i] /= denom;
+            if (rotate_v) uqo_wht128_f64(acc, o);
+            else memcpy(o, acc, sizeof(acc));
+        }
+    }
+}
