@@ -1,0 +1,203 @@
+/*
+ * uq.h -- C ABI of libuq: FP4 (E2M1 + UE8M0) KV-cache decode attention for
+ * AMD Instinct MI355X (gfx950), after "UltraQuant" (arXiv 2606.20474).
+ *
+ * The library implements the two halves of the paper's Algorithm 1:
+ *   Write  (uq_quantize_kv)      rotate K (and V when rotate_v) with the
+ *                                fixed 128-point Walsh-Hadamard transform,
+ *                                pick one UE8M0 exponent per 32 channels,
+ *                                round every element onto the E2M1 grid and
+ *                                store 2 codes per byte + 1 scale byte.
+ *   Decode (uq_decode_attention) rotate the query, cast it to FP8 E4M3 once,
+ *                                compute QK^T on the block-scaled FP8 x FP4
+ *                                MFMA with the stored UE8M0 bytes as operand
+ *                                scales, convert V through the hardware
+ *                                FP4 -> BF16 path, and run softmax attention
+ *                                split over context partitions, then merge.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ *  - All pointers except `desc` and the host-side scalars are DEVICE
+ *    pointers on the current HIP device.  `stream` is a hipStream_t (NULL =
+ *    the default stream).  Every call only enqueues work on `stream`; none
+ *    synchronises.  The library allocates nothing and keeps no pointer after
+ *    a call returns; the caller owns every buffer.  Calls are thread-safe.
+ *  - Arguments are validated on the host before any HIP call: a failed
+ *    check returns its status and enqueues nothing.  Device-resident
+ *    indices (page ids, slots, context lengths) cannot be checked without a
+ *    synchronisation; kernels clamp them so that no access leaves the pools
+ *    (an out-of-range page id reads page 0, an out-of-range slot is
+ *    skipped), but such results are unspecified.
+ *  - Supported shape: head_dim 128, page_size 16, group_size 32, up to 16
+ *    query heads per KV head.  Other values return UQ_ERR_UNSUPPORTED.
+ *  - Inputs must be finite.
+ *
+ * Cache format (the "pools")
+ * --------------------------
+ * One tile holds one (page, kv head, K or V): 16 tokens x 128 channels.
+ *   kv_codes  : uint8 [num_pages][num_kv_heads][2 (K=0, V=1)][1024]
+ *   kv_scales : uint8 [num_pages][num_kv_heads][2 (K=0, V=1)][4 groups][16 tokens]
+ * 17 bytes per 32 elements = 4.25 bits per element (paper, "Cache Layout");
+ * 136 bytes per token and kv head for K and V together.
+ * Inside a 1024-byte code tile, for token t (0..15) and channel ch (0..127),
+ * the even channel of a pair in the low nibble:
+ *   K: byte ((ch/32)*16 + t)*16 + (ch%32)/2
+ *      ([group][token][16 bytes] -- one lane of the QK MFMA reads one
+ *       token's 32-channel group as 16 contiguous bytes, and its scale byte
+ *       sits at the same [group][token] index: the scale layout matches the
+ *       operand layout of the block-scaled MFMA, paper "Kernel
+ *       Implementation in vLLM")
+ *   V: byte ((t/4)*16 + ch/8)*16 + (t%4)*4 + (ch%8)/2
+ *      ([token/4][channel/8][token%4][4 bytes] -- one lane of the PV step
+ *       reads 4 tokens x 8 channels as 16 contiguous bytes)
+ * A code is sign(1) | E2M1 magnitude index(3) over {0,.5,1,1.5,2,3,4,6};
+ * a scale byte is E + 127 and the element value is code * 2^(byte-127)
+ * (paper, "Dequantization").
+ */
+#ifndef UQ_H_
+#define UQ_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum uq_status {
+    UQ_OK = 0,
+    UQ_ERR_INVALID_ARGUMENT = 1,   /* null pointer, negative size, inconsistent shape */
+    UQ_ERR_UNSUPPORTED = 2,        /* valid request outside the supported shapes */
+    UQ_ERR_WORKSPACE_TOO_SMALL = 3,
+    UQ_ERR_HIP = 4                 /* a HIP launch failed (hipGetLastError) */
+} uq_status;
+
+typedef enum uq_dtype {
+    UQ_F32 = 0,
+    UQ_BF16 = 1,
+    UQ_F16 = 2,
+    UQ_FP8_E4M3 = 3                /* OCP e4m3fn */
+} uq_dtype;
+
+typedef struct uq_cache_desc {
+    int32_t num_kv_heads;   /* >= 1 */
+    int32_t head_dim;       /* must be 128 */
+    int32_t page_size;      /* must be 16 */
+    int32_t group_size;     /* must be 32 */
+    int64_t num_pages;      /* pages in the pools, >= 1 */
+    float c;                /* global scale constant, finite and > 0; the paper deploys 0.156 */
+    int32_t rotate_v;       /* 0: V stored unrotated (Algorithm 1 as printed); 1: V rotated like K */
+} uq_cache_desc;
+
+/* Human-readable name of a status code; never NULL. */
+const char *uq_status_string(uq_status s);
+
+/* Library version, major*10000 + minor*100 + patch. */
+int32_t uq_version(void);
+
+/*
+ * uq_quantize_kv -- quantize-on-write (Algorithm 1, "Write").
+ *   k, v          : [num_tokens][num_kv_heads][128] of in_dtype (F32, BF16 or
+ *                   F16); token t starts at element t * token_stride, heads
+ *                   are contiguous inside a token (token_stride >=
+ *                   num_kv_heads * 128).
+ *   slot_mapping  : int64 [num_tokens].  With page_table == NULL it holds the
+ *                   physical slot page * 16 + offset (vLLM convention).  With
+ *                   a page table it holds the logical slot
+ *                   seq * (max_pages_per_seq * 16) + position, and the page
+ *                   is page_table[seq][position / 16].  Negative = padding,
+ *                   skipped; a slot beyond the pool (or a sequence index
+ *                   >= num_seqs) is skipped too.
+ *   page_table    : int32 [num_seqs][max_pages_per_seq] or NULL.
+ *   k, v must be 16-byte aligned and token_stride a multiple of 16 bytes.
+ *   kv_codes, kv_scales : the pools described above; only the slots named
+ *                   by slot_mapping are written.
+ * Per token and head the K vector is always rotated, V only with rotate_v.
+ * Codes and scale bytes are a pure function of the inputs and `c`.
+ * Errors: INVALID_ARGUMENT for null k/v/slot_mapping/pools, num_tokens < 0,
+ * token_stride too small or misaligned, non-finite or non-positive c,
+ * num_seqs < 1 or max_pages_per_seq < 1 with a page table; UNSUPPORTED for other head_dim/page/group sizes or
+ * an unknown in_dtype.  num_tokens == 0 is a no-op.
+ */
+uq_status uq_quantize_kv(const uq_cache_desc *desc, const void *k, const void *v, uq_dtype in_dtype,
+                         int64_t num_tokens, int64_t token_stride, const int32_t *page_table, int32_t num_seqs,
+                         int32_t max_pages_per_seq, const int64_t *slot_mapping, uint8_t *kv_codes,
+                         uint8_t *kv_scales, void *stream);
+
+/*
+ * uq_prepare_query -- the query half of Algorithm 1, "Decode":
+ * q8 = e4m3fn(R q) for `rows` 128-vectors (round to nearest even, saturate
+ * at +-448, no query scale).  q: [rows][128] F32/BF16/F16; q_fp8: [rows][128]
+ * bytes.  uq_decode_attention does this itself; this entry point exposes the
+ * step for callers that cache the FP8 query and for tests.
+ */
+uq_status uq_prepare_query(const uq_cache_desc *desc, const void *q, uq_dtype q_dtype, int64_t rows,
+                           uint8_t *q_fp8, void *stream);
+
+/*
+ * Workspace needed by uq_decode_attention / uq_decode_split for these sizes
+ * (partial results: per (sequence, query head, partition) a running max,
+ * a running sum and 128 fp32 accumulators).  partition_tokens == 0 selects
+ * the library's default partition for the shape.  Returns 0 for invalid
+ * arguments.
+ */
+size_t uq_decode_workspace_bytes(const uq_cache_desc *desc, int32_t batch, int32_t num_q_heads,
+                                 int32_t max_context, int32_t partition_tokens);
+
+/* Partition length (tokens) the library picks when partition_tokens == 0. */
+int32_t uq_default_partition(const uq_cache_desc *desc, int32_t batch, int32_t num_q_heads, int32_t max_context);
+
+/*
+ * uq_decode_attention -- decode attention over the FP4 cache (Algorithm 1,
+ * "Decode"), one new query token per sequence.
+ *   q             : [batch][num_q_heads][128].  F32/BF16/F16: rotated and
+ *                   cast to FP8 inside the call.  FP8_E4M3: already
+ *                   prepared by uq_prepare_query.
+ *   page_table    : int32 [batch][max_pages_per_seq], physical page ids.
+ *   context_lens  : int32 [batch] on the device; tokens 0..len-1 attend.
+ *   max_context   : host-side upper bound of every context_lens[b]
+ *                   (<= max_pages_per_seq * 16); sizes the grid without a
+ *                   device read.  Lengths above it are clamped to it.
+ *   softmax_scale : multiplies q.k (usually 1/sqrt(128)).
+ *   partition_tokens : context tokens per split-context partition, a
+ *                   multiple of 32, or 0 for the default.
+ *   workspace     : >= uq_decode_workspace_bytes(...) bytes, device.
+ *   out           : [batch][num_q_heads][128] F32 or BF16.  With rotate_v
+ *                   the output is rotated back (o <- R o), so it is in the
+ *                   same basis as an unrotated V.  An empty context gives 0.
+ * Query head h reads kv head h / (num_q_heads / num_kv_heads).
+ * Errors: INVALID_ARGUMENT for null pointers, batch/num_q_heads < 1,
+ * num_q_heads % num_kv_heads != 0, max_context < 0 or above
+ * max_pages_per_seq * 16, partition_tokens not a multiple of 32, a
+ * non-finite softmax_scale; UNSUPPORTED for more than 16 query heads per kv
+ * head or unsupported dtypes; WORKSPACE_TOO_SMALL.
+ */
+uq_status uq_decode_attention(const uq_cache_desc *desc, const void *q, uq_dtype q_dtype, int32_t batch,
+                              int32_t num_q_heads, const uint8_t *kv_codes, const uint8_t *kv_scales,
+                              const int32_t *page_table, int32_t max_pages_per_seq, const int32_t *context_lens,
+                              int32_t max_context, float softmax_scale, int32_t partition_tokens,
+                              void *workspace, size_t workspace_bytes, void *out, uq_dtype out_dtype,
+                              void *stream);
+
+/*
+ * The two launches of uq_decode_attention, exposed for callers that want to
+ * time or overlap them.  uq_decode_split runs the partition kernel and fills
+ * the workspace; uq_decode_reduce merges the partitions into `out`.  Called
+ * back to back on one stream with the same arguments they are exactly
+ * uq_decode_attention.
+ */
+uq_status uq_decode_split(const uq_cache_desc *desc, const void *q, uq_dtype q_dtype, int32_t batch,
+                          int32_t num_q_heads, const uint8_t *kv_codes, const uint8_t *kv_scales,
+                          const int32_t *page_table, int32_t max_pages_per_seq, const int32_t *context_lens,
+                          int32_t max_context, float softmax_scale, int32_t partition_tokens, void *workspace,
+                          size_t workspace_bytes, void *stream);
+uq_status uq_decode_reduce(const uq_cache_desc *desc, int32_t batch, int32_t num_q_heads,
+                           const int32_t *context_lens, int32_t max_context, int32_t partition_tokens,
+                           const void *workspace, size_t workspace_bytes, void *out, uq_dtype out_dtype,
+                           void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* UQ_H_ */

@@ -1,0 +1,236 @@
+// uq_api.hip -- the C ABI of libuq (declared in include/uq.h): argument
+// validation on the host, launch configuration, workspace sizing.
+#include <math.h>
+#include <stdint.h>
+
+#include "uq.h"
+#include "uq_internal.hpp"
+
+namespace {
+
+constexpr int kHeadDim = 128;
+constexpr int kPageSize = 16;
+constexpr int kGroupSize = 32;
+constexpr int kMaxGroup = 16;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+uq_status check_desc(const uq_cache_desc* d) {
+    if (d == nullptr) return UQ_ERR_INVALID_ARGUMENT;
+    if (d->num_kv_heads < 1 || d->num_pages < 1) return UQ_ERR_INVALID_ARGUMENT;
+    if (!(isfinite(d->c) && d->c > 0.0f)) return UQ_ERR_INVALID_ARGUMENT;
+    if (d->head_dim != kHeadDim || d->page_size != kPageSize || d->group_size != kGroupSize)
+        return UQ_ERR_UNSUPPORTED;
+    return UQ_OK;
+}
+
+uq_status from_hip(hipError_t e) { return e == hipSuccess ? UQ_OK : UQ_ERR_HIP; }
+
+int32_t pick_partition(int32_t batch, int32_t num_kv_heads, int32_t max_context) {
+    // Enough blocks to give every one of the 256 CUs several resident
+    // blocks, without splitting a context below 1024 tokens (below that the
+    // per-partition prologue and the partial write stop being negligible).
+    const int64_t heads = int64_t(batch) * num_kv_heads;
+    int32_t part = 4096;
+    while (part > 1024 && heads * ((max_context + part - 1) / part) < 1024) part /= 2;
+    return part;
+}
+
+uq_status check_decode_common(const uq_cache_desc* desc, int32_t batch, int32_t num_q_heads, int32_t max_context,
+                              int32_t partition_tokens) {
+    uq_status s = check_desc(desc);
+    if (s != UQ_OK) return s;
+    if (batch < 1 || num_q_heads < 1 || max_context < 0 || partition_tokens < 0) return UQ_ERR_INVALID_ARGUMENT;
+    if (num_q_heads % desc->num_kv_heads != 0) return UQ_ERR_INVALID_ARGUMENT;
+    if (partition_tokens % 32 != 0) return UQ_ERR_INVALID_ARGUMENT;
+    if (num_q_heads / desc->num_kv_heads > kMaxGroup) return UQ_ERR_UNSUPPORTED;
+    if (batch > 65535 || desc->num_kv_heads > 65535) return UQ_ERR_UNSUPPORTED;
+    return UQ_OK;
+}
+
+size_t workspace_for(int32_t batch, int32_t num_q_heads, int32_t max_context, int32_t part) {
+    const int64_t np = max_context > 0 ? (int64_t(max_context) + part - 1) / part : 1;
+    return size_t(batch) * size_t(num_q_heads) * size_t(np) * (kHeadDim + 2) * sizeof(float);
+}
+
+// Fill the parameter block shared by the split and reduce launches.
+uq_status make_decode_params(const uq_cache_desc* desc, const void* q, uq_dtype q_dtype, int32_t batch,
+                             int32_t num_q_heads, const uint8_t* kv_codes, const uint8_t* kv_scales,
+                             const int32_t* page_table, int32_t max_pages_per_seq, const int32_t* context_lens,
+                             int32_t max_context, float softmax_scale, int32_t partition_tokens, const void* workspace,
+                             size_t workspace_bytes, uq::DecodeParams& p) {
+    const int32_t part = partition_tokens == 0 ? pick_partition(batch, desc->num_kv_heads, max_context) : partition_tokens;
+    const size_t need = workspace_for(batch, num_q_heads, max_context, part);
+    if (workspace == nullptr) return UQ_ERR_INVALID_ARGUMENT;
+    if (workspace_bytes < need) return UQ_ERR_WORKSPACE_TOO_SMALL;
+    if (!aligned16(workspace)) return UQ_ERR_INVALID_ARGUMENT;
+    const int64_t np = max_context > 0 ? (int64_t(max_context) + part - 1) / part : 1;
+    if (np > 0x7FFFFFFF) return UQ_ERR_UNSUPPORTED;
+    p.q = q;
+    p.q_dtype = int32_t(q_dtype);
+    p.codes = kv_codes;
+    p.scales = kv_scales;
+    p.page_table = page_table;
+    p.max_pages_per_seq = max_pages_per_seq;
+    p.context_lens = context_lens;
+    p.max_context = max_context;
+    p.batch = batch;
+    p.num_q_heads = num_q_heads;
+    p.num_kv_heads = desc->num_kv_heads;
+    p.group = num_q_heads / desc->num_kv_heads;
+    p.num_pages = desc->num_pages;
+    p.scale_log2 = float(double(softmax_scale) * 1.4426950408889634);
+    p.partition_tokens = part;
+    p.num_partitions = int32_t(np);
+    const size_t acc_bytes = size_t(batch) * num_q_heads * size_t(np) * kHeadDim * sizeof(float);
+    p.part_acc = static_cast<float*>(const_cast<void*>(workspace));
+    p.part_ml = reinterpret_cast<float*>(static_cast<char*>(const_cast<void*>(workspace)) + acc_bytes);
+    p.out = nullptr;
+    p.out_dtype = 0;
+    p.rotate_v = desc->rotate_v != 0;
+    return UQ_OK;
+}
+
+uq_status check_split_args(const uq_cache_desc* desc, const void* q, uq_dtype q_dtype, int32_t batch,
+                           int32_t num_q_heads, const uint8_t* kv_codes, const uint8_t* kv_scales,
+                           const int32_t* page_table, int32_t max_pages_per_seq, const int32_t* context_lens,
+                           int32_t max_context, float softmax_scale, int32_t partition_tokens) {
+    uq_status s = check_decode_common(desc, batch, num_q_heads, max_context, partition_tokens);
+    if (s != UQ_OK) return s;
+    if (q == nullptr || kv_codes == nullptr || kv_scales == nullptr || page_table == nullptr || context_lens == nullptr)
+        return UQ_ERR_INVALID_ARGUMENT;
+    if (q_dtype != UQ_F32 && q_dtype != UQ_BF16 && q_dtype != UQ_F16 && q_dtype != UQ_FP8_E4M3)
+        return UQ_ERR_UNSUPPORTED;
+    if (max_pages_per_seq < 1) return UQ_ERR_INVALID_ARGUMENT;
+    if (int64_t(max_context) > int64_t(max_pages_per_seq) * kPageSize) return UQ_ERR_INVALID_ARGUMENT;
+    if (!isfinite(softmax_scale)) return UQ_ERR_INVALID_ARGUMENT;
+    if (!aligned16(q) || !aligned16(kv_codes) || !aligned16(kv_scales)) return UQ_ERR_INVALID_ARGUMENT;
+    return UQ_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* uq_status_string(uq_status s) {
+    switch (s) {
+        case UQ_OK: return "UQ_OK";
+        case UQ_ERR_INVALID_ARGUMENT: return "UQ_ERR_INVALID_ARGUMENT";
+        case UQ_ERR_UNSUPPORTED: return "UQ_ERR_UNSUPPORTED";
+        case UQ_ERR_WORKSPACE_TOO_SMALL: return "UQ_ERR_WORKSPACE_TOO_SMALL";
+        case UQ_ERR_HIP: return "UQ_ERR_HIP";
+    }
+    return "UQ_ERR_UNKNOWN";
+}
+
+int32_t uq_version(void) { return 100; }
+
+uq_status uq_quantize_kv(const uq_cache_desc* desc, const void* k, const void* v, uq_dtype in_dtype,
+                         int64_t num_tokens, int64_t token_stride, const int32_t* page_table, int32_t num_seqs,
+                         int32_t max_pages_per_seq, const int64_t* slot_mapping, uint8_t* kv_codes,
+                         uint8_t* kv_scales, void* stream) {
+    uq_status s = check_desc(desc);
+    if (s != UQ_OK) return s;
+    if (in_dtype != UQ_F32 && in_dtype != UQ_BF16 && in_dtype != UQ_F16) return UQ_ERR_UNSUPPORTED;
+    if (num_tokens < 0) return UQ_ERR_INVALID_ARGUMENT;
+    if (k == nullptr || v == nullptr || slot_mapping == nullptr || kv_codes == nullptr || kv_scales == nullptr)
+        return UQ_ERR_INVALID_ARGUMENT;
+    if (token_stride < int64_t(desc->num_kv_heads) * kHeadDim) return UQ_ERR_INVALID_ARGUMENT;
+    const int64_t vec_elems = in_dtype == UQ_F32 ? 4 : 8;   // one 16-byte load
+    if (token_stride % vec_elems != 0 || !aligned16(k) || !aligned16(v)) return UQ_ERR_INVALID_ARGUMENT;
+    if (!aligned16(kv_codes) || !aligned16(kv_scales)) return UQ_ERR_INVALID_ARGUMENT;
+    if (page_table != nullptr && (max_pages_per_seq < 1 || num_seqs < 1)) return UQ_ERR_INVALID_ARGUMENT;
+    if (num_tokens == 0) return UQ_OK;
+    uq::QuantizeParams p;
+    p.k = k;
+    p.v = v;
+    p.num_tokens = num_tokens;
+    p.token_stride = token_stride;
+    p.slot_mapping = slot_mapping;
+    p.page_table = page_table;
+    p.max_pages_per_seq = max_pages_per_seq;
+    p.num_seqs = page_table != nullptr ? num_seqs : 0;
+    p.num_kv_heads = desc->num_kv_heads;
+    p.num_pages = desc->num_pages;
+    p.c = desc->c;
+    p.rotate_v = desc->rotate_v != 0;
+    p.codes = kv_codes;
+    p.scales = kv_scales;
+    return from_hip(uq::launch_quantize_kv(p, int(in_dtype), static_cast<hipStream_t>(stream)));
+}
+
+uq_status uq_prepare_query(const uq_cache_desc* desc, const void* q, uq_dtype q_dtype, int64_t rows, uint8_t* q_fp8,
+                           void* stream) {
+    uq_status s = check_desc(desc);
+    if (s != UQ_OK) return s;
+    if (q_dtype != UQ_F32 && q_dtype != UQ_BF16 && q_dtype != UQ_F16) return UQ_ERR_UNSUPPORTED;
+    if (rows < 0 || q == nullptr || q_fp8 == nullptr) return UQ_ERR_INVALID_ARGUMENT;
+    if (!aligned16(q) || (reinterpret_cast<uintptr_t>(q_fp8) & 7u) != 0) return UQ_ERR_INVALID_ARGUMENT;
+    if (rows == 0) return UQ_OK;
+    return from_hip(uq::launch_prepare_query(q, int(q_dtype), rows, q_fp8, static_cast<hipStream_t>(stream)));
+}
+
+int32_t uq_default_partition(const uq_cache_desc* desc, int32_t batch, int32_t num_q_heads, int32_t max_context) {
+    if (check_decode_common(desc, batch, num_q_heads, max_context, 0) != UQ_OK) return 0;
+    return pick_partition(batch, desc->num_kv_heads, max_context);
+}
+
+size_t uq_decode_workspace_bytes(const uq_cache_desc* desc, int32_t batch, int32_t num_q_heads, int32_t max_context,
+                                 int32_t partition_tokens) {
+    if (check_decode_common(desc, batch, num_q_heads, max_context, partition_tokens) != UQ_OK) return 0;
+    const int32_t part = partition_tokens == 0 ? pick_partition(batch, desc->num_kv_heads, max_context) : partition_tokens;
+    return workspace_for(batch, num_q_heads, max_context, part);
+}
+
+uq_status uq_decode_split(const uq_cache_desc* desc, const void* q, uq_dtype q_dtype, int32_t batch,
+                          int32_t num_q_heads, const uint8_t* kv_codes, const uint8_t* kv_scales,
+                          const int32_t* page_table, int32_t max_pages_per_seq, const int32_t* context_lens,
+                          int32_t max_context, float softmax_scale, int32_t partition_tokens, void* workspace,
+                          size_t workspace_bytes, void* stream) {
+    uq_status s = check_split_args(desc, q, q_dtype, batch, num_q_heads, kv_codes, kv_scales, page_table,
+                                   max_pages_per_seq, context_lens, max_context, softmax_scale, partition_tokens);
+    if (s != UQ_OK) return s;
+    uq::DecodeParams p;
+    s = make_decode_params(desc, q, q_dtype, batch, num_q_heads, kv_codes, kv_scales, page_table, max_pages_per_seq,
+                           context_lens, max_context, softmax_scale, partition_tokens, workspace, workspace_bytes, p);
+    if (s != UQ_OK) return s;
+    if (max_context == 0) return UQ_OK;
+    return from_hip(uq::launch_decode_split(p, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uq_decode_reduce(const uq_cache_desc* desc, int32_t batch, int32_t num_q_heads, const int32_t* context_lens,
+                           int32_t max_context, int32_t partition_tokens, const void* workspace,
+                           size_t workspace_bytes, void* out, uq_dtype out_dtype, void* stream) {
+    uq_status s = check_decode_common(desc, batch, num_q_heads, max_context, partition_tokens);
+    if (s != UQ_OK) return s;
+    if (context_lens == nullptr || out == nullptr) return UQ_ERR_INVALID_ARGUMENT;
+    if (out_dtype != UQ_F32 && out_dtype != UQ_BF16) return UQ_ERR_UNSUPPORTED;
+    if (!aligned16(out)) return UQ_ERR_INVALID_ARGUMENT;
+    uq::DecodeParams p;
+    s = make_decode_params(desc, nullptr, UQ_F32, batch, num_q_heads, nullptr, nullptr, nullptr, 1, context_lens,
+                           max_context, 1.0f, partition_tokens, workspace, workspace_bytes, p);
+    if (s != UQ_OK) return s;
+    p.out = out;
+    p.out_dtype = out_dtype == UQ_F32 ? 0 : 1;
+    return from_hip(uq::launch_decode_reduce(p, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uq_decode_attention(const uq_cache_desc* desc, const void* q, uq_dtype q_dtype, int32_t batch,
+                              int32_t num_q_heads, const uint8_t* kv_codes, const uint8_t* kv_scales,
+                              const int32_t* page_table, int32_t max_pages_per_seq, const int32_t* context_lens,
+                              int32_t max_context, float softmax_scale, int32_t partition_tokens, void* workspace,
+                              size_t workspace_bytes, void* out, uq_dtype out_dtype, void* stream) {
+    uq_status s = check_split_args(desc, q, q_dtype, batch, num_q_heads, kv_codes, kv_scales, page_table,
+                                   max_pages_per_seq, context_lens, max_context, softmax_scale, partition_tokens);
+    if (s != UQ_OK) return s;
+    if (out == nullptr) return UQ_ERR_INVALID_ARGUMENT;
+    if (out_dtype != UQ_F32 && out_dtype != UQ_BF16) return UQ_ERR_UNSUPPORTED;
+    if (!aligned16(out)) return UQ_ERR_INVALID_ARGUMENT;
+    s = uq_decode_split(desc, q, q_dtype, batch, num_q_heads, kv_codes, kv_scales, page_table, max_pages_per_seq,
+                        context_lens, max_context, softmax_scale, partition_tokens, workspace, workspace_bytes, stream);
+    if (s != UQ_OK) return s;
+    return uq_decode_reduce(desc, batch, num_q_heads, context_lens, max_context, partition_tokens, workspace,
+                            workspace_bytes, out, out_dtype, stream);
+}
+
+}  // extern "C"

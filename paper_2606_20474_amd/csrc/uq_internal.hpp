@@ -1,0 +1,56 @@
+// uq_internal.hpp -- kernel parameter blocks and launchers shared between
+// the libuq translation units (not part of the public ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace uq {
+
+struct QuantizeParams {
+    const void* k;
+    const void* v;
+    int64_t num_tokens;
+    int64_t token_stride;      // elements between consecutive tokens
+    const int64_t* slot_mapping;
+    const int32_t* page_table; // nullptr: slot_mapping holds physical slots
+    int32_t max_pages_per_seq;
+    int64_t num_seqs;          // rows of page_table (bound for the logical slot)
+    int32_t num_kv_heads;
+    int64_t num_pages;
+    float c;
+    int32_t rotate_v;
+    uint8_t* codes;
+    uint8_t* scales;
+};
+
+struct DecodeParams {
+    const void* q;             // [B][Hq][128], dtype q_dtype
+    int32_t q_dtype;           // 0 f32, 1 bf16, 2 f16, 3 fp8 (prepared)
+    const uint8_t* codes;
+    const uint8_t* scales;
+    const int32_t* page_table;
+    int32_t max_pages_per_seq;
+    const int32_t* context_lens;
+    int32_t max_context;
+    int32_t batch;
+    int32_t num_q_heads;
+    int32_t num_kv_heads;
+    int32_t group;             // query heads per kv head (<= 16)
+    int64_t num_pages;
+    float scale_log2;          // softmax_scale * log2(e)
+    int32_t partition_tokens;
+    int32_t num_partitions;
+    float* part_acc;           // [B][Hq][NP][128]
+    float* part_ml;            // [B][Hq][NP][2]  (running max in log2 units, running sum)
+    void* out;                 // reduce only
+    int32_t out_dtype;         // 0 f32, 1 bf16
+    int32_t rotate_v;
+};
+
+hipError_t launch_quantize_kv(const QuantizeParams& p, int dtype, hipStream_t stream);
+hipError_t launch_prepare_query(const void* q, int dtype, int64_t rows, uint8_t* q8, hipStream_t stream);
+hipError_t launch_decode_split(const DecodeParams& p, hipStream_t stream);
+hipError_t launch_decode_reduce(const DecodeParams& p, hipStream_t stream);
+
+}  // namespace uq

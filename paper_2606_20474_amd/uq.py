@@ -1,0 +1,213 @@
+"""Python binding of libuq (``include/uq.h``): argument marshalling only.
+
+Every step of the path runs in the HIP kernels of ``libuq.so``; this module
+turns torch tensors into device pointers and the current torch stream into a
+``hipStream_t``, calls the C entry point of the same name and raises
+:class:`UQError` on a non-OK status.  There is no fallback: if the library is
+missing, importing this module fails.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libuq.so")
+
+UQ_OK, UQ_ERR_INVALID_ARGUMENT, UQ_ERR_UNSUPPORTED, UQ_ERR_WORKSPACE_TOO_SMALL, UQ_ERR_HIP = range(5)
+UQ_F32, UQ_BF16, UQ_F16, UQ_FP8_E4M3 = range(4)
+
+HEAD_DIM = 128
+PAGE_SIZE = 16
+GROUP_SIZE = 32
+TILE_CODES = 1024
+TILE_SCALES = 64
+
+# Every symbol include/uq.h declares.
+EXPORTS = (
+    "uq_status_string", "uq_version", "uq_quantize_kv", "uq_prepare_query", "uq_decode_workspace_bytes",
+    "uq_default_partition", "uq_decode_attention", "uq_decode_split", "uq_decode_reduce",
+)
+
+
+class UQError(RuntimeError):
+    def __init__(self, status: int, call: str):
+        self.status = status
+        super().__init__(f"{call} failed: {status_string(status)}")
+
+
+class uq_cache_desc(ctypes.Structure):
+    _fields_ = [
+        ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("page_size", ctypes.c_int32),
+        ("group_size", ctypes.c_int32),
+        ("num_pages", ctypes.c_int64),
+        ("c", ctypes.c_float),
+        ("rotate_v", ctypes.c_int32),
+    ]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2606_20474_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, f32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_size_t
+    D = ctypes.POINTER(uq_cache_desc)
+    L.uq_status_string.argtypes = [i32]
+    L.uq_status_string.restype = ctypes.c_char_p
+    L.uq_version.restype = i32
+    L.uq_quantize_kv.argtypes = [D, vp, vp, i32, i64, i64, vp, i32, i32, vp, vp, vp, vp]
+    L.uq_quantize_kv.restype = i32
+    L.uq_prepare_query.argtypes = [D, vp, i32, i64, vp, vp]
+    L.uq_prepare_query.restype = i32
+    L.uq_decode_workspace_bytes.argtypes = [D, i32, i32, i32, i32]
+    L.uq_decode_workspace_bytes.restype = sz
+    L.uq_default_partition.argtypes = [D, i32, i32, i32]
+    L.uq_default_partition.restype = i32
+    L.uq_decode_attention.argtypes = [D, vp, i32, i32, i32, vp, vp, vp, i32, vp, i32, f32, i32, vp, sz, vp, i32, vp]
+    L.uq_decode_attention.restype = i32
+    L.uq_decode_split.argtypes = [D, vp, i32, i32, i32, vp, vp, vp, i32, vp, i32, f32, i32, vp, sz, vp]
+    L.uq_decode_split.restype = i32
+    L.uq_decode_reduce.argtypes = [D, i32, i32, vp, i32, i32, vp, sz, vp, i32, vp]
+    L.uq_decode_reduce.restype = i32
+    return L
+
+
+lib = _load()
+
+
+def status_string(status: int) -> str:
+    return lib.uq_status_string(int(status)).decode()
+
+
+def _check(status: int, call: str):
+    if status != UQ_OK:
+        raise UQError(status, call)
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream=None):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+_DT = {torch.float32: UQ_F32, torch.bfloat16: UQ_BF16, torch.float16: UQ_F16, torch.uint8: UQ_FP8_E4M3,
+       torch.float8_e4m3fn: UQ_FP8_E4M3}
+
+
+@dataclass
+class CacheDesc:
+    """Python mirror of ``uq_cache_desc``."""
+    num_kv_heads: int
+    num_pages: int
+    c: float = 0.156
+    rotate_v: bool = True
+    head_dim: int = HEAD_DIM
+    page_size: int = PAGE_SIZE
+    group_size: int = GROUP_SIZE
+
+    def c_struct(self):
+        return uq_cache_desc(self.num_kv_heads, self.head_dim, self.page_size, self.group_size, self.num_pages,
+                             self.c, int(bool(self.rotate_v)))
+
+    def codes_bytes(self):
+        return self.num_pages * self.num_kv_heads * 2 * TILE_CODES
+
+    def scales_bytes(self):
+        return self.num_pages * self.num_kv_heads * 2 * TILE_SCALES
+
+    def alloc_pools(self, device="cuda", fill=None):
+        codes = torch.empty(self.codes_bytes(), dtype=torch.uint8, device=device)
+        scales = torch.empty(self.scales_bytes(), dtype=torch.uint8, device=device)
+        if fill is not None:
+            codes.fill_(fill)
+            scales.fill_(fill)
+        return codes, scales
+
+
+def quantize_kv(desc: CacheDesc, k, v, slot_mapping, codes, scales, page_table=None, max_pages_per_seq=0,
+                token_stride=None, stream=None):
+    """k, v: [T, Hkv, 128] (or strided rows); slot_mapping int64 [T]."""
+    T = k.shape[0]
+    if token_stride is None:
+        token_stride = k.stride(0)
+    num_seqs = 0 if page_table is None else page_table.shape[0]
+    mpps = 0 if page_table is None else (max_pages_per_seq or page_table.shape[1])
+    d = desc.c_struct()
+    st = lib.uq_quantize_kv(ctypes.byref(d), _ptr(k), _ptr(v), _DT[k.dtype], T, token_stride, _ptr(page_table),
+                            num_seqs, mpps, _ptr(slot_mapping), _ptr(codes), _ptr(scales), _stream(stream))
+    _check(st, "uq_quantize_kv")
+
+
+def prepare_query(desc: CacheDesc, q, out=None, stream=None):
+    rows = q.numel() // HEAD_DIM
+    if out is None:
+        out = torch.empty(q.shape, dtype=torch.uint8, device=q.device)
+    d = desc.c_struct()
+    _check(lib.uq_prepare_query(ctypes.byref(d), _ptr(q), _DT[q.dtype], rows, _ptr(out), _stream(stream)),
+           "uq_prepare_query")
+    return out
+
+
+def workspace_bytes(desc: CacheDesc, batch, num_q_heads, max_context, partition_tokens=0):
+    d = desc.c_struct()
+    return int(lib.uq_decode_workspace_bytes(ctypes.byref(d), batch, num_q_heads, max_context, partition_tokens))
+
+
+def default_partition(desc: CacheDesc, batch, num_q_heads, max_context):
+    d = desc.c_struct()
+    return int(lib.uq_default_partition(ctypes.byref(d), batch, num_q_heads, max_context))
+
+
+def alloc_workspace(desc: CacheDesc, batch, num_q_heads, max_context, partition_tokens=0, device="cuda"):
+    n = max(workspace_bytes(desc, batch, num_q_heads, max_context, partition_tokens), 16)
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def decode_attention(desc: CacheDesc, q, codes, scales, page_table, context_lens, max_context, softmax_scale=None,
+                     partition_tokens=0, workspace=None, out=None, out_dtype=torch.float32, q_dtype=None,
+                     stream=None):
+    """q: [B, Hq, 128] -> out [B, Hq, 128]."""
+    B, Hq = q.shape[0], q.shape[1]
+    if softmax_scale is None:
+        softmax_scale = HEAD_DIM ** -0.5
+    if workspace is None:
+        workspace = alloc_workspace(desc, B, Hq, max_context, partition_tokens, q.device)
+    if out is None:
+        out = torch.empty((B, Hq, HEAD_DIM), dtype=out_dtype, device=q.device)
+    d = desc.c_struct()
+    qdt = _DT[q.dtype] if q_dtype is None else q_dtype
+    st = lib.uq_decode_attention(ctypes.byref(d), _ptr(q), qdt, B, Hq, _ptr(codes), _ptr(scales), _ptr(page_table),
+                                 page_table.shape[1], _ptr(context_lens), max_context, softmax_scale,
+                                 partition_tokens, _ptr(workspace), workspace.numel(), _ptr(out), _DT[out.dtype],
+                                 _stream(stream))
+    _check(st, "uq_decode_attention")
+    return out
+
+
+def decode_split(desc: CacheDesc, q, codes, scales, page_table, context_lens, max_context, softmax_scale,
+                 partition_tokens, workspace, q_dtype=None, stream=None):
+    B, Hq = q.shape[0], q.shape[1]
+    d = desc.c_struct()
+    qdt = _DT[q.dtype] if q_dtype is None else q_dtype
+    st = lib.uq_decode_split(ctypes.byref(d), _ptr(q), qdt, B, Hq, _ptr(codes), _ptr(scales), _ptr(page_table),
+                             page_table.shape[1], _ptr(context_lens), max_context, softmax_scale, partition_tokens,
+                             _ptr(workspace), workspace.numel(), _stream(stream))
+    _check(st, "uq_decode_split")
+
+
+def decode_reduce(desc: CacheDesc, batch, num_q_heads, context_lens, max_context, partition_tokens, workspace, out,
+                  stream=None):
+    d = desc.c_struct()
+    st = lib.uq_decode_reduce(ctypes.byref(d), batch, num_q_heads, _ptr(context_lens), max_context, partition_tokens,
+                              _ptr(workspace), workspace.numel(), _ptr(out), _DT[out.dtype], _stream(stream))
+    _check(st, "uq_decode_reduce")
+    return out

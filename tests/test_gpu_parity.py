@@ -1,0 +1,274 @@
+"""GPU parity of the HIP path (through the C ABI) against the CPU oracle.
+
+Codes, scale bytes and FP8 query bytes must match bit for bit.  Attention
+outputs must match within max-abs 2e-3 and relative L2 1e-3 of the fp64
+oracle, which quantises the same seeded K/V on its own.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_20474_amd import workloads
+
+pytestmark = pytest.mark.gpu
+
+MAX_ABS = 2e-3
+REL_L2 = 1e-3
+
+
+@pytest.fixture(scope="module")
+def uq():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2606_20474_amd import uq as mod
+    return mod
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+def check_attention(got, ref, what):
+    got = np.asarray(got, np.float64)
+    ref = np.asarray(ref, np.float64)
+    err = np.abs(got - ref)
+    rel = np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-30)
+    log(f"{what}: max-abs {err.max():.3e} rel-L2 {rel:.3e}")
+    assert np.all(np.isfinite(got)), what
+    assert err.max() <= MAX_ABS, (what, err.max())
+    assert rel <= REL_L2, (what, rel)
+
+
+def gpu_cache(uq, wl, device, fill=0xA5, in_dtype=torch.float32):
+    desc = uq.CacheDesc(num_kv_heads=wl.num_kv_heads, num_pages=wl.num_pages, rotate_v=wl.rotate_v)
+    codes, scales = desc.alloc_pools(device, fill=fill)
+    for key, lo, hi in wl.segments():
+        k, v = wl.kv(key, lo, hi, device=device, dtype=in_dtype)
+        slots = torch.as_tensor(wl.slots(key, lo, hi), device=device)
+        uq.quantize_kv(desc, k, v, slots, codes, scales)
+    torch.cuda.synchronize()
+    return desc, codes, scales
+
+
+def oracle_cache(wl, seqs, device, in_dtype=torch.float32):
+    """Oracle pools for the sequences `seqs` only, in a compact page pool
+    (page ids renumbered; attention does not depend on the numbering)."""
+    maxp = wl.max_pages_per_seq
+    pt = np.arange(len(seqs) * maxp, dtype=np.int32).reshape(len(seqs), maxp)
+    pools = oracle.alloc_pools(len(seqs) * maxp, wl.num_kv_heads)
+    for i, b in enumerate(seqs):
+        for key, lo, hi in wl.segments():
+            if key not in (-1, b):
+                continue
+            hi_b = min(hi, int(wl.context_lens[b]))
+            if hi_b <= lo:
+                continue
+            k, v = wl.kv(key, lo, hi, device=device, dtype=in_dtype)
+            k = k[: hi_b - lo].float().cpu().numpy()
+            v = v[: hi_b - lo].float().cpu().numpy()
+            pos = np.arange(lo, hi_b, dtype=np.int64)
+            slots = pt[i, pos // 16].astype(np.int64) * 16 + pos % 16
+            oracle.quantize_kv(k, v, slots, len(seqs) * maxp, rotate_v=wl.rotate_v, pools=pools)
+    return pools, pt
+
+
+def run_decode(uq, wl, desc, codes, scales, device, partition=None, q=None, out_dtype=torch.float32, q_dtype=None):
+    q = (wl.q if q is None else q).to(device)
+    pt = torch.as_tensor(wl.page_table, device=device)
+    ctx = torch.as_tensor(wl.context_lens, device=device)
+    part = wl.partition_tokens if partition is None else partition
+    out = uq.decode_attention(desc, q, codes, scales, pt, ctx, wl.max_context, 1 / math.sqrt(128), part,
+                              out_dtype=out_dtype, q_dtype=q_dtype)
+    torch.cuda.synchronize()
+    return out.float().cpu().numpy()
+
+
+# --------------------------------------------------------------------------
+# quantize-on-write: bit-exact codes and scale bytes
+# --------------------------------------------------------------------------
+def test_quantize_tiny_bit_exact(uq):
+    dev = torch.device("cuda:0")
+    wl = workloads.tiny()
+    log("quantize tiny: fp32 4096 tokens")
+    desc, codes, scales = gpu_cache(uq, wl, dev)
+    pools = oracle.alloc_pools(wl.num_pages, 1, fill=0xA5)
+    for key, lo, hi in wl.segments():
+        k, v = wl.kv(key, lo, hi, device=dev)
+        oracle.quantize_kv(k.cpu().numpy(), v.cpu().numpy(), wl.slots(key, lo, hi), wl.num_pages, pools=pools)
+    assert np.array_equal(codes.cpu().numpy(), pools[0])
+    assert np.array_equal(scales.cpu().numpy(), pools[1])
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16, torch.float16])
+@pytest.mark.parametrize("rotate_v", [True, False])
+def test_quantize_dtypes_ragged_bit_exact(uq, dtype, rotate_v):
+    dev = torch.device("cuda:0")
+    log(f"quantize ragged dtype={dtype} rotate_v={rotate_v}")
+    Hkv, T, num_pages = 3, 1001, 80
+    g = torch.Generator(device=dev).manual_seed(11)
+    k = (torch.randn((T, Hkv, 128), generator=g, device=dev) * 3).to(dtype)
+    v = (torch.randn((T, Hkv, 128), generator=g, device=dev) * 0.01).to(dtype)
+    k[:7] = 0          # all-zero groups -> scale byte 0
+    k[7, 0, :] = -0.0
+    v[9, 1, 5] = 1e4   # one huge value in a group
+    perm = torch.randperm(num_pages * 16, generator=torch.Generator().manual_seed(5))[:T].numpy().astype(np.int64)
+    perm[3] = -1                     # padding token
+    perm[4] = num_pages * 16 + 7     # outside the pool: skipped
+    desc = uq.CacheDesc(num_kv_heads=Hkv, num_pages=num_pages, rotate_v=rotate_v)
+    codes, scales = desc.alloc_pools(dev, fill=0x5A)
+    uq.quantize_kv(desc, k, v, torch.as_tensor(perm, device=dev), codes, scales)
+    torch.cuda.synchronize()
+    pools = oracle.alloc_pools(num_pages, Hkv, fill=0x5A)
+    oracle.quantize_kv(k.float().cpu().numpy(), v.float().cpu().numpy(), perm, num_pages, rotate_v=rotate_v,
+                       pools=pools)
+    assert np.array_equal(codes.cpu().numpy(), pools[0])
+    assert np.array_equal(scales.cpu().numpy(), pools[1])
+
+
+def test_quantize_strided_rows(uq):
+    """K and V as views into a fused [T, (Hq + 2 Hkv) * 128] projection output."""
+    dev = torch.device("cuda:0")
+    Hq, Hkv, T = 4, 2, 96
+    g = torch.Generator(device=dev).manual_seed(3)
+    qkv = torch.randn((T, (Hq + 2 * Hkv) * 128), generator=g, device=dev).bfloat16()
+    k = qkv[:, Hq * 128:(Hq + Hkv) * 128].view(T, Hkv, 128)
+    v = qkv[:, (Hq + Hkv) * 128:].view(T, Hkv, 128)
+    slots = torch.arange(T, device=dev, dtype=torch.int64) + 16
+    desc = uq.CacheDesc(num_kv_heads=Hkv, num_pages=8)
+    codes, scales = desc.alloc_pools(dev, fill=0)
+    uq.quantize_kv(desc, k, v, slots, codes, scales, token_stride=qkv.stride(0))
+    torch.cuda.synchronize()
+    pools = oracle.quantize_kv(k.float().cpu().numpy(), v.float().cpu().numpy(), slots.cpu().numpy(), 8)
+    assert np.array_equal(codes.cpu().numpy(), pools[0]) and np.array_equal(scales.cpu().numpy(), pools[1])
+
+
+def test_quantize_write_workload_bit_exact(uq):
+    """65536-token bf16 prefill into random pages + a 1-token append for 256
+    sequences through a page table (logical slots); every pool byte checked."""
+    dev = torch.device("cuda:0")
+    ww = workloads.WriteWorkload()
+    log("quantize write workload: 65536 x 8 heads bf16 + 256 appends")
+    data = ww.build(device=dev)
+    kp, vp, pslots = data["prefill"]
+    ka, va, aslots, pt, ctx = data["append"]
+    desc = uq.CacheDesc(num_kv_heads=ww.num_kv_heads, num_pages=ww.num_pages)
+    codes, scales = desc.alloc_pools(dev, fill=0xA5)
+    uq.quantize_kv(desc, kp, vp, torch.as_tensor(pslots, device=dev), codes, scales)
+    uq.quantize_kv(desc, ka, va, torch.as_tensor(aslots, device=dev), codes, scales,
+                   page_table=torch.as_tensor(pt, device=dev))
+    torch.cuda.synchronize()
+    pools = oracle.alloc_pools(ww.num_pages, ww.num_kv_heads, fill=0xA5)
+    oracle.quantize_kv(kp.float().cpu().numpy(), vp.float().cpu().numpy(), pslots, ww.num_pages, pools=pools)
+    phys = pt[np.arange(ww.append_seqs), ctx // 16].astype(np.int64) * 16 + ctx % 16
+    oracle.quantize_kv(ka.float().cpu().numpy(), va.float().cpu().numpy(), phys, ww.num_pages, pools=pools)
+    assert np.array_equal(codes.cpu().numpy(), pools[0])
+    assert np.array_equal(scales.cpu().numpy(), pools[1])
+
+
+def test_prepare_query_bit_exact(uq):
+    dev = torch.device("cuda:0")
+    g = torch.Generator().manual_seed(9)
+    q = torch.randn((300, 128), generator=g) * torch.logspace(-4, 3, 300).unsqueeze(1)
+    q[0] = 0
+    q[1] = -0.0
+    q[2, 0] = 1e6   # saturates after the rotation
+    desc = uq.CacheDesc(num_kv_heads=1, num_pages=1)
+    for dt in (torch.float32, torch.bfloat16, torch.float16):
+        qd = q.to(dt)
+        got = uq.prepare_query(desc, qd.to(dev)).cpu().numpy()
+        ref = oracle.prepare_query(qd.float().numpy())
+        assert np.array_equal(got, ref), dt
+
+
+# --------------------------------------------------------------------------
+# decode attention
+# --------------------------------------------------------------------------
+@pytest.fixture(scope="module")
+def tiny_case(uq):
+    dev = torch.device("cuda:0")
+    wl = workloads.tiny()
+    desc, codes, scales = gpu_cache(uq, wl, dev)
+    pools, pt = oracle_cache(wl, [0], dev)
+    ref = oracle.decode_attention(wl.q.numpy(), pools, pt, wl.context_lens, 1, 1 / math.sqrt(128), True)
+    return wl, desc, codes, scales, ref
+
+
+@pytest.mark.parametrize("partition", [0, 32, 256, 1024, 4096])
+def test_decode_tiny_partitions(uq, tiny_case, partition):
+    wl, desc, codes, scales, ref = tiny_case
+    log(f"decode tiny partition={partition}")
+    out = run_decode(uq, wl, desc, codes, scales, torch.device("cuda:0"), partition=partition)
+    check_attention(out, ref, f"tiny p={partition}")
+
+
+def test_decode_tiny_dtypes(uq, tiny_case):
+    wl, desc, codes, scales, ref = tiny_case
+    dev = torch.device("cuda:0")
+    out_bf = run_decode(uq, wl, desc, codes, scales, dev, out_dtype=torch.bfloat16)
+    # a bf16 output adds one rounding of the result (relative 2^-9)
+    assert np.all(np.abs(out_bf - ref) <= MAX_ABS + np.abs(ref) * 2.0 ** -8)
+    q8 = uq.prepare_query(desc, wl.q.to(dev))
+    out_fp8 = run_decode(uq, wl, desc, codes, scales, dev, q=q8, q_dtype=uq.UQ_FP8_E4M3)
+    out_f32 = run_decode(uq, wl, desc, codes, scales, dev)
+    assert np.array_equal(out_fp8, out_f32)
+    qb = wl.q.bfloat16()
+    pools, pt = oracle_cache(wl, [0], dev)
+    ref_b = oracle.decode_attention(qb.float().numpy(), pools, pt, wl.context_lens, 1, 1 / math.sqrt(128), True)
+    check_attention(run_decode(uq, wl, desc, codes, scales, dev, q=qb), ref_b, "tiny bf16 q")
+
+
+@pytest.mark.parametrize("rotate_v", [True, False])
+@pytest.mark.parametrize("partition", [0, 64])
+def test_decode_ragged_gqa6(uq, rotate_v, partition):
+    dev = torch.device("cuda:0")
+    wl = workloads.custom(4, 12, 2, [1, 17, 1000, 0], seed=21, paging="random", rotate_v=rotate_v)
+    log(f"decode ragged G=6 rotate_v={rotate_v} partition={partition}")
+    desc, codes, scales = gpu_cache(uq, wl, dev)
+    out = run_decode(uq, wl, desc, codes, scales, dev, partition=partition)
+    pools, pt = oracle_cache(wl, list(range(wl.batch)), dev)
+    ref = oracle.decode_attention(wl.q.numpy(), pools, pt, wl.context_lens, wl.num_kv_heads, 1 / math.sqrt(128),
+                                  rotate_v)
+    assert np.all(out[3] == 0)   # empty context
+    check_attention(out, ref, f"ragged rv={rotate_v} p={partition}")
+
+
+@pytest.mark.parametrize("hq,hkv", [(16, 1), (2, 2), (48, 3)])
+def test_decode_group_sizes(uq, hq, hkv):
+    dev = torch.device("cuda:0")
+    wl = workloads.custom(2, hq, hkv, [300, 77], seed=5, paging="random")
+    log(f"decode groups hq={hq} hkv={hkv}")
+    desc, codes, scales = gpu_cache(uq, wl, dev)
+    out = run_decode(uq, wl, desc, codes, scales, dev, partition=64)
+    pools, pt = oracle_cache(wl, [0, 1], dev)
+    ref = oracle.decode_attention(wl.q.numpy(), pools, pt, wl.context_lens, hkv, 1 / math.sqrt(128), True)
+    check_attention(out, ref, f"groups {hq}/{hkv}")
+
+
+def test_decode_qwen_full_size_sampled(uq):
+    """B=32, Hq=64, Hkv=4, context 32768, random pages: the default launch
+    configuration, checked on sampled sequences; deterministic across runs,
+    and split + reduce equals the one-call entry point."""
+    dev = torch.device("cuda:0")
+    wl = workloads.qwen3_235b_like()
+    log("decode qwen3-235b-like full size")
+    desc, codes, scales = gpu_cache(uq, wl, dev, fill=None)
+    out1 = run_decode(uq, wl, desc, codes, scales, dev)
+    out2 = run_decode(uq, wl, desc, codes, scales, dev)
+    assert np.array_equal(out1, out2)
+    q = wl.q.to(dev)
+    pt = torch.as_tensor(wl.page_table, device=dev)
+    ctx = torch.as_tensor(wl.context_lens, device=dev)
+    part = uq.default_partition(desc, wl.batch, wl.num_q_heads, wl.max_context)
+    ws = uq.alloc_workspace(desc, wl.batch, wl.num_q_heads, wl.max_context, part)
+    out3 = torch.empty_like(q)
+    uq.decode_split(desc, q, codes, scales, pt, ctx, wl.max_context, 1 / math.sqrt(128), part, ws)
+    uq.decode_reduce(desc, wl.batch, wl.num_q_heads, ctx, wl.max_context, part, ws, out3)
+    torch.cuda.synchronize()
+    assert np.array_equal(out3.cpu().numpy(), out1)
+    seqs = [0, 19]
+    pools, ptc = oracle_cache(wl, seqs, dev)
+    ref = oracle.decode_attention(wl.q.numpy()[seqs], pools, ptc, wl.context_lens[seqs], wl.num_kv_heads,
+                                  1 / math.sqrt(128), True)
+    check_attention(out1[seqs], ref, "qwen sampled")

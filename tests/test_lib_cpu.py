@@ -1,0 +1,117 @@
+"""Host-side checks of libuq that need no GPU: the library builds and loads,
+exports every entry point include/uq.h declares, and rejects bad arguments
+with the documented status before any HIP call."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def uq():
+    from paper_2606_20474_amd import build
+    if not os.path.exists(build.LIB):
+        build.build()
+    from paper_2606_20474_amd import uq as mod
+    return mod
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "uq.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(uq_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(uq):
+    names = header_functions()
+    assert len(names) >= 9
+    for n in names:
+        assert hasattr(uq.lib, n), n
+    assert sorted(uq.EXPORTS) == names
+
+
+def test_status_strings_are_total(uq):
+    for s in range(5):
+        assert uq.status_string(s).startswith("UQ_")
+    assert uq.status_string(99) == "UQ_ERR_UNKNOWN"
+    assert uq.lib.uq_version() >= 100
+
+
+FAKE = ctypes.c_void_p(0x10000)   # aligned, never dereferenced: validation fails first or nothing is launched
+
+
+def desc(**kw):
+    from paper_2606_20474_amd.uq import uq_cache_desc
+    d = dict(num_kv_heads=2, head_dim=128, page_size=16, group_size=32, num_pages=10, c=0.156, rotate_v=1)
+    d.update(kw)
+    return uq_cache_desc(**d)
+
+
+def quantize(uq, d, num_tokens=4, stride=256, k=FAKE, pt=None, num_seqs=0, mpps=0, dtype=1, slots=FAKE):
+    return uq.lib.uq_quantize_kv(ctypes.byref(d) if d is not None else None, k, FAKE, dtype, num_tokens, stride, pt,
+                                 num_seqs, mpps, slots, FAKE, FAKE, None)
+
+
+def test_quantize_validation(uq):
+    E = uq
+    assert quantize(uq, None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert quantize(uq, desc(head_dim=64)) == E.UQ_ERR_UNSUPPORTED
+    assert quantize(uq, desc(page_size=32)) == E.UQ_ERR_UNSUPPORTED
+    assert quantize(uq, desc(group_size=16)) == E.UQ_ERR_UNSUPPORTED
+    assert quantize(uq, desc(c=0.0)) == E.UQ_ERR_INVALID_ARGUMENT
+    assert quantize(uq, desc(c=float("nan"))) == E.UQ_ERR_INVALID_ARGUMENT
+    assert quantize(uq, desc(num_kv_heads=0)) == E.UQ_ERR_INVALID_ARGUMENT
+    assert quantize(uq, desc(num_pages=0)) == E.UQ_ERR_INVALID_ARGUMENT
+    assert quantize(uq, desc(), num_tokens=-1) == E.UQ_ERR_INVALID_ARGUMENT
+    assert quantize(uq, desc(), k=None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert quantize(uq, desc(), slots=None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert quantize(uq, desc(), stride=255) == E.UQ_ERR_INVALID_ARGUMENT      # below Hkv * 128
+    assert quantize(uq, desc(), stride=260) == E.UQ_ERR_INVALID_ARGUMENT      # not 16-byte aligned rows
+    assert quantize(uq, desc(), k=ctypes.c_void_p(0x10004)) == E.UQ_ERR_INVALID_ARGUMENT
+    assert quantize(uq, desc(), dtype=3) == E.UQ_ERR_UNSUPPORTED
+    assert quantize(uq, desc(), pt=FAKE, num_seqs=0, mpps=4) == E.UQ_ERR_INVALID_ARGUMENT
+    assert quantize(uq, desc(), pt=FAKE, num_seqs=2, mpps=0) == E.UQ_ERR_INVALID_ARGUMENT
+    assert quantize(uq, desc(), num_tokens=0) == E.UQ_OK                     # no-op, nothing launched
+
+
+def decode(uq, d, q=FAKE, qdt=0, B=2, Hq=4, mpps=4, maxctx=64, scale=0.1, part=0, ws=FAKE, wsb=1 << 30, out=FAKE,
+           odt=0, ctx=FAKE, pt=FAKE):
+    return uq.lib.uq_decode_attention(ctypes.byref(d) if d is not None else None, q, qdt, B, Hq, FAKE, FAKE, pt, mpps,
+                                      ctx, maxctx, scale, part, ws, wsb, out, odt, None)
+
+
+def test_decode_validation(uq):
+    E = uq
+    assert decode(uq, None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert decode(uq, desc(head_dim=256)) == E.UQ_ERR_UNSUPPORTED
+    assert decode(uq, desc(), Hq=3) == E.UQ_ERR_INVALID_ARGUMENT               # Hq % Hkv
+    assert decode(uq, desc(), Hq=34) == E.UQ_ERR_UNSUPPORTED                   # 17 query heads per kv head
+    assert decode(uq, desc(), B=0) == E.UQ_ERR_INVALID_ARGUMENT
+    assert decode(uq, desc(), maxctx=65) == E.UQ_ERR_INVALID_ARGUMENT          # > max_pages_per_seq * 16
+    assert decode(uq, desc(), maxctx=-1) == E.UQ_ERR_INVALID_ARGUMENT
+    assert decode(uq, desc(), part=48) == E.UQ_ERR_INVALID_ARGUMENT            # not a multiple of 32
+    assert decode(uq, desc(), scale=float("inf")) == E.UQ_ERR_INVALID_ARGUMENT
+    assert decode(uq, desc(), q=None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert decode(uq, desc(), pt=None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert decode(uq, desc(), ctx=None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert decode(uq, desc(), out=None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert decode(uq, desc(), qdt=7) == E.UQ_ERR_UNSUPPORTED
+    assert decode(uq, desc(), odt=3) == E.UQ_ERR_UNSUPPORTED
+    assert decode(uq, desc(), ws=None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert decode(uq, desc(), wsb=16) == E.UQ_ERR_WORKSPACE_TOO_SMALL
+    assert decode(uq, desc(), q=ctypes.c_void_p(0x10008)) == E.UQ_ERR_INVALID_ARGUMENT
+
+
+def test_workspace_and_partition_sizes(uq):
+    from paper_2606_20474_amd.uq import CacheDesc
+    d = CacheDesc(num_kv_heads=4, num_pages=65536)
+    p = uq.default_partition(d, 32, 64, 32768)
+    assert p % 32 == 0 and 1024 <= p <= 4096
+    np_ = -(-32768 // p)
+    assert uq.workspace_bytes(d, 32, 64, 32768, 0) == 32 * 64 * np_ * 130 * 4
+    assert uq.workspace_bytes(d, 32, 64, 32768, 4096) == 32 * 64 * 8 * 130 * 4
+    assert uq.workspace_bytes(d, 32, 63, 32768, 4096) == 0   # invalid: returns 0
+    assert uq.workspace_bytes(d, 1, 4, 0, 0) == 4 * 1 * 130 * 4
