@@ -1,0 +1,195 @@
+"""Decode-step benchmark of the FP4 KV path on one MI355X.
+
+One step is the whole hot path for one decode token per sequence:
+  1. uq_quantize_kv writes the step's new K/V token of every sequence into
+     the FP4 cache (Algorithm 1, "Write"), at the last position of its
+     context;
+  2. uq_decode_attention runs decode attention over the full contexts
+     (Algorithm 1, "Decode"), one kernel launch.
+Inputs are resident in HBM before the timed region.  The default workload is
+the Qwen3-235B-like layer: 64 query heads, 4 KV heads, head_dim 128, batch
+32, every context 32768, random page table.  ``value`` is KV tokens/s =
+sum of contexts / step time.
+
+The JSON line also carries the roofline of the dominant kernel (the decode
+kernel: algorithmic KV bytes per launch / its mean launch time from HIP
+events on its stream) and the CPU oracle timed on a sample of the same
+workload.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+KV_BYTES_PER_TOKEN_HEAD = 136   # K and V: 2 x (64 B codes + 4 B scales)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="qwen3-235b-like",
+                    choices=["qwen3-235b-like", "high-concurrency", "minimax-like", "tiny"])
+    ap.add_argument("--partition", type=int, default=-1, help="partition tokens (-1: workload default)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-seqs", type=int, default=4)
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="run one device-to-device copy of this many MiB before the timed steps; its "
+                         "FETCH_SIZE/WRITE_SIZE counters calibrate the HBM-traffic counters")
+    return ap.parse_args()
+
+
+def make_workload(name):
+    from paper_2606_20474_amd import workloads
+    return {"qwen3-235b-like": workloads.qwen3_235b_like, "high-concurrency": workloads.high_concurrency,
+            "minimax-like": workloads.minimax_like, "tiny": workloads.tiny}[name]()
+
+
+def fill_cache(uq, wl, desc, codes, scales, dev):
+    """Quantise every stored segment of the workload into the pools (setup, untimed)."""
+    import torch
+    for key, lo, hi in wl.segments():
+        k, v = wl.kv(key, lo, hi, device=dev)
+        slots = torch.as_tensor(wl.slots(key, lo, hi), device=dev)
+        uq.quantize_kv(desc, k, v, slots, codes, scales)
+        del k, v
+    torch.cuda.synchronize()
+
+
+def cpu_baseline(wl, nseq, dev):
+    """The oracle on `nseq` sequences of the workload (all their query heads,
+    full contexts), timed on the host; KV tokens/s."""
+    import oracle
+    seqs = list(range(min(nseq, wl.batch)))
+    maxp = wl.max_pages_per_seq
+    pt = np.arange(len(seqs) * maxp, dtype=np.int32).reshape(len(seqs), maxp)
+    pools = oracle.alloc_pools(len(seqs) * maxp, wl.num_kv_heads)
+    for i, b in enumerate(seqs):
+        for key, lo, hi in wl.segments():
+            if key not in (-1, b):
+                continue
+            hi_b = min(hi, int(wl.context_lens[b]))
+            if hi_b <= lo:
+                continue
+            k, v = wl.kv(key, lo, hi, device=dev)
+            k = k[: hi_b - lo].cpu().numpy()
+            v = v[: hi_b - lo].cpu().numpy()
+            pos = np.arange(lo, hi_b, dtype=np.int64)
+            slots = pt[i, pos // 16].astype(np.int64) * 16 + pos % 16
+            oracle.quantize_kv(k, v, slots, len(seqs) * maxp, rotate_v=wl.rotate_v, pools=pools)
+    q = wl.q.numpy()[seqs]
+    ctx = wl.context_lens[seqs]
+    t0 = time.perf_counter()
+    oracle.decode_attention(q, pools, pt, ctx, wl.num_kv_heads, 1 / math.sqrt(128), wl.rotate_v)
+    dt = time.perf_counter() - t0
+    toks = int(ctx.astype(np.int64).sum())
+    return {"value": toks / dt, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
+            "sample": f"{len(seqs)} of {wl.batch} sequences, all {wl.num_q_heads} query heads, "
+                      f"{toks} context tokens; fp64 decode attention over the oracle's own FP4 cache; "
+                      f"{dt:.2f} s wall"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no multi-GPU path.",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2606_20474_amd import uq
+
+    dev = torch.device("cuda:0")
+    wl = make_workload(args.workload)
+    part = wl.partition_tokens if args.partition < 0 else args.partition
+    desc = uq.CacheDesc(num_kv_heads=wl.num_kv_heads, num_pages=wl.num_pages, rotate_v=wl.rotate_v)
+    codes, scales = desc.alloc_pools(dev)
+    fill_cache(uq, wl, desc, codes, scales, dev)
+    if part == 0:
+        part = uq.default_partition(desc, wl.batch, wl.num_q_heads, wl.max_context)
+
+    q = wl.q.to(dev)
+    pt = torch.as_tensor(wl.page_table, device=dev)
+    ctx = torch.as_tensor(wl.context_lens, device=dev)
+    ws = uq.alloc_workspace(desc, wl.batch, wl.num_q_heads, wl.max_context, part, dev)
+    out = torch.empty((wl.batch, wl.num_q_heads, 128), dtype=torch.float32, device=dev)
+    # the step's new token of every sequence, written at its last position
+    g = torch.Generator(device=dev).manual_seed(12345)
+    k_new = torch.randn((wl.batch, wl.num_kv_heads, 128), generator=g, device=dev)
+    v_new = torch.randn((wl.batch, wl.num_kv_heads, 128), generator=g, device=dev)
+    last = wl.context_lens.astype(np.int64) - 1
+    new_slots = torch.as_tensor(wl.page_table[np.arange(wl.batch), last // 16].astype(np.int64) * 16 + last % 16,
+                                device=dev)
+    scale = 1 / math.sqrt(128)
+    stream = torch.cuda.current_stream()
+
+    def step(ev_a=None, ev_b=None):
+        uq.quantize_kv(desc, k_new, v_new, new_slots, codes, scales)
+        if ev_a is not None:
+            ev_a.record(stream)
+        uq.decode_attention(desc, q, codes, scales, pt, ctx, wl.max_context, scale, part, ws, out)
+        if ev_b is not None:
+            ev_b.record(stream)
+
+    if args.calib_copy_mib > 0:
+        n = args.calib_copy_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device=dev)
+        dst = torch.empty(n, dtype=torch.uint8, device=dev)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for i in range(args.steps):
+        step(*evs[i])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    ms_step = t_start.elapsed_time(t_end) / args.steps
+    dec_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+
+    tokens = wl.total_tokens()
+    kv_bytes = wl.kv_bytes_fp4()
+    achieved = kv_bytes / (dec_ms * 1e-3) / 1e9
+    result = {
+        "metric": "decode-attention KV tokens/s and achieved HBM GB/s (% of peak) at 32k context",
+        "value": tokens / (ms_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "fp4-e2m1+ue8m0 kv, fp8-e4m3 q, fp32 accum",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "batch": wl.batch, "num_q_heads": wl.num_q_heads,
+                   "num_kv_heads": wl.num_kv_heads, "head_dim": 128, "context": int(wl.max_context),
+                   "page_size": 16, "partition_tokens": int(part), "parallelism": "single-gpu"},
+        "hbm_gbs_step": kv_bytes / (ms_step * 1e-3) / 1e9,
+        "hbm_frac_step": kv_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
+        "roofline": {"bound": "hbm", "kernel": "decode_kernel", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "launch_ms": dec_ms, "bytes_per_launch": kv_bytes},
+    }
+    if not args.no_cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample_seqs, dev)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -135,11 +135,10 @@ uq_status uq_prepare_query(const uq_cache_desc *desc, const void *q, uq_dtype q_
                            uint8_t *q_fp8, void *stream);
 
 /*
- * Workspace needed by uq_decode_attention / uq_decode_split for these sizes
- * (partial results: per (sequence, query head, partition) a running max,
- * a running sum and 128 fp32 accumulators).  partition_tokens == 0 selects
- * the library's default partition for the shape.  Returns 0 for invalid
- * arguments.
+ * Workspace needed by uq_decode_attention for these sizes: per (sequence,
+ * query head, partition) 128 fp32 accumulators, a running max and a running
+ * sum.  partition_tokens == 0 selects the library's default partition for
+ * the shape.  Returns 0 for invalid arguments.
  */
 size_t uq_decode_workspace_bytes(const uq_cache_desc *desc, int32_t batch, int32_t num_q_heads,
                                  int32_t max_context, int32_t partition_tokens);
@@ -149,7 +148,9 @@ int32_t uq_default_partition(const uq_cache_desc *desc, int32_t batch, int32_t n
 
 /*
  * uq_decode_attention -- decode attention over the FP4 cache (Algorithm 1,
- * "Decode"), one new query token per sequence.
+ * "Decode"), one new query token per sequence: one launch of the partition
+ * kernel, plus one launch of the merge kernel when a context can span more
+ * than one partition (max_context > partition).
  *   q             : [batch][num_q_heads][128].  F32/BF16/F16: rotated and
  *                   cast to FP8 inside the call.  FP8_E4M3: already
  *                   prepared by uq_prepare_query.
@@ -158,10 +159,12 @@ int32_t uq_default_partition(const uq_cache_desc *desc, int32_t batch, int32_t n
  *   max_context   : host-side upper bound of every context_lens[b]
  *                   (<= max_pages_per_seq * 16); sizes the grid without a
  *                   device read.  Lengths above it are clamped to it.
- *   softmax_scale : multiplies q.k (usually 1/sqrt(128)).
+ *   softmax_scale : multiplies q.k (usually 1/sqrt(128)); finite and > 0.
  *   partition_tokens : context tokens per split-context partition, a
  *                   multiple of 32, or 0 for the default.
- *   workspace     : >= uq_decode_workspace_bytes(...) bytes, device.
+ *   workspace     : >= uq_decode_workspace_bytes(...) bytes of device
+ *                   memory, 16-byte aligned, no initial contents required.
+ *                   Calls that share a workspace must not run concurrently.
  *   out           : [batch][num_q_heads][128] F32 or BF16.  With rotate_v
  *                   the output is rotated back (o <- R o), so it is in the
  *                   same basis as an unrotated V.  An empty context gives 0.
@@ -169,8 +172,9 @@ int32_t uq_default_partition(const uq_cache_desc *desc, int32_t batch, int32_t n
  * Errors: INVALID_ARGUMENT for null pointers, batch/num_q_heads < 1,
  * num_q_heads % num_kv_heads != 0, max_context < 0 or above
  * max_pages_per_seq * 16, partition_tokens not a multiple of 32, a
- * non-finite softmax_scale; UNSUPPORTED for more than 16 query heads per kv
- * head or unsupported dtypes; WORKSPACE_TOO_SMALL.
+ * non-finite or non-positive softmax_scale, misaligned q/pools/workspace/out; UNSUPPORTED
+ * for more than 16 query heads per kv head or unsupported dtypes;
+ * WORKSPACE_TOO_SMALL.
  */
 uq_status uq_decode_attention(const uq_cache_desc *desc, const void *q, uq_dtype q_dtype, int32_t batch,
                               int32_t num_q_heads, const uint8_t *kv_codes, const uint8_t *kv_scales,
@@ -178,23 +182,6 @@ uq_status uq_decode_attention(const uq_cache_desc *desc, const void *q, uq_dtype
                               int32_t max_context, float softmax_scale, int32_t partition_tokens,
                               void *workspace, size_t workspace_bytes, void *out, uq_dtype out_dtype,
                               void *stream);
-
-/*
- * The two launches of uq_decode_attention, exposed for callers that want to
- * time or overlap them.  uq_decode_split runs the partition kernel and fills
- * the workspace; uq_decode_reduce merges the partitions into `out`.  Called
- * back to back on one stream with the same arguments they are exactly
- * uq_decode_attention.
- */
-uq_status uq_decode_split(const uq_cache_desc *desc, const void *q, uq_dtype q_dtype, int32_t batch,
-                          int32_t num_q_heads, const uint8_t *kv_codes, const uint8_t *kv_scales,
-                          const int32_t *page_table, int32_t max_pages_per_seq, const int32_t *context_lens,
-                          int32_t max_context, float softmax_scale, int32_t partition_tokens, void *workspace,
-                          size_t workspace_bytes, void *stream);
-uq_status uq_decode_reduce(const uq_cache_desc *desc, int32_t batch, int32_t num_q_heads,
-                           const int32_t *context_lens, int32_t max_context, int32_t partition_tokens,
-                           const void *workspace, size_t workspace_bytes, void *out, uq_dtype out_dtype,
-                           void *stream);
 
 #ifdef __cplusplus
 }

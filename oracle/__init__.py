@@ -31,6 +31,7 @@ def lib():
             _build.build()
         L = ctypes.CDLL(_build.LIB)
         vp, i64, i32, f32, f64 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float, ctypes.c_double
+        L.uqo_num_threads.restype = i32
         L.uqo_wht128_f32.argtypes = [vp, i64]
         L.uqo_wht128_f64.argtypes = [vp, vp]
         L.uqo_scale_exponent.argtypes = [f32, f32]
@@ -61,6 +62,11 @@ def _ptr(a):
 
 def _f32(x):
     return np.ascontiguousarray(x, dtype=np.float32)
+
+
+def num_threads():
+    """Threads the oracle's OpenMP loops run on."""
+    return int(lib().uqo_num_threads())
 
 
 def wht128_f32(x):

@@ -47,6 +47,7 @@
  * (no -ffast-math: fp32 results must follow IEEE round-to-nearest-even).
  */
 #include <math.h>
+#include <omp.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -57,6 +58,9 @@
 #define UQO_PAGE 16        /* tokens per page */
 #define UQO_TILE_CODES 1024   /* bytes of codes per (page, head, K|V) tile */
 #define UQO_TILE_SCALES 64    /* bytes of scales per (page, head, K|V) tile */
+
+/* Threads the OpenMP loops of this file use. */
+int uqo_num_threads(void) { return omp_get_max_threads(); }
 
 /* The E2M1 magnitudes, indexed by the low 3 bits of a code (section
  * "Constant-Optimized Scaling", the set F). */

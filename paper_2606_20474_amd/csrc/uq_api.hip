@@ -27,12 +27,12 @@ uq_status check_desc(const uq_cache_desc* d) {
 uq_status from_hip(hipError_t e) { return e == hipSuccess ? UQ_OK : UQ_ERR_HIP; }
 
 int32_t pick_partition(int32_t batch, int32_t num_kv_heads, int32_t max_context) {
-    // Enough blocks to give every one of the 256 CUs several resident
-    // blocks, without splitting a context below 1024 tokens (below that the
-    // per-partition prologue and the partial write stop being negligible).
+    // The longest partition (fewest partials to merge, fewest per-block
+    // prologues) that still gives every one of the 256 CUs at least two
+    // blocks; between 1024 and 16384 tokens.
     const int64_t heads = int64_t(batch) * num_kv_heads;
-    int32_t part = 4096;
-    while (part > 1024 && heads * ((max_context + part - 1) / part) < 1024) part /= 2;
+    int32_t part = 16384;
+    while (part > 1024 && heads * ((int64_t(max_context) + part - 1) / part) < 512) part /= 2;
     return part;
 }
 
@@ -48,23 +48,34 @@ uq_status check_decode_common(const uq_cache_desc* desc, int32_t batch, int32_t 
     return UQ_OK;
 }
 
-size_t workspace_for(int32_t batch, int32_t num_q_heads, int32_t max_context, int32_t part) {
-    const int64_t np = max_context > 0 ? (int64_t(max_context) + part - 1) / part : 1;
-    return size_t(batch) * size_t(num_q_heads) * size_t(np) * (kHeadDim + 2) * sizeof(float);
+size_t align16(size_t x) { return (x + 15) & ~size_t(15); }
+
+int64_t num_partitions(int32_t max_context, int32_t part) {
+    return max_context > 0 ? (int64_t(max_context) + part - 1) / part : 1;
 }
 
-// Fill the parameter block shared by the split and reduce launches.
+size_t partial_bytes(int32_t batch, int32_t num_q_heads, int32_t max_context, int32_t part) {
+    return align16(size_t(batch) * size_t(num_q_heads) * size_t(num_partitions(max_context, part)) * (kHeadDim + 2) *
+                   sizeof(float));
+}
+
+size_t workspace_for(int32_t batch, int32_t num_q_heads, int32_t max_context, int32_t part) {
+    return partial_bytes(batch, num_q_heads, max_context, part);
+}
+
+// Fill the parameter block of the decode launches.  Workspace: the partial
+// accumulators, then the (max, sum) pairs.
 uq_status make_decode_params(const uq_cache_desc* desc, const void* q, uq_dtype q_dtype, int32_t batch,
                              int32_t num_q_heads, const uint8_t* kv_codes, const uint8_t* kv_scales,
                              const int32_t* page_table, int32_t max_pages_per_seq, const int32_t* context_lens,
-                             int32_t max_context, float softmax_scale, int32_t partition_tokens, const void* workspace,
-                             size_t workspace_bytes, uq::DecodeParams& p) {
+                             int32_t max_context, float softmax_scale, int32_t partition_tokens, void* workspace,
+                             size_t workspace_bytes, void* out, uq_dtype out_dtype, uq::DecodeParams& p) {
     const int32_t part = partition_tokens == 0 ? pick_partition(batch, desc->num_kv_heads, max_context) : partition_tokens;
     const size_t need = workspace_for(batch, num_q_heads, max_context, part);
     if (workspace == nullptr) return UQ_ERR_INVALID_ARGUMENT;
     if (workspace_bytes < need) return UQ_ERR_WORKSPACE_TOO_SMALL;
     if (!aligned16(workspace)) return UQ_ERR_INVALID_ARGUMENT;
-    const int64_t np = max_context > 0 ? (int64_t(max_context) + part - 1) / part : 1;
+    const int64_t np = num_partitions(max_context, part);
     if (np > 0x7FFFFFFF) return UQ_ERR_UNSUPPORTED;
     p.q = q;
     p.q_dtype = int32_t(q_dtype);
@@ -82,11 +93,12 @@ uq_status make_decode_params(const uq_cache_desc* desc, const void* q, uq_dtype 
     p.scale_log2 = float(double(softmax_scale) * 1.4426950408889634);
     p.partition_tokens = part;
     p.num_partitions = int32_t(np);
+    char* ws = static_cast<char*>(workspace);
     const size_t acc_bytes = size_t(batch) * num_q_heads * size_t(np) * kHeadDim * sizeof(float);
-    p.part_acc = static_cast<float*>(const_cast<void*>(workspace));
-    p.part_ml = reinterpret_cast<float*>(static_cast<char*>(const_cast<void*>(workspace)) + acc_bytes);
-    p.out = nullptr;
-    p.out_dtype = 0;
+    p.part_acc = reinterpret_cast<float*>(ws);
+    p.part_ml = reinterpret_cast<float*>(ws + acc_bytes);
+    p.out = out;
+    p.out_dtype = out_dtype == UQ_F32 ? 0 : 1;
     p.rotate_v = desc->rotate_v != 0;
     return UQ_OK;
 }
@@ -103,7 +115,7 @@ uq_status check_split_args(const uq_cache_desc* desc, const void* q, uq_dtype q_
         return UQ_ERR_UNSUPPORTED;
     if (max_pages_per_seq < 1) return UQ_ERR_INVALID_ARGUMENT;
     if (int64_t(max_context) > int64_t(max_pages_per_seq) * kPageSize) return UQ_ERR_INVALID_ARGUMENT;
-    if (!isfinite(softmax_scale)) return UQ_ERR_INVALID_ARGUMENT;
+    if (!(isfinite(softmax_scale) && softmax_scale > 0.0f)) return UQ_ERR_INVALID_ARGUMENT;
     if (!aligned16(q) || !aligned16(kv_codes) || !aligned16(kv_scales)) return UQ_ERR_INVALID_ARGUMENT;
     return UQ_OK;
 }
@@ -182,39 +194,6 @@ size_t uq_decode_workspace_bytes(const uq_cache_desc* desc, int32_t batch, int32
     return workspace_for(batch, num_q_heads, max_context, part);
 }
 
-uq_status uq_decode_split(const uq_cache_desc* desc, const void* q, uq_dtype q_dtype, int32_t batch,
-                          int32_t num_q_heads, const uint8_t* kv_codes, const uint8_t* kv_scales,
-                          const int32_t* page_table, int32_t max_pages_per_seq, const int32_t* context_lens,
-                          int32_t max_context, float softmax_scale, int32_t partition_tokens, void* workspace,
-                          size_t workspace_bytes, void* stream) {
-    uq_status s = check_split_args(desc, q, q_dtype, batch, num_q_heads, kv_codes, kv_scales, page_table,
-                                   max_pages_per_seq, context_lens, max_context, softmax_scale, partition_tokens);
-    if (s != UQ_OK) return s;
-    uq::DecodeParams p;
-    s = make_decode_params(desc, q, q_dtype, batch, num_q_heads, kv_codes, kv_scales, page_table, max_pages_per_seq,
-                           context_lens, max_context, softmax_scale, partition_tokens, workspace, workspace_bytes, p);
-    if (s != UQ_OK) return s;
-    if (max_context == 0) return UQ_OK;
-    return from_hip(uq::launch_decode_split(p, static_cast<hipStream_t>(stream)));
-}
-
-uq_status uq_decode_reduce(const uq_cache_desc* desc, int32_t batch, int32_t num_q_heads, const int32_t* context_lens,
-                           int32_t max_context, int32_t partition_tokens, const void* workspace,
-                           size_t workspace_bytes, void* out, uq_dtype out_dtype, void* stream) {
-    uq_status s = check_decode_common(desc, batch, num_q_heads, max_context, partition_tokens);
-    if (s != UQ_OK) return s;
-    if (context_lens == nullptr || out == nullptr) return UQ_ERR_INVALID_ARGUMENT;
-    if (out_dtype != UQ_F32 && out_dtype != UQ_BF16) return UQ_ERR_UNSUPPORTED;
-    if (!aligned16(out)) return UQ_ERR_INVALID_ARGUMENT;
-    uq::DecodeParams p;
-    s = make_decode_params(desc, nullptr, UQ_F32, batch, num_q_heads, nullptr, nullptr, nullptr, 1, context_lens,
-                           max_context, 1.0f, partition_tokens, workspace, workspace_bytes, p);
-    if (s != UQ_OK) return s;
-    p.out = out;
-    p.out_dtype = out_dtype == UQ_F32 ? 0 : 1;
-    return from_hip(uq::launch_decode_reduce(p, static_cast<hipStream_t>(stream)));
-}
-
 uq_status uq_decode_attention(const uq_cache_desc* desc, const void* q, uq_dtype q_dtype, int32_t batch,
                               int32_t num_q_heads, const uint8_t* kv_codes, const uint8_t* kv_scales,
                               const int32_t* page_table, int32_t max_pages_per_seq, const int32_t* context_lens,
@@ -226,11 +205,12 @@ uq_status uq_decode_attention(const uq_cache_desc* desc, const void* q, uq_dtype
     if (out == nullptr) return UQ_ERR_INVALID_ARGUMENT;
     if (out_dtype != UQ_F32 && out_dtype != UQ_BF16) return UQ_ERR_UNSUPPORTED;
     if (!aligned16(out)) return UQ_ERR_INVALID_ARGUMENT;
-    s = uq_decode_split(desc, q, q_dtype, batch, num_q_heads, kv_codes, kv_scales, page_table, max_pages_per_seq,
-                        context_lens, max_context, softmax_scale, partition_tokens, workspace, workspace_bytes, stream);
+    uq::DecodeParams p;
+    s = make_decode_params(desc, q, q_dtype, batch, num_q_heads, kv_codes, kv_scales, page_table, max_pages_per_seq,
+                           context_lens, max_context, softmax_scale, partition_tokens, workspace, workspace_bytes, out,
+                           out_dtype, p);
     if (s != UQ_OK) return s;
-    return uq_decode_reduce(desc, batch, num_q_heads, context_lens, max_context, partition_tokens, workspace,
-                            workspace_bytes, out, out_dtype, stream);
+    return from_hip(uq::launch_decode(p, static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

@@ -43,14 +43,13 @@ struct DecodeParams {
     int32_t num_partitions;
     float* part_acc;           // [B][Hq][NP][128]
     float* part_ml;            // [B][Hq][NP][2]  (running max in log2 units, running sum)
-    void* out;                 // reduce only
+    void* out;                 // [B][Hq][128]
     int32_t out_dtype;         // 0 f32, 1 bf16
     int32_t rotate_v;
 };
 
 hipError_t launch_quantize_kv(const QuantizeParams& p, int dtype, hipStream_t stream);
 hipError_t launch_prepare_query(const void* q, int dtype, int64_t rows, uint8_t* q8, hipStream_t stream);
-hipError_t launch_decode_split(const DecodeParams& p, hipStream_t stream);
-hipError_t launch_decode_reduce(const DecodeParams& p, hipStream_t stream);
+hipError_t launch_decode(const DecodeParams& p, hipStream_t stream);
 
 }  // namespace uq

@@ -29,7 +29,7 @@ TILE_SCALES = 64
 # Every symbol include/uq.h declares.
 EXPORTS = (
     "uq_status_string", "uq_version", "uq_quantize_kv", "uq_prepare_query", "uq_decode_workspace_bytes",
-    "uq_default_partition", "uq_decode_attention", "uq_decode_split", "uq_decode_reduce",
+    "uq_default_partition", "uq_decode_attention",
 )
 
 
@@ -70,10 +70,6 @@ def _load():
     L.uq_default_partition.restype = i32
     L.uq_decode_attention.argtypes = [D, vp, i32, i32, i32, vp, vp, vp, i32, vp, i32, f32, i32, vp, sz, vp, i32, vp]
     L.uq_decode_attention.restype = i32
-    L.uq_decode_split.argtypes = [D, vp, i32, i32, i32, vp, vp, vp, i32, vp, i32, f32, i32, vp, sz, vp]
-    L.uq_decode_split.restype = i32
-    L.uq_decode_reduce.argtypes = [D, i32, i32, vp, i32, i32, vp, sz, vp, i32, vp]
-    L.uq_decode_reduce.restype = i32
     return L
 
 
@@ -168,7 +164,7 @@ def default_partition(desc: CacheDesc, batch, num_q_heads, max_context):
 
 
 def alloc_workspace(desc: CacheDesc, batch, num_q_heads, max_context, partition_tokens=0, device="cuda"):
-    n = max(workspace_bytes(desc, batch, num_q_heads, max_context, partition_tokens), 16)
+    n = workspace_bytes(desc, batch, num_q_heads, max_context, partition_tokens)
     return torch.empty(n, dtype=torch.uint8, device=device)
 
 
@@ -190,24 +186,4 @@ def decode_attention(desc: CacheDesc, q, codes, scales, page_table, context_lens
                                  partition_tokens, _ptr(workspace), workspace.numel(), _ptr(out), _DT[out.dtype],
                                  _stream(stream))
     _check(st, "uq_decode_attention")
-    return out
-
-
-def decode_split(desc: CacheDesc, q, codes, scales, page_table, context_lens, max_context, softmax_scale,
-                 partition_tokens, workspace, q_dtype=None, stream=None):
-    B, Hq = q.shape[0], q.shape[1]
-    d = desc.c_struct()
-    qdt = _DT[q.dtype] if q_dtype is None else q_dtype
-    st = lib.uq_decode_split(ctypes.byref(d), _ptr(q), qdt, B, Hq, _ptr(codes), _ptr(scales), _ptr(page_table),
-                             page_table.shape[1], _ptr(context_lens), max_context, softmax_scale, partition_tokens,
-                             _ptr(workspace), workspace.numel(), _stream(stream))
-    _check(st, "uq_decode_split")
-
-
-def decode_reduce(desc: CacheDesc, batch, num_q_heads, context_lens, max_context, partition_tokens, workspace, out,
-                  stream=None):
-    d = desc.c_struct()
-    st = lib.uq_decode_reduce(ctypes.byref(d), batch, num_q_heads, _ptr(context_lens), max_context, partition_tokens,
-                              _ptr(workspace), workspace.numel(), _ptr(out), _DT[out.dtype], _stream(stream))
-    _check(st, "uq_decode_reduce")
     return out
