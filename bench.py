@@ -4,8 +4,9 @@ One step is the whole hot path for one decode token per sequence:
   1. uq_quantize_kv writes the step's new K/V token of every sequence into
      the FP4 cache (Algorithm 1, "Write"), at the last position of its
      context;
-  2. uq_decode_attention runs decode attention over the full contexts
-     (Algorithm 1, "Decode"), one kernel launch.
+  2. uq_decode_partials + uq_decode_merge (the two launches of
+     uq_decode_attention) run decode attention over the full contexts
+     (Algorithm 1, "Decode").
 Inputs are resident in HBM before the timed region.  The default workload is
 the Qwen3-235B-like layer: 64 query heads, 4 KV heads, head_dim 128, batch
 32, every context 32768, random page table.  ``value`` is KV tokens/s =
@@ -52,6 +53,37 @@ def make_workload(name):
     from paper_2606_20474_amd import workloads
     return {"qwen3-235b-like": workloads.qwen3_235b_like, "high-concurrency": workloads.high_concurrency,
             "minimax-like": workloads.minimax_like, "tiny": workloads.tiny}[name]()
+
+
+def kernel_source_hash():
+    """sha256 of the decode kernel's sources; a profile taken on other sources is stale."""
+    import hashlib
+    h = hashlib.sha256()
+    for name in ("uq_decode.hip", "uq_device.hpp"):
+        with open(os.path.join(ROOT, "paper_2606_20474_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def profiled_traffic(workload_name):
+    """HBM bytes per decode_kernel launch from the committed counter profile of
+    this workload (FETCH_SIZE and WRITE_SIZE, calibrated against a copy of
+    known size), or None when there is none for the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", f"decode_kernel_{workload_name}.md")
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    with open(path) as f:
+        for line in f:
+            if line.startswith("traffic_bytes_per_launch:") or line.startswith("source_sha256:"):
+                k, v = line.split(":", 1)
+                fields[k.strip()] = v.strip()
+    if fields.get("source_sha256") != kernel_source_hash():
+        return None
+    try:
+        return float(fields["traffic_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
 
 
 def fill_cache(uq, wl, desc, codes, scales, dev):
@@ -135,9 +167,10 @@ def main():
         uq.quantize_kv(desc, k_new, v_new, new_slots, codes, scales)
         if ev_a is not None:
             ev_a.record(stream)
-        uq.decode_attention(desc, q, codes, scales, pt, ctx, wl.max_context, scale, part, ws, out)
+        uq.decode_partials(desc, q, codes, scales, pt, ctx, wl.max_context, scale, part, ws, out)
         if ev_b is not None:
             ev_b.record(stream)
+        uq.decode_merge(desc, wl.batch, wl.num_q_heads, ctx, wl.max_context, part, ws, out)
 
     if args.calib_copy_mib > 0:
         n = args.calib_copy_mib << 20
@@ -183,7 +216,7 @@ def main():
         "hbm_gbs_step": kv_bytes / (ms_step * 1e-3) / 1e9,
         "hbm_frac_step": kv_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "roofline": {"bound": "hbm", "kernel": "decode_kernel", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": profiled_traffic(wl.name),
                      "launch_ms": dec_ms, "bytes_per_launch": kv_bytes},
     }
     if not args.no_cpu_baseline:

@@ -183,6 +183,27 @@ uq_status uq_decode_attention(const uq_cache_desc *desc, const void *q, uq_dtype
                               void *workspace, size_t workspace_bytes, void *out, uq_dtype out_dtype,
                               void *stream);
 
+/*
+ * The two launches of uq_decode_attention, for callers that time or overlap
+ * them.  uq_decode_partials runs the partition kernel: it writes the final
+ * output of every sequence whose context fits one partition and a partial
+ * (running max, running sum, 128 accumulators per query head) of every
+ * other partition into the workspace.  uq_decode_merge merges those
+ * partials into `out` (a no-op when max_context <= partition).  Called back
+ * to back on one stream with the same arguments they are exactly
+ * uq_decode_attention; the arguments, validation and errors are the same.
+ */
+uq_status uq_decode_partials(const uq_cache_desc *desc, const void *q, uq_dtype q_dtype, int32_t batch,
+                             int32_t num_q_heads, const uint8_t *kv_codes, const uint8_t *kv_scales,
+                             const int32_t *page_table, int32_t max_pages_per_seq, const int32_t *context_lens,
+                             int32_t max_context, float softmax_scale, int32_t partition_tokens,
+                             void *workspace, size_t workspace_bytes, void *out, uq_dtype out_dtype,
+                             void *stream);
+uq_status uq_decode_merge(const uq_cache_desc *desc, int32_t batch, int32_t num_q_heads,
+                          const int32_t *context_lens, int32_t max_context, int32_t partition_tokens,
+                          const void *workspace, size_t workspace_bytes, void *out, uq_dtype out_dtype,
+                          void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -194,23 +194,65 @@ size_t uq_decode_workspace_bytes(const uq_cache_desc* desc, int32_t batch, int32
     return workspace_for(batch, num_q_heads, max_context, part);
 }
 
-uq_status uq_decode_attention(const uq_cache_desc* desc, const void* q, uq_dtype q_dtype, int32_t batch,
+// Shared set-up of the decode entry points: validation and the parameter block.
+static uq_status decode_setup(const uq_cache_desc* desc, const void* q, uq_dtype q_dtype, int32_t batch,
                               int32_t num_q_heads, const uint8_t* kv_codes, const uint8_t* kv_scales,
                               const int32_t* page_table, int32_t max_pages_per_seq, const int32_t* context_lens,
                               int32_t max_context, float softmax_scale, int32_t partition_tokens, void* workspace,
-                              size_t workspace_bytes, void* out, uq_dtype out_dtype, void* stream) {
+                              size_t workspace_bytes, void* out, uq_dtype out_dtype, uq::DecodeParams& p) {
     uq_status s = check_split_args(desc, q, q_dtype, batch, num_q_heads, kv_codes, kv_scales, page_table,
                                    max_pages_per_seq, context_lens, max_context, softmax_scale, partition_tokens);
     if (s != UQ_OK) return s;
     if (out == nullptr) return UQ_ERR_INVALID_ARGUMENT;
     if (out_dtype != UQ_F32 && out_dtype != UQ_BF16) return UQ_ERR_UNSUPPORTED;
     if (!aligned16(out)) return UQ_ERR_INVALID_ARGUMENT;
+    return make_decode_params(desc, q, q_dtype, batch, num_q_heads, kv_codes, kv_scales, page_table, max_pages_per_seq,
+                              context_lens, max_context, softmax_scale, partition_tokens, workspace, workspace_bytes,
+                              out, out_dtype, p);
+}
+
+uq_status uq_decode_attention(const uq_cache_desc* desc, const void* q, uq_dtype q_dtype, int32_t batch,
+                              int32_t num_q_heads, const uint8_t* kv_codes, const uint8_t* kv_scales,
+                              const int32_t* page_table, int32_t max_pages_per_seq, const int32_t* context_lens,
+                              int32_t max_context, float softmax_scale, int32_t partition_tokens, void* workspace,
+                              size_t workspace_bytes, void* out, uq_dtype out_dtype, void* stream) {
     uq::DecodeParams p;
-    s = make_decode_params(desc, q, q_dtype, batch, num_q_heads, kv_codes, kv_scales, page_table, max_pages_per_seq,
-                           context_lens, max_context, softmax_scale, partition_tokens, workspace, workspace_bytes, out,
+    uq_status s = decode_setup(desc, q, q_dtype, batch, num_q_heads, kv_codes, kv_scales, page_table,
+                               max_pages_per_seq, context_lens, max_context, softmax_scale, partition_tokens, workspace,
+                               workspace_bytes, out, out_dtype, p);
+    if (s != UQ_OK) return s;
+    s = from_hip(uq::launch_decode_partials(p, static_cast<hipStream_t>(stream)));
+    if (s != UQ_OK) return s;
+    return from_hip(uq::launch_decode_merge(p, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uq_decode_partials(const uq_cache_desc* desc, const void* q, uq_dtype q_dtype, int32_t batch,
+                             int32_t num_q_heads, const uint8_t* kv_codes, const uint8_t* kv_scales,
+                             const int32_t* page_table, int32_t max_pages_per_seq, const int32_t* context_lens,
+                             int32_t max_context, float softmax_scale, int32_t partition_tokens, void* workspace,
+                             size_t workspace_bytes, void* out, uq_dtype out_dtype, void* stream) {
+    uq::DecodeParams p;
+    uq_status s = decode_setup(desc, q, q_dtype, batch, num_q_heads, kv_codes, kv_scales, page_table,
+                               max_pages_per_seq, context_lens, max_context, softmax_scale, partition_tokens, workspace,
+                               workspace_bytes, out, out_dtype, p);
+    if (s != UQ_OK) return s;
+    return from_hip(uq::launch_decode_partials(p, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uq_decode_merge(const uq_cache_desc* desc, int32_t batch, int32_t num_q_heads, const int32_t* context_lens,
+                          int32_t max_context, int32_t partition_tokens, const void* workspace, size_t workspace_bytes,
+                          void* out, uq_dtype out_dtype, void* stream) {
+    uq_status s = check_decode_common(desc, batch, num_q_heads, max_context, partition_tokens);
+    if (s != UQ_OK) return s;
+    if (context_lens == nullptr || out == nullptr) return UQ_ERR_INVALID_ARGUMENT;
+    if (out_dtype != UQ_F32 && out_dtype != UQ_BF16) return UQ_ERR_UNSUPPORTED;
+    if (!aligned16(out)) return UQ_ERR_INVALID_ARGUMENT;
+    uq::DecodeParams p;
+    s = make_decode_params(desc, nullptr, UQ_F32, batch, num_q_heads, nullptr, nullptr, nullptr, 1, context_lens,
+                           max_context, 1.0f, partition_tokens, const_cast<void*>(workspace), workspace_bytes, out,
                            out_dtype, p);
     if (s != UQ_OK) return s;
-    return from_hip(uq::launch_decode(p, static_cast<hipStream_t>(stream)));
+    return from_hip(uq::launch_decode_merge(p, static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

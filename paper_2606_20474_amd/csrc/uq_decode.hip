@@ -533,13 +533,16 @@ __global__ void __launch_bounds__(256) merge_kernel(DecodeParams p) {
     write_out(p, int64_t(b) * p.num_q_heads + hq, L, o);
 }
 
-hipError_t launch_decode(const DecodeParams& p, hipStream_t stream) {
+hipError_t launch_decode_partials(const DecodeParams& p, hipStream_t stream) {
     const dim3 grid{unsigned(p.num_partitions), unsigned(p.num_kv_heads), unsigned(p.batch)};
     hipLaunchKernelGGL(decode_kernel, grid, dim3(kThreads), 0, stream, p);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess || p.num_partitions <= 1) return e;
-    const dim3 mgrid{unsigned(p.num_kv_heads), unsigned(p.batch)};
-    hipLaunchKernelGGL(merge_kernel, mgrid, dim3(256), 0, stream, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_decode_merge(const DecodeParams& p, hipStream_t stream) {
+    if (p.num_partitions <= 1) return hipSuccess;   // every sequence was finished in place
+    const dim3 grid{unsigned(p.num_kv_heads), unsigned(p.batch)};
+    hipLaunchKernelGGL(merge_kernel, grid, dim3(256), 0, stream, p);
     return hipGetLastError();
 }
 

@@ -50,6 +50,7 @@ struct DecodeParams {
 
 hipError_t launch_quantize_kv(const QuantizeParams& p, int dtype, hipStream_t stream);
 hipError_t launch_prepare_query(const void* q, int dtype, int64_t rows, uint8_t* q8, hipStream_t stream);
-hipError_t launch_decode(const DecodeParams& p, hipStream_t stream);
+hipError_t launch_decode_partials(const DecodeParams& p, hipStream_t stream);
+hipError_t launch_decode_merge(const DecodeParams& p, hipStream_t stream);
 
 }  // namespace uq

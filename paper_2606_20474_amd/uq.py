@@ -29,7 +29,7 @@ TILE_SCALES = 64
 # Every symbol include/uq.h declares.
 EXPORTS = (
     "uq_status_string", "uq_version", "uq_quantize_kv", "uq_prepare_query", "uq_decode_workspace_bytes",
-    "uq_default_partition", "uq_decode_attention",
+    "uq_default_partition", "uq_decode_attention", "uq_decode_partials", "uq_decode_merge",
 )
 
 
@@ -70,6 +70,10 @@ def _load():
     L.uq_default_partition.restype = i32
     L.uq_decode_attention.argtypes = [D, vp, i32, i32, i32, vp, vp, vp, i32, vp, i32, f32, i32, vp, sz, vp, i32, vp]
     L.uq_decode_attention.restype = i32
+    L.uq_decode_partials.argtypes = [D, vp, i32, i32, i32, vp, vp, vp, i32, vp, i32, f32, i32, vp, sz, vp, i32, vp]
+    L.uq_decode_partials.restype = i32
+    L.uq_decode_merge.argtypes = [D, i32, i32, vp, i32, i32, vp, sz, vp, i32, vp]
+    L.uq_decode_merge.restype = i32
     return L
 
 
@@ -186,4 +190,27 @@ def decode_attention(desc: CacheDesc, q, codes, scales, page_table, context_lens
                                  partition_tokens, _ptr(workspace), workspace.numel(), _ptr(out), _DT[out.dtype],
                                  _stream(stream))
     _check(st, "uq_decode_attention")
+    return out
+
+
+def decode_partials(desc: CacheDesc, q, codes, scales, page_table, context_lens, max_context, softmax_scale,
+                    partition_tokens, workspace, out, q_dtype=None, stream=None):
+    """First launch of decode_attention (partition kernel)."""
+    B, Hq = q.shape[0], q.shape[1]
+    d = desc.c_struct()
+    qdt = _DT[q.dtype] if q_dtype is None else q_dtype
+    st = lib.uq_decode_partials(ctypes.byref(d), _ptr(q), qdt, B, Hq, _ptr(codes), _ptr(scales), _ptr(page_table),
+                                page_table.shape[1], _ptr(context_lens), max_context, softmax_scale, partition_tokens,
+                                _ptr(workspace), workspace.numel(), _ptr(out), _DT[out.dtype], _stream(stream))
+    _check(st, "uq_decode_partials")
+    return out
+
+
+def decode_merge(desc: CacheDesc, batch, num_q_heads, context_lens, max_context, partition_tokens, workspace, out,
+                 stream=None):
+    """Second launch of decode_attention (merge of the partitions)."""
+    d = desc.c_struct()
+    st = lib.uq_decode_merge(ctypes.byref(d), batch, num_q_heads, _ptr(context_lens), max_context, partition_tokens,
+                             _ptr(workspace), workspace.numel(), _ptr(out), _DT[out.dtype], _stream(stream))
+    _check(st, "uq_decode_merge")
     return out

@@ -266,6 +266,13 @@ def test_decode_qwen_full_size_sampled(uq):
         out3 = uq.decode_attention(desc, q, codes, scales, pt, ctx, wl.max_context, 1 / math.sqrt(128), workspace=ws)
     torch.cuda.synchronize()
     assert np.array_equal(out3.cpu().numpy(), out1)
+    # the two launches called one by one give the same result
+    part = uq.default_partition(desc, wl.batch, wl.num_q_heads, wl.max_context)
+    out4 = torch.empty_like(q)
+    uq.decode_partials(desc, q, codes, scales, pt, ctx, wl.max_context, 1 / math.sqrt(128), part, ws, out4)
+    uq.decode_merge(desc, wl.batch, wl.num_q_heads, ctx, wl.max_context, part, ws, out4)
+    torch.cuda.synchronize()
+    assert np.array_equal(out4.cpu().numpy(), out1)
     seqs = [0, 19]
     pools, ptc = oracle_cache(wl, seqs, dev)
     ref = oracle.decode_attention(wl.q.numpy()[seqs], pools, ptc, wl.context_lens[seqs], wl.num_kv_heads,
