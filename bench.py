@@ -14,8 +14,11 @@ sum of contexts / step time.
 
 The JSON line also carries the roofline of the dominant kernel (the decode
 kernel: algorithmic KV bytes per launch / its mean launch time from HIP
-events on its stream) and the CPU oracle timed on a sample of the same
-workload.
+events on its stream), the CPU oracle timed on a sample of the same
+workload, and the same step over the two plain comparison caches the paper
+measures against (FP8 E4M3 with per-tensor scales, 256 B per token and kv
+head; BF16, 512 B), built by the same library with the same decode kernel
+and timed the same way.
 """
 import argparse
 import json
@@ -31,6 +34,8 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 KV_BYTES_PER_TOKEN_HEAD = 136   # K and V: 2 x (64 B codes + 4 B scales)
+REF_BYTES_PER_TOKEN_HEAD = {"fp8": 256, "bf16": 512}
+REF_SCALE = 0.3                 # per-tensor FP8 scale of the comparison cache (|x| up to 134 representable)
 
 
 def parse():
@@ -43,6 +48,8 @@ def parse():
     ap.add_argument("--partition", type=int, default=-1, help="partition tokens (-1: workload default)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-seqs", type=int, default=4)
+    ap.add_argument("--comparators", default="fp8,bf16",
+                    help="comma list of plain comparison caches to time as well (fp8, bf16) or 'none'")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one device-to-device copy of this many MiB before the timed steps; its "
                          "FETCH_SIZE/WRITE_SIZE counters calibrate the HBM-traffic counters")
@@ -95,6 +102,59 @@ def fill_cache(uq, wl, desc, codes, scales, dev):
         uq.quantize_kv(desc, k, v, slots, codes, scales)
         del k, v
     torch.cuda.synchronize()
+
+
+def timed(step, steps, warmup, stream):
+    """Run `warmup` untimed steps, then `steps` timed ones; returns (ms per
+    step over the whole timed region, mean ms of the decode launch between
+    the events each step records)."""
+    import torch
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for i in range(steps):
+        step(*evs[i])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    return t_start.elapsed_time(t_end) / steps, float(np.mean([a.elapsed_time(b) for a, b in evs]))
+
+
+def comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, new_slots, args, dev, stream):
+    """The same step (append one token per sequence, partition launch,
+    merge) over a plain FP8 or BF16 cache holding the same K/V."""
+    import torch
+    desc = uq.RefCacheDesc(num_kv_heads=wl.num_kv_heads, num_pages=wl.num_pages, fmt=fmt, k_scale=REF_SCALE,
+                           v_scale=REF_SCALE)
+    cache = desc.alloc_cache(dev)
+    for key, lo, hi in wl.segments():
+        k, v = wl.kv(key, lo, hi, device=dev)
+        uq.ref_write_kv(desc, k, v, torch.as_tensor(wl.slots(key, lo, hi), device=dev), cache)
+        del k, v
+    ws = uq.ref_alloc_workspace(desc, wl.batch, wl.num_q_heads, wl.max_context, part, dev)
+    out = torch.empty((wl.batch, wl.num_q_heads, 128), dtype=torch.float32, device=dev)
+    scale = 1 / math.sqrt(128)
+
+    def step(ev_a=None, ev_b=None):
+        uq.ref_write_kv(desc, k_new, v_new, new_slots, cache)
+        if ev_a is not None:
+            ev_a.record(stream)
+        uq.ref_decode_partials(desc, q, cache, pt, ctx, wl.max_context, scale, part, ws, out)
+        if ev_b is not None:
+            ev_b.record(stream)
+        uq.ref_decode_merge(desc, wl.batch, wl.num_q_heads, ctx, wl.max_context, part, ws, out)
+
+    ms_step, dec_ms = timed(step, args.steps, args.warmup, stream)
+    nbytes = wl.total_tokens() * wl.num_kv_heads * REF_BYTES_PER_TOKEN_HEAD[fmt]
+    del cache, ws, out
+    torch.cuda.empty_cache()
+    return {"tokens_per_s": wl.total_tokens() / (ms_step * 1e-3), "ms_per_step": ms_step,
+            "decode_kernel_ms": dec_ms, "bytes_per_token_head": REF_BYTES_PER_TOKEN_HEAD[fmt],
+            "kv_gbs": nbytes / (dec_ms * 1e-3) / 1e9, "kv_frac": nbytes / (dec_ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
 
 
 def cpu_baseline(wl, nseq, dev):
@@ -179,20 +239,7 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t_start.record(stream)
-    for i in range(args.steps):
-        step(*evs[i])
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    ms_step = t_start.elapsed_time(t_end) / args.steps
-    dec_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    ms_step, dec_ms = timed(step, args.steps, args.warmup, stream)
 
     tokens = wl.total_tokens()
     kv_bytes = wl.kv_bytes_fp4()
@@ -219,6 +266,15 @@ def main():
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": profiled_traffic(wl.name),
                      "launch_ms": dec_ms, "bytes_per_launch": kv_bytes},
     }
+    fmts = [f for f in args.comparators.split(",") if f and f != "none"]
+    if fmts:
+        comp = {}
+        for fmt in fmts:
+            if fmt not in REF_BYTES_PER_TOKEN_HEAD:
+                sys.exit(f"unknown comparator {fmt!r}")
+            comp[f"{fmt}_kv"] = comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, new_slots, args, dev, stream)
+            comp[f"fp4_over_{fmt}_tokens_per_s"] = result["value"] / comp[f"{fmt}_kv"]["tokens_per_s"]
+        result["comparators"] = comp
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample_seqs, dev)
     print(json.dumps(result), flush=True)

@@ -204,6 +204,84 @@ uq_status uq_decode_merge(const uq_cache_desc *desc, int32_t batch, int32_t num_
                           const void *workspace, size_t workspace_bytes, void *out, uq_dtype out_dtype,
                           void *stream);
 
+/* ------------------------------------------------------------------------
+ * Plain comparison caches.
+ *
+ * The paper measures the FP4 path against a hardware FP8 KV cache and a
+ * BF16 KV cache (section "Performance Results").  These calls build both
+ * with the same paging and the same decode kernel as the FP4 cache (the
+ * same staging ring, online softmax, PV and merge), so a comparison between
+ * them measures the cache format.  Neither format rotates anything.
+ *
+ * Pool layout (one buffer, caller-owned, uq_ref_cache_bytes bytes):
+ * [num_pages][num_kv_heads][K, V][tile], tile = 16 tokens x 128 channels in
+ * the lane order the decode kernel reads:
+ *   FP8  (2048 B): K at ((c%64)/16 * 16 + t) * 32 + c%16 + (c >= 64 ? 16 : 0);
+ *                  V at ((t/4) * 16 + c/8) * 32 + (t%4) * 8 + c%8.
+ *   BF16 (4096 B): K at ((c/8) * 16 + t) * 16 + 2 * (c%8);
+ *                  V at ((t/4) * 16 + c/8) * 64 + (t%4) * 16 + 2 * (c%8).
+ * (t = token within the page, c = channel; FP8 entries are one byte, BF16
+ * entries two, little endian.)
+ * ---------------------------------------------------------------------- */
+
+typedef enum uq_ref_format {
+    UQ_REF_FP8_E4M3 = 1, /* OCP E4M3 (no infinities), one scale per tensor */
+    UQ_REF_BF16 = 2
+} uq_ref_format;
+
+typedef struct uq_ref_cache_desc {
+    int32_t num_kv_heads;
+    int32_t head_dim;  /* must be 128 */
+    int32_t page_size; /* must be 16 */
+    int32_t format;    /* uq_ref_format */
+    int64_t num_pages;
+    float k_scale;     /* FP8: stored byte = e4m3(x / k_scale), value = byte * k_scale;  */
+    float v_scale;     /* finite and > 0.  Ignored for BF16. */
+} uq_ref_cache_desc;
+
+/* Bytes of the pool of a comparison cache; 0 for an invalid descriptor. */
+size_t uq_ref_cache_bytes(const uq_ref_cache_desc *desc);
+
+/*
+ * uq_ref_write_kv -- write K and V rows into a comparison cache: FP8 bytes
+ * are e4m3(x / scale) rounded to nearest even and saturated at +-448; BF16
+ * is round-to-nearest-even.  Arguments, slot addressing (physical slots, or
+ * logical slots through page_table), skipped slots and errors are those of
+ * uq_quantize_kv; `cache` must be 16-byte aligned.
+ */
+uq_status uq_ref_write_kv(const uq_ref_cache_desc *desc, const void *k, const void *v, uq_dtype in_dtype,
+                          int64_t num_tokens, int64_t token_stride, const int32_t *page_table, int32_t num_seqs,
+                          int32_t max_pages_per_seq, const int64_t *slot_mapping, uint8_t *cache, void *stream);
+
+/* Workspace of uq_ref_decode_attention; 0 for invalid arguments. */
+size_t uq_ref_decode_workspace_bytes(const uq_ref_cache_desc *desc, int32_t batch, int32_t num_q_heads,
+                                     int32_t max_context, int32_t partition_tokens);
+
+/*
+ * uq_ref_decode_attention -- decode attention over a comparison cache.  q is
+ * F32, BF16 or F16 (never pre-cast).  FP8 cache: the query is cast to E4M3
+ * (nearest even, saturating) and q.k runs on the FP8 x FP8 matrix
+ * instruction; the scores are multiplied by softmax_scale * k_scale and the
+ * output by v_scale.  BF16 cache: the query is cast to BF16 and q.k runs on
+ * BF16 matrix instructions.  Every other argument, the output and the
+ * errors are those of uq_decode_attention.  uq_ref_decode_partials and
+ * uq_ref_decode_merge are its two launches, as for the FP4 cache.
+ */
+uq_status uq_ref_decode_attention(const uq_ref_cache_desc *desc, const void *q, uq_dtype q_dtype, int32_t batch,
+                                  int32_t num_q_heads, const uint8_t *cache, const int32_t *page_table,
+                                  int32_t max_pages_per_seq, const int32_t *context_lens, int32_t max_context,
+                                  float softmax_scale, int32_t partition_tokens, void *workspace,
+                                  size_t workspace_bytes, void *out, uq_dtype out_dtype, void *stream);
+uq_status uq_ref_decode_partials(const uq_ref_cache_desc *desc, const void *q, uq_dtype q_dtype, int32_t batch,
+                                 int32_t num_q_heads, const uint8_t *cache, const int32_t *page_table,
+                                 int32_t max_pages_per_seq, const int32_t *context_lens, int32_t max_context,
+                                 float softmax_scale, int32_t partition_tokens, void *workspace,
+                                 size_t workspace_bytes, void *out, uq_dtype out_dtype, void *stream);
+uq_status uq_ref_decode_merge(const uq_ref_cache_desc *desc, int32_t batch, int32_t num_q_heads,
+                              const int32_t *context_lens, int32_t max_context, int32_t partition_tokens,
+                              const void *workspace, size_t workspace_bytes, void *out, uq_dtype out_dtype,
+                              void *stream);
+
 #ifdef __cplusplus
 }
 #endif

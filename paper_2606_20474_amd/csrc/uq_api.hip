@@ -100,6 +100,8 @@ uq_status make_decode_params(const uq_cache_desc* desc, const void* q, uq_dtype 
     p.out = out;
     p.out_dtype = out_dtype == UQ_F32 ? 0 : 1;
     p.rotate_v = desc->rotate_v != 0;
+    p.kv_fmt = uq::kFp4;
+    p.out_scale = 1.0f;
     return UQ_OK;
 }
 
@@ -119,6 +121,35 @@ uq_status check_split_args(const uq_cache_desc* desc, const void* q, uq_dtype q_
     if (!aligned16(q) || !aligned16(kv_codes) || !aligned16(kv_scales)) return UQ_ERR_INVALID_ARGUMENT;
     return UQ_OK;
 }
+
+// Comparison caches: the descriptor check and the FP4 descriptor with the
+// same geometry (the decode set-up above is shared; no rotation).
+uq_status check_ref_desc(const uq_ref_cache_desc* d) {
+    if (d == nullptr) return UQ_ERR_INVALID_ARGUMENT;
+    if (d->num_kv_heads < 1 || d->num_pages < 1) return UQ_ERR_INVALID_ARGUMENT;
+    if (d->format != UQ_REF_FP8_E4M3 && d->format != UQ_REF_BF16) return UQ_ERR_UNSUPPORTED;
+    if (d->head_dim != kHeadDim || d->page_size != kPageSize) return UQ_ERR_UNSUPPORTED;
+    if (d->format == UQ_REF_FP8_E4M3 &&
+        !(isfinite(d->k_scale) && d->k_scale > 0.0f && isfinite(d->v_scale) && d->v_scale > 0.0f))
+        return UQ_ERR_INVALID_ARGUMENT;
+    return UQ_OK;
+}
+
+uq_cache_desc geometry_of(const uq_ref_cache_desc* d) {
+    uq_cache_desc g;
+    g.num_kv_heads = d->num_kv_heads;
+    g.head_dim = kHeadDim;
+    g.page_size = kPageSize;
+    g.group_size = kGroupSize;
+    g.num_pages = d->num_pages;
+    g.c = 0.156f;
+    g.rotate_v = 0;
+    return g;
+}
+
+int32_t ref_fmt(const uq_ref_cache_desc* d) { return d->format == UQ_REF_FP8_E4M3 ? uq::kFp8 : uq::kBf16; }
+
+int64_t ref_tile_bytes(const uq_ref_cache_desc* d) { return d->format == UQ_REF_FP8_E4M3 ? 2048 : 4096; }
 
 }  // namespace
 
@@ -252,6 +283,125 @@ uq_status uq_decode_merge(const uq_cache_desc* desc, int32_t batch, int32_t num_
                            max_context, 1.0f, partition_tokens, const_cast<void*>(workspace), workspace_bytes, out,
                            out_dtype, p);
     if (s != UQ_OK) return s;
+    return from_hip(uq::launch_decode_merge(p, static_cast<hipStream_t>(stream)));
+}
+
+size_t uq_ref_cache_bytes(const uq_ref_cache_desc* desc) {
+    if (check_ref_desc(desc) != UQ_OK) return 0;
+    return size_t(desc->num_pages) * size_t(desc->num_kv_heads) * 2 * size_t(ref_tile_bytes(desc));
+}
+
+uq_status uq_ref_write_kv(const uq_ref_cache_desc* desc, const void* k, const void* v, uq_dtype in_dtype,
+                          int64_t num_tokens, int64_t token_stride, const int32_t* page_table, int32_t num_seqs,
+                          int32_t max_pages_per_seq, const int64_t* slot_mapping, uint8_t* cache, void* stream) {
+    uq_status s = check_ref_desc(desc);
+    if (s != UQ_OK) return s;
+    if (in_dtype != UQ_F32 && in_dtype != UQ_BF16 && in_dtype != UQ_F16) return UQ_ERR_UNSUPPORTED;
+    if (num_tokens < 0) return UQ_ERR_INVALID_ARGUMENT;
+    if (k == nullptr || v == nullptr || slot_mapping == nullptr || cache == nullptr) return UQ_ERR_INVALID_ARGUMENT;
+    if (token_stride < int64_t(desc->num_kv_heads) * kHeadDim) return UQ_ERR_INVALID_ARGUMENT;
+    const int64_t vec_elems = in_dtype == UQ_F32 ? 4 : 8;
+    if (token_stride % vec_elems != 0 || !aligned16(k) || !aligned16(v) || !aligned16(cache))
+        return UQ_ERR_INVALID_ARGUMENT;
+    if (page_table != nullptr && (max_pages_per_seq < 1 || num_seqs < 1)) return UQ_ERR_INVALID_ARGUMENT;
+    if (num_tokens == 0) return UQ_OK;
+    uq::RefWriteParams p;
+    p.k = k;
+    p.v = v;
+    p.num_tokens = num_tokens;
+    p.token_stride = token_stride;
+    p.slot_mapping = slot_mapping;
+    p.page_table = page_table;
+    p.max_pages_per_seq = max_pages_per_seq;
+    p.num_seqs = page_table != nullptr ? num_seqs : 0;
+    p.num_kv_heads = desc->num_kv_heads;
+    p.num_pages = desc->num_pages;
+    p.k_scale = desc->format == UQ_REF_FP8_E4M3 ? desc->k_scale : 1.0f;
+    p.v_scale = desc->format == UQ_REF_FP8_E4M3 ? desc->v_scale : 1.0f;
+    p.kv_fmt = ref_fmt(desc);
+    p.cache = cache;
+    return from_hip(uq::launch_write_kv_ref(p, int(in_dtype), static_cast<hipStream_t>(stream)));
+}
+
+size_t uq_ref_decode_workspace_bytes(const uq_ref_cache_desc* desc, int32_t batch, int32_t num_q_heads,
+                                     int32_t max_context, int32_t partition_tokens) {
+    if (check_ref_desc(desc) != UQ_OK) return 0;
+    const uq_cache_desc g = geometry_of(desc);
+    return uq_decode_workspace_bytes(&g, batch, num_q_heads, max_context, partition_tokens);
+}
+
+// Shared set-up of the comparison-cache decode calls: the FP4 set-up on the
+// same geometry, then the format, the K scale folded into the exponent
+// scale and the V scale applied to the output.
+static uq_status ref_decode_setup(const uq_ref_cache_desc* desc, const void* q, uq_dtype q_dtype, int32_t batch,
+                                  int32_t num_q_heads, const uint8_t* cache, const int32_t* page_table,
+                                  int32_t max_pages_per_seq, const int32_t* context_lens, int32_t max_context,
+                                  float softmax_scale, int32_t partition_tokens, void* workspace,
+                                  size_t workspace_bytes, void* out, uq_dtype out_dtype, uq::DecodeParams& p) {
+    uq_status s = check_ref_desc(desc);
+    if (s != UQ_OK) return s;
+    if (q_dtype != UQ_F32 && q_dtype != UQ_BF16 && q_dtype != UQ_F16) return UQ_ERR_UNSUPPORTED;
+    const uq_cache_desc g = geometry_of(desc);
+    s = decode_setup(&g, q, q_dtype, batch, num_q_heads, cache, cache, page_table, max_pages_per_seq, context_lens,
+                     max_context, softmax_scale, partition_tokens, workspace, workspace_bytes, out, out_dtype, p);
+    if (s != UQ_OK) return s;
+    p.kv_fmt = ref_fmt(desc);
+    p.scales = nullptr;
+    if (desc->format == UQ_REF_FP8_E4M3) {
+        p.scale_log2 = float(double(softmax_scale) * double(desc->k_scale) * 1.4426950408889634);
+        p.out_scale = desc->v_scale;
+        if (!(isfinite(p.scale_log2) && p.scale_log2 > 0.0f)) return UQ_ERR_INVALID_ARGUMENT;
+    }
+    return UQ_OK;
+}
+
+uq_status uq_ref_decode_attention(const uq_ref_cache_desc* desc, const void* q, uq_dtype q_dtype, int32_t batch,
+                                  int32_t num_q_heads, const uint8_t* cache, const int32_t* page_table,
+                                  int32_t max_pages_per_seq, const int32_t* context_lens, int32_t max_context,
+                                  float softmax_scale, int32_t partition_tokens, void* workspace,
+                                  size_t workspace_bytes, void* out, uq_dtype out_dtype, void* stream) {
+    uq::DecodeParams p;
+    uq_status s = ref_decode_setup(desc, q, q_dtype, batch, num_q_heads, cache, page_table, max_pages_per_seq,
+                                   context_lens, max_context, softmax_scale, partition_tokens, workspace,
+                                   workspace_bytes, out, out_dtype, p);
+    if (s != UQ_OK) return s;
+    s = from_hip(uq::launch_decode_partials(p, static_cast<hipStream_t>(stream)));
+    if (s != UQ_OK) return s;
+    return from_hip(uq::launch_decode_merge(p, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uq_ref_decode_partials(const uq_ref_cache_desc* desc, const void* q, uq_dtype q_dtype, int32_t batch,
+                                 int32_t num_q_heads, const uint8_t* cache, const int32_t* page_table,
+                                 int32_t max_pages_per_seq, const int32_t* context_lens, int32_t max_context,
+                                 float softmax_scale, int32_t partition_tokens, void* workspace,
+                                 size_t workspace_bytes, void* out, uq_dtype out_dtype, void* stream) {
+    uq::DecodeParams p;
+    uq_status s = ref_decode_setup(desc, q, q_dtype, batch, num_q_heads, cache, page_table, max_pages_per_seq,
+                                   context_lens, max_context, softmax_scale, partition_tokens, workspace,
+                                   workspace_bytes, out, out_dtype, p);
+    if (s != UQ_OK) return s;
+    return from_hip(uq::launch_decode_partials(p, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uq_ref_decode_merge(const uq_ref_cache_desc* desc, int32_t batch, int32_t num_q_heads,
+                              const int32_t* context_lens, int32_t max_context, int32_t partition_tokens,
+                              const void* workspace, size_t workspace_bytes, void* out, uq_dtype out_dtype,
+                              void* stream) {
+    uq_status s = check_ref_desc(desc);
+    if (s != UQ_OK) return s;
+    const uq_cache_desc g = geometry_of(desc);
+    s = check_decode_common(&g, batch, num_q_heads, max_context, partition_tokens);
+    if (s != UQ_OK) return s;
+    if (context_lens == nullptr || out == nullptr) return UQ_ERR_INVALID_ARGUMENT;
+    if (out_dtype != UQ_F32 && out_dtype != UQ_BF16) return UQ_ERR_UNSUPPORTED;
+    if (!aligned16(out)) return UQ_ERR_INVALID_ARGUMENT;
+    uq::DecodeParams p;
+    s = make_decode_params(&g, nullptr, UQ_F32, batch, num_q_heads, nullptr, nullptr, nullptr, 1, context_lens,
+                           max_context, 1.0f, partition_tokens, const_cast<void*>(workspace), workspace_bytes, out,
+                           out_dtype, p);
+    if (s != UQ_OK) return s;
+    p.kv_fmt = ref_fmt(desc);
+    if (desc->format == UQ_REF_FP8_E4M3) p.out_scale = desc->v_scale;
     return from_hip(uq::launch_decode_merge(p, static_cast<hipStream_t>(stream)));
 }
 

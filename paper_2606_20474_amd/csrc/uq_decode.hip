@@ -1,51 +1,89 @@
-// uq_decode.hip -- split-context decode attention over the FP4 cache
+// uq_decode.hip -- split-context decode attention over a paged KV cache
 // (paper, Algorithm 1, "Decode"; section "Kernel Implementation in vLLM").
 //
-// decode_kernel: one 256-thread block (4 waves) per (partition, kv head,
-// sequence).
-//   prologue  the block rotates its G query heads with the in-register WHT
-//             butterfly and casts them to FP8 E4M3 once, into LDS in the
-//             lane order of the MFMA B operand; every wave keeps it in 8
-//             VGPRs for the whole partition (the query is hoisted out of the
-//             K-tile loop).
+// One kernel template serves three cache formats so that the comparison
+// between them measures the format, not the kernel:
+//   kFp4   the UltraQuant cache: FP4 E2M1 codes + UE8M0 scales per 32
+//          channels, K (and V with rotate_v) Walsh-Hadamard rotated;
+//   kFp8   a plain FP8 E4M3 cache with one scale per tensor;
+//   kBf16  a plain BF16 cache.
+//
+// decode_kernel<F>: one block of Fmt<F>::kWaves waves per (partition, kv
+// head, sequence).
+//   prologue  the block loads its G query heads (G <= 16), rotates them
+//             with the in-register WHT butterfly and casts them to FP8
+//             E4M3 (FP4 cache), casts them to FP8 (FP8 cache) or to BF16
+//             (BF16 cache), and stores them in LDS in the lane order of the
+//             MFMA B operand; every wave keeps the operand in registers for
+//             the whole partition (the query is hoisted out of the K-tile
+//             loop).
 //   loop      each wave takes pairs of pages (32 tokens) round-robin and
 //             stages them through its own 2-slot LDS ring with
 //             global_load_lds_dwordx4 (16 bytes per lane, 1 KiB per
-//             instruction): as soon as a slot has been read into registers
-//             it is refilled with the pair two iterations ahead, so two
-//             pairs (8.7 KB) per wave are in flight while one is computed.
-//             QK^T: one v_mfma_scale_f32_16x16x128_f8f6f4 per page, the FP4
-//             K tile as operand A (rows = tokens) with its UE8M0 bytes as
-//             the A scales, the FP8 query as operand B (columns = query
-//             heads) with scale byte 127 (1.0).  Dequantisation is folded
-//             into the instruction.
+//             instruction); a slot is refilled with the pair two iterations
+//             ahead as soon as it has been read into registers, so two pairs
+//             per wave are in flight while one is computed.
+//             QK^T: FP4 -- one v_mfma_scale_f32_16x16x128_f8f6f4 per page,
+//             the FP4 K tile as operand A (rows = tokens) with its UE8M0
+//             bytes as the A scales and the FP8 query as operand B (columns
+//             = query heads): dequantisation is folded into the
+//             instruction.  FP8 -- the same instruction with FP8 on both
+//             sides.  BF16 -- four v_mfma_f32_16x16x32_bf16 per page.
 //             Online softmax in the log2 domain with a lazy rescale (the
 //             running max only moves when it grows by more than 8).
-//             V: v_cvt_scalef32_pk_bf16_fp4 turns code pairs into exact
-//             BF16 values with the token's scale; byte permutes build the
-//             A operand of v_mfma_f32_16x16x32_bf16 (rows = channels, k =
-//             tokens), and P enters as operand B split into a BF16 high
-//             part and a BF16 residual, so the PV product carries ~16
-//             significant bits of P.
-//   epilogue  the 4 waves merge (max, sum, accumulators) through LDS.  A
+//             V: the hardware conversions v_cvt_scalef32_pk_bf16_fp4 (with
+//             the token's UE8M0 scale) or v_cvt_scalef32_pk_bf16_fp8 turn
+//             code pairs into exact BF16 values; byte permutes pair two
+//             tokens per register for the A operand of
+//             v_mfma_f32_16x16x32_bf16 (rows = channels, k = tokens).  P
+//             enters as operand B split into a BF16 high part and a BF16
+//             residual, so PV carries ~16 significant bits of P.
+//   epilogue  the waves merge (max, sum, accumulators) through LDS.  A
 //             sequence that fits one partition is finished in place;
 //             otherwise the block writes one partial per query head.
 // merge_kernel: merges the partitions of every (sequence, query head),
-// divides by the softmax sum and, when V was stored rotated, maps the output
-// back with the same butterfly (R is its own inverse).  A separate launch:
-// merging in the last-arriving block needs cross-XCD visibility of the
-// other blocks' partials, and both ways to get it (an L2 writeback and
-// invalidate per block, or write-through stores) measured slower than the
-// second launch.
+// divides by the softmax sum, applies the per-tensor V scale and, when V was
+// stored rotated, maps the output back with the same butterfly (R is its
+// own inverse).  A separate launch: merging in the last-arriving block needs
+// cross-XCD visibility of the other blocks' partials, and both ways to get
+// it (an L2 writeback and invalidate per block, or write-through stores)
+// measured slower than the second launch.
 #include "uq_device.hpp"
 #include "uq_internal.hpp"
 
 namespace uq {
 
-constexpr int kWaves = 4;
-constexpr int kThreads = 64 * kWaves;
 constexpr float kLazyRescale = 8.0f;   // log2 units
 constexpr int kAccStride = 129;        // LDS row stride (floats) of the merge buffer
+
+// Per-format constants.  kTile: bytes of one (page, kv head) K or V tile;
+// kScaleBlock: scale bytes per (page, kv head) for K and V together.
+template <int F> struct Fmt;
+// kWaves: waves per block; kOccupancy: waves per SIMD the LDS footprint
+// allows (160 KiB per CU), which sets the register budget.
+template <> struct Fmt<kFp4> {
+    static constexpr int kTile = 1024;
+    static constexpr int kScaleBlock = 2 * kTileScales;
+    static constexpr int kWaves = 4;
+    static constexpr int kOccupancy = 4;
+};
+template <> struct Fmt<kFp8> {
+    static constexpr int kTile = 2048;
+    static constexpr int kScaleBlock = 0;
+    static constexpr int kWaves = 4;
+    static constexpr int kOccupancy = 2;
+};
+template <> struct Fmt<kBf16> {
+    static constexpr int kTile = 4096;
+    static constexpr int kScaleBlock = 0;
+    static constexpr int kWaves = 2;
+    static constexpr int kOccupancy = 1;
+};
+
+// One stage of the ring: [K page0][V page0][K page1][V page1][scales0][scales1].
+template <int F> constexpr int stage_bytes() { return 4 * Fmt<F>::kTile + 2 * Fmt<F>::kScaleBlock; }
+template <int F> constexpr int ring_bytes() { return 2 * stage_bytes<F>(); }
+template <int F> constexpr int dma_per_stage() { return 4 * Fmt<F>::kTile / 1024 + (Fmt<F>::kScaleBlock ? 1 : 0); }
 
 // Exchange with the lane 16 (or 32) positions away: after
 // v_permlane16_swap a b (a = b = x on entry) the pair (a, b) holds x of this
@@ -114,73 +152,48 @@ __device__ __forceinline__ void load_q8(const void* q, int64_t elem, float (&x)[
 
 // Page ids of one wave, 64 at a time: lane j holds the id of the wave's
 // page 2*(32*chunk + j/2) + j%2 counted in its own iteration order
-// (iteration k of wave w covers partition pages 2*(w + 4k) and +1).
+// (iteration k of wave w covers partition pages 2*(w + W*k) and +1).
+template <int W>
 __device__ __forceinline__ int32_t load_page_ids(const int32_t* __restrict__ pt_row, int first_page, int n_pages,
                                                  int wave, int chunk, int lane, int64_t num_pages) {
     const int k = 32 * chunk + (lane >> 1);
-    const int pg = 2 * (wave + kWaves * k) + (lane & 1);
+    const int pg = 2 * (wave + W * k) + (lane & 1);
     int32_t id = 0;
     if (pg < n_pages) id = pt_row[first_page + pg];
     if (id < 0 || int64_t(id) >= num_pages) id = 0;   // out-of-range ids never leave the pools
     return id;
 }
 
-// PV for the channel pair selected by byte BS of every V dword: channels
-// 8n+2BS (block 2BS, low halves) and 8n+2BS+1 (block 2BS+1, high halves).
-// The converted BF16 values of tokens (t, t+1) are paired by byte permutes
-// into the k-slot order of the P operand.
-template <int BS>
-__device__ __forceinline__ void pv_pair(const uint32_t (&v0d)[4], const uint32_t (&v1d)[4], const float (&sc0)[4],
-                                        const float (&sc1)[4], const v8bf& Phi, const v8bf& Plo, v4f& acc_e,
-                                        v4f& acc_o) {
-    uint32_t cv0[4], cv1[4];
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-        cv0[t] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(v0d[t], sc0[t], BS));
-        cv1[t] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(v1d[t], sc1[t], BS));
-    }
-    const uint4 ae = {__builtin_amdgcn_perm(cv0[1], cv0[0], 0x05040100u), __builtin_amdgcn_perm(cv0[3], cv0[2], 0x05040100u),
-                      __builtin_amdgcn_perm(cv1[1], cv1[0], 0x05040100u), __builtin_amdgcn_perm(cv1[3], cv1[2], 0x05040100u)};
-    const uint4 ao = {__builtin_amdgcn_perm(cv0[1], cv0[0], 0x07060302u), __builtin_amdgcn_perm(cv0[3], cv0[2], 0x07060302u),
-                      __builtin_amdgcn_perm(cv1[1], cv1[0], 0x07060302u), __builtin_amdgcn_perm(cv1[3], cv1[2], 0x07060302u)};
-    const v8bf Ve = __builtin_bit_cast(v8bf, ae);
-    const v8bf Vo = __builtin_bit_cast(v8bf, ao);
-    acc_e = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ve, Phi, acc_e, 0, 0, 0);
-    acc_e = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ve, Plo, acc_e, 0, 0, 0);
-    acc_o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Vo, Phi, acc_o, 0, 0, 0);
-    acc_o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Vo, Plo, acc_o, 0, 0, 0);
-}
-
-// Per-wave staging ring in LDS: 2 stages of one iteration (2 pages) each:
-//   [K page0 1024][V page0 1024][K page1 1024][V page1 1024][scales page0 128][scales page1 128]
-constexpr int kStageBytes = 4 * kTileCodes + 4 * kTileScales;   // 4352
-constexpr int kRingBytes = 2 * kStageBytes;                      // per wave
-constexpr int kMergeBytes = kWaves * 16 * kAccStride * 4;
-static_assert(kMergeBytes <= kWaves * kRingBytes, "merge buffer aliases the staging rings");
-
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
 // Asynchronous copy of one iteration (two pages of one kv head) from HBM
 // into an LDS stage with global_load_lds_dwordx4: every lane moves 16 bytes
-// and the hardware places lane i's bytes at stage + 16 i, so each 1 KiB tile
-// lands in lane order.  Five instructions per stage; the scale blocks of both
-// pages (2 x 128 bytes) are moved by lanes 0..15.
+// and the hardware places lane i's bytes at dst + 16 i, so each 1 KiB chunk
+// of a tile lands in lane order.  The FP4 scale blocks of both pages
+// (2 x 128 bytes) are moved by lanes 0..15.
+template <int F>
 __device__ __forceinline__ void stage_issue(uint8_t* stage, const uint8_t* __restrict__ codes,
                                             const uint8_t* __restrict__ scales, int64_t tile0, int64_t tile1,
                                             int lane) {
-    const uint8_t* k0 = codes + tile0 * kTileCodes + 16 * lane;
-    const uint8_t* k1 = codes + tile1 * kTileCodes + 16 * lane;
-    __builtin_amdgcn_global_load_lds(k0, (lds_ptr_t)(stage), 16, 0, 0);
-    __builtin_amdgcn_global_load_lds(k0 + kTileCodes, (lds_ptr_t)(stage + kTileCodes), 16, 0, 0);
-    __builtin_amdgcn_global_load_lds(k1, (lds_ptr_t)(stage + 2 * kTileCodes), 16, 0, 0);
-    __builtin_amdgcn_global_load_lds(k1 + kTileCodes, (lds_ptr_t)(stage + 3 * kTileCodes), 16, 0, 0);
-    if (lane < 16) {
-        const int64_t t = lane < 8 ? tile0 : tile1;
-        const uint8_t* sc = scales + t * kTileScales + 16 * (lane & 7);
-        __builtin_amdgcn_global_load_lds(sc, (lds_ptr_t)(stage + 4 * kTileCodes), 16, 0, 0);
+    constexpr int T = Fmt<F>::kTile;
+    const uint8_t* k0 = codes + tile0 * T + 16 * lane;
+    const uint8_t* k1 = codes + tile1 * T + 16 * lane;
+#pragma unroll
+    for (int c = 0; c < 2 * T; c += 1024) {
+        __builtin_amdgcn_global_load_lds(k0 + c, (lds_ptr_t)(stage + c), 16, 0, 0);
+    }
+#pragma unroll
+    for (int c = 0; c < 2 * T; c += 1024) {
+        __builtin_amdgcn_global_load_lds(k1 + c, (lds_ptr_t)(stage + 2 * T + c), 16, 0, 0);
+    }
+    if constexpr (Fmt<F>::kScaleBlock != 0) {
+        if (lane < 16) {
+            const int64_t t = lane < 8 ? tile0 : tile1;
+            const uint8_t* sc = scales + t * kTileScales + 16 * (lane & 7);
+            __builtin_amdgcn_global_load_lds(sc, (lds_ptr_t)(stage + 4 * T), 16, 0, 0);
+        }
     }
 }
-constexpr int kDmaPerStage = 5;
 
 // Wait until at most N of this wave's vector-memory loads are outstanding
 // (loads complete in issue order, so the older stage is then in LDS).
@@ -189,22 +202,28 @@ __device__ __forceinline__ void wait_vmem() {
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(N) : "memory");
 }
 
-struct StageRegs {
-    uint4 k0, v0, k1, v1;   // this lane's 16 bytes of each tile
-    uint32_t ks0, ks1;      // K scale byte (token lane%16, group lane/16)
-    uint32_t vs0, vs1;      // V scale bytes of tokens 4*(lane/16)+0..3, group (lane%16)/4
+// This lane's operands of one stage.  The reads are inline assembly so that
+// the compiler does not guard them with a wait for every outstanding LDS
+// copy (the caller has waited for this stage's copies already); each read
+// block ends with lgkmcnt(0), so the results are safe to use.
+template <int F> struct StageRegs;
+
+template <> struct StageRegs<kFp4> {
+    uint4 k[2], v[2];   // 16 bytes of each tile
+    uint32_t ks[2];     // K scale byte of (token lane%16, group lane/16)
+    uint32_t vs[2];     // V scale bytes of tokens 4*(lane/16)+0..3, group (lane%16)/4
+};
+template <> struct StageRegs<kFp8> {
+    uint4 k[2][2], v[2][2];   // 32 bytes of each tile
+};
+template <> struct StageRegs<kBf16> {
+    uint4 k[2][4], v[2][4];   // K: 4 k-steps x 16 bytes; V: 64 bytes
 };
 
-// Read this lane's operands of one stage.  The reads are inline assembly so
-// that the compiler does not guard them with a wait for every outstanding
-// LDS copy; the caller has already waited for this stage's copies, and the
-// trailing lgkmcnt(0) makes the results safe to use.
-__device__ __forceinline__ StageRegs stage_read(uint32_t stage_addr, uint32_t off_codes, uint32_t off_ks,
-                                                uint32_t off_vs) {
-    StageRegs r;
-    const uint32_t ac = stage_addr + off_codes;
-    const uint32_t ak = stage_addr + off_ks;
-    const uint32_t av = stage_addr + off_vs;
+__device__ __forceinline__ void stage_read(StageRegs<kFp4>& r, uint32_t stage_addr, int lane) {
+    const uint32_t ac = stage_addr + 16 * lane;
+    const uint32_t ak = stage_addr + lane;
+    const uint32_t av = stage_addr + kTileScales + ((lane & 15) >> 2) * 16 + 4 * (lane >> 4);
     asm volatile(
         "ds_read_b128 %0, %8\n\t"
         "ds_read_b128 %1, %8 offset:1024\n\t"
@@ -215,10 +234,127 @@ __device__ __forceinline__ StageRegs stage_read(uint32_t stage_addr, uint32_t of
         "ds_read_b32 %6, %10 offset:4096\n\t"
         "ds_read_b32 %7, %10 offset:4224\n\t"
         "s_waitcnt lgkmcnt(0)"
-        : "=&v"(r.k0), "=&v"(r.v0), "=&v"(r.k1), "=&v"(r.v1), "=&v"(r.ks0), "=&v"(r.ks1), "=&v"(r.vs0), "=&v"(r.vs1)
+        : "=&v"(r.k[0]), "=&v"(r.v[0]), "=&v"(r.k[1]), "=&v"(r.v[1]), "=&v"(r.ks[0]), "=&v"(r.ks[1]), "=&v"(r.vs[0]),
+          "=&v"(r.vs[1])
         : "v"(ac), "v"(ak), "v"(av)
         : "memory");
-    return r;
+}
+
+__device__ __forceinline__ void stage_read(StageRegs<kFp8>& r, uint32_t stage_addr, int lane) {
+    const uint32_t a = stage_addr + 32 * lane;
+    asm volatile(
+        "ds_read_b128 %0, %8\n\t"
+        "ds_read_b128 %1, %8 offset:16\n\t"
+        "ds_read_b128 %2, %8 offset:2048\n\t"
+        "ds_read_b128 %3, %8 offset:2064\n\t"
+        "ds_read_b128 %4, %8 offset:4096\n\t"
+        "ds_read_b128 %5, %8 offset:4112\n\t"
+        "ds_read_b128 %6, %8 offset:6144\n\t"
+        "ds_read_b128 %7, %8 offset:6160\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(r.k[0][0]), "=&v"(r.k[0][1]), "=&v"(r.v[0][0]), "=&v"(r.v[0][1]), "=&v"(r.k[1][0]),
+          "=&v"(r.k[1][1]), "=&v"(r.v[1][0]), "=&v"(r.v[1][1])
+        : "v"(a)
+        : "memory");
+}
+
+__device__ __forceinline__ void stage_read(StageRegs<kBf16>& r, uint32_t stage_addr, int lane) {
+    // K: k-step s at s*1024 + 16*lane; V: 64 bytes at 4096 + 64*lane (page 1: +8192)
+    const uint32_t ak = stage_addr + 16 * lane;
+    const uint32_t av = stage_addr + 64 * lane;
+    asm volatile(
+        "ds_read_b128 %0, %16\n\t"
+        "ds_read_b128 %1, %16 offset:1024\n\t"
+        "ds_read_b128 %2, %16 offset:2048\n\t"
+        "ds_read_b128 %3, %16 offset:3072\n\t"
+        "ds_read_b128 %4, %17 offset:4096\n\t"
+        "ds_read_b128 %5, %17 offset:4112\n\t"
+        "ds_read_b128 %6, %17 offset:4128\n\t"
+        "ds_read_b128 %7, %17 offset:4144\n\t"
+        "ds_read_b128 %8, %16 offset:8192\n\t"
+        "ds_read_b128 %9, %16 offset:9216\n\t"
+        "ds_read_b128 %10, %16 offset:10240\n\t"
+        "ds_read_b128 %11, %16 offset:11264\n\t"
+        "ds_read_b128 %12, %17 offset:12288\n\t"
+        "ds_read_b128 %13, %17 offset:12304\n\t"
+        "ds_read_b128 %14, %17 offset:12320\n\t"
+        "ds_read_b128 %15, %17 offset:12336\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(r.k[0][0]), "=&v"(r.k[0][1]), "=&v"(r.k[0][2]), "=&v"(r.k[0][3]), "=&v"(r.v[0][0]),
+          "=&v"(r.v[0][1]), "=&v"(r.v[0][2]), "=&v"(r.v[0][3]), "=&v"(r.k[1][0]), "=&v"(r.k[1][1]),
+          "=&v"(r.k[1][2]), "=&v"(r.k[1][3]), "=&v"(r.v[1][0]), "=&v"(r.v[1][1]), "=&v"(r.v[1][2]),
+          "=&v"(r.v[1][3])
+        : "v"(ak), "v"(av)
+        : "memory");
+}
+
+// Query operand in registers.
+template <int F> struct QOperand { v8i q; };               // FP8 bytes, 32 per lane
+template <> struct QOperand<kBf16> { v8bf q[4]; };          // 4 k-steps x 8 BF16 per lane
+
+// S^T[token][query head] of one page: rows = the page's 16 tokens (lane's
+// VGPR i holds token 4*(lane/16)+i), columns = query heads (lane%16).
+__device__ __forceinline__ v4f qk_page(const StageRegs<kFp4>& r, int pg, const QOperand<kFp4>& q) {
+    const v8i a = {int(r.k[pg].x), int(r.k[pg].y), int(r.k[pg].z), int(r.k[pg].w), 0, 0, 0, 0};
+    const v4f zero = {0.f, 0.f, 0.f, 0.f};
+    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, q.q, zero, 4, 0, 0, int(r.ks[pg]), 0, 127);
+}
+__device__ __forceinline__ v4f qk_page(const StageRegs<kFp8>& r, int pg, const QOperand<kFp8>& q) {
+    const uint4 lo = r.k[pg][0], hi = r.k[pg][1];
+    const v8i a = {int(lo.x), int(lo.y), int(lo.z), int(lo.w), int(hi.x), int(hi.y), int(hi.z), int(hi.w)};
+    const v4f zero = {0.f, 0.f, 0.f, 0.f};
+    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, q.q, zero, 0, 0, 0, 127, 0, 127);
+}
+__device__ __forceinline__ v4f qk_page(const StageRegs<kBf16>& r, int pg, const QOperand<kBf16>& q) {
+    v4f s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+        s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, r.k[pg][st]), q.q[st], s, 0, 0, 0);
+    return s;
+}
+
+__device__ __forceinline__ uint32_t dword(const uint4& v, int i) { return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w; }
+
+// BF16 pair of this lane's V channels 8n+2C, 8n+2C+1 of token 4*(lane/16)+t
+// of page pg, as one dword (even channel in the low half).
+template <int C>
+__device__ __forceinline__ uint32_t v_pair(const StageRegs<kFp4>& r, int pg, int t, const float (&sc)[2][4]) {
+    return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(dword(r.v[pg], t), sc[pg][t], C));
+}
+template <int C>
+__device__ __forceinline__ uint32_t v_pair(const StageRegs<kFp8>& r, int pg, int t, const float (&)[2][4]) {
+    // 8 bytes per token: dword 2t holds channels 8n..8n+3, dword 2t+1 8n+4..8n+7
+    const uint32_t w = dword(r.v[pg][t >> 1], 2 * (t & 1) + (C >> 1));
+    return __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w, 1.0f, (C & 1) != 0));
+}
+template <int C>
+__device__ __forceinline__ uint32_t v_pair(const StageRegs<kBf16>& r, int pg, int t, const float (&)[2][4]) {
+    // 16 bytes per token: dword C holds channels 8n+2C, 8n+2C+1
+    return dword(r.v[pg][t], C);
+}
+
+// PV for channel pair C of every lane: channels 8n+2C (block 2C, low halves)
+// and 8n+2C+1 (block 2C+1, high halves).  The BF16 values of tokens
+// (t, t+1) are paired by byte permutes into the k-slot order of P.
+template <int C, class R>
+__device__ __forceinline__ void pv_pair(const R& r, const float (&sc)[2][4], const v8bf& Phi, const v8bf& Plo,
+                                        v4f& acc_e, v4f& acc_o) {
+    uint32_t c0[4], c1[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        c0[t] = v_pair<C>(r, 0, t, sc);
+        c1[t] = v_pair<C>(r, 1, t, sc);
+    }
+    const uint4 ae = {__builtin_amdgcn_perm(c0[1], c0[0], 0x05040100u), __builtin_amdgcn_perm(c0[3], c0[2], 0x05040100u),
+                      __builtin_amdgcn_perm(c1[1], c1[0], 0x05040100u), __builtin_amdgcn_perm(c1[3], c1[2], 0x05040100u)};
+    const uint4 ao = {__builtin_amdgcn_perm(c0[1], c0[0], 0x07060302u), __builtin_amdgcn_perm(c0[3], c0[2], 0x07060302u),
+                      __builtin_amdgcn_perm(c1[1], c1[0], 0x07060302u), __builtin_amdgcn_perm(c1[3], c1[2], 0x07060302u)};
+    const v8bf Ve = __builtin_bit_cast(v8bf, ae);
+    const v8bf Vo = __builtin_bit_cast(v8bf, ao);
+    acc_e = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ve, Phi, acc_e, 0, 0, 0);
+    acc_e = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ve, Plo, acc_e, 0, 0, 0);
+    acc_o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Vo, Phi, acc_o, 0, 0, 0);
+    acc_o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Vo, Plo, acc_o, 0, 0, 0);
 }
 
 __device__ __forceinline__ void write_out(const DecodeParams& p, int64_t row, int L, const float (&o)[8]) {
@@ -233,7 +369,32 @@ __device__ __forceinline__ void write_out(const DecodeParams& p, int64_t row, in
     }
 }
 
-__global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4, 4))) decode_kernel(DecodeParams p) {
+// Final scaling of one row: divide by the softmax sum, apply the V tensor
+// scale, rotate back when V was stored rotated.
+__device__ __forceinline__ void finish_row(const DecodeParams& p, float (&o)[8], float lsum, int L) {
+    const float inv = p.out_scale / lsum;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) o[i] *= inv;
+    if (p.rotate_v) wht128_x8(o, L);
+}
+
+// Zero the V bytes of a masked token of a plain cache (garbage bytes past
+// the context may decode to NaN or Inf, and 0 * NaN is NaN).
+__device__ __forceinline__ void zero_token(StageRegs<kFp8>& c, int pg, int t) {
+    uint4& v = c.v[pg][t >> 1];
+    if (t & 1) v = uint4{v.x, v.y, 0u, 0u};
+    else v = uint4{0u, 0u, v.z, v.w};
+}
+__device__ __forceinline__ void zero_token(StageRegs<kBf16>& c, int pg, int t) { c.v[pg][t] = uint4{0u, 0u, 0u, 0u}; }
+__device__ __forceinline__ void zero_token(StageRegs<kFp4>&, int, int) {}   // handled through the scale byte
+
+template <int F>
+__global__ void __launch_bounds__(64 * Fmt<F>::kWaves)
+__attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) decode_kernel(DecodeParams p) {
+    constexpr int W = Fmt<F>::kWaves;
+    constexpr int kThreads = 64 * W;
+    constexpr int kStage = stage_bytes<F>();
+    constexpr int kQRounds = 256 / kThreads;   // 16 threads per query row, 16 rows
     const int part = blockIdx.x;
     const int hk = blockIdx.y;
     const int b = blockIdx.z;
@@ -247,37 +408,46 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4
     const int start = part * p.partition_tokens;
     if (start >= ctx) {
         // nothing of this sequence here; an empty context still gets its zero output
-        if (ctx <= 0 && part == 0 && (tid >> 4) < G) {
-            const float z[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-            write_out(p, int64_t(b) * p.num_q_heads + hk * G + (tid >> 4), tid & 15, z);
+        if (ctx <= 0 && part == 0) {
+            for (int r = tid >> 4; r < G; r += kThreads / 16) {
+                const float z[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+                write_out(p, int64_t(b) * p.num_q_heads + hk * G + r, tid & 15, z);
+            }
         }
         return;
     }
     const int end = (start + p.partition_tokens) < ctx ? (start + p.partition_tokens) : ctx;
     const int np_b = (ctx + p.partition_tokens - 1) / p.partition_tokens;
 
-    __shared__ __attribute__((aligned(16))) uint8_t smem[kWaves * kRingBytes];
-    __shared__ __attribute__((aligned(16))) uint8_t q_lds[64 * 32];
-    __shared__ float red_m[kWaves][16];
-    __shared__ float red_l[kWaves][16];
+    __shared__ __attribute__((aligned(16))) uint8_t smem[W * ring_bytes<F>()];
+    __shared__ __attribute__((aligned(16))) uint8_t q_lds[F == kBf16 ? 4 * 64 * 16 : 64 * 32];
+    __shared__ float red_m[W][16];
+    __shared__ float red_l[W][16];
 
     // ---------------- query load first (its latency overlaps the page walk set-up)
-    const int qr = tid >> 4;        // query head within the group
-    const int qL = tid & 15;        // channels 8*qL..8*qL+7
-    float qx[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    uint32_t qlo = 0, qhi = 0;
-    if (qr < G) {
-        const int64_t elem = (int64_t(b) * p.num_q_heads + hk * G + qr) * kHeadDim + 8 * qL;
-        if (p.q_dtype == 3) {
-            const uint2 w = *reinterpret_cast<const uint2*>(static_cast<const uint8_t*>(p.q) + elem);
-            qlo = w.x;
-            qhi = w.y;
-        } else if (p.q_dtype == 0) {
-            load_q8<0>(p.q, elem, qx);
-        } else if (p.q_dtype == 1) {
-            load_q8<1>(p.q, elem, qx);
-        } else {
-            load_q8<2>(p.q, elem, qx);
+    float qx[kQRounds][8];
+    uint32_t qw[kQRounds][2];
+#pragma unroll
+    for (int h = 0; h < kQRounds; ++h) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) qx[h][i] = 0.f;
+        qw[h][0] = 0u;
+        qw[h][1] = 0u;
+        const int qr = (tid >> 4) + h * (kThreads / 16);
+        const int qL = tid & 15;
+        if (qr < G) {
+            const int64_t elem = (int64_t(b) * p.num_q_heads + hk * G + qr) * kHeadDim + 8 * qL;
+            if (p.q_dtype == 3) {
+                const uint2 w = *reinterpret_cast<const uint2*>(static_cast<const uint8_t*>(p.q) + elem);
+                qw[h][0] = w.x;
+                qw[h][1] = w.y;
+            } else if (p.q_dtype == 0) {
+                load_q8<0>(p.q, elem, qx[h]);
+            } else if (p.q_dtype == 1) {
+                load_q8<1>(p.q, elem, qx[h]);
+            } else {
+                load_q8<2>(p.q, elem, qx[h]);
+            }
         }
     }
 
@@ -285,54 +455,70 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4
     const int first_page = start >> 4;
     const int n_pages = (end - start + 15) >> 4;
     const int n_iter = (n_pages + 1) >> 1;
-    const int n_local = wave < n_iter ? (n_iter - wave + kWaves - 1) / kWaves : 0;
+    const int n_local = wave < n_iter ? (n_iter - wave + W - 1) / W : 0;
     const int32_t* pt_row = p.page_table + int64_t(b) * p.max_pages_per_seq;
     const int g4 = lane >> 4;           // lane group: tokens 4*g4..4*g4+3 of each page
     const int n = lane & 15;
-    uint8_t* ring = smem + wave * kRingBytes;
+    uint8_t* ring = smem + wave * ring_bytes<F>();
     const uint32_t ring_addr = uint32_t(reinterpret_cast<uintptr_t>((lds_ptr_t)ring));
-    const uint32_t off_codes = 16 * lane;
-    const uint32_t off_ks = lane;
-    const uint32_t off_vs = kTileScales + (n >> 2) * 16 + 4 * g4;
     const int64_t head_tile = int64_t(hk) * 2;
     const int64_t tiles_per_page = int64_t(p.num_kv_heads) * 2;
 
     int32_t ids = 0, ids_next = 0;
     if (n_local > 0) {
-        ids = load_page_ids(pt_row, first_page, n_pages, wave, 0, lane, p.num_pages);
-        if (n_local > 32) ids_next = load_page_ids(pt_row, first_page, n_pages, wave, 1, lane, p.num_pages);
+        ids = load_page_ids<W>(pt_row, first_page, n_pages, wave, 0, lane, p.num_pages);
+        if (n_local > 32) ids_next = load_page_ids<W>(pt_row, first_page, n_pages, wave, 1, lane, p.num_pages);
         for (int s = 0; s < 2 && s < n_local; ++s) {
             const int64_t id0 = __builtin_amdgcn_readlane(ids, 2 * s);
             const int64_t id1 = __builtin_amdgcn_readlane(ids, 2 * s + 1);
-            stage_issue(ring + s * kStageBytes, p.codes, p.scales, id0 * tiles_per_page + head_tile,
-                        id1 * tiles_per_page + head_tile, lane);
+            stage_issue<F>(ring + s * kStage, p.codes, p.scales, id0 * tiles_per_page + head_tile,
+                           id1 * tiles_per_page + head_tile, lane);
         }
     }
 
-    // ---------------- query prologue: rotate, cast to FP8, B-operand order
-    if (qr < G && p.q_dtype != 3) {
-        wht128_x8(qx, qL);
+    // ---------------- query prologue: transform and store in B-operand order
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            qlo |= e4m3_byte(qx[i]) << (8 * i);
-            qhi |= e4m3_byte(qx[i + 4]) << (8 * i);
+    for (int h = 0; h < kQRounds; ++h) {
+        const int qr = (tid >> 4) + h * (kThreads / 16);
+        const int qL = tid & 15;
+        if constexpr (F == kBf16) {
+            // channels 8*qL..+7 are k-step qL/4, lane (qL%4)*16 + qr, 16 bytes
+            uint4 w = {0u, 0u, 0u, 0u};
+            if (qr < G)
+                w = uint4{pack_bf16x2(qx[h][0], qx[h][1]), pack_bf16x2(qx[h][2], qx[h][3]),
+                          pack_bf16x2(qx[h][4], qx[h][5]), pack_bf16x2(qx[h][6], qx[h][7])};
+            *reinterpret_cast<uint4*>(q_lds + ((qL >> 2) * 64 + (qL & 3) * 16 + qr) * 16) = w;
+        } else {
+            uint32_t lo = qw[h][0], hi = qw[h][1];
+            if (qr < G && p.q_dtype != 3) {
+                if constexpr (F == kFp4) wht128_x8(qx[h], qL);
+                lo = 0;
+                hi = 0;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    lo |= e4m3_byte(qx[h][i]) << (8 * i);
+                    hi |= e4m3_byte(qx[h][i + 4]) << (8 * i);
+                }
+            }
+            // FP8 operand of the 16x16x128 scaled MFMA: lane 16*g + n holds
+            // column n, channels 16g..16g+15 in bytes 0..15 and
+            // 64+16g..64+16g+15 in bytes 16..31.  Rows qr >= G stay zero.
+            const int ch = 8 * qL;
+            const int g = (ch & 63) >> 4;
+            const int e0 = (ch & 15) + (ch >= 64 ? 16 : 0);
+            *reinterpret_cast<uint2*>(q_lds + (g * 16 + qr) * 32 + e0) = make_uint2(lo, hi);
         }
     }
-    {
-        // FP8 operand of the 16x16x128 scaled MFMA: lane 16*g + n holds
-        // column n, channels 16g..16g+15 in bytes 0..15 and 64+16g..64+16g+15
-        // in bytes 16..31.  Rows qr >= G stay zero.
-        const int ch = 8 * qL;
-        const int g = (ch & 63) >> 4;
-        const int e0 = (ch & 15) + (ch >= 64 ? 16 : 0);
-        *reinterpret_cast<uint2*>(q_lds + (g * 16 + qr) * 32 + e0) = make_uint2(qlo, qhi);
-    }
     __syncthreads();
-    v8i qop;
-    {
+    QOperand<F> qop;
+    if constexpr (F == kBf16) {
+#pragma unroll
+        for (int st = 0; st < 4; ++st)
+            qop.q[st] = __builtin_bit_cast(v8bf, *reinterpret_cast<const uint4*>(q_lds + (st * 64 + lane) * 16));
+    } else {
         const uint4* src = reinterpret_cast<const uint4*>(q_lds + lane * 32);
         const uint4 a = src[0], c = src[1];
-        qop = v8i{int(a.x), int(a.y), int(a.z), int(a.w), int(c.x), int(c.y), int(c.z), int(c.w)};
+        qop.q = v8i{int(a.x), int(a.y), int(a.z), int(a.w), int(c.x), int(c.y), int(c.z), int(c.w)};
     }
 
     const float sl2 = p.scale_log2;
@@ -344,48 +530,55 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4
 
     // ---------------- main loop: one stage (2 pages, 32 tokens) per iteration
     for (int k = 0; k < n_local; ++k) {
-        if (k + 1 < n_local) wait_vmem<kDmaPerStage>();
+        if (k + 1 < n_local) wait_vmem<dma_per_stage<F>()>();
         else wait_vmem<0>();
         const uint32_t slot = uint32_t(k & 1);
-        const StageRegs c = stage_read(ring_addr + slot * kStageBytes, off_codes, off_ks, off_vs);
+        StageRegs<F> c;
+        stage_read(c, ring_addr + slot * kStage, lane);
         if (k + 2 < n_local) {
             // refill this slot with iteration k+2 while iteration k computes
             const int kn = k + 2;
             if ((kn & 31) == 0) {
                 ids = ids_next;
                 if (kn + 32 < n_local)
-                    ids_next = load_page_ids(pt_row, first_page, n_pages, wave, (kn >> 5) + 1, lane, p.num_pages);
+                    ids_next = load_page_ids<W>(pt_row, first_page, n_pages, wave, (kn >> 5) + 1, lane, p.num_pages);
             }
             const int s = 2 * (kn & 31);
             const int64_t id0 = __builtin_amdgcn_readlane(ids, s);
             const int64_t id1 = __builtin_amdgcn_readlane(ids, s + 1);
-            stage_issue(ring + slot * kStageBytes, p.codes, p.scales, id0 * tiles_per_page + head_tile,
-                        id1 * tiles_per_page + head_tile, lane);
+            stage_issue<F>(ring + slot * kStage, p.codes, p.scales, id0 * tiles_per_page + head_tile,
+                           id1 * tiles_per_page + head_tile, lane);
         }
 
-        // ---- QK^T: S^T[token][head] per page, FP4 x FP8 with the UE8M0 bytes as A scales
-        const v4f zero = {0.f, 0.f, 0.f, 0.f};
-        const v8i ka0 = {int(c.k0.x), int(c.k0.y), int(c.k0.z), int(c.k0.w), 0, 0, 0, 0};
-        const v8i ka1 = {int(c.k1.x), int(c.k1.y), int(c.k1.z), int(c.k1.w), 0, 0, 0, 0};
-        const v4f s0 = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(ka0, qop, zero, 4, 0, 0, int(c.ks0), 0, 127);
-        const v4f s1 = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(ka1, qop, zero, 4, 0, 0, int(c.ks1), 0, 127);
-
-        // raw scores; the softmax scale (times log2 e, positive) is applied
-        // inside the exponent's fma
+        // ---- QK^T: raw scores (the softmax scale is applied in the exponent)
+        const v4f s0 = qk_page(c, 0, qop);
+        const v4f s1 = qk_page(c, 1, qop);
         float x[8];
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             x[i] = s0[i];
             x[4 + i] = s1[i];
         }
-        uint32_t vs0 = c.vs0, vs1 = c.vs1;
-        const int it = wave + kWaves * k;
+        uint32_t vs0 = 0, vs1 = 0;   // V scale bytes of the lane's 4 tokens per page (FP4)
+        if constexpr (F == kFp4) {
+            vs0 = c.vs[0];
+            vs1 = c.vs[1];
+        }
+        const int it = wave + W * k;
         const int tok0 = start + 32 * it + 4 * g4;   // token of x[0]; x[4] is tok0 + 16
         if (start + 32 * it + 32 > end) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                if (tok0 + i >= end) { x[i] = -__builtin_inff(); vs0 &= ~(0xFFu << (8 * i)); }
-                if (tok0 + 16 + i >= end) { x[4 + i] = -__builtin_inff(); vs1 &= ~(0xFFu << (8 * i)); }
+                if (tok0 + i >= end) {
+                    x[i] = -__builtin_inff();
+                    vs0 &= ~(0xFFu << (8 * i));
+                    zero_token(c, 0, i);
+                }
+                if (tok0 + 16 + i >= end) {
+                    x[4 + i] = -__builtin_inff();
+                    vs1 &= ~(0xFFu << (8 * i));
+                    zero_token(c, 1, i);
+                }
             }
         }
 
@@ -416,25 +609,24 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4
         const v8bf Phi = __builtin_bit_cast(v8bf, uint4{phi[0], phi[1], phi[2], phi[3]});
         const v8bf Plo = __builtin_bit_cast(v8bf, uint4{plo[0], plo[1], plo[2], plo[3]});
 
-        // ---- V: FP4 -> BF16 with the token scale, then PV on bf16 MFMA
-        const uint32_t v0d[4] = {c.v0.x, c.v0.y, c.v0.z, c.v0.w};
-        const uint32_t v1d[4] = {c.v1.x, c.v1.y, c.v1.z, c.v1.w};
-        float sc0[4], sc1[4];
+        // ---- V to BF16 pairs, then PV on bf16 MFMA
+        float sc[2][4];
 #pragma unroll
         for (int t = 0; t < 4; ++t) {
-            sc0[t] = ue8m0_to_f32(vs0 >> (8 * t));
-            sc1[t] = ue8m0_to_f32(vs1 >> (8 * t));
+            sc[0][t] = ue8m0_to_f32(vs0 >> (8 * t));
+            sc[1][t] = ue8m0_to_f32(vs1 >> (8 * t));
         }
-        pv_pair<0>(v0d, v1d, sc0, sc1, Phi, Plo, acc[0], acc[1]);
-        pv_pair<1>(v0d, v1d, sc0, sc1, Phi, Plo, acc[2], acc[3]);
-        pv_pair<2>(v0d, v1d, sc0, sc1, Phi, Plo, acc[4], acc[5]);
-        pv_pair<3>(v0d, v1d, sc0, sc1, Phi, Plo, acc[6], acc[7]);
+        pv_pair<0>(c, sc, Phi, Plo, acc[0], acc[1]);
+        pv_pair<1>(c, sc, Phi, Plo, acc[2], acc[3]);
+        pv_pair<2>(c, sc, Phi, Plo, acc[4], acc[5]);
+        pv_pair<3>(c, sc, Phi, Plo, acc[6], acc[7]);
     }
 
-    // ---------------- merge the 4 waves through LDS (the rings are free now)
+    // ---------------- merge the waves through LDS (the rings are free now)
     l_run = sum_across_groups(l_run);
     __syncthreads();
     float* red_acc = reinterpret_cast<float*>(smem);
+    static_assert(W * 16 * kAccStride * 4 <= W * ring_bytes<F>(), "merge buffer aliases the staging rings");
     if (g4 == 0) {
         red_m[wave][n] = m_run;
         red_l[wave][n] = l_run;
@@ -447,57 +639,48 @@ __global__ void __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(4
     }
     __syncthreads();
 
-    const int r = tid >> 4;   // query head within the group
-    const int L = tid & 15;   // channels 8L..8L+7
-    const bool row_ok = r < G;
-    const int hq = hk * G + r;
-    float o[8];
-    float M = 0.f, lsum = 0.f;
-    if (row_ok) {
-        M = red_m[0][r];
 #pragma unroll
-        for (int w = 1; w < kWaves; ++w) M = __builtin_fmaxf(M, red_m[w][r]);
-        float f[kWaves];
+    for (int h = 0; h < kQRounds; ++h) {
+        const int r = (tid >> 4) + h * (kThreads / 16);   // query head within the group
+        const int L = tid & 15;                           // channels 8L..8L+7
+        if (r >= G) continue;                             // whole 16-lane rows skip together
+        const int hq = hk * G + r;
+        float M = red_m[0][r];
 #pragma unroll
-        for (int w = 0; w < kWaves; ++w) {
+        for (int w = 1; w < W; ++w) M = __builtin_fmaxf(M, red_m[w][r]);
+        float f[W];
+        float lsum = 0.f;
+#pragma unroll
+        for (int w = 0; w < W; ++w) {
             f[w] = __builtin_amdgcn_exp2f(red_m[w][r] - M);
             lsum += f[w] * red_l[w][r];
         }
+        float o[8];
 #pragma unroll
         for (int cc = 0; cc < 8; ++cc) {
             float s = 0.f;
 #pragma unroll
-            for (int w = 0; w < kWaves; ++w) s += f[w] * red_acc[(w * 16 + r) * kAccStride + 8 * L + cc];
+            for (int w = 0; w < W; ++w) s += f[w] * red_acc[(w * 16 + r) * kAccStride + 8 * L + cc];
             o[cc] = s;
         }
-    }
-
-    if (np_b == 1) {
-        // the whole context is in this block: finish here
-        if (row_ok) {
-            const float inv = 1.0f / lsum;
-#pragma unroll
-            for (int i = 0; i < 8; ++i) o[i] *= inv;
-            if (p.rotate_v) wht128_x8(o, L);
+        if (np_b == 1) {
+            // the whole context is in this block: finish here
+            finish_row(p, o, lsum, L);
             write_out(p, int64_t(b) * p.num_q_heads + hq, L, o);
+        } else {
+            // several partitions: publish this one for the merge kernel
+            const int64_t prow = (int64_t(b) * p.num_q_heads + hq) * p.num_partitions + part;
+            float4* dst = reinterpret_cast<float4*>(p.part_acc + prow * kHeadDim + 8 * L);
+            dst[0] = make_float4(o[0], o[1], o[2], o[3]);
+            dst[1] = make_float4(o[4], o[5], o[6], o[7]);
+            if (L == 0) *reinterpret_cast<float2*>(p.part_ml + prow * 2) = make_float2(M, lsum);
         }
-        return;
-    }
-
-    // several partitions: publish this one for the merge kernel
-    if (row_ok) {
-        const int64_t prow = (int64_t(b) * p.num_q_heads + hq) * p.num_partitions + part;
-        float4* dst = reinterpret_cast<float4*>(p.part_acc + prow * kHeadDim + 8 * L);
-        dst[0] = make_float4(o[0], o[1], o[2], o[3]);
-        dst[1] = make_float4(o[4], o[5], o[6], o[7]);
-        if (L == 0) *reinterpret_cast<float2*>(p.part_ml + prow * 2) = make_float2(M, lsum);
     }
 }
 
 // Merge the partitions of every (sequence, query head) with more than one:
 // online over the partitions (loads independent of the running state, so
-// they overlap), divide by the softmax sum, rotate back when V was stored
-// rotated, write the output.  One 16-lane row per query head.
+// they overlap), then finish the row.  One 16-lane row per query head.
 __global__ void __launch_bounds__(256) merge_kernel(DecodeParams p) {
     const int hk = blockIdx.x;
     const int b = blockIdx.y;
@@ -526,17 +709,21 @@ __global__ void __launch_bounds__(256) merge_kernel(DecodeParams p) {
         o[4] = o[4] * fo + c.x * fn; o[5] = o[5] * fo + c.y * fn; o[6] = o[6] * fo + c.z * fn; o[7] = o[7] * fo + c.w * fn;
         M = Mn;
     }
-    const float inv = 1.0f / lsum;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) o[i] *= inv;
-    if (p.rotate_v) wht128_x8(o, L);
+    finish_row(p, o, lsum, L);
     write_out(p, int64_t(b) * p.num_q_heads + hq, L, o);
 }
 
-hipError_t launch_decode_partials(const DecodeParams& p, hipStream_t stream) {
+template <int F>
+static hipError_t launch_partials(const DecodeParams& p, hipStream_t stream) {
     const dim3 grid{unsigned(p.num_partitions), unsigned(p.num_kv_heads), unsigned(p.batch)};
-    hipLaunchKernelGGL(decode_kernel, grid, dim3(kThreads), 0, stream, p);
+    hipLaunchKernelGGL(decode_kernel<F>, grid, dim3(64 * Fmt<F>::kWaves), 0, stream, p);
     return hipGetLastError();
+}
+
+hipError_t launch_decode_partials(const DecodeParams& p, hipStream_t stream) {
+    if (p.kv_fmt == kFp8) return launch_partials<kFp8>(p, stream);
+    if (p.kv_fmt == kBf16) return launch_partials<kBf16>(p, stream);
+    return launch_partials<kFp4>(p, stream);
 }
 
 hipError_t launch_decode_merge(const DecodeParams& p, hipStream_t stream) {

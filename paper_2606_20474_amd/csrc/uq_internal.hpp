@@ -7,6 +7,10 @@
 
 namespace uq {
 
+// Cache formats of the decode kernel template: the FP4 cache of this library
+// and the two plain comparison caches.
+enum KvFmt : int32_t { kFp4 = 0, kFp8 = 1, kBf16 = 2 };
+
 struct QuantizeParams {
     const void* k;
     const void* v;
@@ -24,7 +28,26 @@ struct QuantizeParams {
     uint8_t* scales;
 };
 
+struct RefWriteParams {
+    const void* k;
+    const void* v;
+    int64_t num_tokens;
+    int64_t token_stride;
+    const int64_t* slot_mapping;
+    const int32_t* page_table;
+    int32_t max_pages_per_seq;
+    int64_t num_seqs;
+    int32_t num_kv_heads;
+    int64_t num_pages;
+    float k_scale;             // FP8: stored = e4m3(x / k_scale)
+    float v_scale;
+    int32_t kv_fmt;            // kFp8 or kBf16
+    uint8_t* cache;            // [pages][Hkv][2][tile bytes]
+};
+
 struct DecodeParams {
+    int32_t kv_fmt;            // KvFmt
+    float out_scale;           // V tensor scale (FP8 cache), else 1
     const void* q;             // [B][Hq][128], dtype q_dtype
     int32_t q_dtype;           // 0 f32, 1 bf16, 2 f16, 3 fp8 (prepared)
     const uint8_t* codes;
@@ -49,6 +72,7 @@ struct DecodeParams {
 };
 
 hipError_t launch_quantize_kv(const QuantizeParams& p, int dtype, hipStream_t stream);
+hipError_t launch_write_kv_ref(const RefWriteParams& p, int dtype, hipStream_t stream);
 hipError_t launch_prepare_query(const void* q, int dtype, int64_t rows, uint8_t* q8, hipStream_t stream);
 hipError_t launch_decode_partials(const DecodeParams& p, hipStream_t stream);
 hipError_t launch_decode_merge(const DecodeParams& p, hipStream_t stream);

@@ -105,6 +105,72 @@ __global__ void __launch_bounds__(256) quantize_kv_kernel(QuantizeParams p) {
     }
 }
 
+// Writer of the plain comparison caches (FP8 E4M3 with one scale per
+// tensor, or BF16), no rotation, in the lane order the decode kernel reads:
+//   FP8  K tile [group g][token][32 B]: bytes 0..15 = channels 16g..16g+15,
+//        bytes 16..31 = channels 64+16g..64+16g+15 (the FP8 operand order of
+//        the 16x16x128 MFMA); V tile [token/4][channel/8][token%4][8 B].
+//   BF16 K tile [k-step s][group g][token][16 B] = channels 32s+8g..+7;
+//        V tile [token/4][channel/8][token%4][16 B].
+template <int DT, int FMT>
+__global__ void __launch_bounds__(256) write_kv_ref_kernel(RefWriteParams p) {
+    const int lane16 = threadIdx.x & 15;
+    const int64_t vec = int64_t(blockIdx.x) * 16 + (threadIdx.x >> 4);
+    const int64_t nvec = p.num_tokens * p.num_kv_heads;
+    if (vec >= nvec) return;
+    const int64_t t = vec / p.num_kv_heads;
+    const int h = int(vec - t * p.num_kv_heads);
+    const int64_t slot = p.slot_mapping[t];
+    if (slot < 0) return;
+    int64_t page;
+    int off;
+    if (p.page_table != nullptr) {
+        const int64_t per_seq = int64_t(p.max_pages_per_seq) * kPage;
+        const int64_t seq = slot / per_seq;
+        const int64_t pos = slot - seq * per_seq;
+        if (seq >= p.num_seqs) return;
+        page = p.page_table[seq * p.max_pages_per_seq + pos / kPage];
+        off = int(pos % kPage);
+    } else {
+        page = slot / kPage;
+        off = int(slot % kPage);
+    }
+    if (page < 0 || page >= p.num_pages) return;
+    const int64_t elem = t * p.token_stride + int64_t(h) * kHeadDim + 8 * lane16;
+    float xk[8], xv[8];
+    load_x8<DT>(p.k, elem, xk);
+    load_x8<DT>(p.v, elem, xv);
+    constexpr int kTileBytes = FMT == kFp8 ? 2048 : 4096;
+    uint8_t* kt = p.cache + ((page * p.num_kv_heads + h) * 2) * kTileBytes;
+    uint8_t* vt = kt + kTileBytes;
+    if constexpr (FMT == kFp8) {
+        uint32_t kw[2] = {0u, 0u}, vw[2] = {0u, 0u};
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            kw[i >> 2] |= e4m3_byte(xk[i] / p.k_scale) << (8 * (i & 3));
+            vw[i >> 2] |= e4m3_byte(xv[i] / p.v_scale) << (8 * (i & 3));
+        }
+        const int c0 = 8 * lane16;
+        const int g = (c0 & 63) >> 4;
+        const int e0 = (c0 & 15) + (c0 >= 64 ? 16 : 0);
+        *reinterpret_cast<uint2*>(kt + (g * kPage + off) * 32 + e0) = make_uint2(kw[0], kw[1]);
+        *reinterpret_cast<uint2*>(vt + ((off >> 2) * 16 + lane16) * 32 + (off & 3) * 8) = make_uint2(vw[0], vw[1]);
+    } else {
+        uint32_t kw[4], vw[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const v2bf hk = {__bf16(xk[2 * i]), __bf16(xk[2 * i + 1])};
+            const v2bf hv = {__bf16(xv[2 * i]), __bf16(xv[2 * i + 1])};
+            kw[i] = __builtin_bit_cast(uint32_t, hk);
+            vw[i] = __builtin_bit_cast(uint32_t, hv);
+        }
+        const int st = lane16 >> 2;
+        const int g = lane16 & 3;
+        *reinterpret_cast<uint4*>(kt + ((st * 4 + g) * kPage + off) * 16) = uint4{kw[0], kw[1], kw[2], kw[3]};
+        *reinterpret_cast<uint4*>(vt + ((off >> 2) * 16 + lane16) * 64 + (off & 3) * 16) = uint4{vw[0], vw[1], vw[2], vw[3]};
+    }
+}
+
 template <int DT>
 __global__ void __launch_bounds__(256) prepare_query_kernel(const void* q, int64_t rows, uint8_t* q8) {
     const int lane16 = threadIdx.x & 15;
@@ -132,6 +198,24 @@ hipError_t launch_quantize_kv(const QuantizeParams& p, int dtype, hipStream_t st
     else if (dtype == 1) hipLaunchKernelGGL(quantize_kv_kernel<1>, grid, block, 0, stream, p);
     else hipLaunchKernelGGL(quantize_kv_kernel<2>, grid, block, 0, stream, p);
     return hipGetLastError();
+}
+
+template <int DT>
+static hipError_t launch_ref(const RefWriteParams& p, const dim3& grid, hipStream_t stream) {
+    if (p.kv_fmt == kFp8) hipLaunchKernelGGL((write_kv_ref_kernel<DT, kFp8>), grid, dim3(256), 0, stream, p);
+    else hipLaunchKernelGGL((write_kv_ref_kernel<DT, kBf16>), grid, dim3(256), 0, stream, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_write_kv_ref(const RefWriteParams& p, int dtype, hipStream_t stream) {
+    const int64_t nvec = p.num_tokens * p.num_kv_heads;
+    const int64_t blocks = (nvec + 15) / 16;
+    if (blocks == 0) return hipSuccess;
+    if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
+    const dim3 grid{unsigned(blocks)};
+    if (dtype == 0) return launch_ref<0>(p, grid, stream);
+    if (dtype == 1) return launch_ref<1>(p, grid, stream);
+    return launch_ref<2>(p, grid, stream);
 }
 
 hipError_t launch_prepare_query(const void* q, int dtype, int64_t rows, uint8_t* q8, hipStream_t stream) {

@@ -30,7 +30,11 @@ TILE_SCALES = 64
 EXPORTS = (
     "uq_status_string", "uq_version", "uq_quantize_kv", "uq_prepare_query", "uq_decode_workspace_bytes",
     "uq_default_partition", "uq_decode_attention", "uq_decode_partials", "uq_decode_merge",
+    "uq_ref_cache_bytes", "uq_ref_write_kv", "uq_ref_decode_workspace_bytes", "uq_ref_decode_attention",
+    "uq_ref_decode_partials", "uq_ref_decode_merge",
 )
+
+UQ_REF_FP8_E4M3, UQ_REF_BF16 = 1, 2
 
 
 class UQError(RuntimeError):
@@ -48,6 +52,18 @@ class uq_cache_desc(ctypes.Structure):
         ("num_pages", ctypes.c_int64),
         ("c", ctypes.c_float),
         ("rotate_v", ctypes.c_int32),
+    ]
+
+
+class uq_ref_cache_desc(ctypes.Structure):
+    _fields_ = [
+        ("num_kv_heads", ctypes.c_int32),
+        ("head_dim", ctypes.c_int32),
+        ("page_size", ctypes.c_int32),
+        ("format", ctypes.c_int32),
+        ("num_pages", ctypes.c_int64),
+        ("k_scale", ctypes.c_float),
+        ("v_scale", ctypes.c_float),
     ]
 
 
@@ -74,6 +90,19 @@ def _load():
     L.uq_decode_partials.restype = i32
     L.uq_decode_merge.argtypes = [D, i32, i32, vp, i32, i32, vp, sz, vp, i32, vp]
     L.uq_decode_merge.restype = i32
+    R = ctypes.POINTER(uq_ref_cache_desc)
+    L.uq_ref_cache_bytes.argtypes = [R]
+    L.uq_ref_cache_bytes.restype = sz
+    L.uq_ref_write_kv.argtypes = [R, vp, vp, i32, i64, i64, vp, i32, i32, vp, vp, vp]
+    L.uq_ref_write_kv.restype = i32
+    L.uq_ref_decode_workspace_bytes.argtypes = [R, i32, i32, i32, i32]
+    L.uq_ref_decode_workspace_bytes.restype = sz
+    for name in ("uq_ref_decode_attention", "uq_ref_decode_partials"):
+        fn = getattr(L, name)
+        fn.argtypes = [R, vp, i32, i32, i32, vp, vp, i32, vp, i32, f32, i32, vp, sz, vp, i32, vp]
+        fn.restype = i32
+    L.uq_ref_decode_merge.argtypes = [R, i32, i32, vp, i32, i32, vp, sz, vp, i32, vp]
+    L.uq_ref_decode_merge.restype = i32
     return L
 
 
@@ -213,4 +242,101 @@ def decode_merge(desc: CacheDesc, batch, num_q_heads, context_lens, max_context,
     st = lib.uq_decode_merge(ctypes.byref(d), batch, num_q_heads, _ptr(context_lens), max_context, partition_tokens,
                              _ptr(workspace), workspace.numel(), _ptr(out), _DT[out.dtype], _stream(stream))
     _check(st, "uq_decode_merge")
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Plain comparison caches (FP8 E4M3 with per-tensor scales, BF16)
+
+
+@dataclass
+class RefCacheDesc:
+    """Python mirror of ``uq_ref_cache_desc``; ``fmt`` is "fp8" or "bf16"."""
+    num_kv_heads: int
+    num_pages: int
+    fmt: str = "fp8"
+    k_scale: float = 1.0
+    v_scale: float = 1.0
+    head_dim: int = HEAD_DIM
+    page_size: int = PAGE_SIZE
+
+    def c_struct(self):
+        code = {"fp8": UQ_REF_FP8_E4M3, "bf16": UQ_REF_BF16}.get(self.fmt, 0)
+        return uq_ref_cache_desc(self.num_kv_heads, self.head_dim, self.page_size, code, self.num_pages,
+                                 self.k_scale, self.v_scale)
+
+    def cache_bytes(self):
+        d = self.c_struct()
+        return int(lib.uq_ref_cache_bytes(ctypes.byref(d)))
+
+    def alloc_cache(self, device="cuda", fill=None):
+        n = self.cache_bytes()
+        if n == 0:
+            raise UQError(UQ_ERR_INVALID_ARGUMENT, "uq_ref_cache_bytes")
+        cache = torch.empty(n, dtype=torch.uint8, device=device)
+        if fill is not None:
+            cache.fill_(fill)
+        return cache
+
+
+def ref_write_kv(desc: RefCacheDesc, k, v, slot_mapping, cache, page_table=None, max_pages_per_seq=0,
+                 token_stride=None, stream=None):
+    T = k.shape[0]
+    if token_stride is None:
+        token_stride = k.stride(0)
+    num_seqs = 0 if page_table is None else page_table.shape[0]
+    mpps = 0 if page_table is None else (max_pages_per_seq or page_table.shape[1])
+    d = desc.c_struct()
+    st = lib.uq_ref_write_kv(ctypes.byref(d), _ptr(k), _ptr(v), _DT[k.dtype], T, token_stride, _ptr(page_table),
+                             num_seqs, mpps, _ptr(slot_mapping), _ptr(cache), _stream(stream))
+    _check(st, "uq_ref_write_kv")
+
+
+def ref_workspace_bytes(desc: RefCacheDesc, batch, num_q_heads, max_context, partition_tokens=0):
+    d = desc.c_struct()
+    return int(lib.uq_ref_decode_workspace_bytes(ctypes.byref(d), batch, num_q_heads, max_context, partition_tokens))
+
+
+def ref_alloc_workspace(desc: RefCacheDesc, batch, num_q_heads, max_context, partition_tokens=0, device="cuda"):
+    n = ref_workspace_bytes(desc, batch, num_q_heads, max_context, partition_tokens)
+    return torch.empty(n, dtype=torch.uint8, device=device)
+
+
+def ref_decode_attention(desc: RefCacheDesc, q, cache, page_table, context_lens, max_context, softmax_scale=None,
+                         partition_tokens=0, workspace=None, out=None, out_dtype=torch.float32, stream=None):
+    B, Hq = q.shape[0], q.shape[1]
+    if softmax_scale is None:
+        softmax_scale = HEAD_DIM ** -0.5
+    if workspace is None:
+        workspace = ref_alloc_workspace(desc, B, Hq, max_context, partition_tokens, q.device)
+    if out is None:
+        out = torch.empty((B, Hq, HEAD_DIM), dtype=out_dtype, device=q.device)
+    d = desc.c_struct()
+    st = lib.uq_ref_decode_attention(ctypes.byref(d), _ptr(q), _DT[q.dtype], B, Hq, _ptr(cache), _ptr(page_table),
+                                     page_table.shape[1], _ptr(context_lens), max_context, softmax_scale,
+                                     partition_tokens, _ptr(workspace), workspace.numel(), _ptr(out), _DT[out.dtype],
+                                     _stream(stream))
+    _check(st, "uq_ref_decode_attention")
+    return out
+
+
+def ref_decode_partials(desc: RefCacheDesc, q, cache, page_table, context_lens, max_context, softmax_scale,
+                        partition_tokens, workspace, out, stream=None):
+    B, Hq = q.shape[0], q.shape[1]
+    d = desc.c_struct()
+    st = lib.uq_ref_decode_partials(ctypes.byref(d), _ptr(q), _DT[q.dtype], B, Hq, _ptr(cache), _ptr(page_table),
+                                    page_table.shape[1], _ptr(context_lens), max_context, softmax_scale,
+                                    partition_tokens, _ptr(workspace), workspace.numel(), _ptr(out), _DT[out.dtype],
+                                    _stream(stream))
+    _check(st, "uq_ref_decode_partials")
+    return out
+
+
+def ref_decode_merge(desc: RefCacheDesc, batch, num_q_heads, context_lens, max_context, partition_tokens, workspace,
+                     out, stream=None):
+    d = desc.c_struct()
+    st = lib.uq_ref_decode_merge(ctypes.byref(d), batch, num_q_heads, _ptr(context_lens), max_context,
+                                 partition_tokens, _ptr(workspace), workspace.numel(), _ptr(out), _DT[out.dtype],
+                                 _stream(stream))
+    _check(st, "uq_ref_decode_merge")
     return out

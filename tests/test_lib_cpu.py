@@ -117,3 +117,64 @@ def test_workspace_and_partition_sizes(uq):
     assert uq.workspace_bytes(d, 32, 64, 32768, 4096) == 32 * 64 * 8 * 130 * 4
     assert uq.workspace_bytes(d, 32, 63, 32768, 4096) == 0   # invalid: returns 0
     assert uq.workspace_bytes(d, 1, 4, 0, 0) == 4 * 1 * 130 * 4
+
+
+def rdesc(**kw):
+    from paper_2606_20474_amd.uq import uq_ref_cache_desc
+    d = dict(num_kv_heads=2, head_dim=128, page_size=16, format=1, num_pages=10, k_scale=0.5, v_scale=0.25)
+    d.update(kw)
+    return uq_ref_cache_desc(**d)
+
+
+def test_ref_cache_sizes_and_validation(uq):
+    E = uq
+    lib = uq.lib
+    assert lib.uq_ref_cache_bytes(ctypes.byref(rdesc())) == 10 * 2 * 2 * 2048
+    assert lib.uq_ref_cache_bytes(ctypes.byref(rdesc(format=2))) == 10 * 2 * 2 * 4096
+    assert lib.uq_ref_cache_bytes(ctypes.byref(rdesc(format=3))) == 0
+    assert lib.uq_ref_cache_bytes(ctypes.byref(rdesc(k_scale=0.0))) == 0
+    assert lib.uq_ref_cache_bytes(ctypes.byref(rdesc(format=2, k_scale=0.0))) > 0   # scales unused for BF16
+    assert lib.uq_ref_cache_bytes(None) == 0
+
+    def write(d, **kw):
+        a = dict(k=FAKE, dtype=1, num_tokens=4, stride=256, pt=None, num_seqs=0, mpps=0, cache=FAKE)
+        a.update(kw)
+        return lib.uq_ref_write_kv(ctypes.byref(d) if d is not None else None, a["k"], FAKE, a["dtype"],
+                                   a["num_tokens"], a["stride"], a["pt"], a["num_seqs"], a["mpps"], FAKE,
+                                   a["cache"], None)
+
+    assert write(None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert write(rdesc(format=0)) == E.UQ_ERR_UNSUPPORTED
+    assert write(rdesc(head_dim=64)) == E.UQ_ERR_UNSUPPORTED
+    assert write(rdesc(v_scale=float("inf"))) == E.UQ_ERR_INVALID_ARGUMENT
+    assert write(rdesc(k_scale=-1.0)) == E.UQ_ERR_INVALID_ARGUMENT
+    assert write(rdesc(), dtype=3) == E.UQ_ERR_UNSUPPORTED
+    assert write(rdesc(), cache=None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert write(rdesc(), cache=ctypes.c_void_p(0x10008)) == E.UQ_ERR_INVALID_ARGUMENT
+    assert write(rdesc(), stride=128) == E.UQ_ERR_INVALID_ARGUMENT
+    assert write(rdesc(), pt=FAKE, num_seqs=1, mpps=0) == E.UQ_ERR_INVALID_ARGUMENT
+    assert write(rdesc(), num_tokens=0) == E.UQ_OK
+
+    def rdecode(d, **kw):
+        a = dict(q=FAKE, qdt=0, B=2, Hq=4, mpps=4, ctx=FAKE, maxctx=64, scale=0.1, part=0, ws=FAKE, wsb=1 << 30,
+                 out=FAKE, odt=0)
+        a.update(kw)
+        return lib.uq_ref_decode_attention(ctypes.byref(d), a["q"], a["qdt"], a["B"], a["Hq"], FAKE, FAKE, a["mpps"],
+                                           a["ctx"], a["maxctx"], a["scale"], a["part"], a["ws"], a["wsb"],
+                                           a["out"], a["odt"], None)
+
+    assert rdecode(rdesc(), qdt=3) == E.UQ_ERR_UNSUPPORTED          # the query is never pre-cast here
+    assert rdecode(rdesc(), Hq=3) == E.UQ_ERR_INVALID_ARGUMENT
+    assert rdecode(rdesc(), maxctx=65) == E.UQ_ERR_INVALID_ARGUMENT
+    assert rdecode(rdesc(), part=16) == E.UQ_ERR_INVALID_ARGUMENT
+    assert rdecode(rdesc(), scale=0.0) == E.UQ_ERR_INVALID_ARGUMENT
+    assert rdecode(rdesc(), wsb=16) == E.UQ_ERR_WORKSPACE_TOO_SMALL
+    assert rdecode(rdesc(format=5)) == E.UQ_ERR_UNSUPPORTED
+    assert rdecode(rdesc(), out=None) == E.UQ_ERR_INVALID_ARGUMENT
+    # the same workspace formula as the FP4 cache
+    from paper_2606_20474_amd.uq import CacheDesc
+    d4 = CacheDesc(num_kv_heads=2, num_pages=10)
+    assert uq.ref_workspace_bytes(uq.RefCacheDesc(2, 10, "bf16"), 32, 64, 32768, 0) == \
+        uq.workspace_bytes(d4, 32, 64, 32768, 0)
+    assert lib.uq_ref_decode_merge(ctypes.byref(rdesc()), 2, 4, None, 64, 0, FAKE, 1 << 30, FAKE, 0, None) == \
+        E.UQ_ERR_INVALID_ARGUMENT
