@@ -1,12 +1,13 @@
 """Decode-step benchmark of the FP4 KV path on one MI355X.
 
-One step is the whole hot path for one decode token per sequence:
-  1. uq_quantize_kv writes the step's new K/V token of every sequence into
-     the FP4 cache (Algorithm 1, "Write"), at the last position of its
-     context;
-  2. uq_decode_partials + uq_decode_merge (the two launches of
-     uq_decode_attention) run decode attention over the full contexts
-     (Algorithm 1, "Decode").
+One step is the whole hot path for one decode token per sequence, the two
+launches of uq_decode_step:
+  1. uq_decode_step_partials writes the step's new K/V token of every
+     sequence into the FP4 cache at the last position of its context
+     (Algorithm 1, "Write"; done by the block that reads that page) and runs
+     the partition kernel of decode attention over the full contexts
+     (Algorithm 1, "Decode");
+  2. uq_decode_merge merges the partitions.
 Inputs are resident in HBM before the timed region.  The default workload is
 the Qwen3-235B-like layer: 64 query heads, 4 KV heads, head_dim 128, batch
 32, every context 32768, random page table.  ``value`` is KV tokens/s =
@@ -124,9 +125,10 @@ def timed(step, steps, warmup, stream):
     return t_start.elapsed_time(t_end) / steps, float(np.mean([a.elapsed_time(b) for a, b in evs]))
 
 
-def comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, new_slots, args, dev, stream):
-    """The same step (append one token per sequence, partition launch,
-    merge) over a plain FP8 or BF16 cache holding the same K/V."""
+def comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, args, dev, stream):
+    """The same step (uq_ref_decode_step: the new token of every sequence
+    written by the partition launch, then the merge) over a plain FP8 or
+    BF16 cache holding the same K/V."""
     import torch
     desc = uq.RefCacheDesc(num_kv_heads=wl.num_kv_heads, num_pages=wl.num_pages, fmt=fmt, k_scale=REF_SCALE,
                            v_scale=REF_SCALE)
@@ -140,10 +142,10 @@ def comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, new_slots, args, dev
     scale = 1 / math.sqrt(128)
 
     def step(ev_a=None, ev_b=None):
-        uq.ref_write_kv(desc, k_new, v_new, new_slots, cache)
         if ev_a is not None:
             ev_a.record(stream)
-        uq.ref_decode_partials(desc, q, cache, pt, ctx, wl.max_context, scale, part, ws, out)
+        uq.ref_decode_step(desc, q, k_new, v_new, cache, pt, ctx, wl.max_context, scale, part, ws, out,
+                           partials_only=True)
         if ev_b is not None:
             ev_b.record(stream)
         uq.ref_decode_merge(desc, wl.batch, wl.num_q_heads, ctx, wl.max_context, part, ws, out)
@@ -213,21 +215,18 @@ def main():
     ctx = torch.as_tensor(wl.context_lens, device=dev)
     ws = uq.alloc_workspace(desc, wl.batch, wl.num_q_heads, wl.max_context, part, dev)
     out = torch.empty((wl.batch, wl.num_q_heads, 128), dtype=torch.float32, device=dev)
-    # the step's new token of every sequence, written at its last position
+    # the step's new token of every sequence (written at its last position by the step)
     g = torch.Generator(device=dev).manual_seed(12345)
     k_new = torch.randn((wl.batch, wl.num_kv_heads, 128), generator=g, device=dev)
     v_new = torch.randn((wl.batch, wl.num_kv_heads, 128), generator=g, device=dev)
-    last = wl.context_lens.astype(np.int64) - 1
-    new_slots = torch.as_tensor(wl.page_table[np.arange(wl.batch), last // 16].astype(np.int64) * 16 + last % 16,
-                                device=dev)
     scale = 1 / math.sqrt(128)
     stream = torch.cuda.current_stream()
 
     def step(ev_a=None, ev_b=None):
-        uq.quantize_kv(desc, k_new, v_new, new_slots, codes, scales)
         if ev_a is not None:
             ev_a.record(stream)
-        uq.decode_partials(desc, q, codes, scales, pt, ctx, wl.max_context, scale, part, ws, out)
+        uq.decode_step(desc, q, k_new, v_new, codes, scales, pt, ctx, wl.max_context, scale, part, ws, out,
+                       partials_only=True)
         if ev_b is not None:
             ev_b.record(stream)
         uq.decode_merge(desc, wl.batch, wl.num_q_heads, ctx, wl.max_context, part, ws, out)
@@ -272,7 +271,7 @@ def main():
         for fmt in fmts:
             if fmt not in REF_BYTES_PER_TOKEN_HEAD:
                 sys.exit(f"unknown comparator {fmt!r}")
-            comp[f"{fmt}_kv"] = comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, new_slots, args, dev, stream)
+            comp[f"{fmt}_kv"] = comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, args, dev, stream)
             comp[f"fp4_over_{fmt}_tokens_per_s"] = result["value"] / comp[f"{fmt}_kv"]["tokens_per_s"]
         result["comparators"] = comp
     if not args.no_cpu_baseline:

@@ -199,6 +199,42 @@ uq_status uq_decode_partials(const uq_cache_desc *desc, const void *q, uq_dtype 
                              int32_t max_context, float softmax_scale, int32_t partition_tokens,
                              void *workspace, size_t workspace_bytes, void *out, uq_dtype out_dtype,
                              void *stream);
+
+/*
+ * uq_decode_step -- one decode step of Algorithm 1 in one call: write each
+ * sequence's new K and V token into the FP4 cache ("Write"), then decode
+ * attention over the context that now ends with it ("Decode").
+ *   k_new, v_new : [batch][num_kv_heads][128] rows of new_dtype (F32, BF16
+ *                  or F16), 16-byte aligned.  Sequence b's token is
+ *                  quantised exactly as uq_quantize_kv does and stored at
+ *                  position len_b - 1, len_b = min(context_lens[b],
+ *                  max_context), through page_table; it is part of the
+ *                  attended context.  A sequence with len_b <= 0 writes
+ *                  nothing.  The page holding position len_b - 1 must not
+ *                  be a page another sequence of the call reads.
+ *   kv_codes, kv_scales : the pools, read and (one token per sequence and
+ *                  kv head) written.
+ * The write is done inside the partition kernel by the block that reads
+ * that page, so the step costs the launches of uq_decode_attention.
+ * Every other argument, the output and the errors are those of
+ * uq_decode_attention (plus INVALID_ARGUMENT for null or misaligned
+ * k_new/v_new and UNSUPPORTED for other new_dtype).
+ * uq_decode_step_partials is its first launch; uq_decode_merge with the
+ * same arguments finishes it.
+ */
+uq_status uq_decode_step(const uq_cache_desc *desc, const void *q, uq_dtype q_dtype, const void *k_new,
+                         const void *v_new, uq_dtype new_dtype, int32_t batch, int32_t num_q_heads,
+                         uint8_t *kv_codes, uint8_t *kv_scales, const int32_t *page_table, int32_t max_pages_per_seq,
+                         const int32_t *context_lens, int32_t max_context, float softmax_scale,
+                         int32_t partition_tokens, void *workspace, size_t workspace_bytes, void *out,
+                         uq_dtype out_dtype, void *stream);
+uq_status uq_decode_step_partials(const uq_cache_desc *desc, const void *q, uq_dtype q_dtype, const void *k_new,
+                                  const void *v_new, uq_dtype new_dtype, int32_t batch, int32_t num_q_heads,
+                                  uint8_t *kv_codes, uint8_t *kv_scales, const int32_t *page_table,
+                                  int32_t max_pages_per_seq, const int32_t *context_lens, int32_t max_context,
+                                  float softmax_scale, int32_t partition_tokens, void *workspace,
+                                  size_t workspace_bytes, void *out, uq_dtype out_dtype, void *stream);
+
 uq_status uq_decode_merge(const uq_cache_desc *desc, int32_t batch, int32_t num_q_heads,
                           const int32_t *context_lens, int32_t max_context, int32_t partition_tokens,
                           const void *workspace, size_t workspace_bytes, void *out, uq_dtype out_dtype,
@@ -277,6 +313,20 @@ uq_status uq_ref_decode_partials(const uq_ref_cache_desc *desc, const void *q, u
                                  int32_t max_pages_per_seq, const int32_t *context_lens, int32_t max_context,
                                  float softmax_scale, int32_t partition_tokens, void *workspace,
                                  size_t workspace_bytes, void *out, uq_dtype out_dtype, void *stream);
+/* The decode step over a comparison cache: uq_decode_step with the token
+ * stored as uq_ref_write_kv stores it. */
+uq_status uq_ref_decode_step(const uq_ref_cache_desc *desc, const void *q, uq_dtype q_dtype, const void *k_new,
+                             const void *v_new, uq_dtype new_dtype, int32_t batch, int32_t num_q_heads,
+                             uint8_t *cache, const int32_t *page_table, int32_t max_pages_per_seq,
+                             const int32_t *context_lens, int32_t max_context, float softmax_scale,
+                             int32_t partition_tokens, void *workspace, size_t workspace_bytes, void *out,
+                             uq_dtype out_dtype, void *stream);
+uq_status uq_ref_decode_step_partials(const uq_ref_cache_desc *desc, const void *q, uq_dtype q_dtype,
+                                      const void *k_new, const void *v_new, uq_dtype new_dtype, int32_t batch,
+                                      int32_t num_q_heads, uint8_t *cache, const int32_t *page_table,
+                                      int32_t max_pages_per_seq, const int32_t *context_lens, int32_t max_context,
+                                      float softmax_scale, int32_t partition_tokens, void *workspace,
+                                      size_t workspace_bytes, void *out, uq_dtype out_dtype, void *stream);
 uq_status uq_ref_decode_merge(const uq_ref_cache_desc *desc, int32_t batch, int32_t num_q_heads,
                               const int32_t *context_lens, int32_t max_context, int32_t partition_tokens,
                               const void *workspace, size_t workspace_bytes, void *out, uq_dtype out_dtype,

@@ -79,8 +79,14 @@ uq_status make_decode_params(const uq_cache_desc* desc, const void* q, uq_dtype 
     if (np > 0x7FFFFFFF) return UQ_ERR_UNSUPPORTED;
     p.q = q;
     p.q_dtype = int32_t(q_dtype);
-    p.codes = kv_codes;
-    p.scales = kv_scales;
+    p.codes = const_cast<uint8_t*>(kv_codes);     // written only by the decode-step calls
+    p.scales = const_cast<uint8_t*>(kv_scales);
+    p.k_new = nullptr;
+    p.v_new = nullptr;
+    p.new_dtype = 0;
+    p.c = desc->c;
+    p.k_scale = 1.0f;
+    p.v_scale = 1.0f;
     p.page_table = page_table;
     p.max_pages_per_seq = max_pages_per_seq;
     p.context_lens = context_lens;
@@ -242,6 +248,17 @@ static uq_status decode_setup(const uq_cache_desc* desc, const void* q, uq_dtype
                               out, out_dtype, p);
 }
 
+// The new-token arguments of the decode-step calls.
+static uq_status step_args(const void* k_new, const void* v_new, uq_dtype new_dtype, uq::DecodeParams& p) {
+    if (k_new == nullptr || v_new == nullptr) return UQ_ERR_INVALID_ARGUMENT;
+    if (new_dtype != UQ_F32 && new_dtype != UQ_BF16 && new_dtype != UQ_F16) return UQ_ERR_UNSUPPORTED;
+    if (!aligned16(k_new) || !aligned16(v_new)) return UQ_ERR_INVALID_ARGUMENT;
+    p.k_new = k_new;
+    p.v_new = v_new;
+    p.new_dtype = int32_t(new_dtype);
+    return UQ_OK;
+}
+
 uq_status uq_decode_attention(const uq_cache_desc* desc, const void* q, uq_dtype q_dtype, int32_t batch,
                               int32_t num_q_heads, const uint8_t* kv_codes, const uint8_t* kv_scales,
                               const int32_t* page_table, int32_t max_pages_per_seq, const int32_t* context_lens,
@@ -266,6 +283,40 @@ uq_status uq_decode_partials(const uq_cache_desc* desc, const void* q, uq_dtype 
     uq_status s = decode_setup(desc, q, q_dtype, batch, num_q_heads, kv_codes, kv_scales, page_table,
                                max_pages_per_seq, context_lens, max_context, softmax_scale, partition_tokens, workspace,
                                workspace_bytes, out, out_dtype, p);
+    if (s != UQ_OK) return s;
+    return from_hip(uq::launch_decode_partials(p, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uq_decode_step(const uq_cache_desc* desc, const void* q, uq_dtype q_dtype, const void* k_new,
+                         const void* v_new, uq_dtype new_dtype, int32_t batch, int32_t num_q_heads,
+                         uint8_t* kv_codes, uint8_t* kv_scales, const int32_t* page_table, int32_t max_pages_per_seq,
+                         const int32_t* context_lens, int32_t max_context, float softmax_scale,
+                         int32_t partition_tokens, void* workspace, size_t workspace_bytes, void* out,
+                         uq_dtype out_dtype, void* stream) {
+    uq::DecodeParams p;
+    uq_status s = decode_setup(desc, q, q_dtype, batch, num_q_heads, kv_codes, kv_scales, page_table,
+                               max_pages_per_seq, context_lens, max_context, softmax_scale, partition_tokens, workspace,
+                               workspace_bytes, out, out_dtype, p);
+    if (s != UQ_OK) return s;
+    s = step_args(k_new, v_new, new_dtype, p);
+    if (s != UQ_OK) return s;
+    s = from_hip(uq::launch_decode_partials(p, static_cast<hipStream_t>(stream)));
+    if (s != UQ_OK) return s;
+    return from_hip(uq::launch_decode_merge(p, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uq_decode_step_partials(const uq_cache_desc* desc, const void* q, uq_dtype q_dtype, const void* k_new,
+                                  const void* v_new, uq_dtype new_dtype, int32_t batch, int32_t num_q_heads,
+                                  uint8_t* kv_codes, uint8_t* kv_scales, const int32_t* page_table,
+                                  int32_t max_pages_per_seq, const int32_t* context_lens, int32_t max_context,
+                                  float softmax_scale, int32_t partition_tokens, void* workspace,
+                                  size_t workspace_bytes, void* out, uq_dtype out_dtype, void* stream) {
+    uq::DecodeParams p;
+    uq_status s = decode_setup(desc, q, q_dtype, batch, num_q_heads, kv_codes, kv_scales, page_table,
+                               max_pages_per_seq, context_lens, max_context, softmax_scale, partition_tokens, workspace,
+                               workspace_bytes, out, out_dtype, p);
+    if (s != UQ_OK) return s;
+    s = step_args(k_new, v_new, new_dtype, p);
     if (s != UQ_OK) return s;
     return from_hip(uq::launch_decode_partials(p, static_cast<hipStream_t>(stream)));
 }
@@ -350,6 +401,8 @@ static uq_status ref_decode_setup(const uq_ref_cache_desc* desc, const void* q, 
     if (desc->format == UQ_REF_FP8_E4M3) {
         p.scale_log2 = float(double(softmax_scale) * double(desc->k_scale) * 1.4426950408889634);
         p.out_scale = desc->v_scale;
+        p.k_scale = desc->k_scale;
+        p.v_scale = desc->v_scale;
         if (!(isfinite(p.scale_log2) && p.scale_log2 > 0.0f)) return UQ_ERR_INVALID_ARGUMENT;
     }
     return UQ_OK;
@@ -379,6 +432,40 @@ uq_status uq_ref_decode_partials(const uq_ref_cache_desc* desc, const void* q, u
     uq_status s = ref_decode_setup(desc, q, q_dtype, batch, num_q_heads, cache, page_table, max_pages_per_seq,
                                    context_lens, max_context, softmax_scale, partition_tokens, workspace,
                                    workspace_bytes, out, out_dtype, p);
+    if (s != UQ_OK) return s;
+    return from_hip(uq::launch_decode_partials(p, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uq_ref_decode_step(const uq_ref_cache_desc* desc, const void* q, uq_dtype q_dtype, const void* k_new,
+                             const void* v_new, uq_dtype new_dtype, int32_t batch, int32_t num_q_heads,
+                             uint8_t* cache, const int32_t* page_table, int32_t max_pages_per_seq,
+                             const int32_t* context_lens, int32_t max_context, float softmax_scale,
+                             int32_t partition_tokens, void* workspace, size_t workspace_bytes, void* out,
+                             uq_dtype out_dtype, void* stream) {
+    uq::DecodeParams p;
+    uq_status s = ref_decode_setup(desc, q, q_dtype, batch, num_q_heads, cache, page_table, max_pages_per_seq,
+                                   context_lens, max_context, softmax_scale, partition_tokens, workspace,
+                                   workspace_bytes, out, out_dtype, p);
+    if (s != UQ_OK) return s;
+    s = step_args(k_new, v_new, new_dtype, p);
+    if (s != UQ_OK) return s;
+    s = from_hip(uq::launch_decode_partials(p, static_cast<hipStream_t>(stream)));
+    if (s != UQ_OK) return s;
+    return from_hip(uq::launch_decode_merge(p, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uq_ref_decode_step_partials(const uq_ref_cache_desc* desc, const void* q, uq_dtype q_dtype,
+                                      const void* k_new, const void* v_new, uq_dtype new_dtype, int32_t batch,
+                                      int32_t num_q_heads, uint8_t* cache, const int32_t* page_table,
+                                      int32_t max_pages_per_seq, const int32_t* context_lens, int32_t max_context,
+                                      float softmax_scale, int32_t partition_tokens, void* workspace,
+                                      size_t workspace_bytes, void* out, uq_dtype out_dtype, void* stream) {
+    uq::DecodeParams p;
+    uq_status s = ref_decode_setup(desc, q, q_dtype, batch, num_q_heads, cache, page_table, max_pages_per_seq,
+                                   context_lens, max_context, softmax_scale, partition_tokens, workspace,
+                                   workspace_bytes, out, out_dtype, p);
+    if (s != UQ_OK) return s;
+    s = step_args(k_new, v_new, new_dtype, p);
     if (s != UQ_OK) return s;
     return from_hip(uq::launch_decode_partials(p, static_cast<hipStream_t>(stream)));
 }

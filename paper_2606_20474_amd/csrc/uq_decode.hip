@@ -54,6 +54,7 @@
 namespace uq {
 
 constexpr float kLazyRescale = 8.0f;   // log2 units
+constexpr int kWaitVmcnt0 = 0x0F70;    // s_waitcnt vmcnt(0) expcnt(7) lgkmcnt(15) (gfx9 encoding)
 constexpr int kAccStride = 129;        // LDS row stride (floats) of the merge buffer
 
 // Per-format constants.  kTile: bytes of one (page, kv head) K or V tile;
@@ -126,29 +127,6 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
 
 __device__ __forceinline__ float bf16_lo_f32(uint32_t w) { return bits_f32(w << 16); }
 __device__ __forceinline__ float bf16_hi_f32(uint32_t w) { return bits_f32(w & 0xFFFF0000u); }
-
-template <int DT>
-__device__ __forceinline__ void load_q8(const void* q, int64_t elem, float (&x)[8]) {
-    if constexpr (DT == 0) {
-        const float4* p = reinterpret_cast<const float4*>(static_cast<const float*>(q) + elem);
-        float4 a = p[0], b = p[1];
-        x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
-        x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
-    } else {
-        const uint4 w = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(q) + elem);
-        const uint32_t d[4] = {w.x, w.y, w.z, w.w};
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            if constexpr (DT == 1) {
-                x[2 * i] = bits_f32(d[i] << 16);
-                x[2 * i + 1] = bits_f32(d[i] & 0xFFFF0000u);
-            } else {
-                x[2 * i] = float(__builtin_bit_cast(_Float16, uint16_t(d[i] & 0xFFFFu)));
-                x[2 * i + 1] = float(__builtin_bit_cast(_Float16, uint16_t(d[i] >> 16)));
-            }
-        }
-    }
-}
 
 // Page ids of one wave, 64 at a time: lane j holds the id of the wave's
 // page 2*(32*chunk + j/2) + j%2 counted in its own iteration order
@@ -418,6 +396,16 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
     }
     const int end = (start + p.partition_tokens) < ctx ? (start + p.partition_tokens) : ctx;
     const int np_b = (ctx + p.partition_tokens - 1) / p.partition_tokens;
+    // Decode step: the block whose partition holds the last position writes
+    // the sequence's new token there.  The wave that will read that page
+    // encodes the token in its prologue, stores it to the pools without
+    // waiting, and patches its staged copy of the page in LDS once the copy
+    // has landed, so no wave waits for the store.  Only this block reads the
+    // page for this kv head (partitions are whole pages).
+    const int pos_new = ctx - 1;
+    const int it_new = (pos_new - start) >> 5;                       // iteration holding the token
+    const bool append = p.k_new != nullptr && pos_new >= start && wave == it_new % W;   // wave-uniform
+    const int k_new_local = it_new / W;                              // that wave's local iteration
 
     __shared__ __attribute__((aligned(16))) uint8_t smem[W * ring_bytes<F>()];
     __shared__ __attribute__((aligned(16))) uint8_t q_lds[F == kBf16 ? 4 * 64 * 16 : 64 * 32];
@@ -442,12 +430,29 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
                 qw[h][0] = w.x;
                 qw[h][1] = w.y;
             } else if (p.q_dtype == 0) {
-                load_q8<0>(p.q, elem, qx[h]);
+                load_x8<0>(p.q, elem, qx[h]);
             } else if (p.q_dtype == 1) {
-                load_q8<1>(p.q, elem, qx[h]);
+                load_x8<1>(p.q, elem, qx[h]);
             } else {
-                load_q8<2>(p.q, elem, qx[h]);
+                load_x8<2>(p.q, elem, qx[h]);
             }
+        }
+    }
+
+    float xk[8], xv[8];   // the new token's K and V (decode step, lanes 0..15 of the owning wave)
+    int32_t page_new = -1;
+    if (append && lane < 16) {
+        page_new = p.page_table[int64_t(b) * p.max_pages_per_seq + (pos_new >> 4)];
+        const int64_t elem = (int64_t(b) * p.num_kv_heads + hk) * kHeadDim + 8 * lane;
+        if (p.new_dtype == 0) {
+            load_x8<0>(p.k_new, elem, xk);
+            load_x8<0>(p.v_new, elem, xv);
+        } else if (p.new_dtype == 1) {
+            load_x8<1>(p.k_new, elem, xk);
+            load_x8<1>(p.v_new, elem, xv);
+        } else {
+            load_x8<2>(p.k_new, elem, xk);
+            load_x8<2>(p.v_new, elem, xv);
         }
     }
 
@@ -468,6 +473,12 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
     if (n_local > 0) {
         ids = load_page_ids<W>(pt_row, first_page, n_pages, wave, 0, lane, p.num_pages);
         if (n_local > 32) ids_next = load_page_ids<W>(pt_row, first_page, n_pages, wave, 1, lane, p.num_pages);
+    }
+    // The query, the new token and the page ids are in registers before the
+    // first page copies are issued (one wait for all of them, so that the
+    // query transform below overlaps the copies instead of waiting for them).
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    if (n_local > 0) {
         for (int s = 0; s < 2 && s < n_local; ++s) {
             const int64_t id0 = __builtin_amdgcn_readlane(ids, 2 * s);
             const int64_t id1 = __builtin_amdgcn_readlane(ids, 2 * s + 1);
@@ -521,6 +532,15 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
         qop.q = v8i{int(a.x), int(a.y), int(a.z), int(a.w), int(c.x), int(c.y), int(c.z), int(c.w)};
     }
 
+    // Decode step, owning wave: encode and store the new token while its
+    // first two stages are in flight (the store is not waited for).
+    TokenBits<F> tok{};
+    if (append && lane < 16) {
+        tok = encode_token<F>(xk, xv, lane, p.c, p.rotate_v != 0, p.k_scale, p.v_scale);
+        if (page_new >= 0 && int64_t(page_new) < p.num_pages)
+            store_token<F>(p.codes, p.scales, (int64_t(page_new) * p.num_kv_heads + hk) * 2, pos_new & 15, lane, tok);
+    }
+
     const float sl2 = p.scale_log2;
     float m_run = -__builtin_inff();
     float l_run = 0.0f;
@@ -533,6 +553,13 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
         if (k + 1 < n_local) wait_vmem<dma_per_stage<F>()>();
         else wait_vmem<0>();
         const uint32_t slot = uint32_t(k & 1);
+        if (append && k == k_new_local && lane < 16) {
+            // the staged page holds what the pools held before this step
+            lds_u8* st0 = (lds_u8*)(ring + slot * kStage);
+            const int pg = ((pos_new - start) >> 4) & 1;
+            place_token<F>(st0 + pg * 2 * Fmt<F>::kTile, st0 + 4 * Fmt<F>::kTile + pg * Fmt<F>::kScaleBlock,
+                           pos_new & 15, lane, tok);
+        }
         StageRegs<F> c;
         stage_read(c, ring_addr + slot * kStage, lane);
         if (k + 2 < n_local) {

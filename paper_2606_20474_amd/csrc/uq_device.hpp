@@ -8,10 +8,14 @@
 //                     section "Constant-Optimized Scaling").
 //  * e2m1_code        nearest E2M1 level of x / 2^E, ties to the even code.
 //  * e4m3_byte        OCP e4m3fn, round to nearest even, saturating.
+//  * load_x8, encode_token, place_token, store_token
+//                     one token's K/V from the input rows into a cache tile.
 #pragma once
 
 #include <hip/hip_runtime.h>
 #include <stdint.h>
+
+#include "uq_internal.hpp"
 
 namespace uq {
 
@@ -119,6 +123,158 @@ __device__ __forceinline__ uint32_t e4m3_byte(float x) {
         mag = mag > 0x7Eu ? 0x7Eu : mag;
     }
     return sign | mag;
+}
+
+// Eight consecutive channels starting at element `elem` as fp32 (DT: 0 f32,
+// 1 bf16, 2 f16; 16-byte aligned).
+template <int DT>
+__device__ __forceinline__ void load_x8(const void* base, int64_t elem, float (&x)[8]) {
+    if constexpr (DT == 0) {  // f32
+        const float4* p = reinterpret_cast<const float4*>(static_cast<const float*>(base) + elem);
+        float4 a = p[0], b = p[1];
+        x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+        x[4] = b.x; x[5] = b.y; x[6] = b.z; x[7] = b.w;
+    } else {  // bf16 (1) or f16 (2): 16 bytes
+        const uint4 w = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(base) + elem);
+        const uint32_t d[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if constexpr (DT == 1) {
+                x[2 * i] = bits_f32(d[i] << 16);
+                x[2 * i + 1] = bits_f32(d[i] & 0xFFFF0000u);
+            } else {
+                x[2 * i] = float(__builtin_bit_cast(_Float16, uint16_t(d[i] & 0xFFFFu)));
+                x[2 * i + 1] = float(__builtin_bit_cast(_Float16, uint16_t(d[i] >> 16)));
+            }
+        }
+    }
+}
+
+// Quantise the 8 channels this lane holds; returns the packed codes and
+// (in the first lane of every 4-lane group) the scale byte.
+__device__ __forceinline__ uint32_t quantize_x8(float (&x)[8], int L, float c, bool rotate, uint32_t& scale_byte) {
+    if (rotate) wht128_x8(x, L);
+    float m = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) m = __builtin_fmaxf(m, __builtin_fabsf(x[i]));
+    m = __builtin_fmaxf(m, __shfl_xor(m, 1, 16));
+    m = __builtin_fmaxf(m, __shfl_xor(m, 2, 16));
+    const int E = ue8m0_exponent(m, c);
+    scale_byte = uint32_t(E + 127);
+    uint32_t w = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) w |= e2m1_code(x[i], E) << (4 * i);
+    return w;
+}
+
+// One token's K and V as this lane (8 channels 8*lane16..+7 of each)
+// stores them, per cache format:
+//   kFp4   E2M1 codes (8 per dword) of the rotated K and (rotate_v) V, and
+//          the UE8M0 byte of the lane's 32-channel group;
+//   kFp8   e4m3(x / scale) bytes, 8 per uint2;
+//   kBf16  round-to-nearest-even BF16, 8 per uint4.
+template <int F> struct TokenBits;
+template <> struct TokenBits<kFp4> { uint32_t k, v, ks, vs; };
+template <> struct TokenBits<kFp8> { uint2 k, v; };
+template <> struct TokenBits<kBf16> { uint4 k, v; };
+
+// Encode (all 16 lanes of the vector take part: the FP4 rotation and group
+// maximum exchange values between them).
+template <int F>
+__device__ __forceinline__ TokenBits<F> encode_token(float (&xk)[8], float (&xv)[8], int lane16, float c,
+                                                     bool rotate_v, float k_scale, float v_scale) {
+    TokenBits<F> t;
+    if constexpr (F == kFp4) {
+        t.k = quantize_x8(xk, lane16, c, true, t.ks);
+        t.v = quantize_x8(xv, lane16, c, rotate_v, t.vs);
+    } else if constexpr (F == kFp8) {
+        uint32_t kw[2] = {0u, 0u}, vw[2] = {0u, 0u};
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            kw[i >> 2] |= e4m3_byte(xk[i] / k_scale) << (8 * (i & 3));
+            vw[i >> 2] |= e4m3_byte(xv[i] / v_scale) << (8 * (i & 3));
+        }
+        t.k = make_uint2(kw[0], kw[1]);
+        t.v = make_uint2(vw[0], vw[1]);
+    } else {
+        uint32_t kw[4], vw[4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const v2bf hk = {__bf16(xk[2 * i]), __bf16(xk[2 * i + 1])};
+            const v2bf hv = {__bf16(xv[2 * i]), __bf16(xv[2 * i + 1])};
+            kw[i] = __builtin_bit_cast(uint32_t, hk);
+            vw[i] = __builtin_bit_cast(uint32_t, hv);
+        }
+        t.k = uint4{kw[0], kw[1], kw[2], kw[3]};
+        t.v = uint4{vw[0], vw[1], vw[2], vw[3]};
+    }
+    return t;
+}
+
+// Bytes of one (page, head) K or V tile per format.
+template <int F> constexpr int tile_bytes() { return F == kFp4 ? kTileCodes : F == kFp8 ? 2048 : 4096; }
+
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
+
+// Stores of 1, 4, 8 and 16 bytes at base + off, to global memory or LDS.
+__device__ __forceinline__ void st(uint8_t* base, int off, uint8_t x) { base[off] = x; }
+__device__ __forceinline__ void st(uint8_t* base, int off, uint32_t x) { *reinterpret_cast<uint32_t*>(base + off) = x; }
+__device__ __forceinline__ void st(uint8_t* base, int off, uint2 x) { *reinterpret_cast<uint2*>(base + off) = x; }
+__device__ __forceinline__ void st(uint8_t* base, int off, uint4 x) { *reinterpret_cast<uint4*>(base + off) = x; }
+__device__ __forceinline__ void st(lds_u8* base, int off, uint8_t x) { base[off] = x; }
+__device__ __forceinline__ void st(lds_u8* base, int off, uint32_t x) {
+    *reinterpret_cast<__attribute__((address_space(3))) uint32_t*>(base + off) = x;
+}
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ void st(lds_u8* base, int off, uint2 x) {
+    *reinterpret_cast<__attribute__((address_space(3))) u32x2*>(base + off) = u32x2{x.x, x.y};
+}
+__device__ __forceinline__ void st(lds_u8* base, int off, uint4 x) {
+    *reinterpret_cast<__attribute__((address_space(3))) u32x4*>(base + off) = u32x4{x.x, x.y, x.z, x.w};
+}
+
+// Place this lane's part of token `off` into a (page, head) tile pair
+// (`tiles`: the K tile, the V tile follows it; `scales`: the pair's 128
+// scale bytes, K then V, FP4 only).  Layouts, t = token, c = channel:
+//   kFp4   K codes [c/32][t][16 B], nibble order = channel order;
+//          V codes [t/4][c/8][t%4][4 B]; scales [K|V][c/32][t].
+//   kFp8   K [(c%64)/16][t][32 B]: bytes 0..15 = channels 16g..16g+15,
+//          16..31 = channels 64+16g..64+16g+15 (the FP8 operand order of
+//          the 16x16x128 MFMA); V [t/4][c/8][t%4][8 B].
+//   kBf16  K [c/8][t][16 B]; V [t/4][c/8][t%4][16 B].
+// PTR is a global or an LDS byte pointer: the decode kernel also patches its
+// staged copy of a page with a token it has just written.
+template <int F, class PTR>
+__device__ __forceinline__ void place_token(PTR tiles, PTR scales, int off, int lane16, const TokenBits<F>& t) {
+    constexpr int T = tile_bytes<F>();
+    if constexpr (F == kFp4) {
+        const int g = lane16 >> 2;
+        st(tiles, (g * kPage + off) * 16 + 4 * (lane16 & 3), t.k);
+        st(tiles, T + ((off >> 2) * 16 + lane16) * 16 + (off & 3) * 4, t.v);
+        if ((lane16 & 3) == 0) {
+            st(scales, g * kPage + off, uint8_t(t.ks));
+            st(scales, kTileScales + g * kPage + off, uint8_t(t.vs));
+        }
+    } else if constexpr (F == kFp8) {
+        const int c0 = 8 * lane16;
+        const int g = (c0 & 63) >> 4;
+        const int e0 = (c0 & 15) + (c0 >= 64 ? 16 : 0);
+        st(tiles, (g * kPage + off) * 32 + e0, t.k);
+        st(tiles, T + ((off >> 2) * 16 + lane16) * 32 + (off & 3) * 8, t.v);
+    } else {
+        st(tiles, (lane16 * kPage + off) * 16, t.k);
+        st(tiles, T + ((off >> 2) * 16 + lane16) * 64 + (off & 3) * 16, t.v);
+    }
+}
+
+// Global-memory write of one token into the cache pools (tile = K tile index
+// of (page, head); FP4 scales at tile * 64).
+template <int F>
+__device__ __forceinline__ void store_token(uint8_t* codes, uint8_t* scales, int64_t tile, int off, int lane16,
+                                            const TokenBits<F>& t) {
+    uint8_t* sc = F == kFp4 ? scales + tile * kTileScales : nullptr;
+    place_token<F>(codes + tile * tile_bytes<F>(), sc, off, lane16, t);
 }
 
 // Scale float 2^(byte-127) for the hardware conversions.  Byte 0 maps to

@@ -50,8 +50,15 @@ struct DecodeParams {
     float out_scale;           // V tensor scale (FP8 cache), else 1
     const void* q;             // [B][Hq][128], dtype q_dtype
     int32_t q_dtype;           // 0 f32, 1 bf16, 2 f16, 3 fp8 (prepared)
-    const uint8_t* codes;
-    const uint8_t* scales;
+    uint8_t* codes;            // written only by a decode step (k_new != nullptr)
+    uint8_t* scales;
+    // decode step: each sequence's new token, written at its last position
+    const void* k_new;         // [B][Hkv][128] or nullptr
+    const void* v_new;
+    int32_t new_dtype;         // 0 f32, 1 bf16, 2 f16
+    float c;                   // FP4 scale constant
+    float k_scale;             // FP8 cache: per-tensor scales of the writer
+    float v_scale;
     const int32_t* page_table;
     int32_t max_pages_per_seq;
     const int32_t* context_lens;

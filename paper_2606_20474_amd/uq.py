@@ -29,9 +29,10 @@ TILE_SCALES = 64
 # Every symbol include/uq.h declares.
 EXPORTS = (
     "uq_status_string", "uq_version", "uq_quantize_kv", "uq_prepare_query", "uq_decode_workspace_bytes",
-    "uq_default_partition", "uq_decode_attention", "uq_decode_partials", "uq_decode_merge",
-    "uq_ref_cache_bytes", "uq_ref_write_kv", "uq_ref_decode_workspace_bytes", "uq_ref_decode_attention",
-    "uq_ref_decode_partials", "uq_ref_decode_merge",
+    "uq_default_partition", "uq_decode_attention", "uq_decode_partials", "uq_decode_merge", "uq_decode_step",
+    "uq_decode_step_partials", "uq_ref_cache_bytes", "uq_ref_write_kv", "uq_ref_decode_workspace_bytes",
+    "uq_ref_decode_attention", "uq_ref_decode_partials", "uq_ref_decode_merge", "uq_ref_decode_step",
+    "uq_ref_decode_step_partials",
 )
 
 UQ_REF_FP8_E4M3, UQ_REF_BF16 = 1, 2
@@ -90,6 +91,10 @@ def _load():
     L.uq_decode_partials.restype = i32
     L.uq_decode_merge.argtypes = [D, i32, i32, vp, i32, i32, vp, sz, vp, i32, vp]
     L.uq_decode_merge.restype = i32
+    for name in ("uq_decode_step", "uq_decode_step_partials"):
+        fn = getattr(L, name)
+        fn.argtypes = [D, vp, i32, vp, vp, i32, i32, i32, vp, vp, vp, i32, vp, i32, f32, i32, vp, sz, vp, i32, vp]
+        fn.restype = i32
     R = ctypes.POINTER(uq_ref_cache_desc)
     L.uq_ref_cache_bytes.argtypes = [R]
     L.uq_ref_cache_bytes.restype = sz
@@ -103,6 +108,10 @@ def _load():
         fn.restype = i32
     L.uq_ref_decode_merge.argtypes = [R, i32, i32, vp, i32, i32, vp, sz, vp, i32, vp]
     L.uq_ref_decode_merge.restype = i32
+    for name in ("uq_ref_decode_step", "uq_ref_decode_step_partials"):
+        fn = getattr(L, name)
+        fn.argtypes = [R, vp, i32, vp, vp, i32, i32, i32, vp, vp, i32, vp, i32, f32, i32, vp, sz, vp, i32, vp]
+        fn.restype = i32
     return L
 
 
@@ -235,6 +244,28 @@ def decode_partials(desc: CacheDesc, q, codes, scales, page_table, context_lens,
     return out
 
 
+def decode_step(desc: CacheDesc, q, k_new, v_new, codes, scales, page_table, context_lens, max_context,
+                softmax_scale=None, partition_tokens=0, workspace=None, out=None, out_dtype=torch.float32,
+                q_dtype=None, stream=None, partials_only=False):
+    """Write each sequence's new token (k_new, v_new: [B, Hkv, 128]) at its
+    last position, then decode attention; q: [B, Hq, 128] -> out."""
+    B, Hq = q.shape[0], q.shape[1]
+    if softmax_scale is None:
+        softmax_scale = HEAD_DIM ** -0.5
+    if workspace is None:
+        workspace = alloc_workspace(desc, B, Hq, max_context, partition_tokens, q.device)
+    if out is None:
+        out = torch.empty((B, Hq, HEAD_DIM), dtype=out_dtype, device=q.device)
+    d = desc.c_struct()
+    qdt = _DT[q.dtype] if q_dtype is None else q_dtype
+    fn = lib.uq_decode_step_partials if partials_only else lib.uq_decode_step
+    st = fn(ctypes.byref(d), _ptr(q), qdt, _ptr(k_new), _ptr(v_new), _DT[k_new.dtype], B, Hq, _ptr(codes),
+            _ptr(scales), _ptr(page_table), page_table.shape[1], _ptr(context_lens), max_context, softmax_scale,
+            partition_tokens, _ptr(workspace), workspace.numel(), _ptr(out), _DT[out.dtype], _stream(stream))
+    _check(st, "uq_decode_step_partials" if partials_only else "uq_decode_step")
+    return out
+
+
 def decode_merge(desc: CacheDesc, batch, num_q_heads, context_lens, max_context, partition_tokens, workspace, out,
                  stream=None):
     """Second launch of decode_attention (merge of the partitions)."""
@@ -339,4 +370,23 @@ def ref_decode_merge(desc: RefCacheDesc, batch, num_q_heads, context_lens, max_c
                                  partition_tokens, _ptr(workspace), workspace.numel(), _ptr(out), _DT[out.dtype],
                                  _stream(stream))
     _check(st, "uq_ref_decode_merge")
+    return out
+
+
+def ref_decode_step(desc: RefCacheDesc, q, k_new, v_new, cache, page_table, context_lens, max_context,
+                    softmax_scale=None, partition_tokens=0, workspace=None, out=None, out_dtype=torch.float32,
+                    stream=None, partials_only=False):
+    B, Hq = q.shape[0], q.shape[1]
+    if softmax_scale is None:
+        softmax_scale = HEAD_DIM ** -0.5
+    if workspace is None:
+        workspace = ref_alloc_workspace(desc, B, Hq, max_context, partition_tokens, q.device)
+    if out is None:
+        out = torch.empty((B, Hq, HEAD_DIM), dtype=out_dtype, device=q.device)
+    d = desc.c_struct()
+    fn = lib.uq_ref_decode_step_partials if partials_only else lib.uq_ref_decode_step
+    st = fn(ctypes.byref(d), _ptr(q), _DT[q.dtype], _ptr(k_new), _ptr(v_new), _DT[k_new.dtype], B, Hq, _ptr(cache),
+            _ptr(page_table), page_table.shape[1], _ptr(context_lens), max_context, softmax_scale, partition_tokens,
+            _ptr(workspace), workspace.numel(), _ptr(out), _DT[out.dtype], _stream(stream))
+    _check(st, "uq_ref_decode_step_partials" if partials_only else "uq_ref_decode_step")
     return out

@@ -1,0 +1,161 @@
+"""The fused decode step (uq_decode_step / uq_ref_decode_step: write every
+sequence's new token at its last position, then decode attention) through
+the C ABI.
+
+It must leave the pools and produce the output bit for bit as the two calls
+it replaces (uq_quantize_kv or uq_ref_write_kv of the new tokens, then
+uq_decode_attention or uq_ref_decode_attention), which the other GPU tests
+hold to the oracle and to the CPU reference; the small FP4 case is also
+checked against the oracle directly.  Context lengths put the new token in
+the first stages of a wave (where the block holds back its first page
+copies until the token is stored), at page, stage and partition edges, and
+one context is empty.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2606_20474_amd import workloads
+
+pytestmark = pytest.mark.gpu
+
+SCALE = 1 / math.sqrt(128)
+CTX = [1, 17, 32, 33, 100, 257, 1000, 0]
+
+
+@pytest.fixture(scope="module")
+def uq():
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    from paper_2606_20474_amd import uq as mod
+    return mod
+
+
+def log(msg):
+    print(msg, flush=True)
+
+
+def new_tokens(wl, dev, dtype=torch.float32, seed=99):
+    g = torch.Generator(device=dev).manual_seed(seed)
+    k = torch.randn((wl.batch, wl.num_kv_heads, 128), generator=g, device=dev)
+    v = torch.randn((wl.batch, wl.num_kv_heads, 128), generator=g, device=dev)
+    return k.to(dtype), v.to(dtype)
+
+
+def last_slots(wl, dev):
+    ctx = wl.context_lens.astype(np.int64)
+    last = np.maximum(ctx - 1, 0)
+    slots = wl.page_table[np.arange(wl.batch), last // 16].astype(np.int64) * 16 + last % 16
+    return torch.as_tensor(np.where(ctx > 0, slots, -1), device=dev)
+
+
+class Cache:
+    """One cache of any of the three formats, filled with every stored token of the workload."""
+
+    def __init__(self, uq, fmt, wl, dev):
+        self.uq, self.fmt, self.wl = uq, fmt, wl
+        if fmt == "fp4":
+            self.desc = uq.CacheDesc(num_kv_heads=wl.num_kv_heads, num_pages=wl.num_pages, rotate_v=wl.rotate_v)
+            self.bufs = self.desc.alloc_pools(dev, fill=0x5A)
+        else:
+            self.desc = uq.RefCacheDesc(num_kv_heads=wl.num_kv_heads, num_pages=wl.num_pages, fmt=fmt, k_scale=0.3,
+                                        v_scale=0.3)
+            self.bufs = (self.desc.alloc_cache(dev, fill=0x5A),)
+        for key, lo, hi in wl.segments():
+            k, v = wl.kv(key, lo, hi, device=dev)
+            self.write(k, v, torch.as_tensor(wl.slots(key, lo, hi), device=dev))
+
+    def write(self, k, v, slots):
+        if self.fmt == "fp4":
+            self.uq.quantize_kv(self.desc, k, v, slots, *self.bufs)
+        else:
+            self.uq.ref_write_kv(self.desc, k, v, slots, *self.bufs)
+
+    def attend(self, q, pt, ctx, part):
+        if self.fmt == "fp4":
+            return self.uq.decode_attention(self.desc, q, *self.bufs, pt, ctx, self.wl.max_context, SCALE, part)
+        return self.uq.ref_decode_attention(self.desc, q, *self.bufs, pt, ctx, self.wl.max_context, SCALE, part)
+
+    def step(self, q, k_new, v_new, pt, ctx, part):
+        if self.fmt == "fp4":
+            return self.uq.decode_step(self.desc, q, k_new, v_new, *self.bufs, pt, ctx, self.wl.max_context, SCALE,
+                                       part)
+        return self.uq.ref_decode_step(self.desc, q, k_new, v_new, *self.bufs, pt, ctx, self.wl.max_context, SCALE,
+                                       part)
+
+    def bytes(self):
+        return [b.cpu().numpy() for b in self.bufs]
+
+
+def compare_step(uq, fmt, wl, dev, part, new_dtype=torch.float32):
+    q = wl.q.to(dev)
+    pt = torch.as_tensor(wl.page_table, device=dev)
+    ctx = torch.as_tensor(wl.context_lens, device=dev)
+    k_new, v_new = new_tokens(wl, dev, new_dtype)
+    two = Cache(uq, fmt, wl, dev)
+    two.write(k_new, v_new, last_slots(wl, dev))
+    out_two = two.attend(q, pt, ctx, part)
+    one = Cache(uq, fmt, wl, dev)
+    out_one = one.step(q, k_new, v_new, pt, ctx, part)
+    torch.cuda.synchronize()
+    for a, b in zip(one.bytes(), two.bytes()):
+        assert np.array_equal(a, b), f"{fmt}: pools differ"
+    assert torch.equal(out_one, out_two), f"{fmt}: outputs differ"
+    return out_one
+
+
+@pytest.mark.parametrize("fmt", ["fp4", "fp8", "bf16"])
+@pytest.mark.parametrize("partition", [0, 32, 64, 256])
+def test_step_equals_write_then_decode(uq, fmt, partition):
+    dev = torch.device("cuda:0")
+    wl = workloads.custom(8, 16, 2, CTX, seed=21, paging="random")
+    log(f"decode step {fmt} partition={partition}")
+    out = compare_step(uq, fmt, wl, dev, partition)
+    assert torch.all(out[7] == 0)
+
+
+@pytest.mark.parametrize("new_dtype", [torch.bfloat16, torch.float16])
+def test_step_new_token_dtypes(uq, new_dtype):
+    dev = torch.device("cuda:0")
+    wl = workloads.custom(3, 8, 1, [5, 48, 700], seed=22, paging="random", rotate_v=False)
+    log(f"decode step fp4 new tokens {new_dtype}")
+    compare_step(uq, "fp4", wl, dev, 0, new_dtype)
+
+
+def test_step_against_oracle(uq):
+    dev = torch.device("cuda:0")
+    wl = workloads.custom(8, 16, 2, CTX, seed=21, paging="random")
+    log("decode step fp4 vs oracle")
+    q = wl.q.to(dev)
+    pt = torch.as_tensor(wl.page_table, device=dev)
+    ctx = torch.as_tensor(wl.context_lens, device=dev)
+    k_new, v_new = new_tokens(wl, dev)
+    c = Cache(uq, "fp4", wl, dev)
+    out = c.step(q, k_new, v_new, pt, ctx, 64).cpu().numpy()
+    pools = oracle.alloc_pools(wl.num_pages, wl.num_kv_heads, fill=0x5A)
+    for key, lo, hi in wl.segments():
+        k, v = wl.kv(key, lo, hi, device=dev)
+        oracle.quantize_kv(k.cpu().numpy(), v.cpu().numpy(), wl.slots(key, lo, hi), wl.num_pages,
+                           rotate_v=wl.rotate_v, pools=pools)
+    oracle.quantize_kv(k_new.cpu().numpy(), v_new.cpu().numpy(), last_slots(wl, dev).cpu().numpy(), wl.num_pages,
+                       rotate_v=wl.rotate_v, pools=pools)
+    got = c.bytes()
+    assert np.array_equal(got[0], pools[0]) and np.array_equal(got[1], pools[1])
+    ref = oracle.decode_attention(wl.q.numpy(), pools, wl.page_table, wl.context_lens, wl.num_kv_heads, SCALE,
+                                  wl.rotate_v)
+    err = np.abs(out - ref).max()
+    rel = np.linalg.norm(out - ref) / np.linalg.norm(ref)
+    log(f"step vs oracle: max-abs {err:.3e} rel-L2 {rel:.3e}")
+    assert err <= 2e-3 and rel <= 1e-3
+
+
+@pytest.mark.parametrize("fmt", ["fp4", "fp8"])
+def test_step_qwen_full_size(uq, fmt):
+    """B=32, Hq=64, Hkv=4, context 32768, random pages, the default
+    partition: the launch configuration the benchmark times."""
+    dev = torch.device("cuda:0")
+    wl = workloads.qwen3_235b_like()
+    log(f"decode step {fmt} qwen3-235b-like full size")
+    compare_step(uq, fmt, wl, dev, 0)

@@ -178,3 +178,28 @@ def test_ref_cache_sizes_and_validation(uq):
         uq.workspace_bytes(d4, 32, 64, 32768, 0)
     assert lib.uq_ref_decode_merge(ctypes.byref(rdesc()), 2, 4, None, 64, 0, FAKE, 1 << 30, FAKE, 0, None) == \
         E.UQ_ERR_INVALID_ARGUMENT
+
+
+def test_decode_step_validation(uq):
+    E = uq
+    lib = uq.lib
+
+    def step(d, **kw):
+        a = dict(q=FAKE, kn=FAKE, vn=FAKE, ndt=0, B=2, Hq=4, ctx=FAKE, maxctx=64, scale=0.1, wsb=1 << 30)
+        a.update(kw)
+        return lib.uq_decode_step(ctypes.byref(d), a["q"], 0, a["kn"], a["vn"], a["ndt"], a["B"], a["Hq"], FAKE, FAKE,
+                                  FAKE, 4, a["ctx"], a["maxctx"], a["scale"], 0, FAKE, a["wsb"], FAKE, 0, None)
+
+    assert step(desc(), kn=None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert step(desc(), vn=None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert step(desc(), kn=ctypes.c_void_p(0x10004)) == E.UQ_ERR_INVALID_ARGUMENT
+    assert step(desc(), ndt=3) == E.UQ_ERR_UNSUPPORTED
+    assert step(desc(), Hq=3) == E.UQ_ERR_INVALID_ARGUMENT
+    assert step(desc(), wsb=16) == E.UQ_ERR_WORKSPACE_TOO_SMALL
+    assert step(desc(head_dim=64)) == E.UQ_ERR_UNSUPPORTED
+    r = lib.uq_ref_decode_step(ctypes.byref(rdesc()), FAKE, 0, None, FAKE, 0, 2, 4, FAKE, FAKE, 4, FAKE, 64, 0.1, 0,
+                               FAKE, 1 << 30, FAKE, 0, None)
+    assert r == E.UQ_ERR_INVALID_ARGUMENT
+    r = lib.uq_ref_decode_step_partials(ctypes.byref(rdesc()), FAKE, 0, FAKE, FAKE, 3, 2, 4, FAKE, FAKE, 4, FAKE, 64,
+                                        0.1, 0, FAKE, 1 << 30, FAKE, 0, None)
+    assert r == E.UQ_ERR_UNSUPPORTED
