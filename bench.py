@@ -73,23 +73,25 @@ def kernel_source_hash():
     return h.hexdigest()
 
 
-def profiled_traffic(workload_name):
-    """HBM bytes per decode_kernel launch from the committed counter profile of
-    this workload (FETCH_SIZE and WRITE_SIZE, calibrated against a copy of
-    known size), or None when there is none for the current kernel sources."""
+def profiled_traffic(workload_name, fmt="fp4"):
+    """HBM bytes per decode-kernel launch (fmt: fp4, fp8 or bf16 cache) from
+    the committed counter profile of this workload (FETCH_SIZE and
+    WRITE_SIZE, calibrated against a copy of known size), or None when there
+    is none for the current kernel sources."""
     path = os.path.join(ROOT, "profiles", f"decode_kernel_{workload_name}.md")
     if not os.path.exists(path):
         return None
+    field = "traffic_bytes_per_launch" + ("" if fmt == "fp4" else f"_{fmt}")
     fields = {}
     with open(path) as f:
         for line in f:
-            if line.startswith("traffic_bytes_per_launch:") or line.startswith("source_sha256:"):
+            if ":" in line and (line.startswith("traffic_bytes_per_launch") or line.startswith("source_sha256:")):
                 k, v = line.split(":", 1)
                 fields[k.strip()] = v.strip()
     if fields.get("source_sha256") != kernel_source_hash():
         return None
     try:
-        return float(fields["traffic_bytes_per_launch"])
+        return float(fields[field])
     except (KeyError, ValueError):
         return None
 
@@ -156,7 +158,8 @@ def comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, args, dev, stream):
     torch.cuda.empty_cache()
     return {"tokens_per_s": wl.total_tokens() / (ms_step * 1e-3), "ms_per_step": ms_step,
             "decode_kernel_ms": dec_ms, "bytes_per_token_head": REF_BYTES_PER_TOKEN_HEAD[fmt],
-            "kv_gbs": nbytes / (dec_ms * 1e-3) / 1e9, "kv_frac": nbytes / (dec_ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+            "kv_gbs": nbytes / (dec_ms * 1e-3) / 1e9, "kv_frac": nbytes / (dec_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "traffic": profiled_traffic(wl.name, fmt)}
 
 
 def cpu_baseline(wl, nseq, dev):
