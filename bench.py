@@ -99,9 +99,9 @@ def profiled_traffic(workload_name, fmt="fp4"):
 def fill_cache(uq, wl, desc, codes, scales, dev):
     """Quantise every stored segment of the workload into the pools (setup, untimed)."""
     import torch
-    for key, lo, hi in wl.segments():
+    for key, lo, hi, row in wl.segments():
         k, v = wl.kv(key, lo, hi, device=dev)
-        slots = torch.as_tensor(wl.slots(key, lo, hi), device=dev)
+        slots = torch.as_tensor(wl.slots(key, lo, hi, row), device=dev)
         uq.quantize_kv(desc, k, v, slots, codes, scales)
         del k, v
     torch.cuda.synchronize()
@@ -135,9 +135,9 @@ def comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, args, dev, stream):
     desc = uq.RefCacheDesc(num_kv_heads=wl.num_kv_heads, num_pages=wl.num_pages, fmt=fmt, k_scale=REF_SCALE,
                            v_scale=REF_SCALE)
     cache = desc.alloc_cache(dev)
-    for key, lo, hi in wl.segments():
+    for key, lo, hi, row in wl.segments():
         k, v = wl.kv(key, lo, hi, device=dev)
-        uq.ref_write_kv(desc, k, v, torch.as_tensor(wl.slots(key, lo, hi), device=dev), cache)
+        uq.ref_write_kv(desc, k, v, torch.as_tensor(wl.slots(key, lo, hi, row), device=dev), cache)
         del k, v
     ws = uq.ref_alloc_workspace(desc, wl.batch, wl.num_q_heads, wl.max_context, part, dev)
     out = torch.empty((wl.batch, wl.num_q_heads, 128), dtype=torch.float32, device=dev)
@@ -171,18 +171,12 @@ def cpu_baseline(wl, nseq, dev):
     pt = np.arange(len(seqs) * maxp, dtype=np.int32).reshape(len(seqs), maxp)
     pools = oracle.alloc_pools(len(seqs) * maxp, wl.num_kv_heads)
     for i, b in enumerate(seqs):
-        for key, lo, hi in wl.segments():
-            if key not in (-1, b):
-                continue
-            hi_b = min(hi, int(wl.context_lens[b]))
-            if hi_b <= lo:
-                continue
+        for key, lo, hi in wl.sequence_segments(b):
             k, v = wl.kv(key, lo, hi, device=dev)
-            k = k[: hi_b - lo].cpu().numpy()
-            v = v[: hi_b - lo].cpu().numpy()
-            pos = np.arange(lo, hi_b, dtype=np.int64)
+            pos = np.arange(lo, hi, dtype=np.int64)
             slots = pt[i, pos // 16].astype(np.int64) * 16 + pos % 16
-            oracle.quantize_kv(k, v, slots, len(seqs) * maxp, rotate_v=wl.rotate_v, pools=pools)
+            oracle.quantize_kv(k.cpu().numpy(), v.cpu().numpy(), slots, len(seqs) * maxp, rotate_v=wl.rotate_v,
+                               pools=pools)
     q = wl.q.numpy()[seqs]
     ctx = wl.context_lens[seqs]
     t0 = time.perf_counter()

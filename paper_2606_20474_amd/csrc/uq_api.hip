@@ -76,7 +76,8 @@ uq_status make_decode_params(const uq_cache_desc* desc, const void* q, uq_dtype 
     if (workspace_bytes < need) return UQ_ERR_WORKSPACE_TOO_SMALL;
     if (!aligned16(workspace)) return UQ_ERR_INVALID_ARGUMENT;
     const int64_t np = num_partitions(max_context, part);
-    if (np > 0x7FFFFFFF) return UQ_ERR_UNSUPPORTED;
+    // one linear grid of partitions x kv heads x sequences
+    if (np * desc->num_kv_heads * batch > 0x7FFFFFFF) return UQ_ERR_UNSUPPORTED;
     p.q = q;
     p.q_dtype = int32_t(q_dtype);
     p.codes = const_cast<uint8_t*>(kv_codes);     // written only by the decode-step calls

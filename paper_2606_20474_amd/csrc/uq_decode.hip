@@ -9,7 +9,7 @@
 //   kBf16  a plain BF16 cache.
 //
 // decode_kernel<F>: one block of Fmt<F>::kWaves waves per (partition, kv
-// head, sequence).
+// head, sequence), in an XCD-aware linear order (kv head fastest).
 //   prologue  the block loads its G query heads (G <= 16), rotates them
 //             with the in-register WHT butterfly and casts them to FP8
 //             E4M3 (FP4 cache), casts them to FP8 (FP8 cache) or to BF16
@@ -373,9 +373,17 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
     constexpr int kThreads = 64 * W;
     constexpr int kStage = stage_bytes<F>();
     constexpr int kQRounds = 256 / kThreads;   // 16 threads per query row, 16 rows
-    const int part = blockIdx.x;
-    const int hk = blockIdx.y;
-    const int b = blockIdx.z;
+    // Linear block order: kv head fastest, then sequence, then partition.
+    // Workgroups go to the 8 XCDs round-robin by linear id, so this spreads
+    // the work of every sequence evenly over the XCDs whatever the context
+    // lengths (with the partition fastest, XCD k would get partition k of
+    // every sequence and the XCDs holding the late partitions of short
+    // sequences would idle), and it keeps one kv head on the same XCDs, whose
+    // L2 then serves pages that several sequences share.
+    const int lin = blockIdx.x;
+    const int hk = lin % p.num_kv_heads;
+    const int b = (lin / p.num_kv_heads) % p.batch;
+    const int part = lin / (p.num_kv_heads * p.batch);
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: scalar control flow
@@ -742,7 +750,7 @@ __global__ void __launch_bounds__(256) merge_kernel(DecodeParams p) {
 
 template <int F>
 static hipError_t launch_partials(const DecodeParams& p, hipStream_t stream) {
-    const dim3 grid{unsigned(p.num_partitions), unsigned(p.num_kv_heads), unsigned(p.batch)};
+    const dim3 grid{unsigned(int64_t(p.num_partitions) * p.num_kv_heads * p.batch)};
     hipLaunchKernelGGL(decode_kernel<F>, grid, dim3(64 * Fmt<F>::kWaves), 0, stream, p);
     return hipGetLastError();
 }

@@ -12,7 +12,9 @@ and agent-trace contexts, which are not available):
   * pages of 16 tokens; page tables are identity (tiny case) or a random
     permutation of the page pool; the MiniMax-like case shares its first
     16384 tokens (1024 pages) between all sequences and draws contexts from
-    lognormal(ln 32768, 0.8) clipped to [8192, 131072].
+    lognormal(ln 32768, 0.8) clipped to [8192, 131072]; a context shorter
+    than the shared prefix shares its first tokens and owns a copy of its
+    last page (copy on write).
 Small index tables, outlier channels and queries come from a CPU
 ``torch.Generator``; the bulk K/V of every sequence comes from its own
 generator on the target device, seeded from (workload seed, sequence), so any
@@ -43,6 +45,8 @@ class DecodeWorkload:
     num_pages: int
     seed: int
     shared_prefix_tokens: int = 0     # tokens 0..n-1 of every sequence live in shared pages
+    private_tail: np.ndarray = field(default=None)   # bool [B]: last page copied out of the shared prefix
+    prefix_pages: np.ndarray = field(default=None)   # int64 [shared pages]: the shared prefix's pages
     partition_tokens: int = 0         # 0 = library default
     rotate_v: bool = True
     k_outliers: np.ndarray = field(default=None)   # int64 [Hkv, 4]
@@ -70,29 +74,59 @@ class DecodeWorkload:
 
     # -- bulk data ---------------------------------------------------------
     def segments(self):
-        """(key, first token, last token + 1) of every stored run of tokens:
-        the shared prefix once (key -1), then each sequence's own tokens."""
+        """(key, first token, last token + 1, row) of every stored run of
+        tokens: the shared prefix once (key -1, row None: its own page list),
+        each sequence's own tokens (key b, row b), and, for a sequence
+        whose context ends inside the shared prefix, the prefix tokens of its
+        last page again (key -1, row b): that page is a private copy, so a
+        decode step can append to it without touching pages others read."""
         out = []
         if self.shared_prefix_tokens:
-            out.append((-1, 0, self.shared_prefix_tokens))
+            out.append((-1, 0, self.shared_prefix_tokens, None))
         for b in range(self.batch):
-            lo = min(self.shared_prefix_tokens, int(self.context_lens[b]))
-            if self.context_lens[b] > lo:
-                out.append((b, lo, int(self.context_lens[b])))
+            ctx = int(self.context_lens[b])
+            lo = min(self.shared_prefix_tokens, ctx)
+            if self.private_tail is not None and self.private_tail[b]:
+                out.append((-1, ((ctx - 1) // PAGE) * PAGE, ctx, b))
+            if ctx > lo:
+                out.append((b, lo, ctx, b))
         return out
 
-    def slots(self, key: int, lo: int, hi: int) -> np.ndarray:
-        row = 0 if key < 0 else key
+    def sequence_segments(self, b: int):
+        """(key, first token, last token + 1) covering tokens 0..len-1 of
+        sequence b once each, in order."""
+        ctx = int(self.context_lens[b])
+        lo = min(self.shared_prefix_tokens, ctx)
+        out = [(-1, 0, lo)] if lo > 0 else []
+        if ctx > lo:
+            out.append((b, lo, ctx))
+        return out
+
+    def slots(self, key: int, lo: int, hi: int, row=None) -> np.ndarray:
+        """Physical slots of tokens lo..hi-1 through page-table row `row`
+        (None: the shared prefix's page list)."""
         pos = np.arange(lo, hi, dtype=np.int64)
-        return self.page_table[row, pos // PAGE].astype(np.int64) * PAGE + pos % PAGE
+        if row is None and key >= 0:
+            row = key
+        pages = self.prefix_pages[pos // PAGE] if row is None else self.page_table[row, pos // PAGE].astype(np.int64)
+        return pages * PAGE + pos % PAGE
 
     def kv(self, key: int, lo: int, hi: int, device="cpu", dtype=torch.float32):
-        """K, V [hi-lo, Hkv, 128] of one segment, regenerated from its own seed."""
+        """K, V [hi-lo, Hkv, 128] of one segment, regenerated from its own
+        seed.  A sequence's stream (key >= 0) starts at the segment; the
+        shared prefix (key -1) is always drawn whole and then sliced, so any
+        part of it can be regenerated (a generator's leading values depend
+        on the size of the draw)."""
         g = torch.Generator(device=device)
         g.manual_seed(self.seed * 1_000_003 + (key + 1))
-        n = hi - lo
+        if key < 0:
+            assert 0 <= lo <= hi <= self.shared_prefix_tokens
+            n, skip = self.shared_prefix_tokens, lo
+        else:
+            n, skip = hi - lo, 0
         k = torch.randn((n, self.num_kv_heads, HEAD_DIM), generator=g, device=device, dtype=torch.float32)
         v = torch.randn((n, self.num_kv_heads, HEAD_DIM), generator=g, device=device, dtype=torch.float32)
+        k, v = k[skip:skip + hi - lo], v[skip:skip + hi - lo]
         for h in range(self.num_kv_heads):
             k[:, h, torch.as_tensor(self.k_outliers[h], device=device)] *= OUTLIER_GAIN
             v[:, h, torch.as_tensor(self.v_outliers[h], device=device)] *= OUTLIER_GAIN
@@ -116,7 +150,10 @@ def custom(batch, num_q_heads, num_kv_heads, context_lens, seed=0, paging="rando
     shared = shared_prefix_tokens // PAGE
     assert shared_prefix_tokens % PAGE == 0
     own = [max(0, p - shared) for p in pages_per]
-    num_pages = shared + sum(own) + spare_pages
+    # a context that ends inside the shared prefix gets a private copy of its
+    # last page (copy on write), so that appends never touch shared pages
+    tail = np.array([0 < pages_per[b] <= shared for b in range(batch)], dtype=bool)
+    num_pages = shared + sum(own) + int(tail.sum()) + spare_pages
     if paging == "identity":
         perm = np.arange(num_pages, dtype=np.int64)
     else:
@@ -128,10 +165,14 @@ def custom(batch, num_q_heads, num_kv_heads, context_lens, seed=0, paging="rando
         pt[b, :n_sh] = perm[:n_sh]
         pt[b, n_sh:pages_per[b]] = perm[cur:cur + own[b]]
         cur += own[b]
+        if tail[b]:
+            pt[b, pages_per[b] - 1] = perm[cur]
+            cur += 1
     pt[pt < 0] = 0   # unused entries point at a valid page; they are never read
     wl = DecodeWorkload(name, batch, num_q_heads, num_kv_heads, ctx, pt, num_pages, seed,
                         shared_prefix_tokens=shared_prefix_tokens, partition_tokens=partition_tokens,
-                        rotate_v=rotate_v)
+                        rotate_v=rotate_v, private_tail=tail if tail.any() else None,
+                        prefix_pages=np.asarray(perm[:shared], dtype=np.int64))
     return _meta(gen, wl)
 
 

@@ -44,9 +44,9 @@ def check_attention(got, ref, what):
 def gpu_cache(uq, wl, device, fill=0xA5, in_dtype=torch.float32):
     desc = uq.CacheDesc(num_kv_heads=wl.num_kv_heads, num_pages=wl.num_pages, rotate_v=wl.rotate_v)
     codes, scales = desc.alloc_pools(device, fill=fill)
-    for key, lo, hi in wl.segments():
+    for key, lo, hi, row in wl.segments():
         k, v = wl.kv(key, lo, hi, device=device, dtype=in_dtype)
-        slots = torch.as_tensor(wl.slots(key, lo, hi), device=device)
+        slots = torch.as_tensor(wl.slots(key, lo, hi, row), device=device)
         uq.quantize_kv(desc, k, v, slots, codes, scales)
     torch.cuda.synchronize()
     return desc, codes, scales
@@ -59,16 +59,11 @@ def oracle_cache(wl, seqs, device, in_dtype=torch.float32):
     pt = np.arange(len(seqs) * maxp, dtype=np.int32).reshape(len(seqs), maxp)
     pools = oracle.alloc_pools(len(seqs) * maxp, wl.num_kv_heads)
     for i, b in enumerate(seqs):
-        for key, lo, hi in wl.segments():
-            if key not in (-1, b):
-                continue
-            hi_b = min(hi, int(wl.context_lens[b]))
-            if hi_b <= lo:
-                continue
+        for key, lo, hi in wl.sequence_segments(b):
             k, v = wl.kv(key, lo, hi, device=device, dtype=in_dtype)
-            k = k[: hi_b - lo].float().cpu().numpy()
-            v = v[: hi_b - lo].float().cpu().numpy()
-            pos = np.arange(lo, hi_b, dtype=np.int64)
+            k = k.float().cpu().numpy()
+            v = v.float().cpu().numpy()
+            pos = np.arange(lo, hi, dtype=np.int64)
             slots = pt[i, pos // 16].astype(np.int64) * 16 + pos % 16
             oracle.quantize_kv(k, v, slots, len(seqs) * maxp, rotate_v=wl.rotate_v, pools=pools)
     return pools, pt
@@ -94,9 +89,9 @@ def test_quantize_tiny_bit_exact(uq):
     log("quantize tiny: fp32 4096 tokens")
     desc, codes, scales = gpu_cache(uq, wl, dev)
     pools = oracle.alloc_pools(wl.num_pages, 1, fill=0xA5)
-    for key, lo, hi in wl.segments():
+    for key, lo, hi, row in wl.segments():
         k, v = wl.kv(key, lo, hi, device=dev)
-        oracle.quantize_kv(k.cpu().numpy(), v.cpu().numpy(), wl.slots(key, lo, hi), wl.num_pages, pools=pools)
+        oracle.quantize_kv(k.cpu().numpy(), v.cpu().numpy(), wl.slots(key, lo, hi, row), wl.num_pages, pools=pools)
     assert np.array_equal(codes.cpu().numpy(), pools[0])
     assert np.array_equal(scales.cpu().numpy(), pools[1])
 
@@ -244,6 +239,40 @@ def test_decode_group_sizes(uq, hq, hkv):
     pools, pt = oracle_cache(wl, [0, 1], dev)
     ref = oracle.decode_attention(wl.q.numpy(), pools, pt, wl.context_lens, hkv, 1 / math.sqrt(128), True)
     check_attention(out, ref, f"groups {hq}/{hkv}")
+
+
+def test_decode_minimax_full_size_sampled(uq):
+    """B=64, Hq=48, Hkv=8, lognormal contexts 8k..128k, a 16k-token prefix
+    shared by every sequence (shorter contexts own a copy of their last
+    page), the default partition: the shortest and the longest sequence
+    against the oracle."""
+    dev = torch.device("cuda:0")
+    wl = workloads.minimax_like()
+    log("decode minimax-like full size")
+    desc, codes, scales = gpu_cache(uq, wl, dev, fill=None)
+    out = run_decode(uq, wl, desc, codes, scales, dev)
+    seqs = [int(np.argmin(wl.context_lens)), int(np.argmax(wl.context_lens))]
+    pools, ptc = oracle_cache(wl, seqs, dev)
+    ref = oracle.decode_attention(wl.q.numpy()[seqs], pools, ptc, wl.context_lens[seqs], wl.num_kv_heads,
+                                  1 / math.sqrt(128), True)
+    check_attention(out[seqs], ref, "minimax sampled")
+
+
+def test_decode_high_concurrency_sampled(uq):
+    """B=256, Hq=64, Hkv=8, every context 131072 (36.5 GB of FP4 KV),
+    partitions of 4096: one sequence against the oracle."""
+    dev = torch.device("cuda:0")
+    wl = workloads.high_concurrency()
+    log("decode high-concurrency full size")
+    desc, codes, scales = gpu_cache(uq, wl, dev, fill=None)
+    out = run_decode(uq, wl, desc, codes, scales, dev)
+    del codes, scales
+    torch.cuda.empty_cache()
+    seqs = [201]
+    pools, ptc = oracle_cache(wl, seqs, dev)
+    ref = oracle.decode_attention(wl.q.numpy()[seqs], pools, ptc, wl.context_lens[seqs], wl.num_kv_heads,
+                                  1 / math.sqrt(128), True)
+    check_attention(out[seqs], ref, "high-concurrency sampled")
 
 
 def test_decode_qwen_full_size_sampled(uq):

@@ -124,15 +124,10 @@ def attention(qd, kd, vd, group):
 def seq_values(fmt, wl, b, device, ks, vs, in_dtype=torch.float32):
     """Dequantized K, V of every token of sequence b (shared prefix first)."""
     ks_, vs_ = [], []
-    for key, lo, hi in wl.segments():
-        if key not in (-1, b):
-            continue
-        hi_b = min(hi, int(wl.context_lens[b]))
-        if hi_b <= lo:
-            continue
+    for key, lo, hi in wl.sequence_segments(b):
         k, v = wl.kv(key, lo, hi, device=device, dtype=in_dtype)
-        ks_.append(encode(fmt, k[: hi_b - lo], ks)[1])
-        vs_.append(encode(fmt, v[: hi_b - lo], vs)[1])
+        ks_.append(encode(fmt, k, ks)[1])
+        vs_.append(encode(fmt, v, vs)[1])
     if not ks_:
         z = np.zeros((0, wl.num_kv_heads, 128))
         return z, z
@@ -149,9 +144,9 @@ def make_desc(uq, fmt, wl, ks=0.3, vs=0.3):
 def gpu_cache(uq, fmt, wl, device, fill=0xA5, in_dtype=torch.float32, ks=0.3, vs=0.3):
     desc = make_desc(uq, fmt, wl, ks, vs)
     cache = desc.alloc_cache(device, fill=fill)
-    for key, lo, hi in wl.segments():
+    for key, lo, hi, row in wl.segments():
         k, v = wl.kv(key, lo, hi, device=device, dtype=in_dtype)
-        slots = torch.as_tensor(wl.slots(key, lo, hi), device=device)
+        slots = torch.as_tensor(wl.slots(key, lo, hi, row), device=device)
         uq.ref_write_kv(desc, k, v, slots, cache)
     torch.cuda.synchronize()
     return desc, cache
@@ -185,11 +180,11 @@ def test_ref_write_bit_exact(uq, fmt, dtype):
     log(f"ref write {fmt} {dtype}")
     desc, cache = gpu_cache(uq, fmt, wl, dev, in_dtype=dtype)
     pool = np.full(desc.cache_bytes(), 0xA5, np.uint8)
-    for key, lo, hi in wl.segments():
+    for key, lo, hi, row in wl.segments():
         k, v = wl.kv(key, lo, hi, device=dev, dtype=dtype)
         kb, _ = encode(fmt, k, 0.3)
         vb, _ = encode(fmt, v, 0.3)
-        place(fmt, pool, kb, vb, wl.slots(key, lo, hi), wl.num_kv_heads)
+        place(fmt, pool, kb, vb, wl.slots(key, lo, hi, row), wl.num_kv_heads)
     assert np.array_equal(cache.cpu().numpy(), pool)
 
 
@@ -204,10 +199,10 @@ def test_ref_write_fp8_saturates_and_skips(uq):
     cache = desc.alloc_cache(dev, fill=0x11)
     pool = np.full(desc.cache_bytes(), 0x11, np.uint8)
     pt = torch.as_tensor(wl.page_table, device=dev)
-    for key, lo, hi in wl.segments():
+    for key, lo, hi, row in wl.segments():
         k, v = wl.kv(key, lo, hi, device=dev)
-        phys = wl.slots(key, lo, hi)
-        logical = key * wl.max_pages_per_seq * 16 + np.arange(lo, hi, dtype=np.int64)
+        phys = wl.slots(key, lo, hi, row)
+        logical = row * wl.max_pages_per_seq * 16 + np.arange(lo, hi, dtype=np.int64)
         logical[::5] = -1
         phys = np.where(logical < 0, -1, phys)
         uq.ref_write_kv(desc, k, v, torch.as_tensor(logical, device=dev), cache, page_table=pt)
@@ -292,10 +287,10 @@ def test_ref_decode_fp8_integer_inputs(uq):
     desc = make_desc(uq, "fp8", wl, 1.0, 1.0)
     cache = desc.alloc_cache(dev, fill=0)
     kd, vd = [], []
-    for key, lo, hi in wl.segments():
+    for key, lo, hi, row in wl.segments():
         k = torch.clamp(torch.round(torch.randn((hi - lo, wl.num_kv_heads, 128), generator=g) * 5), -16, 16)
         v = torch.clamp(torch.round(torch.randn((hi - lo, wl.num_kv_heads, 128), generator=g) * 5), -16, 16)
-        uq.ref_write_kv(desc, k.to(dev), v.to(dev), torch.as_tensor(wl.slots(key, lo, hi), device=dev), cache)
+        uq.ref_write_kv(desc, k.to(dev), v.to(dev), torch.as_tensor(wl.slots(key, lo, hi, row), device=dev), cache)
         kd.append(k.double().numpy())
         vd.append(v.double().numpy())
     wl.q = torch.clamp(torch.round(torch.randn(wl.q.shape, generator=g) * 3), -8, 8)

@@ -7,9 +7,10 @@ it replaces (uq_quantize_kv or uq_ref_write_kv of the new tokens, then
 uq_decode_attention or uq_ref_decode_attention), which the other GPU tests
 hold to the oracle and to the CPU reference; the small FP4 case is also
 checked against the oracle directly.  Context lengths put the new token in
-the first stages of a wave (where the block holds back its first page
-copies until the token is stored), at page, stage and partition edges, and
-one context is empty.
+the first stages of a wave (whose page copy is already in flight when the
+token is encoded, so the staged copy has to be patched), at page, stage and
+partition edges, and one context is empty; the shared-prefix cases append
+to private copies of pages whose other tokens several sequences share.
 """
 import math
 
@@ -63,9 +64,9 @@ class Cache:
             self.desc = uq.RefCacheDesc(num_kv_heads=wl.num_kv_heads, num_pages=wl.num_pages, fmt=fmt, k_scale=0.3,
                                         v_scale=0.3)
             self.bufs = (self.desc.alloc_cache(dev, fill=0x5A),)
-        for key, lo, hi in wl.segments():
+        for key, lo, hi, row in wl.segments():
             k, v = wl.kv(key, lo, hi, device=dev)
-            self.write(k, v, torch.as_tensor(wl.slots(key, lo, hi), device=dev))
+            self.write(k, v, torch.as_tensor(wl.slots(key, lo, hi, row), device=dev))
 
     def write(self, k, v, slots):
         if self.fmt == "fp4":
@@ -135,9 +136,9 @@ def test_step_against_oracle(uq):
     c = Cache(uq, "fp4", wl, dev)
     out = c.step(q, k_new, v_new, pt, ctx, 64).cpu().numpy()
     pools = oracle.alloc_pools(wl.num_pages, wl.num_kv_heads, fill=0x5A)
-    for key, lo, hi in wl.segments():
+    for key, lo, hi, row in wl.segments():
         k, v = wl.kv(key, lo, hi, device=dev)
-        oracle.quantize_kv(k.cpu().numpy(), v.cpu().numpy(), wl.slots(key, lo, hi), wl.num_pages,
+        oracle.quantize_kv(k.cpu().numpy(), v.cpu().numpy(), wl.slots(key, lo, hi, row), wl.num_pages,
                            rotate_v=wl.rotate_v, pools=pools)
     oracle.quantize_kv(k_new.cpu().numpy(), v_new.cpu().numpy(), last_slots(wl, dev).cpu().numpy(), wl.num_pages,
                        rotate_v=wl.rotate_v, pools=pools)
@@ -149,6 +150,25 @@ def test_step_against_oracle(uq):
     rel = np.linalg.norm(out - ref) / np.linalg.norm(ref)
     log(f"step vs oracle: max-abs {err:.3e} rel-L2 {rel:.3e}")
     assert err <= 2e-3 and rel <= 1e-3
+
+
+@pytest.mark.parametrize("fmt", ["fp4", "bf16"])
+def test_step_shared_prefix(uq, fmt):
+    """Contexts shorter and longer than a 64-token shared prefix."""
+    dev = torch.device("cuda:0")
+    wl = workloads.custom(5, 12, 2, [20, 64, 65, 90, 300], seed=23, paging="random", shared_prefix_tokens=64)
+    assert wl.private_tail is not None and wl.private_tail.sum() == 2
+    log(f"decode step {fmt} shared prefix")
+    compare_step(uq, fmt, wl, dev, 32)
+
+
+def test_step_minimax_full_size(uq):
+    """B=64, Hq=48, Hkv=8, lognormal contexts with a 16k shared prefix, the
+    default partition."""
+    dev = torch.device("cuda:0")
+    wl = workloads.minimax_like()
+    log("decode step fp4 minimax-like full size")
+    compare_step(uq, "fp4", wl, dev, 0)
 
 
 @pytest.mark.parametrize("fmt", ["fp4", "fp8"])

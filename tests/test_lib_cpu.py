@@ -105,6 +105,9 @@ def test_decode_validation(uq):
     assert decode(uq, desc(), ws=None) == E.UQ_ERR_INVALID_ARGUMENT
     assert decode(uq, desc(), wsb=16) == E.UQ_ERR_WORKSPACE_TOO_SMALL
     assert decode(uq, desc(), q=ctypes.c_void_p(0x10008)) == E.UQ_ERR_INVALID_ARGUMENT
+    # partitions x kv heads x sequences beyond one 2^31 linear grid
+    big = desc(num_kv_heads=65535)
+    assert decode(uq, big, B=65535, Hq=65535, part=32, wsb=1 << 62) == E.UQ_ERR_UNSUPPORTED
 
 
 def test_workspace_and_partition_sizes(uq):

@@ -436,3 +436,17 @@ def test_attention_page_permutation_invariance():
     out2 = oracle.decode_attention(q, (new_codes.reshape(-1), new_scales.reshape(-1)), perm[pt].astype(np.int32),
                                    ctx, Hkv, 0.1, True)
     assert np.array_equal(out, out2)
+
+
+def test_workload_prefix_stream_is_positional():
+    """Any slice of the shared prefix regenerates the same values as the
+    whole prefix (both the HIP path and the oracle rely on it)."""
+    import torch
+    from paper_2606_20474_amd import workloads
+    wl = workloads.custom(2, 4, 1, [40, 20], seed=3, shared_prefix_tokens=32)
+    k, v = wl.kv(-1, 0, 32)
+    k2, v2 = wl.kv(-1, 16, 20)
+    assert torch.equal(k[16:20], k2) and torch.equal(v[16:20], v2)
+    seen = [(key, lo, hi) for key, lo, hi in wl.sequence_segments(1)]
+    assert seen == [(-1, 0, 20)]
+    assert bool(wl.private_tail[1]) and not bool(wl.private_tail[0])
