@@ -51,6 +51,8 @@ def parse():
     ap.add_argument("--cpu-sample-seqs", type=int, default=4)
     ap.add_argument("--comparators", default="fp8,bf16",
                     help="comma list of plain comparison caches to time as well (fp8, bf16) or 'none'")
+    ap.add_argument("--no-write-path", action="store_true",
+                    help="skip the quantize-on-write measurement (65536-token bf16 prefill + 256 appends)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one device-to-device copy of this many MiB before the timed steps; its "
                          "FETCH_SIZE/WRITE_SIZE counters calibrate the HBM-traffic counters")
@@ -162,6 +164,49 @@ def comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, args, dev, stream):
             "traffic": profiled_traffic(wl.name, fmt)}
 
 
+def write_path(uq, args, dev, stream):
+    """Quantize-on-write (Algorithm 1, Write) on its own: a 65536-token bf16
+    prefill of 8 KV heads into random pages, and a 1-token append for each of
+    256 sequences through a page table. Algorithmic bytes of the prefill:
+    the bf16 K and V rows read plus 136 B per token and KV head written."""
+    import torch
+    from paper_2606_20474_amd import workloads
+    ww = workloads.WriteWorkload()
+    data = ww.build(device=dev)
+    kp, vp, pslots = data["prefill"]
+    ka, va, aslots, pt, _ = data["append"]
+    desc = uq.CacheDesc(num_kv_heads=ww.num_kv_heads, num_pages=ww.num_pages)
+    codes, scales = desc.alloc_pools(dev)
+    pslots = torch.as_tensor(pslots, device=dev)
+    aslots = torch.as_tensor(aslots, device=dev)
+    pt = torch.as_tensor(pt, device=dev)
+
+    def prefill(ev_a=None, ev_b=None):
+        if ev_a is not None:
+            ev_a.record(stream)
+        uq.quantize_kv(desc, kp, vp, pslots, codes, scales)
+        if ev_b is not None:
+            ev_b.record(stream)
+
+    def append(ev_a=None, ev_b=None):
+        if ev_a is not None:
+            ev_a.record(stream)
+        uq.quantize_kv(desc, ka, va, aslots, codes, scales, page_table=pt)
+        if ev_b is not None:
+            ev_b.record(stream)
+
+    n = max(args.steps, 10)
+    _, pre_ms = timed(prefill, n, 3, stream)
+    _, app_ms = timed(append, n, 3, stream)
+    rd = 2 * kp.numel() * kp.element_size()
+    wr = ww.prefill_tokens * ww.num_kv_heads * KV_BYTES_PER_TOKEN_HEAD
+    gbs = (rd + wr) / (pre_ms * 1e-3) / 1e9
+    return {"prefill_tokens": ww.prefill_tokens, "num_kv_heads": ww.num_kv_heads, "in_dtype": "bf16",
+            "prefill_us": pre_ms * 1e3, "prefill_tokens_per_s": ww.prefill_tokens / (pre_ms * 1e-3),
+            "prefill_bytes": rd + wr, "prefill_gbs": gbs, "prefill_frac": gbs / HBM_PEAK_GBS,
+            "append_seqs": ww.append_seqs, "append_us": app_ms * 1e3}
+
+
 def cpu_baseline(wl, nseq, dev):
     """The oracle on `nseq` sequences of the workload (all their query heads,
     full contexts), timed on the host; KV tokens/s."""
@@ -271,6 +316,8 @@ def main():
             comp[f"{fmt}_kv"] = comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, args, dev, stream)
             comp[f"fp4_over_{fmt}_tokens_per_s"] = result["value"] / comp[f"{fmt}_kv"]["tokens_per_s"]
         result["comparators"] = comp
+    if not args.no_write_path:
+        result["write_path"] = write_path(uq, args, dev, stream)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample_seqs, dev)
     print(json.dumps(result), flush=True)

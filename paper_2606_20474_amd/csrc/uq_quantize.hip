@@ -2,24 +2,117 @@
 // Algorithm 1, "Write") and the FP8 query preparation (Algorithm 1,
 // "Decode", first step).
 //
-// One 128-vector is handled by 16 lanes holding 8 channels each, so a
-// wave64 processes 4 (token, kv head) pairs and a 256-thread block 16.
-// Per vector and per K/V: coalesced 16/32-byte loads, the in-register WHT
-// butterfly (3 in-lane + 4 cross-lane stages), the group absmax over the 4
-// lanes of a 32-channel group, the UE8M0 exponent, E2M1 encoding of 8
-// values into one dword, one dword store of codes and one byte store of the
-// scale per group.  The path is bound by HBM traffic.
+// One 128-vector is handled by a quad of 4 lanes holding 32 channels each,
+// so a wave64 processes 16 (token, kv head) pairs and a 256-thread block 64.
+// Per vector and per K/V: 16-byte loads, the in-register WHT butterfly (5
+// in-lane stages and 2 DPP quad-permute stages), the group maxima, the
+// UE8M0 exponents, the hardware E2M1 conversion, 4 dword stores of codes
+// and one scale byte per lane.
 #include "uq_device.hpp"
 #include "uq_internal.hpp"
 
 namespace uq {
 
+// Lane exchange inside a quad (4 consecutive lanes) with DPP quad_perm:
+// partner lane L^1 or L^2.
+template <int S>
+__device__ __forceinline__ float quad_xor(float x) {
+    constexpr int ctrl = S == 1 ? 0xB1 : 0x4E;   // quad_perm [1,0,3,2] / [2,3,0,1]
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), ctrl, 0xF, 0xF, true));
+}
+
+// The rotation of one 128-vector held by 4 lanes of a quad: lane L holds
+// channels 32j + 8L + i in x[j][i] (j = 0..3, i = 0..7).  The stages run in
+// the order of the format (widths 1, 2, 4, 8, 16, 32, 64): 1, 2, 4 inside a
+// lane over i, 8 and 16 across lanes L^1, L^2, 32 and 64 inside a lane over
+// j; each maps (a, b) to (a + b, a - b) in fp32 (the upper element of a
+// cross-lane pair takes fma(-1, b, a) = a - b, exactly rounded), then one
+// multiply by fl32(1/sqrt(128)).  The values equal those of wht128_x8
+// bit for bit.
+__device__ __forceinline__ void wht128_x32(float (&x)[4][8], int L) {
+#pragma clang fp contract(off)
+#pragma unroll
+    for (int h = 1; h < 8; h <<= 1) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                if (i & h) continue;
+                const float a = x[j][i], b = x[j][i + h];
+                x[j][i] = a + b;
+                x[j][i + h] = a - b;
+            }
+        }
+    }
+    const float s1 = (L & 1) ? -1.0f : 1.0f;
+    const float s2 = (L & 2) ? -1.0f : 1.0f;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) x[j][i] = __builtin_fmaf(s1, x[j][i], quad_xor<1>(x[j][i]));
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) x[j][i] = __builtin_fmaf(s2, x[j][i], quad_xor<2>(x[j][i]));
+#pragma unroll
+    for (int h = 1; h < 4; h <<= 1) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            if (j & h) continue;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const float a = x[j][i], b = x[j + h][i];
+                x[j][i] = a + b;
+                x[j + h][i] = a - b;
+            }
+        }
+    }
+    const float r = inv_sqrt128();
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) x[j][i] = x[j][i] * r;
+}
+
+// Quantise one 128-vector held by a quad (rotated first if `rotate`): per
+// 32-channel group j the UE8M0 exponent E_j of the group maximum, and the
+// E2M1 codes of the lane's 8 channels of the group in w[j] (channel order,
+// low nibble first) by the hardware conversion, which rounds x / 2^E_j to
+// the nearest E2M1 level with ties to the even code, saturates at 6 and
+// keeps the sign: the same codes as e2m1_code.
+__device__ __forceinline__ void quantize_x32(float (&x)[4][8], int L, float c, bool rotate, uint32_t (&w)[4],
+                                             int (&E)[4]) {
+    if (rotate) wht128_x32(x, L);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        float m = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) m = __builtin_fmaxf(m, __builtin_fabsf(x[j][i]));
+        m = __builtin_fmaxf(m, quad_xor<1>(m));
+        m = __builtin_fmaxf(m, quad_xor<2>(m));
+        E[j] = ue8m0_exponent(m, c);
+        const float sc = __builtin_ldexpf(1.0f, E[j]);   // 2^E exactly (subnormal for E = -127)
+        uint32_t v = 0u;
+        v = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(v, x[j][0], x[j][1], sc, 0);
+        v = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(v, x[j][2], x[j][3], sc, 1);
+        v = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(v, x[j][4], x[j][5], sc, 2);
+        v = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(v, x[j][6], x[j][7], sc, 3);
+        w[j] = v;
+    }
+}
+
+// Quantize-on-write, 4 lanes (one quad) per (token, kv head) vector, 64
+// vectors per 256-thread block.  Lane L loads and keeps channels
+// 32j + 8L + i (16-byte loads, a quad covers 64 contiguous bytes per j), so
+// the two cross-lane stages of the rotation and the group maxima are DPP
+// quad permutes.  Stores: one codes dword per group for K and V, and the
+// scale bytes of group L for K and V.
 template <int DT>
 __global__ void __launch_bounds__(256) quantize_kv_kernel(QuantizeParams p) {
-    const int lane16 = threadIdx.x & 15;
-    const int64_t vec = int64_t(blockIdx.x) * 16 + (threadIdx.x >> 4);
+    const int L = threadIdx.x & 3;
+    const int64_t vec = int64_t(blockIdx.x) * 64 + (threadIdx.x >> 2);
     const int64_t nvec = p.num_tokens * p.num_kv_heads;
-    if (vec >= nvec) return;
+    if (vec >= nvec) return;   // whole quads leave together
     const int64_t t = vec / p.num_kv_heads;
     const int h = int(vec - t * p.num_kv_heads);
 
@@ -40,13 +133,34 @@ __global__ void __launch_bounds__(256) quantize_kv_kernel(QuantizeParams p) {
     }
     if (page < 0 || page >= p.num_pages) return;
 
-    const int64_t elem = t * p.token_stride + int64_t(h) * kHeadDim + 8 * lane16;
-    float xk[8], xv[8];
-    load_x8<DT>(p.k, elem, xk);
-    load_x8<DT>(p.v, elem, xv);
+    const int64_t row = t * p.token_stride + int64_t(h) * kHeadDim + 8 * L;
+    float xk[4][8], xv[4][8];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        load_x8<DT>(p.k, row + 32 * j, xk[j]);
+        load_x8<DT>(p.v, row + 32 * j, xv[j]);
+    }
+    uint32_t wk[4], wv[4];
+    int ek[4], ev[4];
+    quantize_x32(xk, L, p.c, true, wk, ek);
+    quantize_x32(xv, L, p.c, p.rotate_v != 0, wv, ev);
 
-    const TokenBits<kFp4> tb = encode_token<kFp4>(xk, xv, lane16, p.c, p.rotate_v != 0, 1.0f, 1.0f);
-    store_token<kFp4>(p.codes, p.scales, (page * p.num_kv_heads + h) * 2, off, lane16, tb);
+    const int64_t tile = (page * p.num_kv_heads + h) * 2;
+    uint8_t* kc = p.codes + tile * kTileCodes;
+    uint8_t* vc = kc + kTileCodes;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        // K tile [group][token][16 B]: channels 32j+8L.. are bytes 4L..4L+3 of the row
+        *reinterpret_cast<uint32_t*>(kc + (j * kPage + off) * 16 + 4 * L) = wk[j];
+        // V tile [token/4][channel/8][token%4][4 B]: channel block 4j+L
+        *reinterpret_cast<uint32_t*>(vc + ((off >> 2) * 16 + 4 * j + L) * 16 + (off & 3) * 4) = wv[j];
+    }
+    // scale bytes [K|V][group][token]: lane L writes group L
+    const int eks = L == 0 ? ek[0] : L == 1 ? ek[1] : L == 2 ? ek[2] : ek[3];
+    const int evs = L == 0 ? ev[0] : L == 1 ? ev[1] : L == 2 ? ev[2] : ev[3];
+    uint8_t* ks = p.scales + tile * kTileScales;
+    ks[L * kPage + off] = uint8_t(eks + 127);
+    ks[kTileScales + L * kPage + off] = uint8_t(evs + 127);
 }
 
 // Writer of the plain comparison caches (FP8 E4M3 with one scale per
@@ -102,7 +216,7 @@ __global__ void __launch_bounds__(256) prepare_query_kernel(const void* q, int64
 
 hipError_t launch_quantize_kv(const QuantizeParams& p, int dtype, hipStream_t stream) {
     const int64_t nvec = p.num_tokens * p.num_kv_heads;
-    const int64_t blocks = (nvec + 15) / 16;
+    const int64_t blocks = (nvec + 63) / 64;   // 64 quads per block
     if (blocks == 0) return hipSuccess;
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
     const dim3 grid{unsigned(blocks)}, block{256u};
