@@ -110,23 +110,35 @@ __device__ __forceinline__ float max_across_groups(float x) {
     return __builtin_fmaxf(a, b);
 }
 
-__device__ __forceinline__ float sum_across_groups(float x) {
-    float a = x, b = x;
-    swap16(a, b);
-    x = a + b;
-    a = x;
-    b = x;
-    swap32(a, b);
-    return a + b;
-}
-
 __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
     v2bf h = {__bf16(a), __bf16(b)};
     return __builtin_bit_cast(uint32_t, h);
 }
 
-__device__ __forceinline__ float bf16_lo_f32(uint32_t w) { return bits_f32(w << 16); }
-__device__ __forceinline__ float bf16_hi_f32(uint32_t w) { return bits_f32(w & 0xFFFF0000u); }
+// Scale float 2^(b-127) of byte B of a word of UE8M0 bytes: one SDWA shift
+// (b << 23; byte 0 gives 0.0, as ue8m0_to_f32).
+#define UQ_BYTE_SCALE(B)                                                                                     \
+    __device__ __forceinline__ float byte_scale##B(uint32_t w, uint32_t k23) {                                \
+        float r;                                                                                           \
+        asm("v_lshlrev_b32_sdwa %0, %1, %2 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_" #B \
+            : "=v"(r)                                                                                      \
+            : "v"(k23), "v"(w));                                                                           \
+        return r;                                                                                          \
+    }
+UQ_BYTE_SCALE(0)
+UQ_BYTE_SCALE(1)
+UQ_BYTE_SCALE(2)
+UQ_BYTE_SCALE(3)
+#undef UQ_BYTE_SCALE
+
+// The two BF16 terms of P = hi + lo for two values a, b: hi keeps the upper
+// 16 bits of each fp32 pattern (one byte permute for both), lo is the
+// remainder, exact in fp32, rounded to BF16; |P - hi - lo| <= 2^-16 |P|.
+__device__ __forceinline__ void split_p(float a, float b, uint32_t& hi, uint32_t& lo) {
+    const uint32_t ua = f32_bits(a), ub = f32_bits(b);
+    hi = __builtin_amdgcn_perm(ub, ua, 0x07060302u);
+    lo = pack_bf16x2(a - bits_f32(ua & 0xFFFF0000u), b - bits_f32(ub & 0xFFFF0000u));
+}
 
 // Page ids of one wave, 64 at a time: lane j holds the id of the wave's
 // page 2*(32*chunk + j/2) + j%2 counted in its own iteration order
@@ -550,8 +562,12 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
     }
 
     const float sl2 = p.scale_log2;
+    const uint32_t k23 = 23u;
     float m_run = -__builtin_inff();
-    float l_run = 0.0f;
+    // running softmax sum per column, on the matrix unit: every row of
+    // (all ones) x P is the column sum of P
+    const v8bf ones = __builtin_bit_cast(v8bf, uint4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u});
+    v4f acc_l = {0.f, 0.f, 0.f, 0.f};
     v4f acc[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[j] = v4f{0.f, 0.f, 0.f, 0.f};
@@ -617,40 +633,44 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
             }
         }
 
-        // ---- online softmax (log2 domain, m_run in scaled units), lazy rescale
+        // ---- online softmax (log2 domain, m_run in scaled units), lazy rescale:
+        // the running max of a column moves only when a score exceeds it by
+        // more than kLazyRescale; a wave-wide vote skips the cross-lane maximum
+        // when no lane holds such a score (then no column would move)
         float smax = x[0];
 #pragma unroll
         for (int i = 1; i < 8; ++i) smax = __builtin_fmaxf(smax, x[i]);
-        const float mloc = max_across_groups(smax) * sl2;
-        if (mloc > m_run + kLazyRescale) {
-            const float alpha = __builtin_amdgcn_exp2f(m_run - mloc);
-            l_run *= alpha;
+        if (__builtin_amdgcn_ballot_w64(smax * sl2 > m_run + kLazyRescale) != 0) {
+            const float mloc = max_across_groups(smax) * sl2;
+            if (mloc > m_run + kLazyRescale) {
+                const float alpha = __builtin_amdgcn_exp2f(m_run - mloc);
+                acc_l *= alpha;
 #pragma unroll
-            for (int j = 0; j < 8; ++j) acc[j] *= alpha;
-            m_run = mloc;
+                for (int j = 0; j < 8; ++j) acc[j] *= alpha;
+                m_run = mloc;
+            }
         }
         float pr[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-            pr[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(x[i], sl2, -m_run));
-            l_run += pr[i];
-        }
+        for (int i = 0; i < 8; ++i) pr[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(x[i], sl2, -m_run));
         uint32_t phi[4], plo[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-            phi[r] = pack_bf16x2(pr[2 * r], pr[2 * r + 1]);
-            plo[r] = pack_bf16x2(pr[2 * r] - bf16_lo_f32(phi[r]), pr[2 * r + 1] - bf16_hi_f32(phi[r]));
-        }
+        for (int r = 0; r < 4; ++r) split_p(pr[2 * r], pr[2 * r + 1], phi[r], plo[r]);
         const v8bf Phi = __builtin_bit_cast(v8bf, uint4{phi[0], phi[1], phi[2], phi[3]});
         const v8bf Plo = __builtin_bit_cast(v8bf, uint4{plo[0], plo[1], plo[2], plo[3]});
+        acc_l = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, Phi, acc_l, 0, 0, 0);
+        acc_l = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, Plo, acc_l, 0, 0, 0);
 
         // ---- V to BF16 pairs, then PV on bf16 MFMA
         float sc[2][4];
-#pragma unroll
-        for (int t = 0; t < 4; ++t) {
-            sc[0][t] = ue8m0_to_f32(vs0 >> (8 * t));
-            sc[1][t] = ue8m0_to_f32(vs1 >> (8 * t));
-        }
+        sc[0][0] = byte_scale0(vs0, k23);
+        sc[0][1] = byte_scale1(vs0, k23);
+        sc[0][2] = byte_scale2(vs0, k23);
+        sc[0][3] = byte_scale3(vs0, k23);
+        sc[1][0] = byte_scale0(vs1, k23);
+        sc[1][1] = byte_scale1(vs1, k23);
+        sc[1][2] = byte_scale2(vs1, k23);
+        sc[1][3] = byte_scale3(vs1, k23);
         pv_pair<0>(c, sc, Phi, Plo, acc[0], acc[1]);
         pv_pair<1>(c, sc, Phi, Plo, acc[2], acc[3]);
         pv_pair<2>(c, sc, Phi, Plo, acc[4], acc[5]);
@@ -658,7 +678,7 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
     }
 
     // ---------------- merge the waves through LDS (the rings are free now)
-    l_run = sum_across_groups(l_run);
+    const float l_run = acc_l[0];   // the column sum, in every lane of the column
     __syncthreads();
     float* red_acc = reinterpret_cast<float*>(smem);
     static_assert(W * 16 * kAccStride * 4 <= W * ring_bytes<F>(), "merge buffer aliases the staging rings");
