@@ -8,6 +8,9 @@ launches of uq_decode_step:
      the partition kernel of decode attention over the full contexts
      (Algorithm 1, "Decode");
   2. uq_decode_merge merges the partitions.
+For a workload whose sequences share a prefix (minimax-like), the step is
+the same pair of launches of uq_decode_cascade: the prefix pages are read
+once per kv head for 16 (sequence, query head) columns at a time.
 Inputs are resident in HBM before the timed region.  The default workload is
 the Qwen3-235B-like layer: 64 query heads, 4 KV heads, head_dim 128, batch
 32, every context 32768, random page table.  ``value`` is KV tokens/s =
@@ -51,6 +54,8 @@ def parse():
     ap.add_argument("--cpu-sample-seqs", type=int, default=4)
     ap.add_argument("--comparators", default="fp8,bf16",
                     help="comma list of plain comparison caches to time as well (fp8, bf16) or 'none'")
+    ap.add_argument("--no-cascade", action="store_true",
+                    help="workloads with a shared prefix: read it per sequence instead of once per kv head")
     ap.add_argument("--no-write-path", action="store_true",
                     help="skip the quantize-on-write measurement (65536-token bf16 prefill + 256 appends)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
@@ -109,6 +114,16 @@ def fill_cache(uq, wl, desc, codes, scales, dev):
     torch.cuda.synchronize()
 
 
+def alg_token_heads(wl, cascade):
+    """(token, kv head) pairs one decode launch must read: every context
+    whole, or with the cascade the shared prefix once per kv head plus each
+    sequence's tokens after it."""
+    if not cascade:
+        return wl.total_tokens() * wl.num_kv_heads
+    own = int((wl.context_lens.astype(np.int64) - wl.prefix_lens().astype(np.int64)).sum())
+    return (own + wl.shared_prefix_tokens) * wl.num_kv_heads
+
+
 def timed(step, steps, warmup, stream):
     """Run `warmup` untimed steps, then `steps` timed ones; returns (ms per
     step over the whole timed region, mean ms of the decode launch between
@@ -129,7 +144,7 @@ def timed(step, steps, warmup, stream):
     return t_start.elapsed_time(t_end) / steps, float(np.mean([a.elapsed_time(b) for a, b in evs]))
 
 
-def comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, args, dev, stream):
+def comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, args, dev, stream, prefix=None):
     """The same step (uq_ref_decode_step: the new token of every sequence
     written by the partition launch, then the merge) over a plain FP8 or
     BF16 cache holding the same K/V."""
@@ -141,21 +156,32 @@ def comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, args, dev, stream):
         k, v = wl.kv(key, lo, hi, device=dev)
         uq.ref_write_kv(desc, k, v, torch.as_tensor(wl.slots(key, lo, hi, row), device=dev), cache)
         del k, v
-    ws = uq.ref_alloc_workspace(desc, wl.batch, wl.num_q_heads, wl.max_context, part, dev)
+    if prefix is None:
+        ws = uq.ref_alloc_workspace(desc, wl.batch, wl.num_q_heads, wl.max_context, part, dev)
+    else:
+        ws = torch.empty(uq.cascade_workspace_bytes(wl.num_kv_heads, wl.batch, wl.num_q_heads, wl.max_context, prefix,
+                                                    part), dtype=torch.uint8, device=dev)
     out = torch.empty((wl.batch, wl.num_q_heads, 128), dtype=torch.float32, device=dev)
     scale = 1 / math.sqrt(128)
 
     def step(ev_a=None, ev_b=None):
         if ev_a is not None:
             ev_a.record(stream)
-        uq.ref_decode_step(desc, q, k_new, v_new, cache, pt, ctx, wl.max_context, scale, part, ws, out,
-                           partials_only=True)
+        if prefix is None:
+            uq.ref_decode_step(desc, q, k_new, v_new, cache, pt, ctx, wl.max_context, scale, part, ws, out,
+                               partials_only=True)
+        else:
+            uq.ref_decode_cascade(desc, q, cache, pt, ctx, wl.max_context, prefix, scale, part, ws, out,
+                                  k_new=k_new, v_new=v_new, partials_only=True)
         if ev_b is not None:
             ev_b.record(stream)
-        uq.ref_decode_merge(desc, wl.batch, wl.num_q_heads, ctx, wl.max_context, part, ws, out)
+        if prefix is None:
+            uq.ref_decode_merge(desc, wl.batch, wl.num_q_heads, ctx, wl.max_context, part, ws, out)
+        else:
+            uq.ref_decode_cascade_merge(desc, wl.batch, wl.num_q_heads, ctx, wl.max_context, prefix, part, ws, out)
 
     ms_step, dec_ms = timed(step, args.steps, args.warmup, stream)
-    nbytes = wl.total_tokens() * wl.num_kv_heads * REF_BYTES_PER_TOKEN_HEAD[fmt]
+    nbytes = alg_token_heads(wl, prefix is not None) * REF_BYTES_PER_TOKEN_HEAD[fmt]
     del cache, ws, out
     torch.cuda.empty_cache()
     return {"tokens_per_s": wl.total_tokens() / (ms_step * 1e-3), "ms_per_step": ms_step,
@@ -255,7 +281,14 @@ def main():
     q = wl.q.to(dev)
     pt = torch.as_tensor(wl.page_table, device=dev)
     ctx = torch.as_tensor(wl.context_lens, device=dev)
-    ws = uq.alloc_workspace(desc, wl.batch, wl.num_q_heads, wl.max_context, part, dev)
+    prefix = None
+    if wl.shared_prefix_tokens and not args.no_cascade:
+        prefix = uq.SharedPrefix(torch.as_tensor(wl.prefix_pages.astype(np.int32), device=dev),
+                                 torch.as_tensor(wl.prefix_lens(), device=dev), wl.shared_prefix_tokens)
+        ws = torch.empty(uq.cascade_workspace_bytes(wl.num_kv_heads, wl.batch, wl.num_q_heads, wl.max_context, prefix,
+                                                    part), dtype=torch.uint8, device=dev)
+    else:
+        ws = uq.alloc_workspace(desc, wl.batch, wl.num_q_heads, wl.max_context, part, dev)
     out = torch.empty((wl.batch, wl.num_q_heads, 128), dtype=torch.float32, device=dev)
     # the step's new token of every sequence (written at its last position by the step)
     g = torch.Generator(device=dev).manual_seed(12345)
@@ -267,11 +300,18 @@ def main():
     def step(ev_a=None, ev_b=None):
         if ev_a is not None:
             ev_a.record(stream)
-        uq.decode_step(desc, q, k_new, v_new, codes, scales, pt, ctx, wl.max_context, scale, part, ws, out,
-                       partials_only=True)
+        if prefix is None:
+            uq.decode_step(desc, q, k_new, v_new, codes, scales, pt, ctx, wl.max_context, scale, part, ws, out,
+                           partials_only=True)
+        else:
+            uq.decode_cascade(desc, q, codes, scales, pt, ctx, wl.max_context, prefix, scale, part, ws, out,
+                              k_new=k_new, v_new=v_new, partials_only=True)
         if ev_b is not None:
             ev_b.record(stream)
-        uq.decode_merge(desc, wl.batch, wl.num_q_heads, ctx, wl.max_context, part, ws, out)
+        if prefix is None:
+            uq.decode_merge(desc, wl.batch, wl.num_q_heads, ctx, wl.max_context, part, ws, out)
+        else:
+            uq.decode_cascade_merge(desc, wl.batch, wl.num_q_heads, ctx, wl.max_context, prefix, part, ws, out)
 
     if args.calib_copy_mib > 0:
         n = args.calib_copy_mib << 20
@@ -283,8 +323,10 @@ def main():
     ms_step, dec_ms = timed(step, args.steps, args.warmup, stream)
 
     tokens = wl.total_tokens()
-    kv_bytes = wl.kv_bytes_fp4()
-    achieved = kv_bytes / (dec_ms * 1e-3) / 1e9
+    kv_bytes = wl.kv_bytes_fp4()            # logical: every sequence's whole context
+    alg_tokens = alg_token_heads(wl, prefix is not None) // wl.num_kv_heads
+    alg_bytes = alg_tokens * wl.num_kv_heads * KV_BYTES_PER_TOKEN_HEAD
+    achieved = alg_bytes / (dec_ms * 1e-3) / 1e9
     result = {
         "metric": "decode-attention KV tokens/s and achieved HBM GB/s (% of peak) at 32k context",
         "value": tokens / (ms_step * 1e-3),
@@ -300,12 +342,13 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "batch": wl.batch, "num_q_heads": wl.num_q_heads,
                    "num_kv_heads": wl.num_kv_heads, "head_dim": 128, "context": int(wl.max_context),
-                   "page_size": 16, "partition_tokens": int(part), "parallelism": "single-gpu"},
+                   "page_size": 16, "partition_tokens": int(part), "parallelism": "single-gpu",
+                   "shared_prefix_tokens": int(wl.shared_prefix_tokens), "cascade": prefix is not None},
         "hbm_gbs_step": kv_bytes / (ms_step * 1e-3) / 1e9,
         "hbm_frac_step": kv_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "roofline": {"bound": "hbm", "kernel": "decode_kernel", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": profiled_traffic(wl.name),
-                     "launch_ms": dec_ms, "bytes_per_launch": kv_bytes},
+                     "launch_ms": dec_ms, "bytes_per_launch": alg_bytes, "logical_bytes_per_launch": kv_bytes},
     }
     fmts = [f for f in args.comparators.split(",") if f and f != "none"]
     if fmts:
@@ -313,7 +356,7 @@ def main():
         for fmt in fmts:
             if fmt not in REF_BYTES_PER_TOKEN_HEAD:
                 sys.exit(f"unknown comparator {fmt!r}")
-            comp[f"{fmt}_kv"] = comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, args, dev, stream)
+            comp[f"{fmt}_kv"] = comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, args, dev, stream, prefix)
             comp[f"fp4_over_{fmt}_tokens_per_s"] = result["value"] / comp[f"{fmt}_kv"]["tokens_per_s"]
         result["comparators"] = comp
     if not args.no_write_path:

@@ -241,6 +241,66 @@ uq_status uq_decode_merge(const uq_cache_desc *desc, int32_t batch, int32_t num_
                           void *stream);
 
 /* ------------------------------------------------------------------------
+ * Cascade decode over a shared prefix.
+ *
+ * Many sequences of a batch often begin with the same pages (a shared system
+ * prompt or document: the prefix reuse the paper's agent traces show,
+ * section "Introduction" and the MiniMax-like workload).  The cascade calls
+ * read those pages once per KV head for all sequences together: a prefix
+ * block takes 16 (sequence, query head) pairs as the 16 query columns of
+ * its matrix instructions, whatever the group size, and the context blocks
+ * start each sequence after its prefix.  The two kinds of partial results
+ * are merged per (sequence, query head) as split contexts are.  The output
+ * is the attention over the same tokens as uq_decode_attention; only the
+ * order of the floating-point sums differs.
+ * ---------------------------------------------------------------------- */
+
+typedef struct uq_shared_prefix {
+    const int32_t *pages;     /* [num_tokens / 16] physical page ids of the shared prefix (device) */
+    const int32_t *lens;      /* [batch] (device): the first lens[b] tokens of sequence b are the first
+                                 lens[b] tokens of the shared prefix; a multiple of 16, at most num_tokens
+                                 and below context_lens[b] (larger values are clamped to that).  The
+                                 tokens from lens[b] on are read through page_table as usual. */
+    int32_t num_tokens;       /* prefix length in tokens, a positive multiple of 16 */
+    int32_t partition_tokens; /* prefix tokens per prefix block, a multiple of 32, or 0 for the default */
+} uq_shared_prefix;
+
+/* Workspace of the cascade calls (FP4 and comparison caches); 0 for invalid
+ * arguments. */
+size_t uq_decode_cascade_workspace_bytes(int32_t num_kv_heads, int32_t batch, int32_t num_q_heads,
+                                         int32_t max_context, int32_t partition_tokens,
+                                         const uq_shared_prefix *prefix);
+
+/*
+ * uq_decode_cascade -- uq_decode_attention (k_new == v_new == NULL) or
+ * uq_decode_step (both given) with a shared prefix.  The new token of a
+ * step is written at position len_b - 1, which lies after lens[b].
+ * Arguments, output and errors are those of uq_decode_step, plus
+ * INVALID_ARGUMENT for a NULL prefix, pages or lens, a num_tokens that is not
+ * a positive multiple of 16, a partition_tokens that is not a multiple of 32,
+ * or only one of k_new, v_new.  uq_decode_cascade_partials is its first
+ * launch and uq_decode_cascade_merge (with the same prefix and partition)
+ * its second.
+ */
+uq_status uq_decode_cascade(const uq_cache_desc *desc, const void *q, uq_dtype q_dtype, const void *k_new,
+                            const void *v_new, uq_dtype new_dtype, int32_t batch, int32_t num_q_heads,
+                            uint8_t *kv_codes, uint8_t *kv_scales, const int32_t *page_table,
+                            int32_t max_pages_per_seq, const int32_t *context_lens, int32_t max_context,
+                            const uq_shared_prefix *prefix, float softmax_scale, int32_t partition_tokens,
+                            void *workspace, size_t workspace_bytes, void *out, uq_dtype out_dtype, void *stream);
+uq_status uq_decode_cascade_partials(const uq_cache_desc *desc, const void *q, uq_dtype q_dtype, const void *k_new,
+                                     const void *v_new, uq_dtype new_dtype, int32_t batch, int32_t num_q_heads,
+                                     uint8_t *kv_codes, uint8_t *kv_scales, const int32_t *page_table,
+                                     int32_t max_pages_per_seq, const int32_t *context_lens, int32_t max_context,
+                                     const uq_shared_prefix *prefix, float softmax_scale, int32_t partition_tokens,
+                                     void *workspace, size_t workspace_bytes, void *out, uq_dtype out_dtype,
+                                     void *stream);
+uq_status uq_decode_cascade_merge(const uq_cache_desc *desc, int32_t batch, int32_t num_q_heads,
+                                  const int32_t *context_lens, int32_t max_context, const uq_shared_prefix *prefix,
+                                  int32_t partition_tokens, const void *workspace, size_t workspace_bytes, void *out,
+                                  uq_dtype out_dtype, void *stream);
+
+/* ------------------------------------------------------------------------
  * Plain comparison caches.
  *
  * The paper measures the FP4 path against a hardware FP8 KV cache and a
@@ -327,6 +387,26 @@ uq_status uq_ref_decode_step_partials(const uq_ref_cache_desc *desc, const void 
                                       int32_t max_pages_per_seq, const int32_t *context_lens, int32_t max_context,
                                       float softmax_scale, int32_t partition_tokens, void *workspace,
                                       size_t workspace_bytes, void *out, uq_dtype out_dtype, void *stream);
+/* Cascade decode over a comparison cache: uq_decode_cascade with the cache
+ * and token format of uq_ref_decode_step. */
+uq_status uq_ref_decode_cascade(const uq_ref_cache_desc *desc, const void *q, uq_dtype q_dtype, const void *k_new,
+                                const void *v_new, uq_dtype new_dtype, int32_t batch, int32_t num_q_heads,
+                                uint8_t *cache, const int32_t *page_table, int32_t max_pages_per_seq,
+                                const int32_t *context_lens, int32_t max_context, const uq_shared_prefix *prefix,
+                                float softmax_scale, int32_t partition_tokens, void *workspace,
+                                size_t workspace_bytes, void *out, uq_dtype out_dtype, void *stream);
+uq_status uq_ref_decode_cascade_partials(const uq_ref_cache_desc *desc, const void *q, uq_dtype q_dtype,
+                                         const void *k_new, const void *v_new, uq_dtype new_dtype, int32_t batch,
+                                         int32_t num_q_heads, uint8_t *cache, const int32_t *page_table,
+                                         int32_t max_pages_per_seq, const int32_t *context_lens,
+                                         int32_t max_context, const uq_shared_prefix *prefix, float softmax_scale,
+                                         int32_t partition_tokens, void *workspace, size_t workspace_bytes,
+                                         void *out, uq_dtype out_dtype, void *stream);
+uq_status uq_ref_decode_cascade_merge(const uq_ref_cache_desc *desc, int32_t batch, int32_t num_q_heads,
+                                      const int32_t *context_lens, int32_t max_context,
+                                      const uq_shared_prefix *prefix, int32_t partition_tokens,
+                                      const void *workspace, size_t workspace_bytes, void *out, uq_dtype out_dtype,
+                                      void *stream);
 uq_status uq_ref_decode_merge(const uq_ref_cache_desc *desc, int32_t batch, int32_t num_q_heads,
                               const int32_t *context_lens, int32_t max_context, int32_t partition_tokens,
                               const void *workspace, size_t workspace_bytes, void *out, uq_dtype out_dtype,

@@ -59,8 +59,9 @@ size_t partial_bytes(int32_t batch, int32_t num_q_heads, int32_t max_context, in
                    sizeof(float));
 }
 
-size_t workspace_for(int32_t batch, int32_t num_q_heads, int32_t max_context, int32_t part) {
-    return partial_bytes(batch, num_q_heads, max_context, part);
+size_t workspace_for(int32_t batch, int32_t num_q_heads, int32_t max_context, int32_t part, int64_t extra_slots = 0) {
+    return align16(size_t(batch) * size_t(num_q_heads) * size_t(num_partitions(max_context, part) + extra_slots) *
+                   (kHeadDim + 2) * sizeof(float));
 }
 
 // Fill the parameter block of the decode launches.  Workspace: the partial
@@ -69,13 +70,15 @@ uq_status make_decode_params(const uq_cache_desc* desc, const void* q, uq_dtype 
                              int32_t num_q_heads, const uint8_t* kv_codes, const uint8_t* kv_scales,
                              const int32_t* page_table, int32_t max_pages_per_seq, const int32_t* context_lens,
                              int32_t max_context, float softmax_scale, int32_t partition_tokens, void* workspace,
-                             size_t workspace_bytes, void* out, uq_dtype out_dtype, uq::DecodeParams& p) {
+                             size_t workspace_bytes, void* out, uq_dtype out_dtype, uq::DecodeParams& p,
+                             int64_t extra_slots = 0) {
     const int32_t part = partition_tokens == 0 ? pick_partition(batch, desc->num_kv_heads, max_context) : partition_tokens;
-    const size_t need = workspace_for(batch, num_q_heads, max_context, part);
+    const size_t need = workspace_for(batch, num_q_heads, max_context, part, extra_slots);
     if (workspace == nullptr) return UQ_ERR_INVALID_ARGUMENT;
     if (workspace_bytes < need) return UQ_ERR_WORKSPACE_TOO_SMALL;
     if (!aligned16(workspace)) return UQ_ERR_INVALID_ARGUMENT;
-    const int64_t np = num_partitions(max_context, part);
+    const int64_t np_ctx = num_partitions(max_context, part);
+    const int64_t np = np_ctx + extra_slots;
     // one linear grid of partitions x kv heads x sequences
     if (np * desc->num_kv_heads * batch > 0x7FFFFFFF) return UQ_ERR_UNSUPPORTED;
     p.q = q;
@@ -109,6 +112,52 @@ uq_status make_decode_params(const uq_cache_desc* desc, const void* q, uq_dtype 
     p.rotate_v = desc->rotate_v != 0;
     p.kv_fmt = uq::kFp4;
     p.out_scale = 1.0f;
+    p.prefix_pages = nullptr;
+    p.prefix_lens = nullptr;
+    p.prefix_tokens = 0;
+    p.prefix_partition = 0;
+    p.prefix_chunks = 0;
+    p.prefix_blocks = 0;
+    p.suffix_partitions = int32_t(np_ctx);
+    return UQ_OK;
+}
+
+// Cascade decode: the prefix partition (tokens per prefix block; the
+// default gives about 1024 prefix blocks, at least 32 tokens each) and the
+// number of prefix partial slots per (sequence, query head).
+int32_t prefix_partition(const uq_shared_prefix* pre, int32_t num_kv_heads, int32_t batch, int32_t group) {
+    if (pre->partition_tokens > 0) return pre->partition_tokens;
+    const int64_t chunks = (int64_t(batch) * group + 15) / 16;
+    int64_t parts = (1024 + num_kv_heads * chunks - 1) / (num_kv_heads * chunks);
+    parts = parts < 1 ? 1 : parts;
+    int64_t pp = (int64_t(pre->num_tokens) + parts - 1) / parts;
+    pp = (pp + 31) & ~int64_t(31);
+    return int32_t(pp < 32 ? 32 : pp);
+}
+
+uq_status check_prefix(const uq_shared_prefix* pre) {
+    if (pre == nullptr || pre->pages == nullptr || pre->lens == nullptr) return UQ_ERR_INVALID_ARGUMENT;
+    if (pre->num_tokens < 16 || pre->num_tokens % 16 != 0) return UQ_ERR_INVALID_ARGUMENT;
+    if (pre->partition_tokens < 0 || pre->partition_tokens % 32 != 0) return UQ_ERR_INVALID_ARGUMENT;
+    return UQ_OK;
+}
+
+int64_t prefix_slots(const uq_shared_prefix* pre, int32_t num_kv_heads, int32_t batch, int32_t group) {
+    const int32_t pp = prefix_partition(pre, num_kv_heads, batch, group);
+    return (int64_t(pre->num_tokens) + pp - 1) / pp;
+}
+
+// Fill the cascade fields of a parameter block made with the prefix slots.
+uq_status apply_prefix(const uq_shared_prefix* pre, uq::DecodeParams& p) {
+    p.prefix_pages = pre->pages;
+    p.prefix_lens = pre->lens;
+    p.prefix_tokens = pre->num_tokens;
+    p.prefix_partition = prefix_partition(pre, p.num_kv_heads, p.batch, p.group);
+    p.prefix_chunks = int32_t((int64_t(p.batch) * p.group + 15) / 16);
+    const int64_t blocks = int64_t(p.num_kv_heads) * p.prefix_chunks *
+                           ((int64_t(pre->num_tokens) + p.prefix_partition - 1) / p.prefix_partition);
+    if (blocks + int64_t(p.suffix_partitions) * p.num_kv_heads * p.batch > 0x7FFFFFFF) return UQ_ERR_UNSUPPORTED;
+    p.prefix_blocks = int32_t(blocks);
     return UQ_OK;
 }
 
@@ -237,7 +286,8 @@ static uq_status decode_setup(const uq_cache_desc* desc, const void* q, uq_dtype
                               int32_t num_q_heads, const uint8_t* kv_codes, const uint8_t* kv_scales,
                               const int32_t* page_table, int32_t max_pages_per_seq, const int32_t* context_lens,
                               int32_t max_context, float softmax_scale, int32_t partition_tokens, void* workspace,
-                              size_t workspace_bytes, void* out, uq_dtype out_dtype, uq::DecodeParams& p) {
+                              size_t workspace_bytes, void* out, uq_dtype out_dtype, uq::DecodeParams& p,
+                              int64_t extra_slots = 0) {
     uq_status s = check_split_args(desc, q, q_dtype, batch, num_q_heads, kv_codes, kv_scales, page_table,
                                    max_pages_per_seq, context_lens, max_context, softmax_scale, partition_tokens);
     if (s != UQ_OK) return s;
@@ -246,7 +296,7 @@ static uq_status decode_setup(const uq_cache_desc* desc, const void* q, uq_dtype
     if (!aligned16(out)) return UQ_ERR_INVALID_ARGUMENT;
     return make_decode_params(desc, q, q_dtype, batch, num_q_heads, kv_codes, kv_scales, page_table, max_pages_per_seq,
                               context_lens, max_context, softmax_scale, partition_tokens, workspace, workspace_bytes,
-                              out, out_dtype, p);
+                              out, out_dtype, p, extra_slots);
 }
 
 // The new-token arguments of the decode-step calls.
@@ -389,13 +439,15 @@ static uq_status ref_decode_setup(const uq_ref_cache_desc* desc, const void* q, 
                                   int32_t num_q_heads, const uint8_t* cache, const int32_t* page_table,
                                   int32_t max_pages_per_seq, const int32_t* context_lens, int32_t max_context,
                                   float softmax_scale, int32_t partition_tokens, void* workspace,
-                                  size_t workspace_bytes, void* out, uq_dtype out_dtype, uq::DecodeParams& p) {
+                                  size_t workspace_bytes, void* out, uq_dtype out_dtype, uq::DecodeParams& p,
+                                  int64_t extra_slots = 0) {
     uq_status s = check_ref_desc(desc);
     if (s != UQ_OK) return s;
     if (q_dtype != UQ_F32 && q_dtype != UQ_BF16 && q_dtype != UQ_F16) return UQ_ERR_UNSUPPORTED;
     const uq_cache_desc g = geometry_of(desc);
     s = decode_setup(&g, q, q_dtype, batch, num_q_heads, cache, cache, page_table, max_pages_per_seq, context_lens,
-                     max_context, softmax_scale, partition_tokens, workspace, workspace_bytes, out, out_dtype, p);
+                     max_context, softmax_scale, partition_tokens, workspace, workspace_bytes, out, out_dtype, p,
+                     extra_slots);
     if (s != UQ_OK) return s;
     p.kv_fmt = ref_fmt(desc);
     p.scales = nullptr;
@@ -487,6 +539,185 @@ uq_status uq_ref_decode_merge(const uq_ref_cache_desc* desc, int32_t batch, int3
     s = make_decode_params(&g, nullptr, UQ_F32, batch, num_q_heads, nullptr, nullptr, nullptr, 1, context_lens,
                            max_context, 1.0f, partition_tokens, const_cast<void*>(workspace), workspace_bytes, out,
                            out_dtype, p);
+    if (s != UQ_OK) return s;
+    p.kv_fmt = ref_fmt(desc);
+    if (desc->format == UQ_REF_FP8_E4M3) p.out_scale = desc->v_scale;
+    return from_hip(uq::launch_decode_merge(p, static_cast<hipStream_t>(stream)));
+}
+
+// ---------------------------------------------------------------- cascade decode
+
+static int32_t group_of(int32_t num_q_heads, int32_t num_kv_heads) {
+    return num_kv_heads > 0 && num_q_heads % num_kv_heads == 0 ? num_q_heads / num_kv_heads : 1;
+}
+
+size_t uq_decode_cascade_workspace_bytes(int32_t num_kv_heads, int32_t batch, int32_t num_q_heads,
+                                         int32_t max_context, int32_t partition_tokens,
+                                         const uq_shared_prefix* prefix) {
+    if (check_prefix(prefix) != UQ_OK) return 0;
+    uq_cache_desc d;
+    d.num_kv_heads = num_kv_heads;
+    d.head_dim = kHeadDim;
+    d.page_size = kPageSize;
+    d.group_size = kGroupSize;
+    d.num_pages = 1;
+    d.c = 0.156f;
+    d.rotate_v = 0;
+    if (check_decode_common(&d, batch, num_q_heads, max_context, partition_tokens) != UQ_OK) return 0;
+    const int32_t part = partition_tokens == 0 ? pick_partition(batch, num_kv_heads, max_context) : partition_tokens;
+    return workspace_for(batch, num_q_heads, max_context, part,
+                         prefix_slots(prefix, num_kv_heads, batch, group_of(num_q_heads, num_kv_heads)));
+}
+
+static uq_status cascade_finish_setup(const void* k_new, const void* v_new, uq_dtype new_dtype,
+                                      const uq_shared_prefix* prefix, uq::DecodeParams& p) {
+    if (k_new != nullptr || v_new != nullptr) {
+        const uq_status s = step_args(k_new, v_new, new_dtype, p);
+        if (s != UQ_OK) return s;
+    }
+    return apply_prefix(prefix, p);
+}
+
+static uq_status cascade_setup(const uq_cache_desc* desc, const void* q, uq_dtype q_dtype, const void* k_new,
+                               const void* v_new, uq_dtype new_dtype, int32_t batch, int32_t num_q_heads,
+                               uint8_t* kv_codes, uint8_t* kv_scales, const int32_t* page_table,
+                               int32_t max_pages_per_seq, const int32_t* context_lens, int32_t max_context,
+                               const uq_shared_prefix* prefix, float softmax_scale, int32_t partition_tokens,
+                               void* workspace, size_t workspace_bytes, void* out, uq_dtype out_dtype,
+                               uq::DecodeParams& p) {
+    uq_status s = check_prefix(prefix);
+    if (s != UQ_OK) return s;
+    s = check_desc(desc);
+    if (s != UQ_OK) return s;
+    s = decode_setup(desc, q, q_dtype, batch, num_q_heads, kv_codes, kv_scales, page_table, max_pages_per_seq,
+                     context_lens, max_context, softmax_scale, partition_tokens, workspace, workspace_bytes, out,
+                     out_dtype, p, prefix_slots(prefix, desc->num_kv_heads, batch, group_of(num_q_heads, desc->num_kv_heads)));
+    if (s != UQ_OK) return s;
+    return cascade_finish_setup(k_new, v_new, new_dtype, prefix, p);
+}
+
+uq_status uq_decode_cascade(const uq_cache_desc* desc, const void* q, uq_dtype q_dtype, const void* k_new,
+                            const void* v_new, uq_dtype new_dtype, int32_t batch, int32_t num_q_heads,
+                            uint8_t* kv_codes, uint8_t* kv_scales, const int32_t* page_table,
+                            int32_t max_pages_per_seq, const int32_t* context_lens, int32_t max_context,
+                            const uq_shared_prefix* prefix, float softmax_scale, int32_t partition_tokens,
+                            void* workspace, size_t workspace_bytes, void* out, uq_dtype out_dtype, void* stream) {
+    uq::DecodeParams p;
+    uq_status s = cascade_setup(desc, q, q_dtype, k_new, v_new, new_dtype, batch, num_q_heads, kv_codes, kv_scales,
+                                page_table, max_pages_per_seq, context_lens, max_context, prefix, softmax_scale,
+                                partition_tokens, workspace, workspace_bytes, out, out_dtype, p);
+    if (s != UQ_OK) return s;
+    s = from_hip(uq::launch_decode_partials(p, static_cast<hipStream_t>(stream)));
+    if (s != UQ_OK) return s;
+    return from_hip(uq::launch_decode_merge(p, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uq_decode_cascade_partials(const uq_cache_desc* desc, const void* q, uq_dtype q_dtype, const void* k_new,
+                                     const void* v_new, uq_dtype new_dtype, int32_t batch, int32_t num_q_heads,
+                                     uint8_t* kv_codes, uint8_t* kv_scales, const int32_t* page_table,
+                                     int32_t max_pages_per_seq, const int32_t* context_lens, int32_t max_context,
+                                     const uq_shared_prefix* prefix, float softmax_scale, int32_t partition_tokens,
+                                     void* workspace, size_t workspace_bytes, void* out, uq_dtype out_dtype,
+                                     void* stream) {
+    uq::DecodeParams p;
+    uq_status s = cascade_setup(desc, q, q_dtype, k_new, v_new, new_dtype, batch, num_q_heads, kv_codes, kv_scales,
+                                page_table, max_pages_per_seq, context_lens, max_context, prefix, softmax_scale,
+                                partition_tokens, workspace, workspace_bytes, out, out_dtype, p);
+    if (s != UQ_OK) return s;
+    return from_hip(uq::launch_decode_partials(p, static_cast<hipStream_t>(stream)));
+}
+
+// Shared set-up of the two cascade merge calls.
+static uq_status cascade_merge_setup(const uq_cache_desc* g, int32_t batch, int32_t num_q_heads,
+                                     const int32_t* context_lens, int32_t max_context, const uq_shared_prefix* prefix,
+                                     int32_t partition_tokens, const void* workspace, size_t workspace_bytes,
+                                     void* out, uq_dtype out_dtype, uq::DecodeParams& p) {
+    uq_status s = check_prefix(prefix);
+    if (s != UQ_OK) return s;
+    s = check_decode_common(g, batch, num_q_heads, max_context, partition_tokens);
+    if (s != UQ_OK) return s;
+    if (context_lens == nullptr || out == nullptr) return UQ_ERR_INVALID_ARGUMENT;
+    if (out_dtype != UQ_F32 && out_dtype != UQ_BF16) return UQ_ERR_UNSUPPORTED;
+    if (!aligned16(out)) return UQ_ERR_INVALID_ARGUMENT;
+    s = make_decode_params(g, nullptr, UQ_F32, batch, num_q_heads, nullptr, nullptr, nullptr, 1, context_lens,
+                           max_context, 1.0f, partition_tokens, const_cast<void*>(workspace), workspace_bytes, out,
+                           out_dtype, p, prefix_slots(prefix, g->num_kv_heads, batch, num_q_heads / g->num_kv_heads));
+    if (s != UQ_OK) return s;
+    return apply_prefix(prefix, p);
+}
+
+uq_status uq_decode_cascade_merge(const uq_cache_desc* desc, int32_t batch, int32_t num_q_heads,
+                                  const int32_t* context_lens, int32_t max_context, const uq_shared_prefix* prefix,
+                                  int32_t partition_tokens, const void* workspace, size_t workspace_bytes, void* out,
+                                  uq_dtype out_dtype, void* stream) {
+    uq_status s = check_desc(desc);
+    if (s != UQ_OK) return s;
+    uq::DecodeParams p;
+    s = cascade_merge_setup(desc, batch, num_q_heads, context_lens, max_context, prefix, partition_tokens, workspace,
+                            workspace_bytes, out, out_dtype, p);
+    if (s != UQ_OK) return s;
+    return from_hip(uq::launch_decode_merge(p, static_cast<hipStream_t>(stream)));
+}
+
+static uq_status ref_cascade_setup(const uq_ref_cache_desc* desc, const void* q, uq_dtype q_dtype, const void* k_new,
+                                   const void* v_new, uq_dtype new_dtype, int32_t batch, int32_t num_q_heads,
+                                   uint8_t* cache, const int32_t* page_table, int32_t max_pages_per_seq,
+                                   const int32_t* context_lens, int32_t max_context, const uq_shared_prefix* prefix,
+                                   float softmax_scale, int32_t partition_tokens, void* workspace,
+                                   size_t workspace_bytes, void* out, uq_dtype out_dtype, uq::DecodeParams& p) {
+    uq_status s = check_prefix(prefix);
+    if (s != UQ_OK) return s;
+    s = check_ref_desc(desc);
+    if (s != UQ_OK) return s;
+    s = ref_decode_setup(desc, q, q_dtype, batch, num_q_heads, cache, page_table, max_pages_per_seq, context_lens,
+                         max_context, softmax_scale, partition_tokens, workspace, workspace_bytes, out, out_dtype, p,
+                         prefix_slots(prefix, desc->num_kv_heads, batch, group_of(num_q_heads, desc->num_kv_heads)));
+    if (s != UQ_OK) return s;
+    return cascade_finish_setup(k_new, v_new, new_dtype, prefix, p);
+}
+
+uq_status uq_ref_decode_cascade(const uq_ref_cache_desc* desc, const void* q, uq_dtype q_dtype, const void* k_new,
+                                const void* v_new, uq_dtype new_dtype, int32_t batch, int32_t num_q_heads,
+                                uint8_t* cache, const int32_t* page_table, int32_t max_pages_per_seq,
+                                const int32_t* context_lens, int32_t max_context, const uq_shared_prefix* prefix,
+                                float softmax_scale, int32_t partition_tokens, void* workspace,
+                                size_t workspace_bytes, void* out, uq_dtype out_dtype, void* stream) {
+    uq::DecodeParams p;
+    uq_status s = ref_cascade_setup(desc, q, q_dtype, k_new, v_new, new_dtype, batch, num_q_heads, cache, page_table,
+                                    max_pages_per_seq, context_lens, max_context, prefix, softmax_scale,
+                                    partition_tokens, workspace, workspace_bytes, out, out_dtype, p);
+    if (s != UQ_OK) return s;
+    s = from_hip(uq::launch_decode_partials(p, static_cast<hipStream_t>(stream)));
+    if (s != UQ_OK) return s;
+    return from_hip(uq::launch_decode_merge(p, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uq_ref_decode_cascade_partials(const uq_ref_cache_desc* desc, const void* q, uq_dtype q_dtype,
+                                         const void* k_new, const void* v_new, uq_dtype new_dtype, int32_t batch,
+                                         int32_t num_q_heads, uint8_t* cache, const int32_t* page_table,
+                                         int32_t max_pages_per_seq, const int32_t* context_lens,
+                                         int32_t max_context, const uq_shared_prefix* prefix, float softmax_scale,
+                                         int32_t partition_tokens, void* workspace, size_t workspace_bytes,
+                                         void* out, uq_dtype out_dtype, void* stream) {
+    uq::DecodeParams p;
+    uq_status s = ref_cascade_setup(desc, q, q_dtype, k_new, v_new, new_dtype, batch, num_q_heads, cache, page_table,
+                                    max_pages_per_seq, context_lens, max_context, prefix, softmax_scale,
+                                    partition_tokens, workspace, workspace_bytes, out, out_dtype, p);
+    if (s != UQ_OK) return s;
+    return from_hip(uq::launch_decode_partials(p, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uq_ref_decode_cascade_merge(const uq_ref_cache_desc* desc, int32_t batch, int32_t num_q_heads,
+                                      const int32_t* context_lens, int32_t max_context,
+                                      const uq_shared_prefix* prefix, int32_t partition_tokens,
+                                      const void* workspace, size_t workspace_bytes, void* out, uq_dtype out_dtype,
+                                      void* stream) {
+    uq_status s = check_ref_desc(desc);
+    if (s != UQ_OK) return s;
+    const uq_cache_desc g = geometry_of(desc);
+    uq::DecodeParams p;
+    s = cascade_merge_setup(&g, batch, num_q_heads, context_lens, max_context, prefix, partition_tokens, workspace,
+                            workspace_bytes, out, out_dtype, p);
     if (s != UQ_OK) return s;
     p.kv_fmt = ref_fmt(desc);
     if (desc->format == UQ_REF_FP8_E4M3) p.out_scale = desc->v_scale;

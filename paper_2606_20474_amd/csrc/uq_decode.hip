@@ -392,30 +392,71 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
     // every sequence and the XCDs holding the late partitions of short
     // sequences would idle), and it keeps one kv head on the same XCDs, whose
     // L2 then serves pages that several sequences share.
+    //
+    // Cascade decode puts the prefix blocks first: one per (kv head, chunk of
+    // 16 query columns, prefix partition), same order.  A prefix block's
+    // columns are (sequence, query head) pairs f = 16 * chunk + column of the
+    // flattened batch (b = f / G, head hk * G + f % G), and it reads the
+    // shared prefix pages once for all of them.
     const int lin = blockIdx.x;
-    const int hk = lin % p.num_kv_heads;
-    const int b = (lin / p.num_kv_heads) % p.batch;
-    const int part = lin / (p.num_kv_heads * p.batch);
+    const bool cascade = p.prefix_pages != nullptr;
+    const bool pre = lin < p.prefix_blocks;                           // block-uniform
+    const int lin2 = pre ? lin : lin - p.prefix_blocks;
+    const int hk = lin2 % p.num_kv_heads;
+    const int rest = lin2 / p.num_kv_heads;
+    const int nb = pre ? p.prefix_chunks : p.batch;
+    const int b = pre ? 0 : rest % nb;                                 // sequence (context blocks)
+    const int chunk = pre ? rest % nb : 0;                             // column chunk (prefix blocks)
+    const int part = rest / nb;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: scalar control flow
     const int G = p.group;
+    const int BG = p.batch * G;
 
-    int ctx = p.context_lens[b];
-    ctx = ctx < p.max_context ? ctx : p.max_context;
-    const int start = part * p.partition_tokens;
-    if (start >= ctx) {
-        // nothing of this sequence here; an empty context still gets its zero output
-        if (ctx <= 0 && part == 0) {
-            for (int r = tid >> 4; r < G; r += kThreads / 16) {
-                const float z[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-                write_out(p, int64_t(b) * p.num_q_heads + hk * G + r, tid & 15, z);
-            }
+    int start, end, ctx = 0;
+    if (pre) {
+        start = part * p.prefix_partition;
+        end = (start + p.prefix_partition) < p.prefix_tokens ? (start + p.prefix_partition) : p.prefix_tokens;
+    } else {
+        ctx = p.context_lens[b];
+        ctx = ctx < p.max_context ? ctx : p.max_context;
+        start = part * p.partition_tokens;
+        if (cascade) {
+            // the context blocks start after the tokens the prefix blocks serve
+            int pl = p.prefix_lens[b];
+            pl = pl < p.prefix_tokens ? pl : p.prefix_tokens;
+            pl = pl < ctx - 1 ? pl : ctx - 1;
+            pl = pl > 0 ? (pl & ~15) : 0;
+            if (start + p.partition_tokens <= pl) return;              // wholly inside the prefix
+            start = start > pl ? start : pl;
         }
-        return;
+        if (start >= ctx) {
+            // nothing of this sequence here; an empty context still gets its zero output
+            if (ctx <= 0 && part == 0) {
+                for (int r = tid >> 4; r < G; r += kThreads / 16) {
+                    const float z[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+                    write_out(p, int64_t(b) * p.num_q_heads + hk * G + r, tid & 15, z);
+                }
+            }
+            return;
+        }
+        end = (part * p.partition_tokens + p.partition_tokens) < ctx ? (part * p.partition_tokens + p.partition_tokens) : ctx;
     }
-    const int end = (start + p.partition_tokens) < ctx ? (start + p.partition_tokens) : ctx;
-    const int np_b = (ctx + p.partition_tokens - 1) / p.partition_tokens;
+    // a single partition holding the whole context is finished in place
+    const bool in_place = !cascade && ctx <= p.partition_tokens;
+    // query row r (0..15) of this block: valid, its sequence and query head
+    auto row_of = [&](int r, int& rb, int& rhq) -> bool {
+        if (pre) {
+            const int f = 16 * chunk + r;
+            rb = f / G;
+            rhq = hk * G + (f - rb * G);
+            return f < BG;
+        }
+        rb = b;
+        rhq = hk * G + r;
+        return r < G;
+    };
     // Decode step: the block whose partition holds the last position writes
     // the sequence's new token there.  The wave that will read that page
     // encodes the token in its prologue, stores it to the pools without
@@ -424,7 +465,7 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
     // page for this kv head (partitions are whole pages).
     const int pos_new = ctx - 1;
     const int it_new = (pos_new - start) >> 5;                       // iteration holding the token
-    const bool append = p.k_new != nullptr && pos_new >= start && wave == it_new % W;   // wave-uniform
+    const bool append = !pre && p.k_new != nullptr && pos_new >= start && wave == it_new % W;   // wave-uniform
     const int k_new_local = it_new / W;                              // that wave's local iteration
 
     __shared__ __attribute__((aligned(16))) uint8_t smem[W * ring_bytes<F>()];
@@ -443,8 +484,9 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
         qw[h][1] = 0u;
         const int qr = (tid >> 4) + h * (kThreads / 16);
         const int qL = tid & 15;
-        if (qr < G) {
-            const int64_t elem = (int64_t(b) * p.num_q_heads + hk * G + qr) * kHeadDim + 8 * qL;
+        int rb, rhq;
+        if (qr < 16 && row_of(qr, rb, rhq)) {
+            const int64_t elem = (int64_t(rb) * p.num_q_heads + rhq) * kHeadDim + 8 * qL;
             if (p.q_dtype == 3) {
                 const uint2 w = *reinterpret_cast<const uint2*>(static_cast<const uint8_t*>(p.q) + elem);
                 qw[h][0] = w.x;
@@ -481,7 +523,22 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
     const int n_pages = (end - start + 15) >> 4;
     const int n_iter = (n_pages + 1) >> 1;
     const int n_local = wave < n_iter ? (n_iter - wave + W - 1) / W : 0;
-    const int32_t* pt_row = p.page_table + int64_t(b) * p.max_pages_per_seq;
+    const int32_t* pt_row = pre ? p.prefix_pages : p.page_table + int64_t(b) * p.max_pages_per_seq;
+    // prefix blocks: this lane's column attends to the first `lim` prefix tokens
+    int lim = end;
+    if (pre) {
+        int rb, rhq;
+        lim = 0;
+        if (row_of(lane & 15, rb, rhq)) {
+            int c2 = p.context_lens[rb];
+            c2 = c2 < p.max_context ? c2 : p.max_context;
+            int pl = p.prefix_lens[rb];
+            pl = pl < p.prefix_tokens ? pl : p.prefix_tokens;
+            pl = pl < c2 - 1 ? pl : c2 - 1;
+            lim = pl > 0 ? (pl & ~15) : 0;
+            lim = lim < end ? lim : end;
+        }
+    }
     const int g4 = lane >> 4;           // lane group: tokens 4*g4..4*g4+3 of each page
     const int n = lane & 15;
     uint8_t* ring = smem + wave * ring_bytes<F>();
@@ -512,16 +569,18 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
     for (int h = 0; h < kQRounds; ++h) {
         const int qr = (tid >> 4) + h * (kThreads / 16);
         const int qL = tid & 15;
+        int rb, rhq;
+        const bool qvalid = qr < 16 && row_of(qr, rb, rhq);
         if constexpr (F == kBf16) {
             // channels 8*qL..+7 are k-step qL/4, lane (qL%4)*16 + qr, 16 bytes
             uint4 w = {0u, 0u, 0u, 0u};
-            if (qr < G)
+            if (qvalid)
                 w = uint4{pack_bf16x2(qx[h][0], qx[h][1]), pack_bf16x2(qx[h][2], qx[h][3]),
                           pack_bf16x2(qx[h][4], qx[h][5]), pack_bf16x2(qx[h][6], qx[h][7])};
             *reinterpret_cast<uint4*>(q_lds + ((qL >> 2) * 64 + (qL & 3) * 16 + qr) * 16) = w;
         } else {
             uint32_t lo = qw[h][0], hi = qw[h][1];
-            if (qr < G && p.q_dtype != 3) {
+            if (qvalid && p.q_dtype != 3) {
                 if constexpr (F == kFp4) wht128_x8(qx[h], qL);
                 lo = 0;
                 hi = 0;
@@ -533,7 +592,7 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
             }
             // FP8 operand of the 16x16x128 scaled MFMA: lane 16*g + n holds
             // column n, channels 16g..16g+15 in bytes 0..15 and
-            // 64+16g..64+16g+15 in bytes 16..31.  Rows qr >= G stay zero.
+            // 64+16g..64+16g+15 in bytes 16..31.  Rows without a query stay zero.
             const int ch = 8 * qL;
             const int g = (ch & 63) >> 4;
             const int e0 = (ch & 15) + (ch >= 64 ? 16 : 0);
@@ -563,7 +622,8 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
 
     const float sl2 = p.scale_log2;
     const uint32_t k23 = 23u;
-    float m_run = -__builtin_inff();
+    // finite start: a column with every score masked keeps exp2(-inf - m) = 0
+    float m_run = -1e30f;
     // running softmax sum per column, on the matrix unit: every row of
     // (all ones) x P is the column sum of P
     const v8bf ones = __builtin_bit_cast(v8bf, uint4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u});
@@ -617,18 +677,26 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
         }
         const int it = wave + W * k;
         const int tok0 = start + 32 * it + 4 * g4;   // token of x[0]; x[4] is tok0 + 16
-        if (start + 32 * it + 32 > end) {
+        if (__builtin_amdgcn_ballot_w64(start + 32 * it + 32 > lim) != 0) {
+            // scores past the column's last token (the partition end, or a
+            // prefix column's own length)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                if (tok0 + i >= end) {
-                    x[i] = -__builtin_inff();
-                    vs0 &= ~(0xFFu << (8 * i));
-                    zero_token(c, 0, i);
-                }
-                if (tok0 + 16 + i >= end) {
-                    x[4 + i] = -__builtin_inff();
-                    vs1 &= ~(0xFFu << (8 * i));
-                    zero_token(c, 1, i);
+                if (tok0 + i >= lim) x[i] = -__builtin_inff();
+                if (tok0 + 16 + i >= lim) x[4 + i] = -__builtin_inff();
+            }
+            if (start + 32 * it + 32 > end) {
+                // tokens past the end: no column reads their V
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    if (tok0 + i >= end) {
+                        vs0 &= ~(0xFFu << (8 * i));
+                        zero_token(c, 0, i);
+                    }
+                    if (tok0 + 16 + i >= end) {
+                        vs1 &= ~(0xFFu << (8 * i));
+                        zero_token(c, 1, i);
+                    }
                 }
             }
         }
@@ -696,10 +764,10 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
 
 #pragma unroll
     for (int h = 0; h < kQRounds; ++h) {
-        const int r = (tid >> 4) + h * (kThreads / 16);   // query head within the group
+        const int r = (tid >> 4) + h * (kThreads / 16);   // query row of the block
         const int L = tid & 15;                           // channels 8L..8L+7
-        if (r >= G) continue;                             // whole 16-lane rows skip together
-        const int hq = hk * G + r;
+        int rb, hq;
+        if (r >= 16 || !row_of(r, rb, hq)) continue;     // whole 16-lane rows skip together
         float M = red_m[0][r];
 #pragma unroll
         for (int w = 1; w < W; ++w) M = __builtin_fmaxf(M, red_m[w][r]);
@@ -718,13 +786,14 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
             for (int w = 0; w < W; ++w) s += f[w] * red_acc[(w * 16 + r) * kAccStride + 8 * L + cc];
             o[cc] = s;
         }
-        if (np_b == 1) {
+        if (in_place) {
             // the whole context is in this block: finish here
             finish_row(p, o, lsum, L);
-            write_out(p, int64_t(b) * p.num_q_heads + hq, L, o);
+            write_out(p, int64_t(rb) * p.num_q_heads + hq, L, o);
         } else {
             // several partitions: publish this one for the merge kernel
-            const int64_t prow = (int64_t(b) * p.num_q_heads + hq) * p.num_partitions + part;
+            const int slot = pre ? p.suffix_partitions + part : part;
+            const int64_t prow = (int64_t(rb) * p.num_q_heads + hq) * p.num_partitions + slot;
             float4* dst = reinterpret_cast<float4*>(p.part_acc + prow * kHeadDim + 8 * L);
             dst[0] = make_float4(o[0], o[1], o[2], o[3]);
             dst[1] = make_float4(o[4], o[5], o[6], o[7]);
@@ -736,6 +805,9 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
 // Merge the partitions of every (sequence, query head) with more than one:
 // online over the partitions (loads independent of the running state, so
 // they overlap), then finish the row.  One 16-lane row per query head.
+// Cascade decode: the context partitions after the tokens the prefix serves,
+// then that sequence's prefix partitions; always merged (every block of a
+// cascade call writes a partial).
 __global__ void __launch_bounds__(256) merge_kernel(DecodeParams p) {
     const int hk = blockIdx.x;
     const int b = blockIdx.y;
@@ -745,16 +817,26 @@ __global__ void __launch_bounds__(256) merge_kernel(DecodeParams p) {
     int ctx = p.context_lens[b];
     ctx = ctx < p.max_context ? ctx : p.max_context;
     const int np = ctx > 0 ? (ctx + p.partition_tokens - 1) / p.partition_tokens : 0;
-    if (np <= 1) return;        // finished by the decode kernel
+    int first = 0, nq = 0;
+    if (p.prefix_pages != nullptr) {
+        int pl = p.prefix_lens[b];
+        pl = pl < p.prefix_tokens ? pl : p.prefix_tokens;
+        pl = pl < ctx - 1 ? pl : ctx - 1;
+        pl = pl > 0 ? (pl & ~15) : 0;
+        first = pl / p.partition_tokens;
+        nq = (pl + p.prefix_partition - 1) / p.prefix_partition;
+        if (np - first + nq <= 0) return;   // empty context: written by the decode kernel
+    } else if (np <= 1) {
+        return;                             // finished by the decode kernel
+    }
     const int hq = hk * p.group + r;
     const int64_t row0 = (int64_t(b) * p.num_q_heads + hq) * p.num_partitions;
     float M = -__builtin_inff();
     float lsum = 0.f;
     float o[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-    for (int q = 0; q < np; ++q) {
-        const float2 ml = *reinterpret_cast<const float2*>(p.part_ml + (row0 + q) * 2);
-        const float4* src = reinterpret_cast<const float4*>(p.part_acc + (row0 + q) * kHeadDim + 8 * L);
+    auto merge_slot = [&](int slot) {
+        const float2 ml = *reinterpret_cast<const float2*>(p.part_ml + (row0 + slot) * 2);
+        const float4* src = reinterpret_cast<const float4*>(p.part_acc + (row0 + slot) * kHeadDim + 8 * L);
         const float4 a = src[0], c = src[1];
         const float Mn = __builtin_fmaxf(M, ml.x);
         const float fo = __builtin_amdgcn_exp2f(M - Mn);
@@ -763,14 +845,17 @@ __global__ void __launch_bounds__(256) merge_kernel(DecodeParams p) {
         o[0] = o[0] * fo + a.x * fn; o[1] = o[1] * fo + a.y * fn; o[2] = o[2] * fo + a.z * fn; o[3] = o[3] * fo + a.w * fn;
         o[4] = o[4] * fo + c.x * fn; o[5] = o[5] * fo + c.y * fn; o[6] = o[6] * fo + c.z * fn; o[7] = o[7] * fo + c.w * fn;
         M = Mn;
-    }
+    };
+#pragma unroll 4
+    for (int q = first; q < np; ++q) merge_slot(q);
+    for (int q = 0; q < nq; ++q) merge_slot(p.suffix_partitions + q);
     finish_row(p, o, lsum, L);
     write_out(p, int64_t(b) * p.num_q_heads + hq, L, o);
 }
 
 template <int F>
 static hipError_t launch_partials(const DecodeParams& p, hipStream_t stream) {
-    const dim3 grid{unsigned(int64_t(p.num_partitions) * p.num_kv_heads * p.batch)};
+    const dim3 grid{unsigned(int64_t(p.prefix_blocks) + int64_t(p.suffix_partitions) * p.num_kv_heads * p.batch)};
     hipLaunchKernelGGL(decode_kernel<F>, grid, dim3(64 * Fmt<F>::kWaves), 0, stream, p);
     return hipGetLastError();
 }
@@ -782,7 +867,7 @@ hipError_t launch_decode_partials(const DecodeParams& p, hipStream_t stream) {
 }
 
 hipError_t launch_decode_merge(const DecodeParams& p, hipStream_t stream) {
-    if (p.num_partitions <= 1) return hipSuccess;   // every sequence was finished in place
+    if (p.num_partitions <= 1 && p.prefix_pages == nullptr) return hipSuccess;   // every sequence was finished in place
     const dim3 grid{unsigned(p.num_kv_heads), unsigned(p.batch)};
     hipLaunchKernelGGL(merge_kernel, grid, dim3(256), 0, stream, p);
     return hipGetLastError();

@@ -76,6 +76,16 @@ struct DecodeParams {
     void* out;                 // [B][Hq][128]
     int32_t out_dtype;         // 0 f32, 1 bf16
     int32_t rotate_v;
+    // cascade decode over a shared prefix (prefix_pages == nullptr: off).
+    // Partial slots per (sequence, query head): the suffix_partitions of the
+    // context grid, then the prefix partitions.
+    const int32_t* prefix_pages;   // [prefix_tokens / 16]
+    const int32_t* prefix_lens;    // [B] tokens of each sequence served by the prefix
+    int32_t prefix_tokens;
+    int32_t prefix_partition;      // prefix tokens per prefix block
+    int32_t prefix_chunks;         // ceil(B * G / 16) column chunks per kv head
+    int32_t prefix_blocks;         // Hkv * prefix_chunks * prefix partitions, first in the grid
+    int32_t suffix_partitions;
 };
 
 hipError_t launch_quantize_kv(const QuantizeParams& p, int dtype, hipStream_t stream);

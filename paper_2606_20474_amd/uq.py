@@ -32,7 +32,9 @@ EXPORTS = (
     "uq_default_partition", "uq_decode_attention", "uq_decode_partials", "uq_decode_merge", "uq_decode_step",
     "uq_decode_step_partials", "uq_ref_cache_bytes", "uq_ref_write_kv", "uq_ref_decode_workspace_bytes",
     "uq_ref_decode_attention", "uq_ref_decode_partials", "uq_ref_decode_merge", "uq_ref_decode_step",
-    "uq_ref_decode_step_partials",
+    "uq_ref_decode_step_partials", "uq_decode_cascade_workspace_bytes", "uq_decode_cascade",
+    "uq_decode_cascade_partials", "uq_decode_cascade_merge", "uq_ref_decode_cascade",
+    "uq_ref_decode_cascade_partials", "uq_ref_decode_cascade_merge",
 )
 
 UQ_REF_FP8_E4M3, UQ_REF_BF16 = 1, 2
@@ -68,6 +70,15 @@ class uq_ref_cache_desc(ctypes.Structure):
     ]
 
 
+class uq_shared_prefix(ctypes.Structure):
+    _fields_ = [
+        ("pages", ctypes.c_void_p),
+        ("lens", ctypes.c_void_p),
+        ("num_tokens", ctypes.c_int32),
+        ("partition_tokens", ctypes.c_int32),
+    ]
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise ImportError(f"{LIB_PATH} is not built; run `python -m paper_2606_20474_amd.build`")
@@ -96,6 +107,21 @@ def _load():
         fn.argtypes = [D, vp, i32, vp, vp, i32, i32, i32, vp, vp, vp, i32, vp, i32, f32, i32, vp, sz, vp, i32, vp]
         fn.restype = i32
     R = ctypes.POINTER(uq_ref_cache_desc)
+    S = ctypes.POINTER(uq_shared_prefix)
+    L.uq_decode_cascade_workspace_bytes.argtypes = [i32, i32, i32, i32, i32, S]
+    L.uq_decode_cascade_workspace_bytes.restype = sz
+    for name in ("uq_decode_cascade", "uq_decode_cascade_partials"):
+        fn = getattr(L, name)
+        fn.argtypes = [D, vp, i32, vp, vp, i32, i32, i32, vp, vp, vp, i32, vp, i32, S, f32, i32, vp, sz, vp, i32, vp]
+        fn.restype = i32
+    L.uq_decode_cascade_merge.argtypes = [D, i32, i32, vp, i32, S, i32, vp, sz, vp, i32, vp]
+    L.uq_decode_cascade_merge.restype = i32
+    for name in ("uq_ref_decode_cascade", "uq_ref_decode_cascade_partials"):
+        fn = getattr(L, name)
+        fn.argtypes = [R, vp, i32, vp, vp, i32, i32, i32, vp, vp, i32, vp, i32, S, f32, i32, vp, sz, vp, i32, vp]
+        fn.restype = i32
+    L.uq_ref_decode_cascade_merge.argtypes = [R, i32, i32, vp, i32, S, i32, vp, sz, vp, i32, vp]
+    L.uq_ref_decode_cascade_merge.restype = i32
     L.uq_ref_cache_bytes.argtypes = [R]
     L.uq_ref_cache_bytes.restype = sz
     L.uq_ref_write_kv.argtypes = [R, vp, vp, i32, i64, i64, vp, i32, i32, vp, vp, vp]
@@ -389,4 +415,94 @@ def ref_decode_step(desc: RefCacheDesc, q, k_new, v_new, cache, page_table, cont
             _ptr(page_table), page_table.shape[1], _ptr(context_lens), max_context, softmax_scale, partition_tokens,
             _ptr(workspace), workspace.numel(), _ptr(out), _DT[out.dtype], _stream(stream))
     _check(st, "uq_ref_decode_step_partials" if partials_only else "uq_ref_decode_step")
+    return out
+
+
+# ---------------------------------------------------------------------------
+# Cascade decode over a shared prefix
+
+
+@dataclass
+class SharedPrefix:
+    """Python mirror of ``uq_shared_prefix``: pages int32 [num_tokens / 16]
+    and lens int32 [batch] on the device."""
+    pages: torch.Tensor
+    lens: torch.Tensor
+    num_tokens: int
+    partition_tokens: int = 0
+
+    def c_struct(self):
+        return uq_shared_prefix(self.pages.data_ptr(), self.lens.data_ptr(), self.num_tokens, self.partition_tokens)
+
+
+def cascade_workspace_bytes(num_kv_heads, batch, num_q_heads, max_context, prefix: SharedPrefix, partition_tokens=0):
+    sp = prefix.c_struct()
+    return int(lib.uq_decode_cascade_workspace_bytes(num_kv_heads, batch, num_q_heads, max_context, partition_tokens,
+                                                     ctypes.byref(sp)))
+
+
+def _cascade_common(q, k_new, v_new, max_context, num_kv_heads, prefix, softmax_scale, partition_tokens, workspace,
+                    out, out_dtype):
+    B, Hq = q.shape[0], q.shape[1]
+    if softmax_scale is None:
+        softmax_scale = HEAD_DIM ** -0.5
+    if workspace is None:
+        n = cascade_workspace_bytes(num_kv_heads, B, Hq, max_context, prefix, partition_tokens)
+        workspace = torch.empty(n, dtype=torch.uint8, device=q.device)
+    if out is None:
+        out = torch.empty((B, Hq, HEAD_DIM), dtype=out_dtype, device=q.device)
+    ndt = UQ_F32 if k_new is None else _DT[k_new.dtype]
+    return B, Hq, softmax_scale, workspace, out, ndt
+
+
+def decode_cascade(desc: CacheDesc, q, codes, scales, page_table, context_lens, max_context, prefix: SharedPrefix,
+                   softmax_scale=None, partition_tokens=0, workspace=None, out=None, out_dtype=torch.float32,
+                   k_new=None, v_new=None, stream=None, partials_only=False):
+    """Decode attention (or, with k_new/v_new, a decode step) with a shared prefix."""
+    B, Hq, scale, workspace, out, ndt = _cascade_common(q, k_new, v_new, max_context, desc.num_kv_heads, prefix,
+                                                        softmax_scale, partition_tokens, workspace, out, out_dtype)
+    d = desc.c_struct()
+    sp = prefix.c_struct()
+    fn = lib.uq_decode_cascade_partials if partials_only else lib.uq_decode_cascade
+    st = fn(ctypes.byref(d), _ptr(q), _DT[q.dtype], _ptr(k_new), _ptr(v_new), ndt, B, Hq, _ptr(codes), _ptr(scales),
+            _ptr(page_table), page_table.shape[1], _ptr(context_lens), max_context, ctypes.byref(sp), scale,
+            partition_tokens, _ptr(workspace), workspace.numel(), _ptr(out), _DT[out.dtype], _stream(stream))
+    _check(st, "uq_decode_cascade_partials" if partials_only else "uq_decode_cascade")
+    return out
+
+
+def decode_cascade_merge(desc: CacheDesc, batch, num_q_heads, context_lens, max_context, prefix: SharedPrefix,
+                         partition_tokens, workspace, out, stream=None):
+    d = desc.c_struct()
+    sp = prefix.c_struct()
+    st = lib.uq_decode_cascade_merge(ctypes.byref(d), batch, num_q_heads, _ptr(context_lens), max_context,
+                                     ctypes.byref(sp), partition_tokens, _ptr(workspace), workspace.numel(),
+                                     _ptr(out), _DT[out.dtype], _stream(stream))
+    _check(st, "uq_decode_cascade_merge")
+    return out
+
+
+def ref_decode_cascade(desc: RefCacheDesc, q, cache, page_table, context_lens, max_context, prefix: SharedPrefix,
+                       softmax_scale=None, partition_tokens=0, workspace=None, out=None, out_dtype=torch.float32,
+                       k_new=None, v_new=None, stream=None, partials_only=False):
+    B, Hq, scale, workspace, out, ndt = _cascade_common(q, k_new, v_new, max_context, desc.num_kv_heads, prefix,
+                                                        softmax_scale, partition_tokens, workspace, out, out_dtype)
+    d = desc.c_struct()
+    sp = prefix.c_struct()
+    fn = lib.uq_ref_decode_cascade_partials if partials_only else lib.uq_ref_decode_cascade
+    st = fn(ctypes.byref(d), _ptr(q), _DT[q.dtype], _ptr(k_new), _ptr(v_new), ndt, B, Hq, _ptr(cache),
+            _ptr(page_table), page_table.shape[1], _ptr(context_lens), max_context, ctypes.byref(sp), scale,
+            partition_tokens, _ptr(workspace), workspace.numel(), _ptr(out), _DT[out.dtype], _stream(stream))
+    _check(st, "uq_ref_decode_cascade_partials" if partials_only else "uq_ref_decode_cascade")
+    return out
+
+
+def ref_decode_cascade_merge(desc: RefCacheDesc, batch, num_q_heads, context_lens, max_context, prefix: SharedPrefix,
+                             partition_tokens, workspace, out, stream=None):
+    d = desc.c_struct()
+    sp = prefix.c_struct()
+    st = lib.uq_ref_decode_cascade_merge(ctypes.byref(d), batch, num_q_heads, _ptr(context_lens), max_context,
+                                         ctypes.byref(sp), partition_tokens, _ptr(workspace), workspace.numel(),
+                                         _ptr(out), _DT[out.dtype], _stream(stream))
+    _check(st, "uq_ref_decode_cascade_merge")
     return out

@@ -102,6 +102,15 @@ class DecodeWorkload:
             out.append((b, lo, ctx))
         return out
 
+    def prefix_lens(self) -> np.ndarray:
+        """int32 [B]: tokens of each sequence that are read from the shared
+        prefix pages (whole pages, all before the sequence's last token)."""
+        ctx = self.context_lens.astype(np.int64)
+        full = np.minimum(self.shared_prefix_tokens, ctx)
+        if self.private_tail is not None:
+            full = np.where(self.private_tail, np.maximum(ctx - 1, 0) // PAGE * PAGE, full)
+        return full.astype(np.int32)
+
     def slots(self, key: int, lo: int, hi: int, row=None) -> np.ndarray:
         """Physical slots of tokens lo..hi-1 through page-table row `row`
         (None: the shared prefix's page list)."""

@@ -206,3 +206,42 @@ def test_decode_step_validation(uq):
     r = lib.uq_ref_decode_step_partials(ctypes.byref(rdesc()), FAKE, 0, FAKE, FAKE, 3, 2, 4, FAKE, FAKE, 4, FAKE, 64,
                                         0.1, 0, FAKE, 1 << 30, FAKE, 0, None)
     assert r == E.UQ_ERR_UNSUPPORTED
+
+
+def test_cascade_validation(uq):
+    E = uq
+    lib = uq.lib
+    from paper_2606_20474_amd.uq import uq_shared_prefix
+
+    def pre(**kw):
+        a = dict(pages=0x10000, lens=0x10000, num_tokens=64, partition_tokens=0)
+        a.update(kw)
+        return uq_shared_prefix(**a)
+
+    def casc(sp, **kw):
+        a = dict(kn=None, vn=None, wsb=1 << 30)
+        a.update(kw)
+        return lib.uq_decode_cascade(ctypes.byref(desc()), FAKE, 0, a["kn"], a["vn"], 0, 2, 4, FAKE, FAKE, FAKE, 4,
+                                     FAKE, 64, ctypes.byref(sp) if sp is not None else None, 0.1, 0, FAKE,
+                                     a["wsb"], FAKE, 0, None)
+
+    assert casc(None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert casc(pre(pages=None)) == E.UQ_ERR_INVALID_ARGUMENT
+    assert casc(pre(lens=None)) == E.UQ_ERR_INVALID_ARGUMENT
+    assert casc(pre(num_tokens=40)) == E.UQ_ERR_INVALID_ARGUMENT      # not whole pages
+    assert casc(pre(num_tokens=0)) == E.UQ_ERR_INVALID_ARGUMENT
+    assert casc(pre(partition_tokens=48)) == E.UQ_ERR_INVALID_ARGUMENT
+    assert casc(pre(), kn=FAKE) == E.UQ_ERR_INVALID_ARGUMENT          # k_new without v_new
+    assert casc(pre(), wsb=16) == E.UQ_ERR_WORKSPACE_TOO_SMALL
+    sp = pre(partition_tokens=32)
+    # 64 context tokens in partitions of 32 -> 2 slots, plus 2 prefix partitions of 32
+    plain = uq.workspace_bytes(__import__("paper_2606_20474_amd.uq", fromlist=["CacheDesc"]).CacheDesc(2, 10), 2, 4,
+                               64, 32)
+    assert lib.uq_decode_cascade_workspace_bytes(2, 2, 4, 64, 32, ctypes.byref(sp)) == plain * 2
+    assert lib.uq_decode_cascade_workspace_bytes(2, 2, 3, 64, 32, ctypes.byref(sp)) == 0
+    r = lib.uq_ref_decode_cascade(ctypes.byref(rdesc()), FAKE, 0, None, None, 0, 2, 4, FAKE, FAKE, 4, FAKE, 64,
+                                  None, 0.1, 0, FAKE, 1 << 30, FAKE, 0, None)
+    assert r == E.UQ_ERR_INVALID_ARGUMENT
+    r = lib.uq_decode_cascade_merge(ctypes.byref(desc()), 2, 4, FAKE, 64, ctypes.byref(pre(num_tokens=8)), 0, FAKE,
+                                    1 << 30, FAKE, 0, None)
+    assert r == E.UQ_ERR_INVALID_ARGUMENT
