@@ -52,6 +52,7 @@ def lib():
         L.uqo_load_vector.argtypes = [vp, vp, i32, i64, i32, i32, i32, vp, vp]
         L.uqo_dequant_vector.argtypes = [vp, vp, i32, i64, i32, i32, i32, vp]
         L.uqo_decode_attention.argtypes = [vp, i32, i32, i32, vp, vp, vp, i32, vp, f64, i32, vp]
+        L.uqo_quantize_error.argtypes = [vp, i64, i32, i32, i32, vp, vp]
         _lib = L
     return _lib
 
@@ -185,3 +186,17 @@ def decode_attention(q, pools, page_table, context_lens, num_kv_heads, softmax_s
     lib().uqo_decode_attention(_ptr(q), B, Hq, num_kv_heads, _ptr(pools[0]), _ptr(pools[1]), _ptr(pt),
                                pt.shape[1], _ptr(ctx), float(softmax_scale), int(bool(rotate_v)), _ptr(out))
     return out
+
+
+def quantize_error(x, c_values, rotate=True, pow2=True):
+    """Round-trip error of the FP4 encoder per constant c (section
+    "Constant-Optimized Scaling"): rows x [..., 128] -> array [len(c), 2] of
+    (sum of squared errors, sum of squares), fp64.  ``pow2`` selects the
+    cache's scale 2^round(log2(c m)); otherwise the continuous s = c m."""
+    x = _f32(x)
+    assert x.shape[-1] == HEAD_DIM
+    c = np.ascontiguousarray(np.atleast_1d(c_values), dtype=np.float32)
+    sums = np.zeros((c.size, 2), np.float64)
+    lib().uqo_quantize_error(_ptr(x), x.size // HEAD_DIM, int(bool(rotate)), int(bool(pow2)), c.size, _ptr(c),
+                             _ptr(sums))
+    return sums

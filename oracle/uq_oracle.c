@@ -22,7 +22,9 @@
  *   - dequantisation value = code * 2^(byte - 127)
  *       (section "Dequantization", its single equation),
  *   - the FP8 E4M3 query cast (Algorithm 1, Decode),
- *   - softmax attention over the dequantised cache, in fp64.
+ *   - softmax attention over the dequantised cache, in fp64,
+ *   - the round-trip error sum(z - s q(z / s))^2 behind the offline choice
+ *       of c (section "Constant-Optimized Scaling", the c* equation).
  *
  * Readings where the paper is silent (the same list is kept with the design
  * notes of the repository):
@@ -338,5 +340,66 @@ void uqo_decode_attention(const float *q, int batch, int num_q_heads, int num_kv
             if (rotate_v) uqo_wht128_f64(acc, o);
             else memcpy(o, acc, sizeof(acc));
         }
+    }
+}
+
+/* ---------------------------------------------------------------------- */
+/* Round-trip error of the encoder, for the offline fit of c (section      */
+/* "Constant-Optimized Scaling": c* = argmin_c E[(z - c m q(z/(c m)))^2]   */
+/* over rotated key rows).  Per row of 128 (rotated by R first when         */
+/* `rotate`), per group of 32 with absmax m, for each c_values[i]:          */
+/*   pow2 = 1  the cache's own rule: s = 2^E, E = uqo_scale_exponent(m, c), */
+/*             decoded value F[code] * 2^E;                                 */
+/*   pow2 = 0  the continuous scale of the fitting objective: s = fl32(c m),*/
+/*             code = q(fl32(z / s)), decoded value F[code] * s.            */
+/* sums[2i] += sum of (z - decoded)^2 and sums[2i+1] += sum of z^2, both in */
+/* fp64 over all rows and channels.  Groups with m = 0 add nothing.         */
+/* ---------------------------------------------------------------------- */
+static void error_row(const float *x_in, int rotate, int pow2, int num_c, const float *c_values, double *acc) {
+    float x[UQO_D];
+    memcpy(x, x_in, sizeof(x));
+    if (rotate) uqo_wht128_f32(x, 1);
+    for (int g = 0; g < UQO_NGROUP; ++g) {
+        const float *z = x + g * UQO_GROUP;
+        float m = 0.0f;
+        for (int i = 0; i < UQO_GROUP; ++i) {
+            float a = fabsf(z[i]);
+            if (a > m) m = a;
+        }
+        if (m == 0.0f) continue;
+        double energy = 0.0;
+        for (int i = 0; i < UQO_GROUP; ++i) energy += (double)z[i] * (double)z[i];
+        for (int k = 0; k < num_c; ++k) {
+            double err = 0.0;
+            if (pow2) {
+                int E = uqo_scale_exponent(m, c_values[k]);
+                for (int i = 0; i < UQO_GROUP; ++i) {
+                    double d = (double)z[i] - uqo_e2m1_value(uqo_e2m1_encode(z[i], E), E + 127);
+                    err += d * d;
+                }
+            } else {
+                float s = c_values[k] * m;             /* one fp32 multiply */
+                for (int i = 0; i < UQO_GROUP; ++i) {
+                    float t = z[i] / s;                /* one fp32 division */
+                    double d = (double)z[i] - uqo_e2m1_value(uqo_e2m1_encode(t, 0), 127) * (double)s;
+                    err += d * d;
+                }
+            }
+            acc[2 * k] += err;
+            acc[2 * k + 1] += energy;
+        }
+    }
+}
+
+void uqo_quantize_error(const float *x, int64_t rows, int rotate, int pow2, int num_c, const float *c_values,
+                        double *sums) {
+#pragma omp parallel
+    {
+        double *acc = (double *)calloc((size_t)(2 * num_c), sizeof(double));
+#pragma omp for schedule(static)
+        for (int64_t r = 0; r < rows; ++r) error_row(x + r * UQO_D, rotate, pow2, num_c, c_values, acc);
+#pragma omp critical
+        for (int k = 0; k < 2 * num_c; ++k) sums[k] += acc[k];
+        free(acc);
     }
 }

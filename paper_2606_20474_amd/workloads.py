@@ -15,6 +15,10 @@ and agent-trace contexts, which are not available):
     lognormal(ln 32768, 0.8) clipped to [8192, 131072]; a context shorter
     than the shared prefix shares its first tokens and owns a copy of its
     last page (copy on write).
+Rows for the offline fit of the scale constant: uniform unit vectors
+(normalised N(0, I) draws, the rotated-unit-vector model of the paper's
+codebook analysis) and key rows of the recipe above.
+
 Small index tables, outlier channels and queries come from a CPU
 ``torch.Generator``; the bulk K/V of every sequence comes from its own
 generator on the target device, seeded from (workload seed, sequence), so any
@@ -247,3 +251,19 @@ class WriteWorkload:
         kp, vp = draw(self.prefill_tokens)
         ka, va = draw(self.append_seqs)
         return dict(prefill=(kp, vp, prefill_slots), append=(ka, va, append_slots, pt, ctx))
+
+
+def unit_vectors(n: int, d: int, seed: int = 0) -> np.ndarray:
+    """n uniform unit vectors in R^d (fp32 [n, d]): N(0, I) rows divided by
+    their norms, from numpy's PCG64 seeded with ``seed``."""
+    g = np.random.default_rng(seed).standard_normal((n, d))
+    return (g / np.linalg.norm(g, axis=1, keepdims=True)).astype(np.float32)
+
+
+def key_rows(n: int, seed: int = 0) -> np.ndarray:
+    """n key rows of 128 channels (fp32 [n, 128]) with the cache recipe:
+    N(0, 1) with 4 outlier channels (the same for every row) times 20."""
+    rng = np.random.default_rng(seed)
+    k = rng.standard_normal((n, HEAD_DIM))
+    k[:, rng.permutation(HEAD_DIM)[:OUTLIERS]] *= OUTLIER_GAIN
+    return k.astype(np.float32)
