@@ -240,6 +240,29 @@ uq_status uq_decode_merge(const uq_cache_desc *desc, int32_t batch, int32_t num_
                           const void *workspace, size_t workspace_bytes, void *out, uq_dtype out_dtype,
                           void *stream);
 
+/*
+ * uq_quantize_error -- calibration of the scale constant c (section
+ * "Constant-Optimized Scaling": c is chosen once, offline, to minimise the
+ * reconstruction error of the E2M1 grid on rotated key rows).  For each
+ * candidate c_values[i], every row of x (128 channels, rotated first when
+ * `rotate`) is quantised per 32-channel group with the scale
+ * s = 2^round(log2(c m)) of the cache format (pow2_scale = 1) or the
+ * continuous s = c m of the paper's fitting objective (pow2_scale = 0),
+ * decoded back to code * s, and
+ *   sums[2 i]     += sum over rows and channels of (x - decoded)^2,
+ *   sums[2 i + 1] += sum of x^2 (the same for every i).
+ * The sums accumulate (zero them before the first call; several calls can
+ * cover one large set).  x: F32/BF16/F16 rows, row_stride elements apart,
+ * 16-byte aligned; c_values: num_c floats (device), finite and > 0;
+ * sums: 2 * num_c doubles (device).
+ * rows = 0 launches nothing (x may then be NULL).
+ * Errors: INVALID_ARGUMENT for NULL pointers, rows < 0, num_c outside
+ * [0, 256], row_stride < 128 or misaligned rows; UNSUPPORTED for other
+ * dtypes.  Asynchronous on `stream`; the library keeps no pointer.
+ */
+uq_status uq_quantize_error(const void *x, uq_dtype dtype, int64_t rows, int64_t row_stride, int32_t rotate,
+                            int32_t pow2_scale, int32_t num_c, const float *c_values, double *sums, void *stream);
+
 /* ------------------------------------------------------------------------
  * Cascade decode over a shared prefix.
  *

@@ -269,6 +269,28 @@ uq_status uq_prepare_query(const uq_cache_desc* desc, const void* q, uq_dtype q_
     return from_hip(uq::launch_prepare_query(q, int(q_dtype), rows, q_fp8, static_cast<hipStream_t>(stream)));
 }
 
+uq_status uq_quantize_error(const void* x, uq_dtype dtype, int64_t rows, int64_t row_stride, int32_t rotate,
+                            int32_t pow2_scale, int32_t num_c, const float* c_values, double* sums, void* stream) {
+    if (dtype != UQ_F32 && dtype != UQ_BF16 && dtype != UQ_F16) return UQ_ERR_UNSUPPORTED;
+    if (rows < 0 || num_c < 0 || num_c > uq::kMaxErrorConstants || row_stride < kHeadDim)
+        return UQ_ERR_INVALID_ARGUMENT;
+    if ((x == nullptr && rows > 0) || c_values == nullptr || sums == nullptr) return UQ_ERR_INVALID_ARGUMENT;
+    if (rows == 0 || num_c == 0) return UQ_OK;
+    const int64_t vec_elems = dtype == UQ_F32 ? 4 : 8;
+    if (row_stride % vec_elems != 0 || !aligned16(x)) return UQ_ERR_INVALID_ARGUMENT;
+    if (rows == 0 || num_c == 0) return UQ_OK;
+    uq::ErrorParams p;
+    p.x = x;
+    p.rows = rows;
+    p.row_stride = row_stride;
+    p.rotate = rotate != 0;
+    p.pow2 = pow2_scale != 0;
+    p.num_c = num_c;
+    p.c_values = c_values;
+    p.sums = sums;
+    return from_hip(uq::launch_quantize_error(p, int(dtype), static_cast<hipStream_t>(stream)));
+}
+
 int32_t uq_default_partition(const uq_cache_desc* desc, int32_t batch, int32_t num_q_heads, int32_t max_context) {
     if (check_decode_common(desc, batch, num_q_heads, max_context, 0) != UQ_OK) return 0;
     return pick_partition(batch, desc->num_kv_heads, max_context);

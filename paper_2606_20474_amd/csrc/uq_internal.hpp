@@ -88,7 +88,21 @@ struct DecodeParams {
     int32_t suffix_partitions;
 };
 
+constexpr int kMaxErrorConstants = 256;   // constants per uq_quantize_error call
+
+struct ErrorParams {
+    const void* x;             // rows of 128 channels
+    int64_t rows;
+    int64_t row_stride;        // elements
+    int32_t rotate;
+    int32_t pow2;              // 1: UE8M0 scale 2^round(log2(c m)); 0: scale c m
+    int32_t num_c;
+    const float* c_values;     // [num_c]
+    double* sums;              // [num_c][2]: sum of squared errors, sum of squares (accumulated)
+};
+
 hipError_t launch_quantize_kv(const QuantizeParams& p, int dtype, hipStream_t stream);
+hipError_t launch_quantize_error(const ErrorParams& p, int dtype, hipStream_t stream);
 hipError_t launch_write_kv_ref(const RefWriteParams& p, int dtype, hipStream_t stream);
 hipError_t launch_prepare_query(const void* q, int dtype, int64_t rows, uint8_t* q8, hipStream_t stream);
 hipError_t launch_decode_partials(const DecodeParams& p, hipStream_t stream);

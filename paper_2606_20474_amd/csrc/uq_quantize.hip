@@ -163,6 +163,98 @@ __global__ void __launch_bounds__(256) quantize_kv_kernel(QuantizeParams p) {
     ks[kTileScales + L * kPage + off] = uint8_t(evs + 127);
 }
 
+// Round-trip error of the FP4 encoder for a list of constants c, the
+// one-dimensional fit of section "Constant-Optimized Scaling": per row
+// (rotated like K when `rotate`), per 32-channel group with maximum m, the
+// codes of x / s are decoded back to code * s and the squared error summed,
+// for the deployed scale s = 2^round(log2(c m)) (UE8M0, pow2) or the
+// continuous s = c m.  One quad per row as in quantize_kv_kernel, 64 rows
+// per tile, tiles strided over the grid.  Each wave folds its per-tile sums
+// into its own fp64 LDS slots; at the end the block adds its totals to
+// `sums` with one fp64 atomic per value.
+template <int DT>
+__global__ void __launch_bounds__(256) quantize_error_kernel(ErrorParams p) {
+    __shared__ double acc[4][kMaxErrorConstants];
+    __shared__ double energy[4];
+    for (int i = threadIdx.x; i < 4 * kMaxErrorConstants; i += 256) (&acc[0][0])[i] = 0.0;
+    if (threadIdx.x < 4) energy[threadIdx.x] = 0.0;
+    __syncthreads();
+    const int L = threadIdx.x & 3;
+    const int wave = threadIdx.x >> 6;
+    const bool lead = (threadIdx.x & 63) == 0;
+    const int64_t tiles = (p.rows + 63) / 64;
+    for (int64_t tile = blockIdx.x; tile < tiles; tile += gridDim.x) {
+        const int64_t row = tile * 64 + (threadIdx.x >> 2);
+        float x[4][8];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) x[j][i] = 0.0f;
+        if (row < p.rows) {
+#pragma unroll
+            for (int j = 0; j < 4; ++j) load_x8<DT>(p.x, row * p.row_stride + 32 * j + 8 * L, x[j]);
+        }
+        if (p.rotate) wht128_x32(x, L);   // whole quads: rows past the end rotate zeros
+        float m[4];
+        float sq = 0.0f;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            m[j] = 0.0f;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                m[j] = __builtin_fmaxf(m[j], __builtin_fabsf(x[j][i]));
+                sq = __builtin_fmaf(x[j][i], x[j][i], sq);
+            }
+            m[j] = __builtin_fmaxf(m[j], quad_xor<1>(m[j]));
+            m[j] = __builtin_fmaxf(m[j], quad_xor<2>(m[j]));
+        }
+#pragma unroll
+        for (int s = 1; s < 64; s <<= 1) sq += __shfl_xor(sq, s);
+        if (lead) energy[wave] += double(sq);
+        for (int ci = 0; ci < p.num_c; ++ci) {
+            const float c = p.c_values[ci];
+            float err = 0.0f;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                if (!(m[j] > 0.0f)) continue;   // an all-zero group decodes exactly
+                if (p.pow2) {
+                    // The cache encoder itself: scale operand 2^E, decode by the same scale.
+                    const float sc = __builtin_ldexpf(1.0f, ue8m0_exponent(m[j], c));
+#pragma unroll
+                    for (int i = 0; i < 8; i += 2) {
+                        const uint32_t w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, x[j][i], x[j][i + 1], sc, 0);
+                        const v2f d = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, sc, 0);
+                        const float e0 = x[j][i] - d[0], e1 = x[j][i + 1] - d[1];
+                        err = __builtin_fmaf(e0, e0, err);
+                        err = __builtin_fmaf(e1, e1, err);
+                    }
+                } else {
+                    // Continuous scale: nearest E2M1 level of fl32(x / s), times s.
+                    const float sc = c * m[j];
+#pragma unroll
+                    for (int i = 0; i < 8; i += 2) {
+                        const float t0 = x[j][i] / sc, t1 = x[j][i + 1] / sc;
+                        const uint32_t w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, t0, t1, 1.0f, 0);
+                        const v2f d = __builtin_amdgcn_cvt_scalef32_pk_f32_fp4(w, 1.0f, 0);
+                        const float e0 = x[j][i] - d[0] * sc, e1 = x[j][i + 1] - d[1] * sc;
+                        err = __builtin_fmaf(e0, e0, err);
+                        err = __builtin_fmaf(e1, e1, err);
+                    }
+                }
+            }
+#pragma unroll
+            for (int s = 1; s < 64; s <<= 1) err += __shfl_xor(err, s);
+            if (lead) acc[wave][ci] += double(err);
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x < p.num_c) {
+        const int ci = threadIdx.x;
+        atomicAdd(&p.sums[2 * ci], acc[0][ci] + acc[1][ci] + acc[2][ci] + acc[3][ci]);
+        atomicAdd(&p.sums[2 * ci + 1], energy[0] + energy[1] + energy[2] + energy[3]);
+    }
+}
+
 // Writer of the plain comparison caches (FP8 E4M3 with one scale per
 // tensor, or BF16); the layouts are those of place_token.
 template <int DT, int FMT>
@@ -242,6 +334,18 @@ hipError_t launch_write_kv_ref(const RefWriteParams& p, int dtype, hipStream_t s
     if (dtype == 0) return launch_ref<0>(p, grid, stream);
     if (dtype == 1) return launch_ref<1>(p, grid, stream);
     return launch_ref<2>(p, grid, stream);
+}
+
+hipError_t launch_quantize_error(const ErrorParams& p, int dtype, hipStream_t stream) {
+    const int64_t tiles = (p.rows + 63) / 64;
+    if (tiles == 0 || p.num_c == 0) return hipSuccess;
+    if (p.num_c > kMaxErrorConstants) return hipErrorInvalidValue;
+    // 8 blocks of 4 waves per CU over 256 CUs; each block strides over the tiles.
+    const dim3 grid{unsigned(tiles < 2048 ? tiles : 2048)}, block{256u};
+    if (dtype == 0) hipLaunchKernelGGL(quantize_error_kernel<0>, grid, block, 0, stream, p);
+    else if (dtype == 1) hipLaunchKernelGGL(quantize_error_kernel<1>, grid, block, 0, stream, p);
+    else hipLaunchKernelGGL(quantize_error_kernel<2>, grid, block, 0, stream, p);
+    return hipGetLastError();
 }
 
 hipError_t launch_prepare_query(const void* q, int dtype, int64_t rows, uint8_t* q8, hipStream_t stream) {

@@ -34,7 +34,7 @@ EXPORTS = (
     "uq_ref_decode_attention", "uq_ref_decode_partials", "uq_ref_decode_merge", "uq_ref_decode_step",
     "uq_ref_decode_step_partials", "uq_decode_cascade_workspace_bytes", "uq_decode_cascade",
     "uq_decode_cascade_partials", "uq_decode_cascade_merge", "uq_ref_decode_cascade",
-    "uq_ref_decode_cascade_partials", "uq_ref_decode_cascade_merge",
+    "uq_ref_decode_cascade_partials", "uq_ref_decode_cascade_merge", "uq_quantize_error",
 )
 
 UQ_REF_FP8_E4M3, UQ_REF_BF16 = 1, 2
@@ -92,6 +92,8 @@ def _load():
     L.uq_quantize_kv.restype = i32
     L.uq_prepare_query.argtypes = [D, vp, i32, i64, vp, vp]
     L.uq_prepare_query.restype = i32
+    L.uq_quantize_error.argtypes = [vp, i32, i64, i64, i32, i32, i32, vp, vp, vp]
+    L.uq_quantize_error.restype = i32
     L.uq_decode_workspace_bytes.argtypes = [D, i32, i32, i32, i32]
     L.uq_decode_workspace_bytes.restype = sz
     L.uq_default_partition.argtypes = [D, i32, i32, i32]
@@ -219,6 +221,23 @@ def prepare_query(desc: CacheDesc, q, out=None, stream=None):
     _check(lib.uq_prepare_query(ctypes.byref(d), _ptr(q), _DT[q.dtype], rows, _ptr(out), _stream(stream)),
            "uq_prepare_query")
     return out
+
+
+def quantize_error(x, c_values, rotate=True, pow2=True, sums=None, stream=None):
+    """Round-trip error of the encoder per constant c: x rows [N, 128]
+    (last dimension contiguous), c_values float32 [n] on the device ->
+    ``sums`` float64 [n, 2] (sum of squared errors, sum of squares),
+    accumulated into ``sums`` if given, else into a new zeroed tensor."""
+    rows = x.reshape(-1, HEAD_DIM) if x.dim() != 2 else x
+    if rows.shape[-1] != HEAD_DIM or rows.stride(-1) != 1:
+        raise ValueError("rows of 128 contiguous channels expected")
+    c = c_values.to(device=x.device, dtype=torch.float32).contiguous()
+    if sums is None:
+        sums = torch.zeros((c.numel(), 2), dtype=torch.float64, device=x.device)
+    st = lib.uq_quantize_error(_ptr(rows), _DT[x.dtype], rows.shape[0], rows.stride(0), int(bool(rotate)),
+                               int(bool(pow2)), c.numel(), _ptr(c), _ptr(sums), _stream(stream))
+    _check(st, "uq_quantize_error")
+    return sums
 
 
 def workspace_bytes(desc: CacheDesc, batch, num_q_heads, max_context, partition_tokens=0):

@@ -245,3 +245,22 @@ def test_cascade_validation(uq):
     r = lib.uq_decode_cascade_merge(ctypes.byref(desc()), 2, 4, FAKE, 64, ctypes.byref(pre(num_tokens=8)), 0, FAKE,
                                     1 << 30, FAKE, 0, None)
     assert r == E.UQ_ERR_INVALID_ARGUMENT
+
+
+def test_quantize_error_validation(uq):
+    E = uq
+    f = uq.lib.uq_quantize_error
+    assert f(FAKE, E.UQ_FP8_E4M3, 4, 128, 1, 1, 1, FAKE, FAKE, None) == E.UQ_ERR_UNSUPPORTED
+    assert f(None, E.UQ_F32, 4, 128, 1, 1, 1, FAKE, FAKE, None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert f(None, E.UQ_F32, 0, 128, 1, 1, 1, FAKE, FAKE, None) == E.UQ_OK
+    assert f(FAKE, E.UQ_F32, 4, 128, 1, 1, 1, None, FAKE, None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert f(FAKE, E.UQ_F32, 4, 128, 1, 1, 1, FAKE, None, None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert f(FAKE, E.UQ_F32, -1, 128, 1, 1, 1, FAKE, FAKE, None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert f(FAKE, E.UQ_F32, 4, 127, 1, 1, 1, FAKE, FAKE, None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert f(FAKE, E.UQ_F32, 4, 130, 1, 1, 1, FAKE, FAKE, None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert f(FAKE, E.UQ_BF16, 4, 132, 1, 1, 1, FAKE, FAKE, None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert f(ctypes.c_void_p(0x10008), E.UQ_F32, 4, 128, 1, 1, 1, FAKE, FAKE, None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert f(FAKE, E.UQ_F32, 4, 128, 1, 1, -1, FAKE, FAKE, None) == E.UQ_ERR_INVALID_ARGUMENT
+    # nothing to do: no launch
+    assert f(FAKE, E.UQ_F32, 0, 128, 1, 1, 3, FAKE, FAKE, None) == E.UQ_OK
+    assert f(FAKE, E.UQ_BF16, 4, 136, 1, 0, 0, FAKE, FAKE, None) == E.UQ_OK
