@@ -84,6 +84,17 @@ def main(argv=None):
     x, rotate = synthetic_rows(args.source, args.rows, args.dim, args.seed, torch.device("cuda:0"))
     consts = [float(c) for c in args.constants.split(",")]
     report = {"source": args.source, "dim": args.dim, "rows": int(x.shape[0]), "rotate": rotate}
+    # time one sweep of 46 constants per scale rule (after one untimed call)
+    grid = np.linspace(0.05, 0.5, 46, dtype=np.float32)
+    for pow2 in (False, True):
+        round_trip_error(x, grid, rotate, pow2)
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record()
+        round_trip_error(x, grid, rotate, pow2)
+        t1.record()
+        t1.synchronize()
+        ms = t0.elapsed_time(t1)
+        report["sweep46_ms_pow2" if pow2 else "sweep46_ms_continuous"] = round(ms, 3)
     for pow2 in (False, True):
         key = "pow2" if pow2 else "continuous"
         c, r, _, _ = fit_c(x, rotate=rotate, pow2=pow2)
