@@ -53,6 +53,14 @@ def lib():
         L.uqo_dequant_vector.argtypes = [vp, vp, i32, i64, i32, i32, i32, vp]
         L.uqo_decode_attention.argtypes = [vp, i32, i32, i32, vp, vp, vp, i32, vp, f64, i32, vp]
         L.uqo_quantize_error.argtypes = [vp, i64, i32, i32, i32, vp, vp]
+        L.uqo_bf16_rne.argtypes = [f32]
+        L.uqo_bf16_rne.restype = f32
+        L.uqo_tq4_encode_vector.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp]
+        L.uqo_tq4_write.argtypes = [vp, vp, i64, i32, i64, vp, i64, vp, vp]
+        L.uqo_tq4_write.restype = i64
+        L.uqo_tq4_load.argtypes = [vp, i32, i64, i32, i32, vp, vp, vp, vp, vp]
+        L.uqo_tq4_dequant.argtypes = [vp, i32, i64, i32, i32, vp, vp, vp]
+        L.uqo_tq4_decode_attention.argtypes = [vp, i32, i32, i32, vp, vp, i32, vp, f64, vp, vp]
         _lib = L
     return _lib
 
@@ -200,3 +208,85 @@ def quantize_error(x, c_values, rotate=True, pow2=True):
     lib().uqo_quantize_error(_ptr(x), x.size // HEAD_DIM, int(bool(rotate)), int(bool(pow2)), c.size, _ptr(c),
                              _ptr(sums))
     return sums
+
+
+# ---------------------------------------------------------------------------
+# Ultra-TQ comparison cache (appendix "Calibrated LUT int4 KV Encoding
+# (Ultra-TQ)"); readings T1-T5 in uq_oracle.c.
+
+TQ_BLOCK = 2368
+
+
+def _levels(levels):
+    lv = np.ascontiguousarray(levels, dtype=np.float32)
+    assert lv.shape == (16,)
+    return lv
+
+
+def bf16_rne(x):
+    return float(lib().uqo_bf16_rne(float(np.float32(x))))
+
+
+def tq4_encode_vector(k, v, levels):
+    """One token -> (K indices [128], norm, V codes [128], s [4], z [4])."""
+    k = _f32(k).reshape(HEAD_DIM)
+    v = _f32(v).reshape(HEAD_DIM)
+    kidx = np.empty(HEAD_DIM, np.uint8)
+    vcode = np.empty(HEAD_DIM, np.uint8)
+    n = np.empty(1, np.float32)
+    s = np.empty(4, np.float32)
+    z = np.empty(4, np.float32)
+    lib().uqo_tq4_encode_vector(_ptr(k), _ptr(v), _ptr(_levels(levels)), _ptr(kidx), _ptr(n), _ptr(vcode), _ptr(s),
+                                _ptr(z))
+    return kidx, float(n[0]), vcode, s, z
+
+
+def tq4_alloc_cache(num_pages, num_kv_heads, fill=0):
+    return np.full(num_pages * num_kv_heads * TQ_BLOCK, fill, np.uint8)
+
+
+def tq4_write(k, v, slot_mapping, num_pages, levels, cache=None):
+    """k, v: [T, Hkv, 128] -> the Ultra-TQ cache (written into ``cache``)."""
+    k = _f32(k)
+    v = _f32(v)
+    T, Hkv, D = k.shape
+    assert D == HEAD_DIM and v.shape == k.shape
+    slots = np.ascontiguousarray(slot_mapping, dtype=np.int64)
+    if cache is None:
+        cache = tq4_alloc_cache(num_pages, Hkv)
+    lib().uqo_tq4_write(_ptr(k), _ptr(v), T, Hkv, Hkv * HEAD_DIM, _ptr(slots), int(num_pages), _ptr(_levels(levels)),
+                        _ptr(cache))
+    return cache
+
+
+def tq4_load(cache, num_kv_heads, page, head, t):
+    kidx = np.empty(HEAD_DIM, np.uint8)
+    vcode = np.empty(HEAD_DIM, np.uint8)
+    n = np.empty(1, np.float32)
+    s = np.empty(4, np.float32)
+    z = np.empty(4, np.float32)
+    lib().uqo_tq4_load(_ptr(cache), num_kv_heads, page, head, t, _ptr(kidx), _ptr(n), _ptr(vcode), _ptr(s), _ptr(z))
+    return kidx, float(n[0]), vcode, s, z
+
+
+def tq4_dequant(cache, num_kv_heads, page, head, t, levels):
+    """(rotated K, V) of one token as fp64 [128] each."""
+    kv = np.empty(HEAD_DIM, np.float64)
+    vv = np.empty(HEAD_DIM, np.float64)
+    lib().uqo_tq4_dequant(_ptr(cache), num_kv_heads, page, head, t, _ptr(_levels(levels)), _ptr(kv), _ptr(vv))
+    return kv, vv
+
+
+def tq4_decode_attention(q, cache, page_table, context_lens, num_kv_heads, levels, softmax_scale=None):
+    """q [B, Hq, 128] -> fp64 attention over the Ultra-TQ cache."""
+    q = _f32(q)
+    B, Hq, D = q.shape
+    assert D == HEAD_DIM and Hq % num_kv_heads == 0
+    pt = np.ascontiguousarray(page_table, dtype=np.int32)
+    ctx = np.ascontiguousarray(context_lens, dtype=np.int32)
+    if softmax_scale is None:
+        softmax_scale = 1.0 / np.sqrt(HEAD_DIM)
+    out = np.empty((B, Hq, HEAD_DIM), np.float64)
+    lib().uqo_tq4_decode_attention(_ptr(q), B, Hq, num_kv_heads, _ptr(cache), _ptr(pt), pt.shape[1], _ptr(ctx),
+                                   float(softmax_scale), _ptr(_levels(levels)), _ptr(out))
+    return out

@@ -403,3 +403,225 @@ void uqo_quantize_error(const float *x, int64_t rows, int rotate, int pow2, int 
         free(acc);
     }
 }
+
+/* ====================================================================== */
+/* Ultra-TQ comparison cache: the codebook encoding UltraQuant replaces    */
+/* (appendix "Calibrated LUT int4 KV Encoding (Ultra-TQ)", its algorithm,  */
+/* and section "Calibrated Centroids").  Readings where the paper leaves    */
+/* the details open (kept with the design notes too):                       */
+/*   T1 K is rotated by R, V is not.  K's block is the whole head vector    */
+/*      (the production per-token l2 norm); V's blocks are the 32-channel  */
+/*      groups.                                                             */
+/*   T2 the norm n is fp32: per 8-channel slice s (channels 8s..8s+7) a     */
+/*      fused multiply-add chain p_s = fma(x, x, p_s) in channel order,     */
+/*      then the pairwise tree ((p0+p1)+(p2+p3))+... over the 16 slices,    */
+/*      then a correctly rounded sqrtf.  Codes are decided from n, so this  */
+/*      order is part of the format.                                        */
+/*   T3 the 16 levels are used as BF16 (round to nearest even), the matrix  */
+/*      operand type; the K index is the number of midpoints m_j =          */
+/*      fl32((c_j + c_{j+1}) / 2) with x > fl32(m_j * n) (nearest level of  */
+/*      x / n, ties to the lower one).  The dequantised key is n * c[idx],  */
+/*      exact.                                                              */
+/*   T4 V per group: zero z = bf16(min), scale s = bf16(max(max - z, 0) /  */
+/*      15) (fp32 subtract and divide), code = clamp(rint((x - z) / s),    */
+/*      0, 15), or 0 when s = 0; the dequantised value is                  */
+/*      bf16(fma(s, code, z)), the BF16 operand of the PV product.          */
+/*   T5 the query is R q rounded to BF16.                                    */
+/* Cache block per (page, kv head), 2368 bytes:                             */
+/*   [0, 1024)     K indices: (token t, channel c) at byte                  */
+/*                 16 * (t + 16 * ((c % 32) / 8)) + 4 * (c / 32) + (c % 8)/2*/
+/*   [1024, 2048)  V codes: 1024 + 16 * (c / 8 + 16 * (t / 4)) + 4 * (t % 4)*/
+/*                 + (c % 8) / 2                                            */
+/*   (low nibble = even channel in both)                                     */
+/*   [2048, 2112)  K norms, fp32, token t at 2048 + 4 t                      */
+/*   [2112, 2368)  V (s, z) BF16 pairs, s in the low half: token t, group g */
+/*                 at 2112 + 16 * (4 * (t / 4) + g) + 4 * (t % 4)            */
+/* ====================================================================== */
+#define UQO_TQ_BLOCK 2368
+
+static float f32_of_bits(uint32_t u) { float f; memcpy(&f, &u, 4); return f; }
+static uint32_t bits_of_f32(float f) { uint32_t u; memcpy(&u, &f, 4); return u; }
+
+/* fp32 -> nearest BF16 (ties to even), as the fp32 value it stands for. */
+float uqo_bf16_rne(float x) {
+    uint32_t u = bits_of_f32(x);
+    if (isnan(x)) return x;
+    uint32_t lsb = (u >> 16) & 1u;
+    u += 0x7FFFu + lsb;
+    return f32_of_bits(u & 0xFFFF0000u);
+}
+
+static void tq_tables(const float *levels, float lv[16], float mid[15]) {
+    for (int j = 0; j < 16; ++j) lv[j] = uqo_bf16_rne(levels[j]);
+    for (int j = 0; j < 15; ++j) mid[j] = (lv[j] + lv[j + 1]) * 0.5f;
+}
+
+/* Encode one token's K and V (128 channels each) per readings T1-T4. */
+void uqo_tq4_encode_vector(const float *k_in, const float *v, const float *levels, uint8_t kidx[UQO_D], float *norm,
+                           uint8_t vcode[UQO_D], float s_out[UQO_NGROUP], float z_out[UQO_NGROUP]) {
+    float lv[16], mid[15];
+    tq_tables(levels, lv, mid);
+    float x[UQO_D];
+    memcpy(x, k_in, sizeof(x));
+    uqo_wht128_f32(x, 1);
+    float part[16];
+    for (int sl = 0; sl < 16; ++sl) {
+        float p = 0.0f;
+        for (int i = 0; i < 8; ++i) p = fmaf(x[8 * sl + i], x[8 * sl + i], p);
+        part[sl] = p;
+    }
+    for (int w = 16; w > 1; w /= 2)
+        for (int i = 0; i < w / 2; ++i) part[i] = part[2 * i] + part[2 * i + 1];
+    const float n = sqrtf(part[0]);
+    *norm = n;
+    float thr[15];
+    for (int j = 0; j < 15; ++j) thr[j] = mid[j] * n;
+    for (int c = 0; c < UQO_D; ++c) {
+        int idx = 0;
+        for (int j = 0; j < 15; ++j) idx += x[c] > thr[j];
+        kidx[c] = (uint8_t)idx;
+    }
+    for (int g = 0; g < UQO_NGROUP; ++g) {
+        const float *vg = v + g * UQO_GROUP;
+        float mn = vg[0], mx = vg[0];
+        for (int i = 1; i < UQO_GROUP; ++i) {
+            if (vg[i] < mn) mn = vg[i];
+            if (vg[i] > mx) mx = vg[i];
+        }
+        const float z = uqo_bf16_rne(mn);
+        float d = mx - z;
+        if (!(d > 0.0f)) d = 0.0f;
+        const float s = uqo_bf16_rne(d / 15.0f);
+        s_out[g] = s;
+        z_out[g] = z;
+        for (int i = 0; i < UQO_GROUP; ++i) {
+            int code = 0;
+            if (s > 0.0f) {
+                float r = rintf((vg[i] - z) / s);
+                code = r < 0.0f ? 0 : r > 15.0f ? 15 : (int)r;
+            }
+            vcode[g * UQO_GROUP + i] = (uint8_t)code;
+        }
+    }
+}
+
+static int tq_k_byte(int t, int c) { return 16 * (t + 16 * ((c % 32) / 8)) + 4 * (c / 32) + (c % 8) / 2; }
+static int tq_v_byte(int t, int c) { return 1024 + 16 * (c / 8 + 16 * (t / 4)) + 4 * (t % 4) + (c % 8) / 2; }
+static int tq_meta_byte(int t, int g) { return 2112 + 16 * (4 * (t / 4) + g) + 4 * (t % 4); }
+
+static void put_nibble(uint8_t *b, int c, uint8_t code) {
+    if (c & 1) *b = (uint8_t)((*b & 0x0F) | (code << 4));
+    else *b = (uint8_t)((*b & 0xF0) | (code & 0x0F));
+}
+static uint8_t get_nibble(const uint8_t *b, int c) { return (c & 1) ? (uint8_t)(*b >> 4) : (uint8_t)(*b & 0x0F); }
+
+/* Write tokens into the Ultra-TQ cache through physical slots (page * 16 +
+ * offset; negative or out-of-pool slots write nothing).  k, v: rows of
+ * num_kv_heads * 128 floats, token_stride floats apart.  Returns the number
+ * of (token, head) vectors written. */
+int64_t uqo_tq4_write(const float *k, const float *v, int64_t num_tokens, int num_kv_heads, int64_t token_stride,
+                      const int64_t *slots, int64_t num_pages, const float *levels, uint8_t *cache) {
+    int64_t written = 0;
+    for (int64_t t = 0; t < num_tokens; ++t) {
+        const int64_t slot = slots[t];
+        if (slot < 0 || slot / UQO_PAGE >= num_pages) continue;
+        const int64_t page = slot / UQO_PAGE;
+        const int off = (int)(slot % UQO_PAGE);
+        for (int h = 0; h < num_kv_heads; ++h) {
+            uint8_t kidx[UQO_D], vcode[UQO_D];
+            float n, s[UQO_NGROUP], z[UQO_NGROUP];
+            uqo_tq4_encode_vector(k + t * token_stride + h * UQO_D, v + t * token_stride + h * UQO_D, levels, kidx, &n,
+                                  vcode, s, z);
+            uint8_t *blk = cache + (page * num_kv_heads + h) * UQO_TQ_BLOCK;
+            for (int c = 0; c < UQO_D; ++c) {
+                put_nibble(blk + tq_k_byte(off, c), c, kidx[c]);
+                put_nibble(blk + tq_v_byte(off, c), c, vcode[c]);
+            }
+            memcpy(blk + 2048 + 4 * off, &n, 4);
+            for (int g = 0; g < UQO_NGROUP; ++g) {
+                uint32_t w = (bits_of_f32(s[g]) >> 16) | (bits_of_f32(z[g]) & 0xFFFF0000u);
+                memcpy(blk + tq_meta_byte(off, g), &w, 4);
+            }
+            ++written;
+        }
+    }
+    return written;
+}
+
+/* Read back one token's indices, codes, norm and (s, z) from the cache. */
+void uqo_tq4_load(const uint8_t *cache, int num_kv_heads, int64_t page, int head, int t, uint8_t kidx[UQO_D],
+                  float *norm, uint8_t vcode[UQO_D], float s[UQO_NGROUP], float z[UQO_NGROUP]) {
+    const uint8_t *blk = cache + (page * num_kv_heads + head) * UQO_TQ_BLOCK;
+    for (int c = 0; c < UQO_D; ++c) {
+        kidx[c] = get_nibble(blk + tq_k_byte(t, c), c);
+        vcode[c] = get_nibble(blk + tq_v_byte(t, c), c);
+    }
+    memcpy(norm, blk + 2048 + 4 * t, 4);
+    for (int g = 0; g < UQO_NGROUP; ++g) {
+        uint32_t w;
+        memcpy(&w, blk + tq_meta_byte(t, g), 4);
+        s[g] = f32_of_bits(w << 16);
+        z[g] = f32_of_bits(w & 0xFFFF0000u);
+    }
+}
+
+/* Dequantise one token (algorithm's Decode, reading T3/T4): K = n * c[idx]
+ * (the rotated key), V = bf16(fma(s, code, z)). */
+void uqo_tq4_dequant(const uint8_t *cache, int num_kv_heads, int64_t page, int head, int t, const float *levels,
+                     double kout[UQO_D], double vout[UQO_D]) {
+    float lv[16], mid[15];
+    tq_tables(levels, lv, mid);
+    uint8_t kidx[UQO_D], vcode[UQO_D];
+    float n, s[UQO_NGROUP], z[UQO_NGROUP];
+    uqo_tq4_load(cache, num_kv_heads, page, head, t, kidx, &n, vcode, s, z);
+    for (int c = 0; c < UQO_D; ++c) {
+        kout[c] = (double)n * (double)lv[kidx[c]];
+        vout[c] = (double)uqo_bf16_rne(fmaf(s[c / UQO_GROUP], (float)vcode[c], z[c / UQO_GROUP]));
+    }
+}
+
+/* Decode attention over the Ultra-TQ cache (its algorithm, Decode): the
+ * query rotated and rounded to BF16 (T5), scores scale * <q, K> over the
+ * dequantised rotated keys, softmax and the weighted sum of the (unrotated)
+ * dequantised values, all in fp64. */
+void uqo_tq4_decode_attention(const float *q, int batch, int num_q_heads, int num_kv_heads, const uint8_t *cache,
+                              const int32_t *page_table, int max_pages_per_seq, const int32_t *context_lens,
+                              double softmax_scale, const float *levels, double *out) {
+    const int G = num_q_heads / num_kv_heads;
+#pragma omp parallel for collapse(2) schedule(dynamic)
+    for (int b = 0; b < batch; ++b) {
+        for (int hq = 0; hq < num_q_heads; ++hq) {
+            double *o = out + ((int64_t)b * num_q_heads + hq) * UQO_D;
+            const int ctx = context_lens[b];
+            memset(o, 0, UQO_D * sizeof(double));
+            if (ctx <= 0) continue;
+            float qr[UQO_D];
+            memcpy(qr, q + ((int64_t)b * num_q_heads + hq) * UQO_D, sizeof(qr));
+            uqo_wht128_f32(qr, 1);
+            double qb[UQO_D];
+            for (int c = 0; c < UQO_D; ++c) qb[c] = (double)uqo_bf16_rne(qr[c]);
+            const int hk = hq / G;
+            double *sc = (double *)malloc((size_t)ctx * sizeof(double));
+            double mx = -INFINITY;
+            double kv[UQO_D], vv[UQO_D];
+            for (int j = 0; j < ctx; ++j) {
+                const int64_t page = page_table[(int64_t)b * max_pages_per_seq + j / UQO_PAGE];
+                uqo_tq4_dequant(cache, num_kv_heads, page, hk, j % UQO_PAGE, levels, kv, vv);
+                double d = 0.0;
+                for (int c = 0; c < UQO_D; ++c) d += qb[c] * kv[c];
+                sc[j] = softmax_scale * d;
+                if (sc[j] > mx) mx = sc[j];
+            }
+            double l = 0.0;
+            for (int j = 0; j < ctx; ++j) {
+                const int64_t page = page_table[(int64_t)b * max_pages_per_seq + j / UQO_PAGE];
+                uqo_tq4_dequant(cache, num_kv_heads, page, hk, j % UQO_PAGE, levels, kv, vv);
+                const double p = exp(sc[j] - mx);
+                l += p;
+                for (int c = 0; c < UQO_D; ++c) o[c] += p * vv[c];
+            }
+            for (int c = 0; c < UQO_D; ++c) o[c] /= l;
+            free(sc);
+        }
+    }
+}

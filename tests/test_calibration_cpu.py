@@ -8,9 +8,9 @@ group, to limits and invariants, and to the cache encoder's own codes.
 Part 2 reproduces the MSE claims on synthetic rotated unit vectors (uniform
 on the sphere; the paper fits c on captured keys, which are not available):
 
-  * Lloyd-Max for the coordinate law of a uniform unit vector, solved here
-    from closed forms and pinned to Max's 16-level Gaussian table (the
-    d -> infinity limit of that law);
+  * Lloyd-Max for the coordinate law of a uniform unit vector (the package's
+    codebook module, solved from closed forms), pinned to Max's 16-level
+    Gaussian table (the d -> infinity limit of that law);
   * the ordering Lloyd-Max < FP4 with s = c m (c = 0.156) < plain per-group
     FP4 (the OCP MX rule s = 2^(floor(log2 m) - 2)), with the constant
     closing more than half of the gap, at d in {64, 128, 256};
@@ -20,14 +20,13 @@ on the sphere; the paper fits c on captured keys, which are not available):
     minimiser lies near 0.195, the value the paper calls power-of-two
     optimal.
 """
-import math
-
 import numpy as np
 import pytest
-from scipy import special, stats
+from scipy import stats
 
 import oracle
 from paper_2606_20474_amd import workloads
+from paper_2606_20474_amd.codebook import default_tq_codebook, gaussian_lloyd_max, sphere_lloyd_max
 
 E2M1 = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0])
 
@@ -122,45 +121,6 @@ def test_rotation_keeps_the_energy():
 # Part 2: Lloyd-Max, the codebook ordering and the c ablation
 
 
-def lloyd_max(cdf, partial_mean, second_moment, levels0, iters=20000):
-    """Lloyd's iteration on a symmetric density given by closed forms:
-    cdf(t) = P(X <= t), partial_mean(t) = E[X; X <= t].  Returns the levels
-    and the MSE E[X^2] - sum_k P_k c_k^2 (valid at the centroid condition)."""
-    lv = np.asarray(levels0, np.float64)
-    for _ in range(iters):
-        t = np.concatenate([[-np.inf], (lv[1:] + lv[:-1]) / 2, [np.inf]])
-        P = np.diff(cdf(t))
-        lv = np.diff(partial_mean(t)) / P
-    t = np.concatenate([[-np.inf], (lv[1:] + lv[:-1]) / 2, [np.inf]])
-    P = np.diff(cdf(t))
-    return lv, second_moment - np.sum(P * lv ** 2)
-
-
-def gaussian_lloyd_max(n=16):
-    cdf = lambda t: stats.norm.cdf(t)
-    pm = lambda t: -stats.norm.pdf(t)
-    return lloyd_max(cdf, pm, 1.0, stats.norm.ppf((np.arange(n) + 0.5) / n))
-
-
-def sphere_lloyd_max(d, n=16):
-    """A coordinate of a uniform unit vector in R^d has density proportional
-    to (1 - x^2)^((d-3)/2) on [-1, 1], i.e. (1 + x) / 2 ~ Beta(a, a) with
-    a = (d-1)/2; its partial first moment is -(1 - t^2)^a / (2 a Z) with
-    Z = 2^(2a-1) B(a, a); E[X^2] = 1/d."""
-    a = (d - 1) / 2
-    logZ = (2 * a - 1) * math.log(2) + special.betaln(a, a)
-
-    def cdf(t):
-        return special.betainc(a, a, np.clip((1 + t) / 2, 0, 1))
-
-    def pm(t):
-        u = np.clip(1 - np.square(np.clip(t, -1, 1)), 0, None)
-        return -np.exp(a * np.log(np.maximum(u, 1e-300)) - logZ) / (2 * a) * (u > 0)
-
-    lv0 = 2 * special.betaincinv(a, a, (np.arange(n) + 0.5) / n) - 1
-    return lloyd_max(cdf, pm, 1.0 / d, lv0)
-
-
 def e2m1_round(t):
     """Nearest E2M1 level of t (sign kept), ties to the even code, beyond 6
     saturating."""
@@ -185,6 +145,22 @@ def test_lloyd_max_reproduces_max_table():
     # the converged MSE, 0.0095010, sits a few units of the last tabulated
     # digit above the table (20.22 dB either way)
     assert abs(mse - MAX_N16_MSE) < 1e-5, mse
+
+
+def test_theoretical_codebook_matches_the_printed_level():
+    """Section "Calibrated Centroids" prints the largest theoretical level at
+    d = 64 as 0.342: the Gaussian Lloyd-Max level over sqrt(64) (the default
+    codebook), not the exact law's Lloyd-Max level."""
+    import os
+    printed = None
+    with open(os.path.join(os.path.dirname(__file__), "golden", "paper_constants.txt")) as f:
+        for line in f:
+            if line.startswith("tq_theory_max_level_d64"):
+                printed = float(line.split()[1])
+    cb = default_tq_codebook(64)
+    assert abs(float(cb.max()) - printed) < 5e-4
+    assert np.allclose(cb, -cb[::-1]) and np.all(np.diff(cb) > 0)
+    assert abs(sphere_lloyd_max(64)[0].max() - printed) > 5e-3
 
 
 def test_sphere_coordinates_follow_the_beta_law():
