@@ -38,7 +38,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 KV_BYTES_PER_TOKEN_HEAD = 136   # K and V: 2 x (64 B codes + 4 B scales)
-REF_BYTES_PER_TOKEN_HEAD = {"fp8": 256, "bf16": 512}
+REF_BYTES_PER_TOKEN_HEAD = {"fp8": 256, "bf16": 512, "tq4": 148}
 REF_SCALE = 0.3                 # per-tensor FP8 scale of the comparison cache (|x| up to 134 representable)
 
 
@@ -52,8 +52,8 @@ def parse():
     ap.add_argument("--partition", type=int, default=-1, help="partition tokens (-1: workload default)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-seqs", type=int, default=4)
-    ap.add_argument("--comparators", default="fp8,bf16",
-                    help="comma list of plain comparison caches to time as well (fp8, bf16) or 'none'")
+    ap.add_argument("--comparators", default="fp8,bf16,tq4",
+                    help="comma list of comparison caches to time as well (fp8, bf16, tq4) or 'none'")
     ap.add_argument("--no-cascade", action="store_true",
                     help="workloads with a shared prefix: read it per sequence instead of once per kv head")
     ap.add_argument("--no-write-path", action="store_true",
@@ -146,8 +146,10 @@ def timed(step, steps, warmup, stream):
 
 def comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, args, dev, stream, prefix=None):
     """The same step (uq_ref_decode_step: the new token of every sequence
-    written by the partition launch, then the merge) over a plain FP8 or
-    BF16 cache holding the same K/V."""
+    written by the partition launch, then the merge) over a comparison cache
+    holding the same K/V: plain FP8 or BF16, or the Ultra-TQ codebook cache
+    (148 B per token and kv head: 64 B of K indices, a 4 B norm, 64 B of V
+    codes and 4 x 4 B of (scale, zero))."""
     import torch
     desc = uq.RefCacheDesc(num_kv_heads=wl.num_kv_heads, num_pages=wl.num_pages, fmt=fmt, k_scale=REF_SCALE,
                            v_scale=REF_SCALE)

@@ -330,7 +330,7 @@ uq_status uq_decode_cascade_merge(const uq_cache_desc *desc, int32_t batch, int3
  * BF16 KV cache (section "Performance Results").  These calls build both
  * with the same paging and the same decode kernel as the FP4 cache (the
  * same staging ring, online softmax, PV and merge), so a comparison between
- * them measures the cache format.  Neither format rotates anything.
+ * them measures the cache format.  FP8 and BF16 rotate nothing.
  *
  * Pool layout (one buffer, caller-owned, uq_ref_cache_bytes bytes):
  * [num_pages][num_kv_heads][K, V][tile], tile = 16 tokens x 128 channels in
@@ -341,11 +341,33 @@ uq_status uq_decode_cascade_merge(const uq_cache_desc *desc, int32_t batch, int3
  *                  V at ((t/4) * 16 + c/8) * 64 + (t%4) * 16 + 2 * (c%8).
  * (t = token within the page, c = channel; FP8 entries are one byte, BF16
  * entries two, little endian.)
+ *
+ * TQ4 is the codebook encoding UltraQuant replaces (appendix "Calibrated LUT
+ * int4 KV Encoding (Ultra-TQ)", its algorithm): K is rotated by the same
+ * R as the FP4 cache, its fp32 norm n is stored per token and each rotated
+ * channel x is coded to the nearest of the 16 codebook levels c_j (rounded
+ * to BF16) as the number of midpoints m_j = (c_j + c_{j+1}) / 2 with
+ * x > m_j * n (fp32); the decoded key is n * c[idx].  The norm is the
+ * fp32 square root of a fused multiply-add sum in a fixed order (per 8
+ * channels in channel order, then a pairwise tree over the 16 slices), so
+ * the codes are reproducible.  V is not rotated: per 32-channel group,
+ * z = bf16(min), s = bf16(max(max - z, 0) / 15), code = clamp(rint((x - z)
+ * / s), 0, 15) (0 when s = 0), decoded as bf16(fma(s, code, z)).  Decode
+ * attention rotates the query and rounds it to BF16.  The block of one
+ * (page, kv head) is 2368 bytes:
+ *   [0, 1024)     K indices, (t, c) at 16 * (t + 16 * ((c%32)/8)) + 4 * (c/32)
+ *                 + (c%8)/2;
+ *   [1024, 2048)  V codes at 1024 + 16 * (c/8 + 16 * (t/4)) + 4 * (t%4) + (c%8)/2;
+ *                 (low nibble = even channel in both);
+ *   [2048, 2112)  K norms, fp32, token t at 2048 + 4 t;
+ *   [2112, 2368)  V (s, z) as two BF16 (s in the low half), token t and
+ *                 group g at 2112 + 16 * (4 * (t/4) + g) + 4 * (t%4).
  * ---------------------------------------------------------------------- */
 
 typedef enum uq_ref_format {
     UQ_REF_FP8_E4M3 = 1, /* OCP E4M3 (no infinities), one scale per tensor */
-    UQ_REF_BF16 = 2
+    UQ_REF_BF16 = 2,
+    UQ_REF_TQ4 = 3       /* the Ultra-TQ codebook cache (see below) */
 } uq_ref_format;
 
 typedef struct uq_ref_cache_desc {
@@ -355,7 +377,10 @@ typedef struct uq_ref_cache_desc {
     int32_t format;    /* uq_ref_format */
     int64_t num_pages;
     float k_scale;     /* FP8: stored byte = e4m3(x / k_scale), value = byte * k_scale;  */
-    float v_scale;     /* finite and > 0.  Ignored for BF16. */
+    float v_scale;     /* finite and > 0.  Ignored for BF16 and TQ4. */
+    const float *codebook; /* TQ4: 16 finite key levels (host memory, read during each
+                              call), strictly ascending once rounded to BF16.  Ignored
+                              for FP8 and BF16. */
 } uq_ref_cache_desc;
 
 /* Bytes of the pool of a comparison cache; 0 for an invalid descriptor. */
@@ -364,9 +389,11 @@ size_t uq_ref_cache_bytes(const uq_ref_cache_desc *desc);
 /*
  * uq_ref_write_kv -- write K and V rows into a comparison cache: FP8 bytes
  * are e4m3(x / scale) rounded to nearest even and saturated at +-448; BF16
- * is round-to-nearest-even.  Arguments, slot addressing (physical slots, or
+ * is round-to-nearest-even; TQ4 as described above.  Arguments, slot addressing (physical slots, or
  * logical slots through page_table), skipped slots and errors are those of
- * uq_quantize_kv; `cache` must be 16-byte aligned.
+ * uq_quantize_kv; `cache` must be 16-byte aligned.  A TQ4 descriptor whose
+ * codebook is NULL, non-finite or not strictly ascending in BF16 is
+ * INVALID_ARGUMENT (for every call taking the descriptor).
  */
 uq_status uq_ref_write_kv(const uq_ref_cache_desc *desc, const void *k, const void *v, uq_dtype in_dtype,
                           int64_t num_tokens, int64_t token_stride, const int32_t *page_table, int32_t num_seqs,
@@ -382,7 +409,10 @@ size_t uq_ref_decode_workspace_bytes(const uq_ref_cache_desc *desc, int32_t batc
  * (nearest even, saturating) and q.k runs on the FP8 x FP8 matrix
  * instruction; the scores are multiplied by softmax_scale * k_scale and the
  * output by v_scale.  BF16 cache: the query is cast to BF16 and q.k runs on
- * BF16 matrix instructions.  Every other argument, the output and the
+ * BF16 matrix instructions.  TQ4 cache: the rotated query is cast to BF16,
+ * the K indices are decoded through the BF16 levels, q.k runs on BF16
+ * matrix instructions and each score is multiplied by its token's norm; V
+ * is decoded to BF16 values.  Every other argument, the output and the
  * errors are those of uq_decode_attention.  uq_ref_decode_partials and
  * uq_ref_decode_merge are its two launches, as for the FP4 cache.
  */

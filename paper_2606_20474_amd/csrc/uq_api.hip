@@ -1,5 +1,6 @@
 // uq_api.hip -- the C ABI of libuq (declared in include/uq.h): argument
 // validation on the host, launch configuration, workspace sizing.
+#include <cstring>
 #include <math.h>
 #include <stdint.h>
 
@@ -180,14 +181,58 @@ uq_status check_split_args(const uq_cache_desc* desc, const void* q, uq_dtype q_
 
 // Comparison caches: the descriptor check and the FP4 descriptor with the
 // same geometry (the decode set-up above is shared; no rotation).
+// fp32 -> nearest BF16 (ties to even) of a finite value, as fp32.
+float bf16_nearest(float x) {
+    uint32_t u;
+    memcpy(&u, &x, 4);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    u &= 0xFFFF0000u;
+    float r;
+    memcpy(&r, &u, 4);
+    return r;
+}
+
+// The Ultra-TQ codebook tables: levels rounded to BF16 (finite, strictly
+// ascending), the encoder's midpoints (c_j + c_{j+1}) / 2 in fp32 and the
+// decoder's byte tables.  False for an unusable codebook.
+bool tq_tables(const float* cb, uq::TqTables& t) {
+    if (cb == nullptr) return false;
+    float lv[16];
+    for (int j = 0; j < 16; ++j) {
+        if (!isfinite(cb[j])) return false;
+        lv[j] = bf16_nearest(cb[j]);
+        if (!isfinite(lv[j])) return false;
+    }
+    for (int j = 0; j < 15; ++j)
+        if (!(lv[j] < lv[j + 1])) return false;
+    for (int j = 0; j < 15; ++j) t.mid[j] = (lv[j] + lv[j + 1]) * 0.5f;
+    for (int w = 0; w < 4; ++w) {
+        uint32_t hi = 0, lo = 0;
+        for (int b = 0; b < 4; ++b) {
+            uint32_t u;
+            memcpy(&u, &lv[4 * w + b], 4);
+            hi |= ((u >> 24) & 0xFFu) << (8 * b);
+            lo |= ((u >> 16) & 0xFFu) << (8 * b);
+        }
+        t.lut[w] = hi;
+        t.lut[4 + w] = lo;
+    }
+    return true;
+}
+
 uq_status check_ref_desc(const uq_ref_cache_desc* d) {
     if (d == nullptr) return UQ_ERR_INVALID_ARGUMENT;
     if (d->num_kv_heads < 1 || d->num_pages < 1) return UQ_ERR_INVALID_ARGUMENT;
-    if (d->format != UQ_REF_FP8_E4M3 && d->format != UQ_REF_BF16) return UQ_ERR_UNSUPPORTED;
+    if (d->format != UQ_REF_FP8_E4M3 && d->format != UQ_REF_BF16 && d->format != UQ_REF_TQ4)
+        return UQ_ERR_UNSUPPORTED;
     if (d->head_dim != kHeadDim || d->page_size != kPageSize) return UQ_ERR_UNSUPPORTED;
     if (d->format == UQ_REF_FP8_E4M3 &&
         !(isfinite(d->k_scale) && d->k_scale > 0.0f && isfinite(d->v_scale) && d->v_scale > 0.0f))
         return UQ_ERR_INVALID_ARGUMENT;
+    if (d->format == UQ_REF_TQ4) {
+        uq::TqTables t;
+        if (!tq_tables(d->codebook, t)) return UQ_ERR_INVALID_ARGUMENT;
+    }
     return UQ_OK;
 }
 
@@ -203,9 +248,15 @@ uq_cache_desc geometry_of(const uq_ref_cache_desc* d) {
     return g;
 }
 
-int32_t ref_fmt(const uq_ref_cache_desc* d) { return d->format == UQ_REF_FP8_E4M3 ? uq::kFp8 : uq::kBf16; }
+int32_t ref_fmt(const uq_ref_cache_desc* d) {
+    return d->format == UQ_REF_FP8_E4M3 ? uq::kFp8 : d->format == UQ_REF_TQ4 ? uq::kTq4 : uq::kBf16;
+}
 
-int64_t ref_tile_bytes(const uq_ref_cache_desc* d) { return d->format == UQ_REF_FP8_E4M3 ? 2048 : 4096; }
+// Half of the bytes of one (page, kv head): the K tile, or for TQ4 half of
+// the block that holds both.
+int64_t ref_tile_bytes(const uq_ref_cache_desc* d) {
+    return d->format == UQ_REF_FP8_E4M3 ? 2048 : d->format == UQ_REF_TQ4 ? uq::kTqBlock / 2 : 4096;
+}
 
 }  // namespace
 
@@ -444,6 +495,7 @@ uq_status uq_ref_write_kv(const uq_ref_cache_desc* desc, const void* k, const vo
     p.v_scale = desc->format == UQ_REF_FP8_E4M3 ? desc->v_scale : 1.0f;
     p.kv_fmt = ref_fmt(desc);
     p.cache = cache;
+    if (desc->format == UQ_REF_TQ4) tq_tables(desc->codebook, p.tq);
     return from_hip(uq::launch_write_kv_ref(p, int(in_dtype), static_cast<hipStream_t>(stream)));
 }
 
@@ -473,6 +525,7 @@ static uq_status ref_decode_setup(const uq_ref_cache_desc* desc, const void* q, 
     if (s != UQ_OK) return s;
     p.kv_fmt = ref_fmt(desc);
     p.scales = nullptr;
+    if (desc->format == UQ_REF_TQ4) tq_tables(desc->codebook, p.tq);
     if (desc->format == UQ_REF_FP8_E4M3) {
         p.scale_log2 = float(double(softmax_scale) * double(desc->k_scale) * 1.4426950408889634);
         p.out_scale = desc->v_scale;

@@ -6,7 +6,14 @@
 //   kFp4   the UltraQuant cache: FP4 E2M1 codes + UE8M0 scales per 32
 //          channels, K (and V with rotate_v) Walsh-Hadamard rotated;
 //   kFp8   a plain FP8 E4M3 cache with one scale per tensor;
-//   kBf16  a plain BF16 cache.
+//   kBf16  a plain BF16 cache;
+//   kTq4   the Ultra-TQ codebook cache (rotated K as 4-bit indices into 16
+//          levels times a per-token norm; V as 4-bit uniform codes with a
+//          BF16 (scale, zero) per 32 channels): K is decoded in registers
+//          by byte-permute table lookups into BF16 levels, QK^T runs on
+//          BF16 matrix instructions and each score is multiplied by its
+//          token's norm; V is decoded with one fused multiply-add per
+//          element into BF16.
 //
 // decode_kernel<F>: one block of Fmt<F>::kWaves waves per (partition, kv
 // head, sequence), in an XCD-aware linear order (kv head fastest).
@@ -79,6 +86,14 @@ template <> struct Fmt<kBf16> {
     static constexpr int kScaleBlock = 0;
     static constexpr int kWaves = 2;
     static constexpr int kOccupancy = 1;
+};
+// Ultra-TQ: per page 1 KiB of K indices, 1 KiB of V codes and 320 bytes of
+// norms and (scale, zero) words ("scale block").
+template <> struct Fmt<kTq4> {
+    static constexpr int kTile = 1024;
+    static constexpr int kScaleBlock = kTqBlock - 2048;
+    static constexpr int kWaves = 4;
+    static constexpr int kOccupancy = 3;
 };
 
 // One stage of the ring: [K page0][V page0][K page1][V page1][scales0][scales1].
@@ -165,6 +180,21 @@ template <int F>
 __device__ __forceinline__ void stage_issue(uint8_t* stage, const uint8_t* __restrict__ codes,
                                             const uint8_t* __restrict__ scales, int64_t tile0, int64_t tile1,
                                             int lane) {
+    if constexpr (F == kTq4) {
+        // stage: [K0][V0][K1][V1] 1 KiB each, then both pages' 320-byte
+        // metadata (lanes 0..19 page 0, lanes 20..39 page 1)
+        const uint8_t* b0 = codes + (tile0 >> 1) * kTqBlock;
+        const uint8_t* b1 = codes + (tile1 >> 1) * kTqBlock;
+        __builtin_amdgcn_global_load_lds(b0 + 16 * lane, (lds_ptr_t)stage, 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(b0 + 1024 + 16 * lane, (lds_ptr_t)(stage + 1024), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(b1 + 16 * lane, (lds_ptr_t)(stage + 2048), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(b1 + 1024 + 16 * lane, (lds_ptr_t)(stage + 3072), 16, 0, 0);
+        if (lane < 40) {
+            const uint8_t* m = lane < 20 ? b0 + kTqMeta + 16 * lane : b1 + kTqMeta + 16 * (lane - 20);
+            __builtin_amdgcn_global_load_lds(m, (lds_ptr_t)(stage + 4096), 16, 0, 0);
+        }
+        return;
+    }
     constexpr int T = Fmt<F>::kTile;
     const uint8_t* k0 = codes + tile0 * T + 16 * lane;
     const uint8_t* k1 = codes + tile1 * T + 16 * lane;
@@ -208,6 +238,12 @@ template <> struct StageRegs<kFp8> {
 };
 template <> struct StageRegs<kBf16> {
     uint4 k[2][4], v[2][4];   // K: 4 k-steps x 16 bytes; V: 64 bytes
+};
+template <> struct StageRegs<kTq4> {
+    uint4 k[2];    // K indices of token lane%16, channels 32s + 8*(lane/16) + 0..7 in dword s
+    uint4 v[2];    // V codes of tokens 4*(lane/16) + 0..3 (dword t), channels 8*(lane%16) + 0..7
+    uint4 kn[2];   // K norms of tokens 4*(lane/16) + 0..3
+    uint4 vm[2];   // V (scale, zero) of the same tokens, group (lane%16)/4
 };
 
 __device__ __forceinline__ void stage_read(StageRegs<kFp4>& r, uint32_t stage_addr, int lane) {
@@ -278,9 +314,58 @@ __device__ __forceinline__ void stage_read(StageRegs<kBf16>& r, uint32_t stage_a
         : "memory");
 }
 
+__device__ __forceinline__ void stage_read(StageRegs<kTq4>& r, uint32_t stage_addr, int lane) {
+    const uint32_t ak = stage_addr + 16 * lane;
+    const uint32_t an = stage_addr + 4096 + 16 * (lane >> 4);
+    const uint32_t am = stage_addr + 4096 + 64 + 16 * (4 * (lane >> 4) + ((lane & 15) >> 2));
+    asm volatile(
+        "ds_read_b128 %0, %8\n\t"
+        "ds_read_b128 %1, %8 offset:1024\n\t"
+        "ds_read_b128 %2, %8 offset:2048\n\t"
+        "ds_read_b128 %3, %8 offset:3072\n\t"
+        "ds_read_b128 %4, %9\n\t"
+        "ds_read_b128 %5, %9 offset:320\n\t"
+        "ds_read_b128 %6, %10\n\t"
+        "ds_read_b128 %7, %10 offset:320\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(r.k[0]), "=&v"(r.v[0]), "=&v"(r.k[1]), "=&v"(r.v[1]), "=&v"(r.kn[0]), "=&v"(r.kn[1]),
+          "=&v"(r.vm[0]), "=&v"(r.vm[1])
+        : "v"(ak), "v"(an), "v"(am)
+        : "memory");
+}
+
 // Query operand in registers.
 template <int F> struct QOperand { v8i q; };               // FP8 bytes, 32 per lane
 template <> struct QOperand<kBf16> { v8bf q[4]; };          // 4 k-steps x 8 BF16 per lane
+// Ultra-TQ: the BF16 query with each k-step's 8 channels in the order
+// 0, 2, 4, 6, 1, 3, 5, 7 (the order the index decoder produces), and the
+// codebook's byte tables.
+template <> struct QOperand<kTq4> {
+    v8bf q[4];
+    uint32_t lut[8];
+};
+
+// BF16 levels of 8 K indices (nibble i of w = channel i): the byte tables
+// are looked up with v_perm (8 entries per instruction, the 4th index bit
+// picks the half), high and low bytes separately, then interleaved into
+// BF16 pairs (channels 0,2), (4,6), (1,3), (5,7).
+__device__ __forceinline__ uint4 tq_decode8(uint32_t w, const uint32_t (&lut)[8]) {
+    const uint32_t e = w & 0x0F0F0F0Fu;            // byte j: index of channel 2j
+    const uint32_t o = (w >> 4) & 0x0F0F0F0Fu;     // byte j: index of channel 2j+1
+    const uint32_t se = e & 0x07070707u, so = o & 0x07070707u;
+    const uint32_t te = ((e >> 1) & 0x04040404u) | 0x03020100u;
+    const uint32_t to = ((o >> 1) & 0x04040404u) | 0x03020100u;
+    const uint32_t he = __builtin_amdgcn_perm(__builtin_amdgcn_perm(lut[3], lut[2], se),
+                                              __builtin_amdgcn_perm(lut[1], lut[0], se), te);
+    const uint32_t le = __builtin_amdgcn_perm(__builtin_amdgcn_perm(lut[7], lut[6], se),
+                                              __builtin_amdgcn_perm(lut[5], lut[4], se), te);
+    const uint32_t ho = __builtin_amdgcn_perm(__builtin_amdgcn_perm(lut[3], lut[2], so),
+                                              __builtin_amdgcn_perm(lut[1], lut[0], so), to);
+    const uint32_t lo = __builtin_amdgcn_perm(__builtin_amdgcn_perm(lut[7], lut[6], so),
+                                              __builtin_amdgcn_perm(lut[5], lut[4], so), to);
+    return uint4{__builtin_amdgcn_perm(he, le, 0x05010400u), __builtin_amdgcn_perm(he, le, 0x07030602u),
+                 __builtin_amdgcn_perm(ho, lo, 0x05010400u), __builtin_amdgcn_perm(ho, lo, 0x07030602u)};
+}
 
 // S^T[token][query head] of one page: rows = the page's 16 tokens (lane's
 // VGPR i holds token 4*(lane/16)+i), columns = query heads (lane%16).
@@ -304,6 +389,18 @@ __device__ __forceinline__ v4f qk_page(const StageRegs<kBf16>& r, int pg, const 
 }
 
 __device__ __forceinline__ uint32_t dword(const uint4& v, int i) { return i == 0 ? v.x : i == 1 ? v.y : i == 2 ? v.z : v.w; }
+
+// Ultra-TQ: <q, c[idx]> on the BF16 levels, then times the token's norm.
+__device__ __forceinline__ v4f qk_page(const StageRegs<kTq4>& r, int pg, const QOperand<kTq4>& q) {
+    v4f s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int st = 0; st < 4; ++st)
+        s = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(v8bf, tq_decode8(dword(r.k[pg], st), q.lut)),
+                                                    q.q[st], s, 0, 0, 0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) s[i] *= bits_f32(dword(r.kn[pg], i));
+    return s;
+}
 
 // BF16 pair of this lane's V channels 8n+2C, 8n+2C+1 of token 4*(lane/16)+t
 // of page pg, as one dword (even channel in the low half).
@@ -347,6 +444,37 @@ __device__ __forceinline__ void pv_pair(const R& r, const float (&sc)[2][4], con
     acc_o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Vo, Plo, acc_o, 0, 0, 0);
 }
 
+// Ultra-TQ PV for channel pair C: each V value is bf16(fma(scale, code,
+// zero)) of its token's group, packed two tokens per register in the k-slot
+// order of P.
+template <int C>
+__device__ __forceinline__ void pv_pair(const StageRegs<kTq4>& r, const float (&)[2][4], const v8bf& Phi,
+                                        const v8bf& Plo, v4f& acc_e, v4f& acc_o) {
+    float ve[2][4], vo[2][4];
+#pragma unroll
+    for (int pg = 0; pg < 2; ++pg) {
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+            const uint32_t w = dword(r.v[pg], t);
+            const uint32_t e = w & 0x0F0F0F0Fu, o = (w >> 4) & 0x0F0F0F0Fu;
+            const uint32_t m = dword(r.vm[pg], t);
+            const float s = bits_f32(m << 16), z = bits_f32(m & 0xFFFF0000u);
+            ve[pg][t] = __builtin_fmaf(s, float((e >> (8 * C)) & 0xFFu), z);
+            vo[pg][t] = __builtin_fmaf(s, float((o >> (8 * C)) & 0xFFu), z);
+        }
+    }
+    const uint4 ae = {pack_bf16x2(ve[0][0], ve[0][1]), pack_bf16x2(ve[0][2], ve[0][3]), pack_bf16x2(ve[1][0], ve[1][1]),
+                      pack_bf16x2(ve[1][2], ve[1][3])};
+    const uint4 ao = {pack_bf16x2(vo[0][0], vo[0][1]), pack_bf16x2(vo[0][2], vo[0][3]), pack_bf16x2(vo[1][0], vo[1][1]),
+                      pack_bf16x2(vo[1][2], vo[1][3])};
+    const v8bf Ve = __builtin_bit_cast(v8bf, ae);
+    const v8bf Vo = __builtin_bit_cast(v8bf, ao);
+    acc_e = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ve, Phi, acc_e, 0, 0, 0);
+    acc_e = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ve, Plo, acc_e, 0, 0, 0);
+    acc_o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Vo, Phi, acc_o, 0, 0, 0);
+    acc_o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Vo, Plo, acc_o, 0, 0, 0);
+}
+
 __device__ __forceinline__ void write_out(const DecodeParams& p, int64_t row, int L, const float (&o)[8]) {
     const int64_t ob = row * kHeadDim + 8 * L;
     if (p.out_dtype == 0) {
@@ -377,6 +505,14 @@ __device__ __forceinline__ void zero_token(StageRegs<kFp8>& c, int pg, int t) {
 }
 __device__ __forceinline__ void zero_token(StageRegs<kBf16>& c, int pg, int t) { c.v[pg][t] = uint4{0u, 0u, 0u, 0u}; }
 __device__ __forceinline__ void zero_token(StageRegs<kFp4>&, int, int) {}   // handled through the scale byte
+__device__ __forceinline__ void zero_token(StageRegs<kTq4>& c, int pg, int t) {
+    // scale and zero 0: the value decodes to 0 whatever the bytes
+    uint4& m = c.vm[pg];
+    if (t == 0) m.x = 0u;
+    else if (t == 1) m.y = 0u;
+    else if (t == 2) m.z = 0u;
+    else m.w = 0u;
+}
 
 template <int F>
 __global__ void __launch_bounds__(64 * Fmt<F>::kWaves)
@@ -469,7 +605,7 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
     const int k_new_local = it_new / W;                              // that wave's local iteration
 
     __shared__ __attribute__((aligned(16))) uint8_t smem[W * ring_bytes<F>()];
-    __shared__ __attribute__((aligned(16))) uint8_t q_lds[F == kBf16 ? 4 * 64 * 16 : 64 * 32];
+    __shared__ __attribute__((aligned(16))) uint8_t q_lds[(F == kBf16 || F == kTq4) ? 4 * 64 * 16 : 64 * 32];
     __shared__ float red_m[W][16];
     __shared__ float red_l[W][16];
 
@@ -571,12 +707,20 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
         const int qL = tid & 15;
         int rb, rhq;
         const bool qvalid = qr < 16 && row_of(qr, rb, rhq);
-        if constexpr (F == kBf16) {
+        if constexpr (F == kBf16 || F == kTq4) {
             // channels 8*qL..+7 are k-step qL/4, lane (qL%4)*16 + qr, 16 bytes
             uint4 w = {0u, 0u, 0u, 0u};
-            if (qvalid)
-                w = uint4{pack_bf16x2(qx[h][0], qx[h][1]), pack_bf16x2(qx[h][2], qx[h][3]),
-                          pack_bf16x2(qx[h][4], qx[h][5]), pack_bf16x2(qx[h][6], qx[h][7])};
+            if (qvalid) {
+                if constexpr (F == kTq4) {
+                    // rotated like the keys, channels in the decoder's order
+                    wht128_x8(qx[h], qL);
+                    w = uint4{pack_bf16x2(qx[h][0], qx[h][2]), pack_bf16x2(qx[h][4], qx[h][6]),
+                              pack_bf16x2(qx[h][1], qx[h][3]), pack_bf16x2(qx[h][5], qx[h][7])};
+                } else {
+                    w = uint4{pack_bf16x2(qx[h][0], qx[h][1]), pack_bf16x2(qx[h][2], qx[h][3]),
+                              pack_bf16x2(qx[h][4], qx[h][5]), pack_bf16x2(qx[h][6], qx[h][7])};
+                }
+            }
             *reinterpret_cast<uint4*>(q_lds + ((qL >> 2) * 64 + (qL & 3) * 16 + qr) * 16) = w;
         } else {
             uint32_t lo = qw[h][0], hi = qw[h][1];
@@ -601,10 +745,14 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
     }
     __syncthreads();
     QOperand<F> qop;
-    if constexpr (F == kBf16) {
+    if constexpr (F == kBf16 || F == kTq4) {
 #pragma unroll
         for (int st = 0; st < 4; ++st)
             qop.q[st] = __builtin_bit_cast(v8bf, *reinterpret_cast<const uint4*>(q_lds + (st * 64 + lane) * 16));
+        if constexpr (F == kTq4) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) qop.lut[j] = p.tq.lut[j];
+        }
     } else {
         const uint4* src = reinterpret_cast<const uint4*>(q_lds + lane * 32);
         const uint4 a = src[0], c = src[1];
@@ -615,7 +763,7 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
     // first two stages are in flight (the store is not waited for).
     TokenBits<F> tok{};
     if (append && lane < 16) {
-        tok = encode_token<F>(xk, xv, lane, p.c, p.rotate_v != 0, p.k_scale, p.v_scale);
+        tok = encode_token<F>(xk, xv, lane, p.c, p.rotate_v != 0, p.k_scale, p.v_scale, p.tq);
         if (page_new >= 0 && int64_t(page_new) < p.num_pages)
             store_token<F>(p.codes, p.scales, (int64_t(page_new) * p.num_kv_heads + hk) * 2, pos_new & 15, lane, tok);
     }
@@ -863,6 +1011,7 @@ static hipError_t launch_partials(const DecodeParams& p, hipStream_t stream) {
 hipError_t launch_decode_partials(const DecodeParams& p, hipStream_t stream) {
     if (p.kv_fmt == kFp8) return launch_partials<kFp8>(p, stream);
     if (p.kv_fmt == kBf16) return launch_partials<kBf16>(p, stream);
+    if (p.kv_fmt == kTq4) return launch_partials<kTq4>(p, stream);
     return launch_partials<kFp4>(p, stream);
 }
 

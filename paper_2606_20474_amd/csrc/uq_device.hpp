@@ -178,14 +178,83 @@ template <int F> struct TokenBits;
 template <> struct TokenBits<kFp4> { uint32_t k, v, ks, vs; };
 template <> struct TokenBits<kFp8> { uint2 k, v; };
 template <> struct TokenBits<kBf16> { uint4 k, v; };
+template <> struct TokenBits<kTq4> { uint32_t k, v; float n; uint32_t vm; };
+
+// BF16 nearest-even of x, as the fp32 it stands for.
+__device__ __forceinline__ float bf16_round(float x) {
+    const v2bf h = {__bf16(x), __bf16(0.0f)};
+    return bits_f32(__builtin_bit_cast(uint32_t, h) << 16);
+}
+
+// Ultra-TQ encoding of the 8 channels this lane holds (all 16 lanes of the
+// vector take part).  K: rotated; the fp32 norm is a fused multiply-add
+// chain over the lane's channels in order, then a pairwise tree over the 16
+// lanes (each butterfly step adds the same two values in every lane, so all
+// lanes hold the same bits), then a correctly rounded square root; index =
+// number of midpoints m_j with x > m_j * n.  V: per 32-channel group (4
+// lanes) zero = bf16(min), scale = bf16(max(max - zero, 0) / 15), code =
+// clamp(rint((x - zero) / scale), 0, 15).
+__device__ __forceinline__ void tq4_encode(float (&xk)[8], const float (&xv)[8], int lane16, const TqTables& tq,
+                                           TokenBits<kTq4>& t) {
+    wht128_x8(xk, lane16);
+    float p = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) p = __builtin_fmaf(xk[i], xk[i], p);
+    p += __shfl_xor(p, 1, 16);
+    p += __shfl_xor(p, 2, 16);
+    p += __shfl_xor(p, 4, 16);
+    p += __shfl_xor(p, 8, 16);
+    const float n = __builtin_sqrtf(p);
+    float thr[15];
+#pragma unroll
+    for (int j = 0; j < 15; ++j) thr[j] = tq.mid[j] * n;
+    uint32_t wk = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+        uint32_t idx = 0;
+#pragma unroll
+        for (int j = 0; j < 15; ++j) idx += xk[i] > thr[j] ? 1u : 0u;
+        wk |= idx << (4 * i);
+    }
+    float mn = xv[0], mx = xv[0];
+#pragma unroll
+    for (int i = 1; i < 8; ++i) {
+        mn = __builtin_fminf(mn, xv[i]);
+        mx = __builtin_fmaxf(mx, xv[i]);
+    }
+    mn = __builtin_fminf(mn, __shfl_xor(mn, 1, 16));
+    mn = __builtin_fminf(mn, __shfl_xor(mn, 2, 16));
+    mx = __builtin_fmaxf(mx, __shfl_xor(mx, 1, 16));
+    mx = __builtin_fmaxf(mx, __shfl_xor(mx, 2, 16));
+    const float z = bf16_round(mn);
+    float d = mx - z;
+    if (!(d > 0.0f)) d = 0.0f;
+    const float s = bf16_round(d / 15.0f);
+    uint32_t wv = 0;
+    if (s > 0.0f) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            float r = __builtin_rintf((xv[i] - z) / s);
+            r = __builtin_fminf(__builtin_fmaxf(r, 0.0f), 15.0f);
+            wv |= uint32_t(r) << (4 * i);
+        }
+    }
+    t.k = wk;
+    t.v = wv;
+    t.n = n;
+    t.vm = (f32_bits(s) >> 16) | (f32_bits(z) & 0xFFFF0000u);
+}
 
 // Encode (all 16 lanes of the vector take part: the FP4 rotation and group
 // maximum exchange values between them).
 template <int F>
 __device__ __forceinline__ TokenBits<F> encode_token(float (&xk)[8], float (&xv)[8], int lane16, float c,
-                                                     bool rotate_v, float k_scale, float v_scale) {
+                                                     bool rotate_v, float k_scale, float v_scale,
+                                                     const TqTables& tq) {
     TokenBits<F> t;
-    if constexpr (F == kFp4) {
+    if constexpr (F == kTq4) {
+        tq4_encode(xk, xv, lane16, tq, t);
+    } else if constexpr (F == kFp4) {
         t.k = quantize_x8(xk, lane16, c, true, t.ks);
         t.v = quantize_x8(xv, lane16, c, rotate_v, t.vs);
     } else if constexpr (F == kFp8) {
@@ -212,8 +281,11 @@ __device__ __forceinline__ TokenBits<F> encode_token(float (&xk)[8], float (&xv)
     return t;
 }
 
-// Bytes of one (page, head) K or V tile per format.
-template <int F> constexpr int tile_bytes() { return F == kFp4 ? kTileCodes : F == kFp8 ? 2048 : 4096; }
+// Bytes of one (page, head) K or V tile per format (Ultra-TQ: half of the
+// page-head block, whose codes, norms and (scale, zero) words sit together).
+template <int F> constexpr int tile_bytes() {
+    return F == kFp4 ? kTileCodes : F == kFp8 ? 2048 : F == kBf16 ? 4096 : kTqBlock / 2;
+}
 
 typedef __attribute__((address_space(3))) uint8_t lds_u8;
 
@@ -244,6 +316,10 @@ __device__ __forceinline__ void st(lds_u8* base, int off, uint4 x) {
 //          16..31 = channels 64+16g..64+16g+15 (the FP8 operand order of
 //          the 16x16x128 MFMA); V [t/4][c/8][t%4][8 B].
 //   kBf16  K [c/8][t][16 B]; V [t/4][c/8][t%4][16 B].
+//   kTq4   K indices [(c%32)/8][t][c/32][4 B]; V codes (at +1024)
+//          [t/4][c/8][t%4][4 B]; `scales` points at the block's norms
+//          (fp32 per token) followed at +64 by the (scale, zero) words
+//          [t/4][c/32][t%4].
 // PTR is a global or an LDS byte pointer: the decode kernel also patches its
 // staged copy of a page with a token it has just written.
 template <int F, class PTR>
@@ -263,9 +339,14 @@ __device__ __forceinline__ void place_token(PTR tiles, PTR scales, int off, int 
         const int e0 = (c0 & 15) + (c0 >= 64 ? 16 : 0);
         st(tiles, (g * kPage + off) * 32 + e0, t.k);
         st(tiles, T + ((off >> 2) * 16 + lane16) * 32 + (off & 3) * 8, t.v);
-    } else {
+    } else if constexpr (F == kBf16) {
         st(tiles, (lane16 * kPage + off) * 16, t.k);
         st(tiles, T + ((off >> 2) * 16 + lane16) * 64 + (off & 3) * 16, t.v);
+    } else {
+        st(tiles, 16 * (off + 16 * (lane16 & 3)) + 4 * (lane16 >> 2), t.k);
+        st(tiles, 1024 + 16 * (lane16 + 16 * (off >> 2)) + 4 * (off & 3), t.v);
+        if (lane16 == 0) st(scales, 4 * off, f32_bits(t.n));
+        if ((lane16 & 3) == 0) st(scales, 64 + 16 * (4 * (off >> 2) + (lane16 >> 2)) + 4 * (off & 3), t.vm);
     }
 }
 
@@ -274,8 +355,9 @@ __device__ __forceinline__ void place_token(PTR tiles, PTR scales, int off, int 
 template <int F>
 __device__ __forceinline__ void store_token(uint8_t* codes, uint8_t* scales, int64_t tile, int off, int lane16,
                                             const TokenBits<F>& t) {
-    uint8_t* sc = F == kFp4 ? scales + tile * kTileScales : nullptr;
-    place_token<F>(codes + tile * tile_bytes<F>(), sc, off, lane16, t);
+    uint8_t* base = codes + tile * tile_bytes<F>();
+    uint8_t* sc = F == kFp4 ? scales + tile * kTileScales : F == kTq4 ? base + kTqMeta : nullptr;
+    place_token<F>(base, sc, off, lane16, t);
 }
 
 // Scale float 2^(byte-127) for the hardware conversions.  Byte 0 maps to

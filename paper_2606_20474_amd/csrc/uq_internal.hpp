@@ -9,7 +9,18 @@ namespace uq {
 
 // Cache formats of the decode kernel template: the FP4 cache of this library
 // and the two plain comparison caches.
-enum KvFmt : int32_t { kFp4 = 0, kFp8 = 1, kBf16 = 2 };
+enum KvFmt : int32_t { kFp4 = 0, kFp8 = 1, kBf16 = 2, kTq4 = 3 };
+
+// Tables of the Ultra-TQ key codebook, built on the host from the 16 levels
+// rounded to BF16: the encoder's midpoints and the decoder's byte lookup
+// (lut[0..3]: high bytes of the BF16 levels, four per dword in level order;
+// lut[4..7]: low bytes).
+struct TqTables {
+    float mid[15];
+    uint32_t lut[8];
+};
+constexpr int kTqBlock = 2368;   // bytes per (page, kv head) of the Ultra-TQ cache
+constexpr int kTqMeta = 2048;    // offset of the norms and (scale, zero) words in a block
 
 struct QuantizeParams {
     const void* k;
@@ -41,8 +52,9 @@ struct RefWriteParams {
     int64_t num_pages;
     float k_scale;             // FP8: stored = e4m3(x / k_scale)
     float v_scale;
-    int32_t kv_fmt;            // kFp8 or kBf16
-    uint8_t* cache;            // [pages][Hkv][2][tile bytes]
+    int32_t kv_fmt;            // kFp8, kBf16 or kTq4
+    uint8_t* cache;            // [pages][Hkv][block bytes]
+    TqTables tq;               // kTq4 only
 };
 
 struct DecodeParams {
@@ -76,6 +88,7 @@ struct DecodeParams {
     void* out;                 // [B][Hq][128]
     int32_t out_dtype;         // 0 f32, 1 bf16
     int32_t rotate_v;
+    TqTables tq;               // Ultra-TQ cache only
     // cascade decode over a shared prefix (prefix_pages == nullptr: off).
     // Partial slots per (sequence, query head): the suffix_partitions of the
     // context grid, then the prefix partitions.

@@ -255,8 +255,9 @@ __global__ void __launch_bounds__(256) quantize_error_kernel(ErrorParams p) {
     }
 }
 
-// Writer of the plain comparison caches (FP8 E4M3 with one scale per
-// tensor, or BF16); the layouts are those of place_token.
+// Writer of the comparison caches (FP8 E4M3 with one scale per tensor,
+// BF16, or the Ultra-TQ codebook cache), 16 lanes per (token, kv head)
+// vector; the layouts are those of place_token.
 template <int DT, int FMT>
 __global__ void __launch_bounds__(256) write_kv_ref_kernel(RefWriteParams p) {
     const int lane16 = threadIdx.x & 15;
@@ -285,7 +286,7 @@ __global__ void __launch_bounds__(256) write_kv_ref_kernel(RefWriteParams p) {
     float xk[8], xv[8];
     load_x8<DT>(p.k, elem, xk);
     load_x8<DT>(p.v, elem, xv);
-    const TokenBits<FMT> tb = encode_token<FMT>(xk, xv, lane16, 0.0f, false, p.k_scale, p.v_scale);
+    const TokenBits<FMT> tb = encode_token<FMT>(xk, xv, lane16, 0.0f, false, p.k_scale, p.v_scale, p.tq);
     store_token<FMT>(p.cache, nullptr, (page * p.num_kv_heads + h) * 2, off, lane16, tb);
 }
 
@@ -321,6 +322,7 @@ hipError_t launch_quantize_kv(const QuantizeParams& p, int dtype, hipStream_t st
 template <int DT>
 static hipError_t launch_ref(const RefWriteParams& p, const dim3& grid, hipStream_t stream) {
     if (p.kv_fmt == kFp8) hipLaunchKernelGGL((write_kv_ref_kernel<DT, kFp8>), grid, dim3(256), 0, stream, p);
+    else if (p.kv_fmt == kTq4) hipLaunchKernelGGL((write_kv_ref_kernel<DT, kTq4>), grid, dim3(256), 0, stream, p);
     else hipLaunchKernelGGL((write_kv_ref_kernel<DT, kBf16>), grid, dim3(256), 0, stream, p);
     return hipGetLastError();
 }

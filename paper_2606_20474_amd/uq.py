@@ -37,7 +37,7 @@ EXPORTS = (
     "uq_ref_decode_cascade_partials", "uq_ref_decode_cascade_merge", "uq_quantize_error",
 )
 
-UQ_REF_FP8_E4M3, UQ_REF_BF16 = 1, 2
+UQ_REF_FP8_E4M3, UQ_REF_BF16, UQ_REF_TQ4 = 1, 2, 3
 
 
 class UQError(RuntimeError):
@@ -67,6 +67,7 @@ class uq_ref_cache_desc(ctypes.Structure):
         ("num_pages", ctypes.c_int64),
         ("k_scale", ctypes.c_float),
         ("v_scale", ctypes.c_float),
+        ("codebook", ctypes.c_void_p),
     ]
 
 
@@ -327,7 +328,9 @@ def decode_merge(desc: CacheDesc, batch, num_q_heads, context_lens, max_context,
 
 @dataclass
 class RefCacheDesc:
-    """Python mirror of ``uq_ref_cache_desc``; ``fmt`` is "fp8" or "bf16"."""
+    """Python mirror of ``uq_ref_cache_desc``; ``fmt`` is "fp8", "bf16" or
+    "tq4" (the Ultra-TQ codebook cache; ``codebook``: 16 ascending levels,
+    default the theoretical codebook for head size 128)."""
     num_kv_heads: int
     num_pages: int
     fmt: str = "fp8"
@@ -335,11 +338,21 @@ class RefCacheDesc:
     v_scale: float = 1.0
     head_dim: int = HEAD_DIM
     page_size: int = PAGE_SIZE
+    codebook: object = None
+
+    def __post_init__(self):
+        if self.fmt == "tq4" and self.codebook is None:
+            from .codebook import default_tq_codebook
+            self.codebook = default_tq_codebook(self.head_dim)
+        if self.codebook is not None:
+            import numpy as np
+            self.codebook = np.ascontiguousarray(self.codebook, dtype=np.float32)
 
     def c_struct(self):
-        code = {"fp8": UQ_REF_FP8_E4M3, "bf16": UQ_REF_BF16}.get(self.fmt, 0)
+        code = {"fp8": UQ_REF_FP8_E4M3, "bf16": UQ_REF_BF16, "tq4": UQ_REF_TQ4}.get(self.fmt, 0)
+        cb = None if self.codebook is None else ctypes.c_void_p(self.codebook.ctypes.data)
         return uq_ref_cache_desc(self.num_kv_heads, self.head_dim, self.page_size, code, self.num_pages,
-                                 self.k_scale, self.v_scale)
+                                 self.k_scale, self.v_scale, cb)
 
     def cache_bytes(self):
         d = self.c_struct()

@@ -110,7 +110,7 @@ def test_cascade_group_sizes(uq, hq, hkv):
     check(out.cpu().numpy(), oracle_ref(wl, dev), f"cascade {hq}/{hkv}")
 
 
-@pytest.mark.parametrize("fmt", ["fp4", "fp8", "bf16"])
+@pytest.mark.parametrize("fmt", ["fp4", "fp8", "bf16", "tq4"])
 def test_cascade_step_equals_write_then_cascade(uq, fmt):
     """The new token (after the prefix) written inside the cascade call."""
     dev = torch.device("cuda:0")

@@ -107,7 +107,7 @@ def compare_step(uq, fmt, wl, dev, part, new_dtype=torch.float32):
     return out_one
 
 
-@pytest.mark.parametrize("fmt", ["fp4", "fp8", "bf16"])
+@pytest.mark.parametrize("fmt", ["fp4", "fp8", "bf16", "tq4"])
 @pytest.mark.parametrize("partition", [0, 32, 64, 256])
 def test_step_equals_write_then_decode(uq, fmt, partition):
     dev = torch.device("cuda:0")
@@ -152,7 +152,7 @@ def test_step_against_oracle(uq):
     assert err <= 2e-3 and rel <= 1e-3
 
 
-@pytest.mark.parametrize("fmt", ["fp4", "bf16"])
+@pytest.mark.parametrize("fmt", ["fp4", "bf16", "tq4"])
 def test_step_shared_prefix(uq, fmt):
     """Contexts shorter and longer than a 64-token shared prefix."""
     dev = torch.device("cuda:0")
@@ -171,7 +171,7 @@ def test_step_minimax_full_size(uq):
     compare_step(uq, "fp4", wl, dev, 0)
 
 
-@pytest.mark.parametrize("fmt", ["fp4", "fp8"])
+@pytest.mark.parametrize("fmt", ["fp4", "fp8", "tq4"])
 def test_step_qwen_full_size(uq, fmt):
     """B=32, Hq=64, Hkv=4, context 32768, random pages, the default
     partition: the launch configuration the benchmark times."""

@@ -134,7 +134,8 @@ def test_ref_cache_sizes_and_validation(uq):
     lib = uq.lib
     assert lib.uq_ref_cache_bytes(ctypes.byref(rdesc())) == 10 * 2 * 2 * 2048
     assert lib.uq_ref_cache_bytes(ctypes.byref(rdesc(format=2))) == 10 * 2 * 2 * 4096
-    assert lib.uq_ref_cache_bytes(ctypes.byref(rdesc(format=3))) == 0
+    assert lib.uq_ref_cache_bytes(ctypes.byref(rdesc(format=3))) == 0              # TQ4 without a codebook
+    assert lib.uq_ref_cache_bytes(ctypes.byref(rdesc(format=4))) == 0
     assert lib.uq_ref_cache_bytes(ctypes.byref(rdesc(k_scale=0.0))) == 0
     assert lib.uq_ref_cache_bytes(ctypes.byref(rdesc(format=2, k_scale=0.0))) > 0   # scales unused for BF16
     assert lib.uq_ref_cache_bytes(None) == 0
@@ -264,3 +265,30 @@ def test_quantize_error_validation(uq):
     # nothing to do: no launch
     assert f(FAKE, E.UQ_F32, 0, 128, 1, 1, 3, FAKE, FAKE, None) == E.UQ_OK
     assert f(FAKE, E.UQ_BF16, 4, 136, 1, 0, 0, FAKE, FAKE, None) == E.UQ_OK
+
+
+def test_tq4_codebook_validation(uq):
+    """The Ultra-TQ descriptor needs 16 finite levels, strictly ascending once
+    rounded to BF16; the cache block is 2368 bytes per page and kv head."""
+    import numpy as np
+    E = uq
+    lib = uq.lib
+    from paper_2606_20474_amd.codebook import default_tq_codebook
+
+    def tq(cb):
+        cb = np.ascontiguousarray(cb, np.float32)
+        d = rdesc(format=3, k_scale=0.0, v_scale=float("nan"))    # the scales are ignored
+        d.codebook = ctypes.c_void_p(cb.ctypes.data)
+        return d, cb
+
+    good = default_tq_codebook(128)
+    d, keep = tq(good)
+    assert lib.uq_ref_cache_bytes(ctypes.byref(d)) == 10 * 2 * 2368
+    bad = [good[::-1], np.where(np.arange(16) == 3, np.nan, good), np.linspace(1.0, 1.0 + 15 * 2 ** -10, 16),
+           np.where(np.arange(16) == 15, np.inf, good)]
+    for cb in bad:
+        d, keep = tq(cb)
+        assert lib.uq_ref_cache_bytes(ctypes.byref(d)) == 0
+        assert lib.uq_ref_write_kv(ctypes.byref(d), FAKE, FAKE, 1, 4, 256, None, 0, 0, FAKE, FAKE, None) == \
+            E.UQ_ERR_INVALID_ARGUMENT
+    assert uq.RefCacheDesc(2, 10, "tq4").cache_bytes() == 10 * 2 * 2368
