@@ -34,6 +34,16 @@ def lib():
         L.uqo_num_threads.restype = i32
         L.uqo_wht128_f32.argtypes = [vp, i64]
         L.uqo_wht128_f64.argtypes = [vp, vp]
+        L.uqo_wht_f32.argtypes = [vp, i64, i32]
+        L.uqo_wht_f64.argtypes = [vp, vp, i32]
+        L.uqo_prepare_query_d.argtypes = [vp, i64, vp, i32]
+        L.uqo_quantize_vector_d.argtypes = [vp, i32, f32, i32, vp, vp]
+        L.uqo_quantize_vectors_d.argtypes = [vp, i64, i32, f32, i32, vp, vp]
+        L.uqo_quantize_kv_d.argtypes = [vp, vp, i64, i32, i64, vp, i64, f32, i32, vp, vp, i32]
+        L.uqo_quantize_kv_d.restype = i64
+        L.uqo_load_vector_d.argtypes = [vp, vp, i32, i64, i32, i32, i32, vp, vp, i32]
+        L.uqo_dequant_vector_d.argtypes = [vp, vp, i32, i64, i32, i32, i32, vp, i32]
+        L.uqo_decode_attention_d.argtypes = [vp, i32, i32, i32, vp, vp, vp, i32, vp, f64, i32, vp, i32]
         L.uqo_scale_exponent.argtypes = [f32, f32]
         L.uqo_scale_exponent.restype = i32
         L.uqo_e2m1_encode.argtypes = [f32, i32]
@@ -78,20 +88,43 @@ def num_threads():
     return int(lib().uqo_num_threads())
 
 
+HEAD_DIMS = (64, 128, 256)
+
+
+def _dim(d):
+    d = int(d)
+    assert d in HEAD_DIMS, d
+    return d
+
+
+def wht_f32(x):
+    """fp32 butterfly rotation R x of each vector along the last axis
+    (64, 128 or 256 channels; reading R1)."""
+    y = _f32(x).copy()
+    d = _dim(y.shape[-1])
+    lib().uqo_wht_f32(_ptr(y), y.size // d, d)
+    return y
+
+
+def wht_f64(x):
+    """Exact fp64 rotation H x / sqrt(d) of one vector."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    d = _dim(x.size)
+    y = np.empty(d, np.float64)
+    lib().uqo_wht_f64(_ptr(x), _ptr(y), d)
+    return y
+
+
 def wht128_f32(x):
     """fp32 butterfly rotation R x of each 128-vector (reading R1)."""
-    y = _f32(x).copy()
-    assert y.shape[-1] == HEAD_DIM
-    lib().uqo_wht128_f32(_ptr(y), y.size // HEAD_DIM)
-    return y
+    assert np.shape(x)[-1] == HEAD_DIM
+    return wht_f32(x)
 
 
 def wht128_f64(x):
     """Exact fp64 rotation H x / sqrt(128) of one 128-vector."""
-    x = np.ascontiguousarray(x, dtype=np.float64)
-    y = np.empty(HEAD_DIM, np.float64)
-    lib().uqo_wht128_f64(_ptr(x), _ptr(y))
-    return y
+    assert np.size(x) == HEAD_DIM
+    return wht_f64(x)
 
 
 def scale_exponent(m, c=C_DEFAULT):
@@ -115,35 +148,40 @@ def e4m3_value(b):
 
 
 def prepare_query(q):
-    """q [..., 128] -> FP8 E4M3 bytes of the rotated query (Algorithm 1, Decode)."""
+    """q [..., d] -> FP8 E4M3 bytes of the rotated query (Algorithm 1, Decode)."""
     q = _f32(q)
+    d = _dim(q.shape[-1])
     out = np.empty(q.shape, np.uint8)
-    lib().uqo_prepare_query(_ptr(q), q.size // HEAD_DIM, _ptr(out))
+    lib().uqo_prepare_query_d(_ptr(q), q.size // d, _ptr(out), d)
     return out
 
 
 def quantize_vector(x, c=C_DEFAULT, rotate=True):
-    """One 128-vector -> (codes[128] one per byte, scale_bytes[4])."""
-    x = _f32(x).reshape(HEAD_DIM)
-    codes = np.empty(HEAD_DIM, np.uint8)
-    sb = np.empty(4, np.uint8)
-    lib().uqo_quantize_vector(_ptr(x), float(np.float32(c)), int(bool(rotate)), _ptr(codes), _ptr(sb))
+    """One d-vector -> (codes[d] one per byte, scale_bytes[d / 32])."""
+    x = _f32(x).reshape(-1)
+    d = _dim(x.size)
+    codes = np.empty(d, np.uint8)
+    sb = np.empty(d // 32, np.uint8)
+    lib().uqo_quantize_vector_d(_ptr(x), d, float(np.float32(c)), int(bool(rotate)), _ptr(codes), _ptr(sb))
     return codes, sb
 
 
 def quantize_vectors(x, c=C_DEFAULT, rotate=True):
-    """[..., 128] -> (codes [..., 128] one per byte, scale_bytes [..., 4])."""
+    """[..., d] -> (codes [..., d] one per byte, scale_bytes [..., d / 32])."""
     x = _f32(x)
-    n = x.size // HEAD_DIM
+    d = _dim(x.shape[-1])
     codes = np.empty(x.shape, np.uint8)
-    sb = np.empty(x.shape[:-1] + (4,), np.uint8)
-    lib().uqo_quantize_vectors(_ptr(x), n, float(np.float32(c)), int(bool(rotate)), _ptr(codes), _ptr(sb))
+    sb = np.empty(x.shape[:-1] + (d // 32,), np.uint8)
+    lib().uqo_quantize_vectors_d(_ptr(x), x.size // d, d, float(np.float32(c)), int(bool(rotate)), _ptr(codes),
+                                 _ptr(sb))
     return codes, sb
 
 
-def alloc_pools(num_pages, num_kv_heads, fill=0):
-    codes = np.full(num_pages * num_kv_heads * 2 * TILE_CODES, fill, np.uint8)
-    scales = np.full(num_pages * num_kv_heads * 2 * TILE_SCALES, fill, np.uint8)
+def alloc_pools(num_pages, num_kv_heads, fill=0, head_dim=HEAD_DIM):
+    """Codes pool (8 d bytes per page, head and K|V) and scales pool (d / 2)."""
+    d = _dim(head_dim)
+    codes = np.full(num_pages * num_kv_heads * 2 * 8 * d, fill, np.uint8)
+    scales = np.full(num_pages * num_kv_heads * 2 * (d // 2), fill, np.uint8)
     return codes, scales
 
 
@@ -156,27 +194,32 @@ def quantize_kv(k, v, slot_mapping, num_pages, c=C_DEFAULT, rotate_v=True, pools
     k = _f32(k)
     v = _f32(v)
     T, Hkv, D = k.shape
-    assert D == HEAD_DIM and v.shape == k.shape
+    D = _dim(D)
+    assert v.shape == k.shape
     slots = np.ascontiguousarray(slot_mapping, dtype=np.int64)
     assert slots.shape == (T,)
     if pools is None:
-        pools = alloc_pools(num_pages, Hkv)
+        pools = alloc_pools(num_pages, Hkv, head_dim=D)
     codes, scales = pools
-    lib().uqo_quantize_kv(_ptr(k), _ptr(v), T, Hkv, Hkv * HEAD_DIM, _ptr(slots), int(num_pages),
-                          float(np.float32(c)), int(bool(rotate_v)), _ptr(codes), _ptr(scales))
+    assert codes.size == num_pages * Hkv * 16 * D
+    lib().uqo_quantize_kv_d(_ptr(k), _ptr(v), T, Hkv, Hkv * D, _ptr(slots), int(num_pages), float(np.float32(c)),
+                            int(bool(rotate_v)), _ptr(codes), _ptr(scales), D)
     return codes, scales
 
 
-def load_vector(pools, num_kv_heads, page, head, kv, t):
-    codes = np.empty(HEAD_DIM, np.uint8)
-    sb = np.empty(4, np.uint8)
-    lib().uqo_load_vector(_ptr(pools[0]), _ptr(pools[1]), num_kv_heads, page, head, kv, t, _ptr(codes), _ptr(sb))
+def load_vector(pools, num_kv_heads, page, head, kv, t, head_dim=HEAD_DIM):
+    d = _dim(head_dim)
+    codes = np.empty(d, np.uint8)
+    sb = np.empty(d // 32, np.uint8)
+    lib().uqo_load_vector_d(_ptr(pools[0]), _ptr(pools[1]), num_kv_heads, page, head, kv, t, _ptr(codes), _ptr(sb),
+                            d)
     return codes, sb
 
 
-def dequant_vector(pools, num_kv_heads, page, head, kv, t):
-    out = np.empty(HEAD_DIM, np.float64)
-    lib().uqo_dequant_vector(_ptr(pools[0]), _ptr(pools[1]), num_kv_heads, page, head, kv, t, _ptr(out))
+def dequant_vector(pools, num_kv_heads, page, head, kv, t, head_dim=HEAD_DIM):
+    d = _dim(head_dim)
+    out = np.empty(d, np.float64)
+    lib().uqo_dequant_vector_d(_ptr(pools[0]), _ptr(pools[1]), num_kv_heads, page, head, kv, t, _ptr(out), d)
     return out
 
 
@@ -184,15 +227,16 @@ def decode_attention(q, pools, page_table, context_lens, num_kv_heads, softmax_s
     """q [B, Hq, 128] -> fp64 attention output [B, Hq, 128] (Algorithm 1, Decode)."""
     q = _f32(q)
     B, Hq, D = q.shape
-    assert D == HEAD_DIM and Hq % num_kv_heads == 0
+    D = _dim(D)
+    assert Hq % num_kv_heads == 0
     pt = np.ascontiguousarray(page_table, dtype=np.int32)
     ctx = np.ascontiguousarray(context_lens, dtype=np.int32)
     assert pt.shape[0] == B and ctx.shape == (B,)
     if softmax_scale is None:
-        softmax_scale = 1.0 / np.sqrt(HEAD_DIM)
-    out = np.empty((B, Hq, HEAD_DIM), np.float64)
-    lib().uqo_decode_attention(_ptr(q), B, Hq, num_kv_heads, _ptr(pools[0]), _ptr(pools[1]), _ptr(pt),
-                               pt.shape[1], _ptr(ctx), float(softmax_scale), int(bool(rotate_v)), _ptr(out))
+        softmax_scale = 1.0 / np.sqrt(D)
+    out = np.empty((B, Hq, D), np.float64)
+    lib().uqo_decode_attention_d(_ptr(q), B, Hq, num_kv_heads, _ptr(pools[0]), _ptr(pools[1]), _ptr(pt), pt.shape[1],
+                                 _ptr(ctx), float(softmax_scale), int(bool(rotate_v)), _ptr(out), D)
     return out
 
 

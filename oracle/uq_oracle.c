@@ -54,12 +54,11 @@
 #include <stdlib.h>
 #include <string.h>
 
-#define UQO_D 128          /* head dimension */
+#define UQO_D 128          /* head dimension of the fixed-size entry points */
+#define UQO_DMAX 256       /* largest head dimension of the _d entry points (64, 128, 256) */
 #define UQO_GROUP 32       /* channels per scale group */
-#define UQO_NGROUP 4       /* groups per head vector */
+#define UQO_NGROUP 4       /* groups per 128-channel head vector */
 #define UQO_PAGE 16        /* tokens per page */
-#define UQO_TILE_CODES 1024   /* bytes of codes per (page, head, K|V) tile */
-#define UQO_TILE_SCALES 64    /* bytes of scales per (page, head, K|V) tile */
 
 /* Threads the OpenMP loops of this file use. */
 int uqo_num_threads(void) { return omp_get_max_threads(); }
@@ -69,34 +68,37 @@ int uqo_num_threads(void) { return omp_get_max_threads(); }
 static const double kE2M1Mag[8] = {0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0};
 
 /* ---------------------------------------------------------------------- */
-/* Rotation (section "Ultra-TurboQuant"; Algorithm 1), reading R1.          */
+/* Rotation (section "Ultra-TurboQuant"; Algorithm 1), reading R1, for a    */
+/* head vector of d = 64, 128 or 256 channels: R = H_d / sqrt(d).           */
 /* ---------------------------------------------------------------------- */
-void uqo_wht128_f32(float *x, int64_t n_vec) {
-    const float inv_sqrt = (float)(1.0 / sqrt(128.0));
+void uqo_wht_f32(float *x, int64_t n_vec, int d) {
+    const float inv_sqrt = (float)(1.0 / sqrt((double)d));
     for (int64_t v = 0; v < n_vec; ++v) {
-        float *p = x + v * UQO_D;
-        for (int h = 1; h < UQO_D; h <<= 1) {
-            for (int i = 0; i < UQO_D; ++i) {
+        float *p = x + v * d;
+        for (int h = 1; h < d; h <<= 1) {
+            for (int i = 0; i < d; ++i) {
                 if (i & h) continue;
                 float a = p[i], b = p[i + h];
                 p[i] = a + b;
                 p[i + h] = a - b;
             }
         }
-        for (int i = 0; i < UQO_D; ++i) p[i] = p[i] * inv_sqrt;
+        for (int i = 0; i < d; ++i) p[i] = p[i] * inv_sqrt;
     }
 }
+void uqo_wht128_f32(float *x, int64_t n_vec) { uqo_wht_f32(x, n_vec, UQO_D); }
 
-/* Exact rotation in fp64: y = H_128 x / sqrt(128), H[i][j] = (-1)^popcount(i&j). */
-void uqo_wht128_f64(const double *x, double *y) {
-    const double inv_sqrt = 1.0 / sqrt(128.0);
-    for (int i = 0; i < UQO_D; ++i) {
+/* Exact rotation in fp64: y = H_d x / sqrt(d), H[i][j] = (-1)^popcount(i&j). */
+void uqo_wht_f64(const double *x, double *y, int d) {
+    const double inv_sqrt = 1.0 / sqrt((double)d);
+    for (int i = 0; i < d; ++i) {
         double s = 0.0;
-        for (int j = 0; j < UQO_D; ++j)
+        for (int j = 0; j < d; ++j)
             s += (__builtin_popcount((unsigned)(i & j)) & 1) ? -x[j] : x[j];
         y[i] = s * inv_sqrt;
     }
 }
+void uqo_wht128_f64(const double *x, double *y) { uqo_wht_f64(x, y, UQO_D); }
 
 /* ---------------------------------------------------------------------- */
 /* Scale exponent (section "Constant-Optimized Scaling"), reading R2.       */
@@ -170,28 +172,30 @@ uint8_t uqo_e4m3_encode(float x) {
     return (uint8_t)((signbit(x) ? 0x80 : 0) | best);
 }
 
-/* Query preparation (Algorithm 1, Decode): q8 = e4m3(R q), per 128-vector. */
-static void prepare_query_row(const float *q, uint8_t *q8) {
-    float tmp[UQO_D];
-    memcpy(tmp, q, sizeof(tmp));
-    uqo_wht128_f32(tmp, 1);
-    for (int i = 0; i < UQO_D; ++i) q8[i] = uqo_e4m3_encode(tmp[i]);
+/* Query preparation (Algorithm 1, Decode): q8 = e4m3(R q), per d-vector. */
+static void prepare_query_row(const float *q, uint8_t *q8, int d) {
+    float tmp[UQO_DMAX];
+    memcpy(tmp, q, sizeof(float) * (size_t)d);
+    uqo_wht_f32(tmp, 1, d);
+    for (int i = 0; i < d; ++i) q8[i] = uqo_e4m3_encode(tmp[i]);
 }
 
-void uqo_prepare_query(const float *q, int64_t rows, uint8_t *q8) {
+void uqo_prepare_query_d(const float *q, int64_t rows, uint8_t *q8, int d) {
 #pragma omp parallel for schedule(static)
-    for (int64_t r = 0; r < rows; ++r) prepare_query_row(q + r * UQO_D, q8 + r * UQO_D);
+    for (int64_t r = 0; r < rows; ++r) prepare_query_row(q + r * d, q8 + r * d, d);
 }
+void uqo_prepare_query(const float *q, int64_t rows, uint8_t *q8) { uqo_prepare_query_d(q, rows, q8, UQO_D); }
 
 /* ---------------------------------------------------------------------- */
-/* Quantise one head vector (Algorithm 1, Write): optional rotation, per-   */
-/* group exponent, per-element code.  codes[128] holds one code per byte.   */
+/* Quantise one head vector of d channels (Algorithm 1, Write): optional    */
+/* rotation, per-group exponent, per-element code.  codes[d] holds one code */
+/* per byte, scale_bytes[d / 32] one byte per group.                        */
 /* ---------------------------------------------------------------------- */
-void uqo_quantize_vector(const float *x_in, float c, int rotate, uint8_t *codes, uint8_t *scale_bytes) {
-    float x[UQO_D];
-    memcpy(x, x_in, sizeof(x));
-    if (rotate) uqo_wht128_f32(x, 1);
-    for (int g = 0; g < UQO_NGROUP; ++g) {
+void uqo_quantize_vector_d(const float *x_in, int d, float c, int rotate, uint8_t *codes, uint8_t *scale_bytes) {
+    float x[UQO_DMAX];
+    memcpy(x, x_in, sizeof(float) * (size_t)d);
+    if (rotate) uqo_wht_f32(x, 1, d);
+    for (int g = 0; g < d / UQO_GROUP; ++g) {
         float m = 0.0f;
         for (int i = 0; i < UQO_GROUP; ++i) {
             float a = fabsf(x[g * UQO_GROUP + i]);
@@ -202,66 +206,81 @@ void uqo_quantize_vector(const float *x_in, float c, int rotate, uint8_t *codes,
         for (int i = 0; i < UQO_GROUP; ++i) codes[g * UQO_GROUP + i] = uqo_e2m1_encode(x[g * UQO_GROUP + i], E);
     }
 }
+void uqo_quantize_vector(const float *x_in, float c, int rotate, uint8_t *codes, uint8_t *scale_bytes) {
+    uqo_quantize_vector_d(x_in, UQO_D, c, rotate, codes, scale_bytes);
+}
 
-/* Batch form of uqo_quantize_vector over n_vec contiguous 128-vectors. */
-void uqo_quantize_vectors(const float *x, int64_t n_vec, float c, int rotate, uint8_t *codes, uint8_t *scale_bytes) {
+/* Batch form over n_vec contiguous d-vectors. */
+void uqo_quantize_vectors_d(const float *x, int64_t n_vec, int d, float c, int rotate, uint8_t *codes,
+                            uint8_t *scale_bytes) {
 #pragma omp parallel for schedule(static)
     for (int64_t i = 0; i < n_vec; ++i)
-        uqo_quantize_vector(x + i * UQO_D, c, rotate, codes + i * UQO_D, scale_bytes + i * UQO_NGROUP);
+        uqo_quantize_vector_d(x + i * d, d, c, rotate, codes + i * d, scale_bytes + i * (d / UQO_GROUP));
+}
+void uqo_quantize_vectors(const float *x, int64_t n_vec, float c, int rotate, uint8_t *codes, uint8_t *scale_bytes) {
+    uqo_quantize_vectors_d(x, n_vec, UQO_D, c, rotate, codes, scale_bytes);
 }
 
 /* ---------------------------------------------------------------------- */
-/* Page layout (the cache format of include/uq.h).  Written out here from   */
-/* that specification, independently of the library.                       */
-/*   codes  pool: [num_pages][num_kv_heads][2 = K,V][1024 B]                */
-/*   scales pool: [num_pages][num_kv_heads][2 = K,V][4 groups][16 tokens]   */
+/* Page layout (the cache format of include/uq.h), for head size d.         */
+/* Written out here from that specification, independently of the library. */
+/*   codes  pool: [num_pages][num_kv_heads][2 = K,V][8 d bytes]             */
+/*   scales pool: [num_pages][num_kv_heads][2 = K,V][d/32 groups][16 tokens]*/
 /*   K tile byte of (token t, channel c): ((c/32)*16 + t)*16 + (c%32)/2     */
 /*   V tile byte of (token t, channel c):                                   */
-/*        ((t/4)*16 + c/8)*16 + (t%4)*4 + (c%8)/2                           */
+/*        ((t/4)*(d/8) + c/8)*16 + (t%4)*4 + (c%8)/2                        */
 /*   even channel in the low nibble, odd channel in the high nibble.         */
 /* ---------------------------------------------------------------------- */
 static inline int64_t tile_index(int64_t page, int num_kv_heads, int head, int kv) {
     return (page * num_kv_heads + head) * 2 + kv;
 }
-static inline int code_byte_offset(int kv, int t, int ch) {
+static inline int code_byte_offset(int kv, int t, int ch, int d) {
     if (kv == 0) return ((ch / 32) * 16 + t) * 16 + (ch % 32) / 2;
-    return ((t / 4) * 16 + ch / 8) * 16 + (t % 4) * 4 + (ch % 8) / 2;
+    return ((t / 4) * (d / 8) + ch / 8) * 16 + (t % 4) * 4 + (ch % 8) / 2;
 }
 
-void uqo_store_vector(uint8_t *codes_pool, uint8_t *scales_pool, int num_kv_heads, int64_t page, int head,
-                      int kv, int t, const uint8_t *codes, const uint8_t *scale_bytes) {
+void uqo_store_vector_d(uint8_t *codes_pool, uint8_t *scales_pool, int num_kv_heads, int64_t page, int head, int kv,
+                        int t, const uint8_t *codes, const uint8_t *scale_bytes, int d) {
     int64_t ti = tile_index(page, num_kv_heads, head, kv);
-    uint8_t *ct = codes_pool + ti * UQO_TILE_CODES;
-    uint8_t *st = scales_pool + ti * UQO_TILE_SCALES;
-    for (int ch = 0; ch < UQO_D; ++ch) {
-        int off = code_byte_offset(kv, t, ch);
+    uint8_t *ct = codes_pool + ti * (8 * d);
+    uint8_t *st = scales_pool + ti * (d / 2);
+    for (int ch = 0; ch < d; ++ch) {
+        int off = code_byte_offset(kv, t, ch, d);
         if (ch % 2 == 0) ct[off] = (uint8_t)((ct[off] & 0xF0) | (codes[ch] & 0x0F));
         else ct[off] = (uint8_t)((ct[off] & 0x0F) | ((codes[ch] & 0x0F) << 4));
     }
-    for (int g = 0; g < UQO_NGROUP; ++g) st[g * UQO_PAGE + t] = scale_bytes[g];
+    for (int g = 0; g < d / UQO_GROUP; ++g) st[g * UQO_PAGE + t] = scale_bytes[g];
+}
+void uqo_store_vector(uint8_t *codes_pool, uint8_t *scales_pool, int num_kv_heads, int64_t page, int head, int kv,
+                      int t, const uint8_t *codes, const uint8_t *scale_bytes) {
+    uqo_store_vector_d(codes_pool, scales_pool, num_kv_heads, page, head, kv, t, codes, scale_bytes, UQO_D);
 }
 
-void uqo_load_vector(const uint8_t *codes_pool, const uint8_t *scales_pool, int num_kv_heads, int64_t page,
-                     int head, int kv, int t, uint8_t *codes, uint8_t *scale_bytes) {
+void uqo_load_vector_d(const uint8_t *codes_pool, const uint8_t *scales_pool, int num_kv_heads, int64_t page,
+                       int head, int kv, int t, uint8_t *codes, uint8_t *scale_bytes, int d) {
     int64_t ti = tile_index(page, num_kv_heads, head, kv);
-    const uint8_t *ct = codes_pool + ti * UQO_TILE_CODES;
-    const uint8_t *st = scales_pool + ti * UQO_TILE_SCALES;
-    for (int ch = 0; ch < UQO_D; ++ch) {
-        uint8_t b = ct[code_byte_offset(kv, t, ch)];
+    const uint8_t *ct = codes_pool + ti * (8 * d);
+    const uint8_t *st = scales_pool + ti * (d / 2);
+    for (int ch = 0; ch < d; ++ch) {
+        uint8_t b = ct[code_byte_offset(kv, t, ch, d)];
         codes[ch] = (ch % 2 == 0) ? (b & 0x0F) : (b >> 4);
     }
-    for (int g = 0; g < UQO_NGROUP; ++g) scale_bytes[g] = st[g * UQO_PAGE + t];
+    for (int g = 0; g < d / UQO_GROUP; ++g) scale_bytes[g] = st[g * UQO_PAGE + t];
+}
+void uqo_load_vector(const uint8_t *codes_pool, const uint8_t *scales_pool, int num_kv_heads, int64_t page, int head,
+                     int kv, int t, uint8_t *codes, uint8_t *scale_bytes) {
+    uqo_load_vector_d(codes_pool, scales_pool, num_kv_heads, page, head, kv, t, codes, scale_bytes, UQO_D);
 }
 
 /* ---------------------------------------------------------------------- */
 /* Quantize-on-write (Algorithm 1, Write) into the paged pools.             */
-/* k, v: [num_tokens][num_kv_heads][128] fp32 with a token stride in floats; */
+/* k, v: [num_tokens][num_kv_heads][d] fp32 with a token stride in floats;   */
 /* slot_mapping[t] = page * 16 + offset, negative = skip.  Returns the      */
 /* number of tokens written.                                                 */
 /* ---------------------------------------------------------------------- */
-int64_t uqo_quantize_kv(const float *k, const float *v, int64_t num_tokens, int num_kv_heads,
-                        int64_t token_stride, const int64_t *slot_mapping, int64_t num_pages, float c,
-                        int rotate_v, uint8_t *codes_pool, uint8_t *scales_pool) {
+int64_t uqo_quantize_kv_d(const float *k, const float *v, int64_t num_tokens, int num_kv_heads, int64_t token_stride,
+                          const int64_t *slot_mapping, int64_t num_pages, float c, int rotate_v, uint8_t *codes_pool,
+                          uint8_t *scales_pool, int d) {
     int64_t written = 0;
 #pragma omp parallel for schedule(static) reduction(+ : written)
     for (int64_t t = 0; t < num_tokens; ++t) {
@@ -270,77 +289,93 @@ int64_t uqo_quantize_kv(const float *k, const float *v, int64_t num_tokens, int 
         int64_t page = slot / UQO_PAGE;
         int off = (int)(slot % UQO_PAGE);
         for (int h = 0; h < num_kv_heads; ++h) {
-            uint8_t codes[UQO_D], sb[UQO_NGROUP];
-            uqo_quantize_vector(k + t * token_stride + (int64_t)h * UQO_D, c, 1, codes, sb);
-            uqo_store_vector(codes_pool, scales_pool, num_kv_heads, page, h, 0, off, codes, sb);
-            uqo_quantize_vector(v + t * token_stride + (int64_t)h * UQO_D, c, rotate_v, codes, sb);
-            uqo_store_vector(codes_pool, scales_pool, num_kv_heads, page, h, 1, off, codes, sb);
+            uint8_t codes[UQO_DMAX], sb[UQO_DMAX / UQO_GROUP];
+            uqo_quantize_vector_d(k + t * token_stride + (int64_t)h * d, d, c, 1, codes, sb);
+            uqo_store_vector_d(codes_pool, scales_pool, num_kv_heads, page, h, 0, off, codes, sb, d);
+            uqo_quantize_vector_d(v + t * token_stride + (int64_t)h * d, d, c, rotate_v, codes, sb);
+            uqo_store_vector_d(codes_pool, scales_pool, num_kv_heads, page, h, 1, off, codes, sb, d);
         }
         written += 1;
     }
     return written;
 }
+int64_t uqo_quantize_kv(const float *k, const float *v, int64_t num_tokens, int num_kv_heads, int64_t token_stride,
+                        const int64_t *slot_mapping, int64_t num_pages, float c, int rotate_v, uint8_t *codes_pool,
+                        uint8_t *scales_pool) {
+    return uqo_quantize_kv_d(k, v, num_tokens, num_kv_heads, token_stride, slot_mapping, num_pages, c, rotate_v,
+                             codes_pool, scales_pool, UQO_D);
+}
 
 /* Dequantise one stored vector to fp64 (section "Dequantization"). */
+void uqo_dequant_vector_d(const uint8_t *codes_pool, const uint8_t *scales_pool, int num_kv_heads, int64_t page,
+                          int head, int kv, int t, double *out, int d) {
+    uint8_t codes[UQO_DMAX], sb[UQO_DMAX / UQO_GROUP];
+    uqo_load_vector_d(codes_pool, scales_pool, num_kv_heads, page, head, kv, t, codes, sb, d);
+    for (int ch = 0; ch < d; ++ch) out[ch] = uqo_e2m1_value(codes[ch], sb[ch / UQO_GROUP]);
+}
 void uqo_dequant_vector(const uint8_t *codes_pool, const uint8_t *scales_pool, int num_kv_heads, int64_t page,
                         int head, int kv, int t, double *out) {
-    uint8_t codes[UQO_D], sb[UQO_NGROUP];
-    uqo_load_vector(codes_pool, scales_pool, num_kv_heads, page, head, kv, t, codes, sb);
-    for (int ch = 0; ch < UQO_D; ++ch) out[ch] = uqo_e2m1_value(codes[ch], sb[ch / UQO_GROUP]);
+    uqo_dequant_vector_d(codes_pool, scales_pool, num_kv_heads, page, head, kv, t, out, UQO_D);
 }
 
 /* ---------------------------------------------------------------------- */
 /* Decode attention over the paged cache, fp64 (Algorithm 1, Decode).       */
-/*   q: [batch][num_q_heads][128] fp32 (rotated and cast to FP8 here),      */
+/*   q: [batch][num_q_heads][d] fp32 (rotated and cast to FP8 here),        */
 /*   page_table: [batch][max_pages_per_seq], context_lens: [batch].         */
 /*   Query head h reads KV head h / (num_q_heads / num_kv_heads).           */
-/*   out: [batch][num_q_heads][128] fp64; an empty context gives zeros.     */
+/*   out: [batch][num_q_heads][d] fp64; an empty context gives zeros.       */
 /* Plain definition: s_j = scale * <q8, k_j>, p = softmax(s), o = sum p_j v_j */
 /* then o <- R o when V was stored rotated.                                  */
 /* ---------------------------------------------------------------------- */
-void uqo_decode_attention(const float *q, int batch, int num_q_heads, int num_kv_heads, const uint8_t *codes_pool,
-                          const uint8_t *scales_pool, const int32_t *page_table, int max_pages_per_seq,
-                          const int32_t *context_lens, double softmax_scale, int rotate_v, double *out) {
+void uqo_decode_attention_d(const float *q, int batch, int num_q_heads, int num_kv_heads, const uint8_t *codes_pool,
+                            const uint8_t *scales_pool, const int32_t *page_table, int max_pages_per_seq,
+                            const int32_t *context_lens, double softmax_scale, int rotate_v, double *out, int d) {
     const int G = num_q_heads / num_kv_heads;
 #pragma omp parallel for schedule(dynamic) collapse(2)
     for (int b = 0; b < batch; ++b) {
         for (int hq = 0; hq < num_q_heads; ++hq) {
             const int hk = hq / G;
             const int ctx = context_lens[b];
-            double *o = out + ((int64_t)b * num_q_heads + hq) * UQO_D;
-            for (int i = 0; i < UQO_D; ++i) o[i] = 0.0;
+            double *o = out + ((int64_t)b * num_q_heads + hq) * d;
+            for (int i = 0; i < d; ++i) o[i] = 0.0;
             if (ctx <= 0) continue;
-            uint8_t q8[UQO_D];
-            prepare_query_row(q + ((int64_t)b * num_q_heads + hq) * UQO_D, q8);
-            double qd[UQO_D];
-            for (int i = 0; i < UQO_D; ++i) qd[i] = uqo_e4m3_value(q8[i]);
+            uint8_t q8[UQO_DMAX];
+            prepare_query_row(q + ((int64_t)b * num_q_heads + hq) * d, q8, d);
+            double qd[UQO_DMAX];
+            for (int i = 0; i < d; ++i) qd[i] = uqo_e4m3_value(q8[i]);
             double *s = (double *)malloc(sizeof(double) * (size_t)ctx);
-            double kv[UQO_D];
+            double kv[UQO_DMAX];
             double smax = -INFINITY;
             for (int j = 0; j < ctx; ++j) {
                 int64_t page = page_table[(int64_t)b * max_pages_per_seq + j / UQO_PAGE];
-                uqo_dequant_vector(codes_pool, scales_pool, num_kv_heads, page, hk, 0, j % UQO_PAGE, kv);
+                uqo_dequant_vector_d(codes_pool, scales_pool, num_kv_heads, page, hk, 0, j % UQO_PAGE, kv, d);
                 double dot = 0.0;
-                for (int i = 0; i < UQO_D; ++i) dot += qd[i] * kv[i];
+                for (int i = 0; i < d; ++i) dot += qd[i] * kv[i];
                 s[j] = softmax_scale * dot;
                 if (s[j] > smax) smax = s[j];
             }
             double denom = 0.0;
-            double acc[UQO_D];
-            for (int i = 0; i < UQO_D; ++i) acc[i] = 0.0;
+            double acc[UQO_DMAX];
+            for (int i = 0; i < d; ++i) acc[i] = 0.0;
             for (int j = 0; j < ctx; ++j) {
                 double p = exp(s[j] - smax);
                 denom += p;
                 int64_t page = page_table[(int64_t)b * max_pages_per_seq + j / UQO_PAGE];
-                uqo_dequant_vector(codes_pool, scales_pool, num_kv_heads, page, hk, 1, j % UQO_PAGE, kv);
-                for (int i = 0; i < UQO_D; ++i) acc[i] += p * kv[i];
+                uqo_dequant_vector_d(codes_pool, scales_pool, num_kv_heads, page, hk, 1, j % UQO_PAGE, kv, d);
+                for (int i = 0; i < d; ++i) acc[i] += p * kv[i];
             }
             free(s);
-            for (int i = 0; i < UQO_D; ++i) acc[i] /= denom;
-            if (rotate_v) uqo_wht128_f64(acc, o);
-            else memcpy(o, acc, sizeof(acc));
+            for (int i = 0; i < d; ++i) acc[i] /= denom;
+            if (rotate_v) uqo_wht_f64(acc, o, d);
+            else memcpy(o, acc, sizeof(double) * (size_t)d);
         }
     }
+}
+void uqo_decode_attention(const float *q, int batch, int num_q_heads, int num_kv_heads, const uint8_t *codes_pool,
+                          const uint8_t *scales_pool, const int32_t *page_table, int max_pages_per_seq,
+                          const int32_t *context_lens, double softmax_scale, int rotate_v, double *out) {
+    uqo_decode_attention_d(q, batch, num_q_heads, num_kv_heads, codes_pool, scales_pool, page_table,
+                           max_pages_per_seq, context_lens, softmax_scale, rotate_v, out, UQO_D);
 }
 
 /* ---------------------------------------------------------------------- */
