@@ -19,10 +19,16 @@ sum of contexts / step time.
 The JSON line also carries the roofline of the dominant kernel (the decode
 kernel: algorithmic KV bytes per launch / its mean launch time from HIP
 events on its stream), the CPU oracle timed on a sample of the same
-workload, and the same step over the two plain comparison caches the paper
-measures against (FP8 E4M3 with per-tensor scales, 256 B per token and kv
-head; BF16, 512 B), built by the same library with the same decode kernel
-and timed the same way.
+workload, and the same step over the comparison caches (FP8 E4M3 with
+per-tensor scales, 256 B per token and kv head; BF16, 512 B; the Ultra-TQ
+codebook cache, 148 B), built by the same library with the same decode
+kernel and timed the same way.
+
+The gpt-oss-like workloads run the FP4 path at head sizes 64 and 256 (64
+query heads, 8 KV heads, batch 32, context 32768): there the step writes the
+new tokens with uq_quantize_kv, then runs uq_decode_partials and
+uq_decode_merge (the fused step and the comparison caches are head-size-128
+calls).
 """
 import argparse
 import json
@@ -48,7 +54,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="qwen3-235b-like",
-                    choices=["qwen3-235b-like", "high-concurrency", "minimax-like", "tiny"])
+                    choices=["qwen3-235b-like", "high-concurrency", "minimax-like", "tiny", "gpt-oss-like-hd64",
+                             "gpt-oss-like-hd256"])
     ap.add_argument("--partition", type=int, default=-1, help="partition tokens (-1: workload default)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-seqs", type=int, default=4)
@@ -67,7 +74,9 @@ def parse():
 def make_workload(name):
     from paper_2606_20474_amd import workloads
     return {"qwen3-235b-like": workloads.qwen3_235b_like, "high-concurrency": workloads.high_concurrency,
-            "minimax-like": workloads.minimax_like, "tiny": workloads.tiny}[name]()
+            "minimax-like": workloads.minimax_like, "tiny": workloads.tiny,
+            "gpt-oss-like-hd64": lambda: workloads.gpt_oss_like(64),
+            "gpt-oss-like-hd256": lambda: workloads.gpt_oss_like(256)}[name]()
 
 
 def kernel_source_hash():
@@ -242,7 +251,7 @@ def cpu_baseline(wl, nseq, dev):
     seqs = list(range(min(nseq, wl.batch)))
     maxp = wl.max_pages_per_seq
     pt = np.arange(len(seqs) * maxp, dtype=np.int32).reshape(len(seqs), maxp)
-    pools = oracle.alloc_pools(len(seqs) * maxp, wl.num_kv_heads)
+    pools = oracle.alloc_pools(len(seqs) * maxp, wl.num_kv_heads, head_dim=wl.head_dim)
     for i, b in enumerate(seqs):
         for key, lo, hi in wl.sequence_segments(b):
             k, v = wl.kv(key, lo, hi, device=dev)
@@ -253,7 +262,7 @@ def cpu_baseline(wl, nseq, dev):
     q = wl.q.numpy()[seqs]
     ctx = wl.context_lens[seqs]
     t0 = time.perf_counter()
-    oracle.decode_attention(q, pools, pt, ctx, wl.num_kv_heads, 1 / math.sqrt(128), wl.rotate_v)
+    oracle.decode_attention(q, pools, pt, ctx, wl.num_kv_heads, 1 / math.sqrt(wl.head_dim), wl.rotate_v)
     dt = time.perf_counter() - t0
     toks = int(ctx.astype(np.int64).sum())
     return {"value": toks / dt, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
@@ -274,7 +283,8 @@ def main():
     dev = torch.device("cuda:0")
     wl = make_workload(args.workload)
     part = wl.partition_tokens if args.partition < 0 else args.partition
-    desc = uq.CacheDesc(num_kv_heads=wl.num_kv_heads, num_pages=wl.num_pages, rotate_v=wl.rotate_v)
+    D = wl.head_dim
+    desc = uq.CacheDesc(num_kv_heads=wl.num_kv_heads, num_pages=wl.num_pages, rotate_v=wl.rotate_v, head_dim=D)
     codes, scales = desc.alloc_pools(dev)
     fill_cache(uq, wl, desc, codes, scales, dev)
     if part == 0:
@@ -291,18 +301,26 @@ def main():
                                                     part), dtype=torch.uint8, device=dev)
     else:
         ws = uq.alloc_workspace(desc, wl.batch, wl.num_q_heads, wl.max_context, part, dev)
-    out = torch.empty((wl.batch, wl.num_q_heads, 128), dtype=torch.float32, device=dev)
+    out = torch.empty((wl.batch, wl.num_q_heads, D), dtype=torch.float32, device=dev)
     # the step's new token of every sequence (written at its last position by the step)
     g = torch.Generator(device=dev).manual_seed(12345)
-    k_new = torch.randn((wl.batch, wl.num_kv_heads, 128), generator=g, device=dev)
-    v_new = torch.randn((wl.batch, wl.num_kv_heads, 128), generator=g, device=dev)
-    scale = 1 / math.sqrt(128)
+    k_new = torch.randn((wl.batch, wl.num_kv_heads, D), generator=g, device=dev)
+    v_new = torch.randn((wl.batch, wl.num_kv_heads, D), generator=g, device=dev)
+    last = wl.context_lens.astype(np.int64) - 1
+    new_slots = torch.as_tensor(wl.page_table[np.arange(wl.batch), last // 16].astype(np.int64) * 16 + last % 16,
+                                device=dev)
+    scale = 1 / math.sqrt(D)
     stream = torch.cuda.current_stream()
 
     def step(ev_a=None, ev_b=None):
+        if D != 128:
+            # head sizes 64 and 256: the write of the new tokens is its own launch
+            uq.quantize_kv(desc, k_new, v_new, new_slots, codes, scales)
         if ev_a is not None:
             ev_a.record(stream)
-        if prefix is None:
+        if D != 128:
+            uq.decode_partials(desc, q, codes, scales, pt, ctx, wl.max_context, scale, part, ws, out)
+        elif prefix is None:
             uq.decode_step(desc, q, k_new, v_new, codes, scales, pt, ctx, wl.max_context, scale, part, ws, out,
                            partials_only=True)
         else:
@@ -327,7 +345,7 @@ def main():
     tokens = wl.total_tokens()
     kv_bytes = wl.kv_bytes_fp4()            # logical: every sequence's whole context
     alg_tokens = alg_token_heads(wl, prefix is not None) // wl.num_kv_heads
-    alg_bytes = alg_tokens * wl.num_kv_heads * KV_BYTES_PER_TOKEN_HEAD
+    alg_bytes = alg_tokens * wl.num_kv_heads * (KV_BYTES_PER_TOKEN_HEAD * D // 128)
     achieved = alg_bytes / (dec_ms * 1e-3) / 1e9
     result = {
         "metric": "decode-attention KV tokens/s and achieved HBM GB/s (% of peak) at 32k context",
@@ -343,7 +361,7 @@ def main():
         "dtype": "fp4-e2m1+ue8m0 kv, fp8-e4m3 q, fp32 accum",
         "data": "synthetic",
         "config": {"workload": wl.name, "batch": wl.batch, "num_q_heads": wl.num_q_heads,
-                   "num_kv_heads": wl.num_kv_heads, "head_dim": 128, "context": int(wl.max_context),
+                   "num_kv_heads": wl.num_kv_heads, "head_dim": D, "context": int(wl.max_context),
                    "page_size": 16, "partition_tokens": int(part), "parallelism": "single-gpu",
                    "shared_prefix_tokens": int(wl.shared_prefix_tokens), "cascade": prefix is not None},
         "hbm_gbs_step": kv_bytes / (ms_step * 1e-3) / 1e9,
@@ -352,7 +370,8 @@ def main():
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": profiled_traffic(wl.name),
                      "launch_ms": dec_ms, "bytes_per_launch": alg_bytes, "logical_bytes_per_launch": kv_bytes},
     }
-    fmts = [f for f in args.comparators.split(",") if f and f != "none"]
+    # the comparison caches exist at head size 128
+    fmts = [f for f in args.comparators.split(",") if f and f != "none"] if D == 128 else []
     if fmts:
         comp = {}
         for fmt in fmts:

@@ -4,7 +4,7 @@
  *
  * The library implements the two halves of the paper's Algorithm 1:
  *   Write  (uq_quantize_kv)      rotate K (and V when rotate_v) with the
- *                                fixed 128-point Walsh-Hadamard transform,
+ *                                fixed d-point Walsh-Hadamard transform,
  *                                pick one UE8M0 exponent per 32 channels,
  *                                round every element onto the E2M1 grid and
  *                                store 2 codes per byte + 1 scale byte.
@@ -28,26 +28,30 @@
  *    synchronisation; kernels clamp them so that no access leaves the pools
  *    (an out-of-range page id reads page 0, an out-of-range slot is
  *    skipped), but such results are unspecified.
- *  - Supported shape: head_dim 128, page_size 16, group_size 32, up to 16
- *    query heads per KV head.  Other values return UQ_ERR_UNSUPPORTED.
+ *  - Supported shape: head_dim d = 64, 128 or 256, page_size 16,
+ *    group_size 32, up to 16 query heads per KV head.  Other values return
+ *    UQ_ERR_UNSUPPORTED.  The paper's layers use d = 128; the decode step,
+ *    cascade decode, the pre-cast FP8 query, uq_prepare_query and the
+ *    comparison caches are d = 128 calls (UNSUPPORTED for 64 and 256).
+ *    Sizes written 128 below are d for head sizes 64 and 256.
  *  - Inputs must be finite.
  *
  * Cache format (the "pools")
  * --------------------------
- * One tile holds one (page, kv head, K or V): 16 tokens x 128 channels.
- *   kv_codes  : uint8 [num_pages][num_kv_heads][2 (K=0, V=1)][1024]
- *   kv_scales : uint8 [num_pages][num_kv_heads][2 (K=0, V=1)][4 groups][16 tokens]
+ * One tile holds one (page, kv head, K or V): 16 tokens x d channels.
+ *   kv_codes  : uint8 [num_pages][num_kv_heads][2 (K=0, V=1)][8 d]
+ *   kv_scales : uint8 [num_pages][num_kv_heads][2 (K=0, V=1)][d/32 groups][16 tokens]
  * 17 bytes per 32 elements = 4.25 bits per element (paper, "Cache Layout");
- * 136 bytes per token and kv head for K and V together.
- * Inside a 1024-byte code tile, for token t (0..15) and channel ch (0..127),
- * the even channel of a pair in the low nibble:
+ * 17 d / 16 bytes (136 at d = 128) per token and kv head for K and V together.
+ * Inside a code tile (8 d bytes), for token t (0..15) and channel ch
+ * (0..d-1), the even channel of a pair in the low nibble:
  *   K: byte ((ch/32)*16 + t)*16 + (ch%32)/2
  *      ([group][token][16 bytes] -- one lane of the QK MFMA reads one
  *       token's 32-channel group as 16 contiguous bytes, and its scale byte
  *       sits at the same [group][token] index: the scale layout matches the
  *       operand layout of the block-scaled MFMA, paper "Kernel
  *       Implementation in vLLM")
- *   V: byte ((t/4)*16 + ch/8)*16 + (t%4)*4 + (ch%8)/2
+ *   V: byte ((t/4)*(d/8) + ch/8)*16 + (t%4)*4 + (ch%8)/2
  *      ([token/4][channel/8][token%4][4 bytes] -- one lane of the PV step
  *       reads 4 tokens x 8 channels as 16 contiguous bytes)
  * A code is sign(1) | E2M1 magnitude index(3) over {0,.5,1,1.5,2,3,4,6};
@@ -81,7 +85,7 @@ typedef enum uq_dtype {
 
 typedef struct uq_cache_desc {
     int32_t num_kv_heads;   /* >= 1 */
-    int32_t head_dim;       /* must be 128 */
+    int32_t head_dim;       /* 64, 128 or 256 */
     int32_t page_size;      /* must be 16 */
     int32_t group_size;     /* must be 32 */
     int64_t num_pages;      /* pages in the pools, >= 1 */

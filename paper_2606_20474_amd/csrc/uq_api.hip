@@ -20,10 +20,15 @@ uq_status check_desc(const uq_cache_desc* d) {
     if (d == nullptr) return UQ_ERR_INVALID_ARGUMENT;
     if (d->num_kv_heads < 1 || d->num_pages < 1) return UQ_ERR_INVALID_ARGUMENT;
     if (!(isfinite(d->c) && d->c > 0.0f)) return UQ_ERR_INVALID_ARGUMENT;
-    if (d->head_dim != kHeadDim || d->page_size != kPageSize || d->group_size != kGroupSize)
+    if ((d->head_dim != 64 && d->head_dim != 128 && d->head_dim != 256) || d->page_size != kPageSize ||
+        d->group_size != kGroupSize)
         return UQ_ERR_UNSUPPORTED;
     return UQ_OK;
 }
+
+// The calls that exist for head size 128 only (the decode step, cascade
+// decode, the FP8-query form and uq_prepare_query).
+uq_status require_128(const uq_cache_desc* d) { return d->head_dim == kHeadDim ? UQ_OK : UQ_ERR_UNSUPPORTED; }
 
 uq_status from_hip(hipError_t e) { return e == hipSuccess ? UQ_OK : UQ_ERR_HIP; }
 
@@ -55,14 +60,10 @@ int64_t num_partitions(int32_t max_context, int32_t part) {
     return max_context > 0 ? (int64_t(max_context) + part - 1) / part : 1;
 }
 
-size_t partial_bytes(int32_t batch, int32_t num_q_heads, int32_t max_context, int32_t part) {
-    return align16(size_t(batch) * size_t(num_q_heads) * size_t(num_partitions(max_context, part)) * (kHeadDim + 2) *
-                   sizeof(float));
-}
-
-size_t workspace_for(int32_t batch, int32_t num_q_heads, int32_t max_context, int32_t part, int64_t extra_slots = 0) {
+size_t workspace_for(int32_t batch, int32_t num_q_heads, int32_t max_context, int32_t part, int64_t extra_slots = 0,
+                     int32_t head_dim = kHeadDim) {
     return align16(size_t(batch) * size_t(num_q_heads) * size_t(num_partitions(max_context, part) + extra_slots) *
-                   (kHeadDim + 2) * sizeof(float));
+                   size_t(head_dim + 2) * sizeof(float));
 }
 
 // Fill the parameter block of the decode launches.  Workspace: the partial
@@ -74,7 +75,7 @@ uq_status make_decode_params(const uq_cache_desc* desc, const void* q, uq_dtype 
                              size_t workspace_bytes, void* out, uq_dtype out_dtype, uq::DecodeParams& p,
                              int64_t extra_slots = 0) {
     const int32_t part = partition_tokens == 0 ? pick_partition(batch, desc->num_kv_heads, max_context) : partition_tokens;
-    const size_t need = workspace_for(batch, num_q_heads, max_context, part, extra_slots);
+    const size_t need = workspace_for(batch, num_q_heads, max_context, part, extra_slots, desc->head_dim);
     if (workspace == nullptr) return UQ_ERR_INVALID_ARGUMENT;
     if (workspace_bytes < need) return UQ_ERR_WORKSPACE_TOO_SMALL;
     if (!aligned16(workspace)) return UQ_ERR_INVALID_ARGUMENT;
@@ -105,13 +106,14 @@ uq_status make_decode_params(const uq_cache_desc* desc, const void* q, uq_dtype 
     p.partition_tokens = part;
     p.num_partitions = int32_t(np);
     char* ws = static_cast<char*>(workspace);
-    const size_t acc_bytes = size_t(batch) * num_q_heads * size_t(np) * kHeadDim * sizeof(float);
+    const size_t acc_bytes = size_t(batch) * num_q_heads * size_t(np) * size_t(desc->head_dim) * sizeof(float);
     p.part_acc = reinterpret_cast<float*>(ws);
     p.part_ml = reinterpret_cast<float*>(ws + acc_bytes);
     p.out = out;
     p.out_dtype = out_dtype == UQ_F32 ? 0 : 1;
     p.rotate_v = desc->rotate_v != 0;
-    p.kv_fmt = uq::kFp4;
+    p.head_dim = desc->head_dim;
+    p.kv_fmt = desc->head_dim == 64 ? uq::kFp4d64 : desc->head_dim == 256 ? uq::kFp4d256 : uq::kFp4;
     p.out_scale = 1.0f;
     p.prefix_pages = nullptr;
     p.prefix_lens = nullptr;
@@ -172,6 +174,7 @@ uq_status check_split_args(const uq_cache_desc* desc, const void* q, uq_dtype q_
         return UQ_ERR_INVALID_ARGUMENT;
     if (q_dtype != UQ_F32 && q_dtype != UQ_BF16 && q_dtype != UQ_F16 && q_dtype != UQ_FP8_E4M3)
         return UQ_ERR_UNSUPPORTED;
+    if (q_dtype == UQ_FP8_E4M3 && desc->head_dim != kHeadDim) return UQ_ERR_UNSUPPORTED;
     if (max_pages_per_seq < 1) return UQ_ERR_INVALID_ARGUMENT;
     if (int64_t(max_context) > int64_t(max_pages_per_seq) * kPageSize) return UQ_ERR_INVALID_ARGUMENT;
     if (!(isfinite(softmax_scale) && softmax_scale > 0.0f)) return UQ_ERR_INVALID_ARGUMENT;
@@ -285,7 +288,7 @@ uq_status uq_quantize_kv(const uq_cache_desc* desc, const void* k, const void* v
     if (num_tokens < 0) return UQ_ERR_INVALID_ARGUMENT;
     if (k == nullptr || v == nullptr || slot_mapping == nullptr || kv_codes == nullptr || kv_scales == nullptr)
         return UQ_ERR_INVALID_ARGUMENT;
-    if (token_stride < int64_t(desc->num_kv_heads) * kHeadDim) return UQ_ERR_INVALID_ARGUMENT;
+    if (token_stride < int64_t(desc->num_kv_heads) * desc->head_dim) return UQ_ERR_INVALID_ARGUMENT;
     const int64_t vec_elems = in_dtype == UQ_F32 ? 4 : 8;   // one 16-byte load
     if (token_stride % vec_elems != 0 || !aligned16(k) || !aligned16(v)) return UQ_ERR_INVALID_ARGUMENT;
     if (!aligned16(kv_codes) || !aligned16(kv_scales)) return UQ_ERR_INVALID_ARGUMENT;
@@ -306,12 +309,15 @@ uq_status uq_quantize_kv(const uq_cache_desc* desc, const void* k, const void* v
     p.rotate_v = desc->rotate_v != 0;
     p.codes = kv_codes;
     p.scales = kv_scales;
+    p.head_dim = desc->head_dim;
     return from_hip(uq::launch_quantize_kv(p, int(in_dtype), static_cast<hipStream_t>(stream)));
 }
 
 uq_status uq_prepare_query(const uq_cache_desc* desc, const void* q, uq_dtype q_dtype, int64_t rows, uint8_t* q_fp8,
                            void* stream) {
     uq_status s = check_desc(desc);
+    if (s != UQ_OK) return s;
+    s = require_128(desc);
     if (s != UQ_OK) return s;
     if (q_dtype != UQ_F32 && q_dtype != UQ_BF16 && q_dtype != UQ_F16) return UQ_ERR_UNSUPPORTED;
     if (rows < 0 || q == nullptr || q_fp8 == nullptr) return UQ_ERR_INVALID_ARGUMENT;
@@ -351,7 +357,7 @@ size_t uq_decode_workspace_bytes(const uq_cache_desc* desc, int32_t batch, int32
                                  int32_t partition_tokens) {
     if (check_decode_common(desc, batch, num_q_heads, max_context, partition_tokens) != UQ_OK) return 0;
     const int32_t part = partition_tokens == 0 ? pick_partition(batch, desc->num_kv_heads, max_context) : partition_tokens;
-    return workspace_for(batch, num_q_heads, max_context, part);
+    return workspace_for(batch, num_q_heads, max_context, part, 0, desc->head_dim);
 }
 
 // Shared set-up of the decode entry points: validation and the parameter block.
@@ -372,8 +378,9 @@ static uq_status decode_setup(const uq_cache_desc* desc, const void* q, uq_dtype
                               out, out_dtype, p, extra_slots);
 }
 
-// The new-token arguments of the decode-step calls.
+// The new-token arguments of the decode-step calls (head size 128).
 static uq_status step_args(const void* k_new, const void* v_new, uq_dtype new_dtype, uq::DecodeParams& p) {
+    if (p.head_dim != kHeadDim) return UQ_ERR_UNSUPPORTED;
     if (k_new == nullptr || v_new == nullptr) return UQ_ERR_INVALID_ARGUMENT;
     if (new_dtype != UQ_F32 && new_dtype != UQ_BF16 && new_dtype != UQ_F16) return UQ_ERR_UNSUPPORTED;
     if (!aligned16(k_new) || !aligned16(v_new)) return UQ_ERR_INVALID_ARGUMENT;
@@ -664,6 +671,8 @@ static uq_status cascade_setup(const uq_cache_desc* desc, const void* q, uq_dtyp
     if (s != UQ_OK) return s;
     s = check_desc(desc);
     if (s != UQ_OK) return s;
+    s = require_128(desc);
+    if (s != UQ_OK) return s;
     s = decode_setup(desc, q, q_dtype, batch, num_q_heads, kv_codes, kv_scales, page_table, max_pages_per_seq,
                      context_lens, max_context, softmax_scale, partition_tokens, workspace, workspace_bytes, out,
                      out_dtype, p, prefix_slots(prefix, desc->num_kv_heads, batch, group_of(num_q_heads, desc->num_kv_heads)));
@@ -726,6 +735,8 @@ uq_status uq_decode_cascade_merge(const uq_cache_desc* desc, int32_t batch, int3
                                   int32_t partition_tokens, const void* workspace, size_t workspace_bytes, void* out,
                                   uq_dtype out_dtype, void* stream) {
     uq_status s = check_desc(desc);
+    if (s != UQ_OK) return s;
+    s = require_128(desc);
     if (s != UQ_OK) return s;
     uq::DecodeParams p;
     s = cascade_merge_setup(desc, batch, num_q_heads, context_lens, max_context, prefix, partition_tokens, workspace,

@@ -62,7 +62,6 @@ namespace uq {
 
 constexpr float kLazyRescale = 8.0f;   // log2 units
 constexpr int kWaitVmcnt0 = 0x0F70;    // s_waitcnt vmcnt(0) expcnt(7) lgkmcnt(15) (gfx9 encoding)
-constexpr int kAccStride = 129;        // LDS row stride (floats) of the merge buffer
 
 // Per-format constants.  kTile: bytes of one (page, kv head) K or V tile;
 // kScaleBlock: scale bytes per (page, kv head) for K and V together.
@@ -87,6 +86,22 @@ template <> struct Fmt<kBf16> {
     static constexpr int kWaves = 2;
     static constexpr int kOccupancy = 1;
 };
+// The FP4 cache at head sizes 64 and 256: tiles of 8 D code bytes and D/2
+// scale bytes per (page, head, K|V).
+template <> struct Fmt<kFp4d64> {
+    static constexpr int kTile = 512;
+    static constexpr int kScaleBlock = 64;
+    static constexpr int kWaves = 4;
+    static constexpr int kOccupancy = 4;
+};
+template <> struct Fmt<kFp4d256> {
+    static constexpr int kTile = 2048;
+    static constexpr int kScaleBlock = 256;
+    static constexpr int kWaves = 4;
+    static constexpr int kOccupancy = 2;
+};
+template <int F> constexpr bool is_fp4() { return F == kFp4 || F == kFp4d64 || F == kFp4d256; }
+template <int F> constexpr int head_dim_of() { return F == kFp4d64 ? 64 : F == kFp4d256 ? 256 : 128; }
 // Ultra-TQ: per page 1 KiB of K indices, 1 KiB of V codes and 320 bytes of
 // norms and (scale, zero) words ("scale block").
 template <> struct Fmt<kTq4> {
@@ -207,9 +222,11 @@ __device__ __forceinline__ void stage_issue(uint8_t* stage, const uint8_t* __res
         __builtin_amdgcn_global_load_lds(k1 + c, (lds_ptr_t)(stage + 2 * T + c), 16, 0, 0);
     }
     if constexpr (Fmt<F>::kScaleBlock != 0) {
-        if (lane < 16) {
-            const int64_t t = lane < 8 ? tile0 : tile1;
-            const uint8_t* sc = scales + t * kTileScales + 16 * (lane & 7);
+        // both pages' scale blocks (K then V scales, kScaleBlock bytes per page)
+        constexpr int SB = Fmt<F>::kScaleBlock;
+        if (lane < SB / 8) {
+            const int64_t t = lane < SB / 16 ? tile0 : tile1;
+            const uint8_t* sc = scales + (t >> 1) * SB + 16 * (lane % (SB / 16));
             __builtin_amdgcn_global_load_lds(sc, (lds_ptr_t)(stage + 4 * T), 16, 0, 0);
         }
     }
@@ -238,6 +255,18 @@ template <> struct StageRegs<kFp8> {
 };
 template <> struct StageRegs<kBf16> {
     uint4 k[2][4], v[2][4];   // K: 4 k-steps x 16 bytes; V: 64 bytes
+};
+// Head size 64: as kFp4, with lanes 32..63 (channels 64..127 of the QK
+// operand) and V lanes with lane%16 >= 8 (channel blocks 8..15) zero.
+template <> struct StageRegs<kFp4d64> {
+    uint4 k[2], v[2];
+    uint32_t ks[2], vs[2];
+};
+// Head size 256: two 128-channel chunks for QK (k[pg][m], ks[pg][m]) and two
+// channel blocks per lane for V (blocks lane%16 and lane%16 + 16).
+template <> struct StageRegs<kFp4d256> {
+    uint4 k[2][2], v[2][2];
+    uint32_t ks[2][2], vs[2][2];
 };
 template <> struct StageRegs<kTq4> {
     uint4 k[2];    // K indices of token lane%16, channels 32s + 8*(lane/16) + 0..7 in dword s
@@ -314,6 +343,74 @@ __device__ __forceinline__ void stage_read(StageRegs<kBf16>& r, uint32_t stage_a
         : "memory");
 }
 
+// Head size 64, stage [K0 512][V0 512][K1 512][V1 512][scales0 64][scales1 64].
+__device__ __forceinline__ void stage_read(StageRegs<kFp4d64>& r, uint32_t stage_addr, int lane) {
+    const int n = lane & 15, g4 = lane >> 4;
+    const uint32_t ak = stage_addr + 16 * lane;
+    const uint32_t av = stage_addr + 512 + 16 * (8 * g4 + (n & 7));
+    const uint32_t as = stage_addr + 2048 + (lane & 31);
+    const uint32_t avs = stage_addr + 2048 + 32 + ((n & 7) >> 2) * 16 + 4 * g4;
+    asm volatile(
+        "ds_read_b128 %0, %8\n\t"
+        "ds_read_b128 %1, %9\n\t"
+        "ds_read_b128 %2, %8 offset:1024\n\t"
+        "ds_read_b128 %3, %9 offset:1024\n\t"
+        "ds_read_u8 %4, %10\n\t"
+        "ds_read_u8 %5, %10 offset:64\n\t"
+        "ds_read_b32 %6, %11\n\t"
+        "ds_read_b32 %7, %11 offset:64\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(r.k[0]), "=&v"(r.v[0]), "=&v"(r.k[1]), "=&v"(r.v[1]), "=&v"(r.ks[0]), "=&v"(r.ks[1]), "=&v"(r.vs[0]),
+          "=&v"(r.vs[1])
+        : "v"(ak), "v"(av), "v"(as), "v"(avs)
+        : "memory");
+    if (lane >= 32) {   // k-blocks 2, 3 of the QK operand: channels 64..127 do not exist
+        r.k[0] = uint4{0u, 0u, 0u, 0u};
+        r.k[1] = uint4{0u, 0u, 0u, 0u};
+        r.ks[0] = 127u;
+        r.ks[1] = 127u;
+    }
+    if (n >= 8) {       // channel blocks 8..15 do not exist
+        r.v[0] = uint4{0u, 0u, 0u, 0u};
+        r.v[1] = uint4{0u, 0u, 0u, 0u};
+        r.vs[0] = 0u;
+        r.vs[1] = 0u;
+    }
+}
+
+// Head size 256, stage [K0 2048][V0 2048][K1 2048][V1 2048][scales0 256][scales1 256].
+__device__ __forceinline__ void stage_read(StageRegs<kFp4d256>& r, uint32_t stage_addr, int lane) {
+    const int n = lane & 15, g4 = lane >> 4;
+    const uint32_t ak = stage_addr + 16 * lane;
+    const uint32_t av = stage_addr + 2048 + 16 * (32 * g4 + n);
+    const uint32_t as = stage_addr + 8192 + lane;
+    const uint32_t avs = stage_addr + 8192 + 128 + (n >> 2) * 16 + 4 * g4;
+    asm volatile(
+        "ds_read_b128 %0, %16\n\t"
+        "ds_read_b128 %1, %16 offset:1024\n\t"
+        "ds_read_b128 %2, %17\n\t"
+        "ds_read_b128 %3, %17 offset:256\n\t"
+        "ds_read_b128 %4, %16 offset:4096\n\t"
+        "ds_read_b128 %5, %16 offset:5120\n\t"
+        "ds_read_b128 %6, %17 offset:4096\n\t"
+        "ds_read_b128 %7, %17 offset:4352\n\t"
+        "ds_read_u8 %8, %18\n\t"
+        "ds_read_u8 %9, %18 offset:64\n\t"
+        "ds_read_u8 %10, %18 offset:256\n\t"
+        "ds_read_u8 %11, %18 offset:320\n\t"
+        "ds_read_b32 %12, %19\n\t"
+        "ds_read_b32 %13, %19 offset:64\n\t"
+        "ds_read_b32 %14, %19 offset:256\n\t"
+        "ds_read_b32 %15, %19 offset:320\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(r.k[0][0]), "=&v"(r.k[0][1]), "=&v"(r.v[0][0]), "=&v"(r.v[0][1]), "=&v"(r.k[1][0]),
+          "=&v"(r.k[1][1]), "=&v"(r.v[1][0]), "=&v"(r.v[1][1]), "=&v"(r.ks[0][0]), "=&v"(r.ks[0][1]),
+          "=&v"(r.ks[1][0]), "=&v"(r.ks[1][1]), "=&v"(r.vs[0][0]), "=&v"(r.vs[0][1]), "=&v"(r.vs[1][0]),
+          "=&v"(r.vs[1][1])
+        : "v"(ak), "v"(av), "v"(as), "v"(avs)
+        : "memory");
+}
+
 __device__ __forceinline__ void stage_read(StageRegs<kTq4>& r, uint32_t stage_addr, int lane) {
     const uint32_t ak = stage_addr + 16 * lane;
     const uint32_t an = stage_addr + 4096 + 16 * (lane >> 4);
@@ -337,6 +434,7 @@ __device__ __forceinline__ void stage_read(StageRegs<kTq4>& r, uint32_t stage_ad
 // Query operand in registers.
 template <int F> struct QOperand { v8i q; };               // FP8 bytes, 32 per lane
 template <> struct QOperand<kBf16> { v8bf q[4]; };          // 4 k-steps x 8 BF16 per lane
+template <> struct QOperand<kFp4d256> { v8i q[2]; };        // FP8 bytes of the two 128-channel chunks
 // Ultra-TQ: the BF16 query with each k-step's 8 channels in the order
 // 0, 2, 4, 6, 1, 3, 5, 7 (the order the index decoder produces), and the
 // codebook's byte tables.
@@ -373,6 +471,18 @@ __device__ __forceinline__ v4f qk_page(const StageRegs<kFp4>& r, int pg, const Q
     const v8i a = {int(r.k[pg].x), int(r.k[pg].y), int(r.k[pg].z), int(r.k[pg].w), 0, 0, 0, 0};
     const v4f zero = {0.f, 0.f, 0.f, 0.f};
     return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, q.q, zero, 4, 0, 0, int(r.ks[pg]), 0, 127);
+}
+__device__ __forceinline__ v4f qk_page(const StageRegs<kFp4d64>& r, int pg, const QOperand<kFp4d64>& q) {
+    const v8i a = {int(r.k[pg].x), int(r.k[pg].y), int(r.k[pg].z), int(r.k[pg].w), 0, 0, 0, 0};
+    const v4f zero = {0.f, 0.f, 0.f, 0.f};
+    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, q.q, zero, 4, 0, 0, int(r.ks[pg]), 0, 127);
+}
+__device__ __forceinline__ v4f qk_page(const StageRegs<kFp4d256>& r, int pg, const QOperand<kFp4d256>& q) {
+    const v8i a0 = {int(r.k[pg][0].x), int(r.k[pg][0].y), int(r.k[pg][0].z), int(r.k[pg][0].w), 0, 0, 0, 0};
+    const v8i a1 = {int(r.k[pg][1].x), int(r.k[pg][1].y), int(r.k[pg][1].z), int(r.k[pg][1].w), 0, 0, 0, 0};
+    const v4f zero = {0.f, 0.f, 0.f, 0.f};
+    const v4f s = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a0, q.q[0], zero, 4, 0, 0, int(r.ks[pg][0]), 0, 127);
+    return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a1, q.q[1], s, 4, 0, 0, int(r.ks[pg][1]), 0, 127);
 }
 __device__ __forceinline__ v4f qk_page(const StageRegs<kFp8>& r, int pg, const QOperand<kFp8>& q) {
     const uint4 lo = r.k[pg][0], hi = r.k[pg][1];
@@ -444,6 +554,30 @@ __device__ __forceinline__ void pv_pair(const R& r, const float (&sc)[2][4], con
     acc_o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Vo, Plo, acc_o, 0, 0, 0);
 }
 
+// FP4 PV for channel pair C of one channel block per lane (v0, v1: the
+// block's codes of the lane's 4 tokens of page 0 and page 1; sc: their
+// scale floats), as pv_pair does for kFp4.
+template <int C>
+__device__ __forceinline__ void pv_pair_fp4(const uint4& v0, const uint4& v1, const float (&sc)[2][4], const v8bf& Phi,
+                                            const v8bf& Plo, v4f& acc_e, v4f& acc_o) {
+    uint32_t c0[4], c1[4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+        c0[t] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(dword(v0, t), sc[0][t], C));
+        c1[t] = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(dword(v1, t), sc[1][t], C));
+    }
+    const uint4 ae = {__builtin_amdgcn_perm(c0[1], c0[0], 0x05040100u), __builtin_amdgcn_perm(c0[3], c0[2], 0x05040100u),
+                      __builtin_amdgcn_perm(c1[1], c1[0], 0x05040100u), __builtin_amdgcn_perm(c1[3], c1[2], 0x05040100u)};
+    const uint4 ao = {__builtin_amdgcn_perm(c0[1], c0[0], 0x07060302u), __builtin_amdgcn_perm(c0[3], c0[2], 0x07060302u),
+                      __builtin_amdgcn_perm(c1[1], c1[0], 0x07060302u), __builtin_amdgcn_perm(c1[3], c1[2], 0x07060302u)};
+    const v8bf Ve = __builtin_bit_cast(v8bf, ae);
+    const v8bf Vo = __builtin_bit_cast(v8bf, ao);
+    acc_e = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ve, Phi, acc_e, 0, 0, 0);
+    acc_e = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Ve, Plo, acc_e, 0, 0, 0);
+    acc_o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Vo, Phi, acc_o, 0, 0, 0);
+    acc_o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Vo, Plo, acc_o, 0, 0, 0);
+}
+
 // Ultra-TQ PV for channel pair C: each V value is bf16(fma(scale, code,
 // zero)) of its token's group, packed two tokens per register in the k-slot
 // order of P.
@@ -475,25 +609,35 @@ __device__ __forceinline__ void pv_pair(const StageRegs<kTq4>& r, const float (&
     acc_o = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Vo, Plo, acc_o, 0, 0, 0);
 }
 
-__device__ __forceinline__ void write_out(const DecodeParams& p, int64_t row, int L, const float (&o)[8]) {
-    const int64_t ob = row * kHeadDim + 8 * L;
+// Lane L of a 16-lane row writes channels N L .. N L + N - 1 of the row
+// (head size 16 N).
+template <int N>
+__device__ __forceinline__ void write_out(const DecodeParams& p, int64_t row, int L, const float (&o)[N]) {
+    const int64_t ob = row * (16 * N) + N * L;
     if (p.out_dtype == 0) {
         float4* dst = reinterpret_cast<float4*>(static_cast<float*>(p.out) + ob);
-        dst[0] = make_float4(o[0], o[1], o[2], o[3]);
-        dst[1] = make_float4(o[4], o[5], o[6], o[7]);
+#pragma unroll
+        for (int i = 0; i < N / 4; ++i) dst[i] = make_float4(o[4 * i], o[4 * i + 1], o[4 * i + 2], o[4 * i + 3]);
+    } else if constexpr (N == 4) {
+        *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.out) + ob) =
+            uint2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
     } else {
-        *reinterpret_cast<uint4*>(static_cast<uint16_t*>(p.out) + ob) =
-            uint4{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3]), pack_bf16x2(o[4], o[5]), pack_bf16x2(o[6], o[7])};
+        uint4* dst = reinterpret_cast<uint4*>(static_cast<uint16_t*>(p.out) + ob);
+#pragma unroll
+        for (int i = 0; i < N / 8; ++i)
+            dst[i] = uint4{pack_bf16x2(o[8 * i], o[8 * i + 1]), pack_bf16x2(o[8 * i + 2], o[8 * i + 3]),
+                           pack_bf16x2(o[8 * i + 4], o[8 * i + 5]), pack_bf16x2(o[8 * i + 6], o[8 * i + 7])};
     }
 }
 
 // Final scaling of one row: divide by the softmax sum, apply the V tensor
 // scale, rotate back when V was stored rotated.
-__device__ __forceinline__ void finish_row(const DecodeParams& p, float (&o)[8], float lsum, int L) {
+template <int N>
+__device__ __forceinline__ void finish_row(const DecodeParams& p, float (&o)[N], float lsum, int L) {
     const float inv = p.out_scale / lsum;
 #pragma unroll
-    for (int i = 0; i < 8; ++i) o[i] *= inv;
-    if (p.rotate_v) wht128_x8(o, L);
+    for (int i = 0; i < N; ++i) o[i] *= inv;
+    if (p.rotate_v) wht_x<N>(o, L);
 }
 
 // Zero the V bytes of a masked token of a plain cache (garbage bytes past
@@ -505,6 +649,12 @@ __device__ __forceinline__ void zero_token(StageRegs<kFp8>& c, int pg, int t) {
 }
 __device__ __forceinline__ void zero_token(StageRegs<kBf16>& c, int pg, int t) { c.v[pg][t] = uint4{0u, 0u, 0u, 0u}; }
 __device__ __forceinline__ void zero_token(StageRegs<kFp4>&, int, int) {}   // handled through the scale byte
+// Head sizes 64 and 256: scale byte 0 (scale 0.0) for the token's V groups.
+__device__ __forceinline__ void zero_token(StageRegs<kFp4d64>& c, int pg, int t) { c.vs[pg] &= ~(0xFFu << (8 * t)); }
+__device__ __forceinline__ void zero_token(StageRegs<kFp4d256>& c, int pg, int t) {
+    c.vs[pg][0] &= ~(0xFFu << (8 * t));
+    c.vs[pg][1] &= ~(0xFFu << (8 * t));
+}
 __device__ __forceinline__ void zero_token(StageRegs<kTq4>& c, int pg, int t) {
     // scale and zero 0: the value decodes to 0 whatever the bytes
     uint4& m = c.vm[pg];
@@ -521,6 +671,9 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
     constexpr int kThreads = 64 * W;
     constexpr int kStage = stage_bytes<F>();
     constexpr int kQRounds = 256 / kThreads;   // 16 threads per query row, 16 rows
+    constexpr int D = head_dim_of<F>();         // head size
+    constexpr int N = D / 16;                   // channels per lane of a 16-lane row
+    constexpr int kAccTiles = D == 256 ? 16 : 8;   // PV output tiles of 16 channel blocks x 16 heads
     // Linear block order: kv head fastest, then sequence, then partition.
     // Workgroups go to the 8 XCDs round-robin by linear id, so this spreads
     // the work of every sequence evenly over the XCDs whatever the context
@@ -571,8 +724,10 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
             // nothing of this sequence here; an empty context still gets its zero output
             if (ctx <= 0 && part == 0) {
                 for (int r = tid >> 4; r < G; r += kThreads / 16) {
-                    const float z[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-                    write_out(p, int64_t(b) * p.num_q_heads + hk * G + r, tid & 15, z);
+                    float z[N];
+#pragma unroll
+                    for (int i = 0; i < N; ++i) z[i] = 0.f;
+                    write_out<N>(p, int64_t(b) * p.num_q_heads + hk * G + r, tid & 15, z);
                 }
             }
             return;
@@ -601,27 +756,53 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
     // page for this kv head (partitions are whole pages).
     const int pos_new = ctx - 1;
     const int it_new = (pos_new - start) >> 5;                       // iteration holding the token
-    const bool append = !pre && p.k_new != nullptr && pos_new >= start && wave == it_new % W;   // wave-uniform
+    // (the step is a head-size-128 call)
+    const bool append = D == 128 && !pre && p.k_new != nullptr && pos_new >= start && wave == it_new % W;
     const int k_new_local = it_new / W;                              // that wave's local iteration
 
     __shared__ __attribute__((aligned(16))) uint8_t smem[W * ring_bytes<F>()];
-    __shared__ __attribute__((aligned(16))) uint8_t q_lds[(F == kBf16 || F == kTq4) ? 4 * 64 * 16 : 64 * 32];
+    __shared__ __attribute__((aligned(16))) uint8_t q_lds[(F == kBf16 || F == kTq4) ? 4 * 64 * 16 : (D / 128 + (D < 128)) * 64 * 32];
     __shared__ float red_m[W][16];
     __shared__ float red_l[W][16];
 
     // ---------------- query load first (its latency overlaps the page walk set-up)
-    float qx[kQRounds][8];
+    float qx[kQRounds][N];
     uint32_t qw[kQRounds][2];
 #pragma unroll
     for (int h = 0; h < kQRounds; ++h) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) qx[h][i] = 0.f;
+        for (int i = 0; i < N; ++i) qx[h][i] = 0.f;
         qw[h][0] = 0u;
         qw[h][1] = 0u;
         const int qr = (tid >> 4) + h * (kThreads / 16);
         const int qL = tid & 15;
         int rb, rhq;
-        if (qr < 16 && row_of(qr, rb, rhq)) {
+        if constexpr (D != 128) {
+            // head sizes 64 and 256: an F32, BF16 or F16 query, N channels per thread
+            if (qr < 16 && row_of(qr, rb, rhq)) {
+                const int64_t elem = (int64_t(rb) * p.num_q_heads + rhq) * D + N * qL;
+                float (&x)[N] = qx[h];
+                if constexpr (N == 4) {
+                    if (p.q_dtype == 0) load_x4<0>(p.q, elem, x);
+                    else if (p.q_dtype == 1) load_x4<1>(p.q, elem, x);
+                    else load_x4<2>(p.q, elem, x);
+                } else {
+                    float (&x0)[8] = *reinterpret_cast<float(*)[8]>(&x[0]);
+                    float (&x1)[8] = *reinterpret_cast<float(*)[8]>(&x[8]);
+                    if (p.q_dtype == 0) {
+                        load_x8<0>(p.q, elem, x0);
+                        load_x8<0>(p.q, elem + 8, x1);
+                    } else if (p.q_dtype == 1) {
+                        load_x8<1>(p.q, elem, x0);
+                        load_x8<1>(p.q, elem + 8, x1);
+                    } else {
+                        load_x8<2>(p.q, elem, x0);
+                        load_x8<2>(p.q, elem + 8, x1);
+                    }
+                }
+            }
+        } else {
+          if (qr < 16 && row_of(qr, rb, rhq)) {
             const int64_t elem = (int64_t(rb) * p.num_q_heads + rhq) * kHeadDim + 8 * qL;
             if (p.q_dtype == 3) {
                 const uint2 w = *reinterpret_cast<const uint2*>(static_cast<const uint8_t*>(p.q) + elem);
@@ -634,6 +815,7 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
             } else {
                 load_x8<2>(p.q, elem, qx[h]);
             }
+          }
         }
     }
 
@@ -722,6 +904,31 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
                 }
             }
             *reinterpret_cast<uint4*>(q_lds + ((qL >> 2) * 64 + (qL & 3) * 16 + qr) * 16) = w;
+        } else if constexpr (F == kFp4d64 || F == kFp4d256) {
+            // rotated (D-point) and cast to FP8; the lane's N channels go to the
+            // B operand of the 128-channel chunk they belong to (layout below)
+            uint32_t wq[N / 4];
+#pragma unroll
+            for (int i = 0; i < N / 4; ++i) wq[i] = 0u;
+            if (qvalid) {
+                wht_x<N>(qx[h], qL);
+#pragma unroll
+                for (int i = 0; i < N / 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) wq[i] |= e4m3_byte(qx[h][4 * i + j]) << (8 * j);
+            }
+            const int ch = N * qL;
+            const int c2 = ch & 127;
+            const int g = (c2 & 63) >> 4;
+            const int e0 = (c2 & 15) + (c2 >= 64 ? 16 : 0);
+            uint8_t* dst = q_lds + (ch >> 7) * 2048 + (g * 16 + qr) * 32 + e0;
+            if constexpr (N == 4) {
+                *reinterpret_cast<uint32_t*>(dst) = wq[0];
+                // channels 64..127 of the chunk do not exist: zero operand
+                if (qL < 4) *reinterpret_cast<uint4*>(q_lds + (qL * 16 + qr) * 32 + 16) = uint4{0u, 0u, 0u, 0u};
+            } else {
+                *reinterpret_cast<uint4*>(dst) = uint4{wq[0], wq[1], wq[2], wq[3]};
+            }
         } else {
             uint32_t lo = qw[h][0], hi = qw[h][1];
             if (qvalid && p.q_dtype != 3) {
@@ -753,6 +960,13 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
 #pragma unroll
             for (int j = 0; j < 8; ++j) qop.lut[j] = p.tq.lut[j];
         }
+    } else if constexpr (F == kFp4d256) {
+#pragma unroll
+        for (int m = 0; m < 2; ++m) {
+            const uint4* src = reinterpret_cast<const uint4*>(q_lds + m * 2048 + lane * 32);
+            const uint4 a = src[0], c = src[1];
+            qop.q[m] = v8i{int(a.x), int(a.y), int(a.z), int(a.w), int(c.x), int(c.y), int(c.z), int(c.w)};
+        }
     } else {
         const uint4* src = reinterpret_cast<const uint4*>(q_lds + lane * 32);
         const uint4 a = src[0], c = src[1];
@@ -761,11 +975,14 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
 
     // Decode step, owning wave: encode and store the new token while its
     // first two stages are in flight (the store is not waited for).
-    TokenBits<F> tok{};
-    if (append && lane < 16) {
-        tok = encode_token<F>(xk, xv, lane, p.c, p.rotate_v != 0, p.k_scale, p.v_scale, p.tq);
-        if (page_new >= 0 && int64_t(page_new) < p.num_pages)
-            store_token<F>(p.codes, p.scales, (int64_t(page_new) * p.num_kv_heads + hk) * 2, pos_new & 15, lane, tok);
+    TokenBits<D == 128 ? F : kFp4> tok{};
+    if constexpr (D == 128) {
+        if (append && lane < 16) {
+            tok = encode_token<F>(xk, xv, lane, p.c, p.rotate_v != 0, p.k_scale, p.v_scale, p.tq);
+            if (page_new >= 0 && int64_t(page_new) < p.num_pages)
+                store_token<F>(p.codes, p.scales, (int64_t(page_new) * p.num_kv_heads + hk) * 2, pos_new & 15, lane,
+                               tok);
+        }
     }
 
     const float sl2 = p.scale_log2;
@@ -776,21 +993,23 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
     // (all ones) x P is the column sum of P
     const v8bf ones = __builtin_bit_cast(v8bf, uint4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u});
     v4f acc_l = {0.f, 0.f, 0.f, 0.f};
-    v4f acc[8];
+    v4f acc[kAccTiles];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc[j] = v4f{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < kAccTiles; ++j) acc[j] = v4f{0.f, 0.f, 0.f, 0.f};
 
     // ---------------- main loop: one stage (2 pages, 32 tokens) per iteration
     for (int k = 0; k < n_local; ++k) {
         if (k + 1 < n_local) wait_vmem<dma_per_stage<F>()>();
         else wait_vmem<0>();
         const uint32_t slot = uint32_t(k & 1);
-        if (append && k == k_new_local && lane < 16) {
-            // the staged page holds what the pools held before this step
-            lds_u8* st0 = (lds_u8*)(ring + slot * kStage);
-            const int pg = ((pos_new - start) >> 4) & 1;
-            place_token<F>(st0 + pg * 2 * Fmt<F>::kTile, st0 + 4 * Fmt<F>::kTile + pg * Fmt<F>::kScaleBlock,
-                           pos_new & 15, lane, tok);
+        if constexpr (D == 128) {
+            if (append && k == k_new_local && lane < 16) {
+                // the staged page holds what the pools held before this step
+                lds_u8* st0 = (lds_u8*)(ring + slot * kStage);
+                const int pg = ((pos_new - start) >> 4) & 1;
+                place_token<F>(st0 + pg * 2 * Fmt<F>::kTile, st0 + 4 * Fmt<F>::kTile + pg * Fmt<F>::kScaleBlock,
+                               pos_new & 15, lane, tok);
+            }
         }
         StageRegs<F> c;
         stage_read(c, ring_addr + slot * kStage, lane);
@@ -862,7 +1081,7 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
                 const float alpha = __builtin_amdgcn_exp2f(m_run - mloc);
                 acc_l *= alpha;
 #pragma unroll
-                for (int j = 0; j < 8; ++j) acc[j] *= alpha;
+                for (int j = 0; j < kAccTiles; ++j) acc[j] *= alpha;
                 m_run = mloc;
             }
         }
@@ -878,42 +1097,83 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
         acc_l = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, Plo, acc_l, 0, 0, 0);
 
         // ---- V to BF16 pairs, then PV on bf16 MFMA
-        float sc[2][4];
-        sc[0][0] = byte_scale0(vs0, k23);
-        sc[0][1] = byte_scale1(vs0, k23);
-        sc[0][2] = byte_scale2(vs0, k23);
-        sc[0][3] = byte_scale3(vs0, k23);
-        sc[1][0] = byte_scale0(vs1, k23);
-        sc[1][1] = byte_scale1(vs1, k23);
-        sc[1][2] = byte_scale2(vs1, k23);
-        sc[1][3] = byte_scale3(vs1, k23);
-        pv_pair<0>(c, sc, Phi, Plo, acc[0], acc[1]);
-        pv_pair<1>(c, sc, Phi, Plo, acc[2], acc[3]);
-        pv_pair<2>(c, sc, Phi, Plo, acc[4], acc[5]);
-        pv_pair<3>(c, sc, Phi, Plo, acc[6], acc[7]);
+        if constexpr (F == kFp4d64 || F == kFp4d256) {
+            // one channel block per lane (two for head size 256), its V scale
+            // bytes already masked past the end
+#pragma unroll
+            for (int bl = 0; bl < (F == kFp4d256 ? 2 : 1); ++bl) {
+                uint32_t w0, w1;
+                uint4 v0, v1;
+                if constexpr (F == kFp4d256) {
+                    w0 = c.vs[0][bl];
+                    w1 = c.vs[1][bl];
+                    v0 = c.v[0][bl];
+                    v1 = c.v[1][bl];
+                } else {
+                    w0 = c.vs[0];
+                    w1 = c.vs[1];
+                    v0 = c.v[0];
+                    v1 = c.v[1];
+                }
+                float sc[2][4];
+                sc[0][0] = byte_scale0(w0, k23);
+                sc[0][1] = byte_scale1(w0, k23);
+                sc[0][2] = byte_scale2(w0, k23);
+                sc[0][3] = byte_scale3(w0, k23);
+                sc[1][0] = byte_scale0(w1, k23);
+                sc[1][1] = byte_scale1(w1, k23);
+                sc[1][2] = byte_scale2(w1, k23);
+                sc[1][3] = byte_scale3(w1, k23);
+                pv_pair_fp4<0>(v0, v1, sc, Phi, Plo, acc[8 * bl + 0], acc[8 * bl + 1]);
+                pv_pair_fp4<1>(v0, v1, sc, Phi, Plo, acc[8 * bl + 2], acc[8 * bl + 3]);
+                pv_pair_fp4<2>(v0, v1, sc, Phi, Plo, acc[8 * bl + 4], acc[8 * bl + 5]);
+                pv_pair_fp4<3>(v0, v1, sc, Phi, Plo, acc[8 * bl + 6], acc[8 * bl + 7]);
+            }
+        } else {
+            float sc[2][4];
+            sc[0][0] = byte_scale0(vs0, k23);
+            sc[0][1] = byte_scale1(vs0, k23);
+            sc[0][2] = byte_scale2(vs0, k23);
+            sc[0][3] = byte_scale3(vs0, k23);
+            sc[1][0] = byte_scale0(vs1, k23);
+            sc[1][1] = byte_scale1(vs1, k23);
+            sc[1][2] = byte_scale2(vs1, k23);
+            sc[1][3] = byte_scale3(vs1, k23);
+            pv_pair<0>(c, sc, Phi, Plo, acc[0], acc[1]);
+            pv_pair<1>(c, sc, Phi, Plo, acc[2], acc[3]);
+            pv_pair<2>(c, sc, Phi, Plo, acc[4], acc[5]);
+            pv_pair<3>(c, sc, Phi, Plo, acc[6], acc[7]);
+        }
     }
 
     // ---------------- merge the waves through LDS (the rings are free now)
     const float l_run = acc_l[0];   // the column sum, in every lane of the column
     __syncthreads();
     float* red_acc = reinterpret_cast<float*>(smem);
-    static_assert(W * 16 * kAccStride * 4 <= W * ring_bytes<F>(), "merge buffer aliases the staging rings");
+    constexpr int kAS = D + 1;   // LDS row stride (floats) of the merge buffer
+    static_assert(W * 16 * kAS * 4 <= W * ring_bytes<F>(), "merge buffer aliases the staging rings");
     if (g4 == 0) {
         red_m[wave][n] = m_run;
         red_l[wave][n] = l_run;
     }
-    // acc[j][i] of lane (n, g4) is O^T[channel 8*(4*g4+i)+j][head n]
+    // acc[8 bl + j][i] of lane (n, g4) is O^T[channel 128 bl + 8*(4*g4+i) + j][head n]
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
+    for (int bl = 0; bl < kAccTiles / 8; ++bl) {
 #pragma unroll
-        for (int i = 0; i < 4; ++i) red_acc[(wave * 16 + n) * kAccStride + 32 * g4 + 8 * i + j] = acc[j][i];
+        for (int j = 0; j < 8; ++j) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                // head size 64: rows of channel blocks 8..15 (g4 >= 2) do not exist
+                if (D != 64 || g4 < 2) red_acc[(wave * 16 + n) * kAS + 128 * bl + 32 * g4 + 8 * i + j] = acc[8 * bl + j][i];
+            }
+        }
     }
     __syncthreads();
 
 #pragma unroll
     for (int h = 0; h < kQRounds; ++h) {
         const int r = (tid >> 4) + h * (kThreads / 16);   // query row of the block
-        const int L = tid & 15;                           // channels 8L..8L+7
+        const int L = tid & 15;                           // channels N L .. N L + N - 1
         int rb, hq;
         if (r >= 16 || !row_of(r, rb, hq)) continue;     // whole 16-lane rows skip together
         float M = red_m[0][r];
@@ -926,25 +1186,25 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
             f[w] = __builtin_amdgcn_exp2f(red_m[w][r] - M);
             lsum += f[w] * red_l[w][r];
         }
-        float o[8];
+        float o[N];
 #pragma unroll
-        for (int cc = 0; cc < 8; ++cc) {
+        for (int cc = 0; cc < N; ++cc) {
             float s = 0.f;
 #pragma unroll
-            for (int w = 0; w < W; ++w) s += f[w] * red_acc[(w * 16 + r) * kAccStride + 8 * L + cc];
+            for (int w = 0; w < W; ++w) s += f[w] * red_acc[(w * 16 + r) * kAS + N * L + cc];
             o[cc] = s;
         }
         if (in_place) {
             // the whole context is in this block: finish here
-            finish_row(p, o, lsum, L);
-            write_out(p, int64_t(rb) * p.num_q_heads + hq, L, o);
+            finish_row<N>(p, o, lsum, L);
+            write_out<N>(p, int64_t(rb) * p.num_q_heads + hq, L, o);
         } else {
             // several partitions: publish this one for the merge kernel
             const int slot = pre ? p.suffix_partitions + part : part;
             const int64_t prow = (int64_t(rb) * p.num_q_heads + hq) * p.num_partitions + slot;
-            float4* dst = reinterpret_cast<float4*>(p.part_acc + prow * kHeadDim + 8 * L);
-            dst[0] = make_float4(o[0], o[1], o[2], o[3]);
-            dst[1] = make_float4(o[4], o[5], o[6], o[7]);
+            float4* dst = reinterpret_cast<float4*>(p.part_acc + prow * D + N * L);
+#pragma unroll
+            for (int i = 0; i < N / 4; ++i) dst[i] = make_float4(o[4 * i], o[4 * i + 1], o[4 * i + 2], o[4 * i + 3]);
             if (L == 0) *reinterpret_cast<float2*>(p.part_ml + prow * 2) = make_float2(M, lsum);
         }
     }
@@ -956,7 +1216,9 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
 // Cascade decode: the context partitions after the tokens the prefix serves,
 // then that sequence's prefix partitions; always merged (every block of a
 // cascade call writes a partial).
+template <int D>
 __global__ void __launch_bounds__(256) merge_kernel(DecodeParams p) {
+    constexpr int N = D / 16;   // channels per lane
     const int hk = blockIdx.x;
     const int b = blockIdx.y;
     const int r = threadIdx.x >> 4;
@@ -981,24 +1243,33 @@ __global__ void __launch_bounds__(256) merge_kernel(DecodeParams p) {
     const int64_t row0 = (int64_t(b) * p.num_q_heads + hq) * p.num_partitions;
     float M = -__builtin_inff();
     float lsum = 0.f;
-    float o[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    float o[N];
+#pragma unroll
+    for (int i = 0; i < N; ++i) o[i] = 0.f;
     auto merge_slot = [&](int slot) {
         const float2 ml = *reinterpret_cast<const float2*>(p.part_ml + (row0 + slot) * 2);
-        const float4* src = reinterpret_cast<const float4*>(p.part_acc + (row0 + slot) * kHeadDim + 8 * L);
-        const float4 a = src[0], c = src[1];
+        const float4* src = reinterpret_cast<const float4*>(p.part_acc + (row0 + slot) * D + N * L);
+        float4 a[N / 4];
+#pragma unroll
+        for (int i = 0; i < N / 4; ++i) a[i] = src[i];
         const float Mn = __builtin_fmaxf(M, ml.x);
         const float fo = __builtin_amdgcn_exp2f(M - Mn);
         const float fn = __builtin_amdgcn_exp2f(ml.x - Mn);
         lsum = lsum * fo + ml.y * fn;
-        o[0] = o[0] * fo + a.x * fn; o[1] = o[1] * fo + a.y * fn; o[2] = o[2] * fo + a.z * fn; o[3] = o[3] * fo + a.w * fn;
-        o[4] = o[4] * fo + c.x * fn; o[5] = o[5] * fo + c.y * fn; o[6] = o[6] * fo + c.z * fn; o[7] = o[7] * fo + c.w * fn;
+#pragma unroll
+        for (int i = 0; i < N / 4; ++i) {
+            o[4 * i] = o[4 * i] * fo + a[i].x * fn;
+            o[4 * i + 1] = o[4 * i + 1] * fo + a[i].y * fn;
+            o[4 * i + 2] = o[4 * i + 2] * fo + a[i].z * fn;
+            o[4 * i + 3] = o[4 * i + 3] * fo + a[i].w * fn;
+        }
         M = Mn;
     };
 #pragma unroll 4
     for (int q = first; q < np; ++q) merge_slot(q);
     for (int q = 0; q < nq; ++q) merge_slot(p.suffix_partitions + q);
-    finish_row(p, o, lsum, L);
-    write_out(p, int64_t(b) * p.num_q_heads + hq, L, o);
+    finish_row<N>(p, o, lsum, L);
+    write_out<N>(p, int64_t(b) * p.num_q_heads + hq, L, o);
 }
 
 template <int F>
@@ -1012,13 +1283,17 @@ hipError_t launch_decode_partials(const DecodeParams& p, hipStream_t stream) {
     if (p.kv_fmt == kFp8) return launch_partials<kFp8>(p, stream);
     if (p.kv_fmt == kBf16) return launch_partials<kBf16>(p, stream);
     if (p.kv_fmt == kTq4) return launch_partials<kTq4>(p, stream);
+    if (p.kv_fmt == kFp4d64) return launch_partials<kFp4d64>(p, stream);
+    if (p.kv_fmt == kFp4d256) return launch_partials<kFp4d256>(p, stream);
     return launch_partials<kFp4>(p, stream);
 }
 
 hipError_t launch_decode_merge(const DecodeParams& p, hipStream_t stream) {
     if (p.num_partitions <= 1 && p.prefix_pages == nullptr) return hipSuccess;   // every sequence was finished in place
     const dim3 grid{unsigned(p.num_kv_heads), unsigned(p.batch)};
-    hipLaunchKernelGGL(merge_kernel, grid, dim3(256), 0, stream, p);
+    if (p.head_dim == 64) hipLaunchKernelGGL(merge_kernel<64>, grid, dim3(256), 0, stream, p);
+    else if (p.head_dim == 256) hipLaunchKernelGGL(merge_kernel<256>, grid, dim3(256), 0, stream, p);
+    else hipLaunchKernelGGL(merge_kernel<128>, grid, dim3(256), 0, stream, p);
     return hipGetLastError();
 }
 

@@ -36,6 +36,11 @@ __device__ __forceinline__ uint32_t f32_bits(float f) { return __builtin_bit_cas
 
 // fl32(1/sqrt(128)).
 __device__ __forceinline__ float inv_sqrt128() { return bits_f32(0x3DB504F3u); }
+// fl32(1/sqrt(d)) of the rotation's normalisation: exact for 64 and 256.
+template <int D> __device__ __forceinline__ float inv_sqrt_d() {
+    static_assert(D == 64 || D == 128 || D == 256, "head size");
+    return D == 64 ? 0.125f : D == 256 ? 0.0625f : inv_sqrt128();
+}
 
 // The rotation R = H_128 / sqrt(128) of one 128-vector held by 16
 // consecutive lanes (lane L of the 16 holds channels 8L..8L+7 in x[0..7]).
@@ -68,6 +73,37 @@ __device__ __forceinline__ void wht128_x8(float (&x)[8], int L) {
     const float r = inv_sqrt128();
 #pragma unroll
     for (int i = 0; i < 8; ++i) x[i] = x[i] * r;
+}
+
+// The same rotation for a head vector of 16 N channels spread over 16 lanes,
+// N per lane (lane L holds channels N L + i): stage widths 1 .. N/2 inside a
+// lane, then N .. 8 N across lanes, then one multiply by fl32(1/sqrt(16 N)).
+// wht_x<8> is wht128_x8.
+template <int N>
+__device__ __forceinline__ void wht_x(float (&x)[N], int L) {
+#pragma clang fp contract(off)
+#pragma unroll
+    for (int h = 1; h < N; h <<= 1) {
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            if (i & h) continue;
+            float a = x[i], b = x[i + h];
+            x[i] = a + b;
+            x[i + h] = a - b;
+        }
+    }
+#pragma unroll
+    for (int s = 1; s < 16; s <<= 1) {
+        const bool upper = (L & s) != 0;
+#pragma unroll
+        for (int i = 0; i < N; ++i) {
+            float o = __shfl_xor(x[i], s, 16);
+            x[i] = upper ? (o - x[i]) : (x[i] + o);
+        }
+    }
+    const float r = inv_sqrt_d<16 * N>();
+#pragma unroll
+    for (int i = 0; i < N; ++i) x[i] = x[i] * r;
 }
 
 // E = round(log2(fl32(c * m))), nearest integer in the log domain: the
@@ -128,6 +164,27 @@ __device__ __forceinline__ uint32_t e4m3_byte(float x) {
 
 // Eight consecutive channels starting at element `elem` as fp32 (DT: 0 f32,
 // 1 bf16, 2 f16; 16-byte aligned).
+template <int DT>
+__device__ __forceinline__ void load_x4(const void* base, int64_t elem, float (&x)[4]) {
+    if constexpr (DT == 0) {
+        const float4 a = *reinterpret_cast<const float4*>(static_cast<const float*>(base) + elem);
+        x[0] = a.x; x[1] = a.y; x[2] = a.z; x[3] = a.w;
+    } else {
+        const uint2 w = *reinterpret_cast<const uint2*>(static_cast<const uint16_t*>(base) + elem);
+        const uint32_t d[2] = {w.x, w.y};
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            if constexpr (DT == 1) {
+                x[2 * i] = bits_f32(d[i] << 16);
+                x[2 * i + 1] = bits_f32(d[i] & 0xFFFF0000u);
+            } else {
+                x[2 * i] = float(__builtin_bit_cast(_Float16, uint16_t(d[i] & 0xFFFFu)));
+                x[2 * i + 1] = float(__builtin_bit_cast(_Float16, uint16_t(d[i] >> 16)));
+            }
+        }
+    }
+}
+
 template <int DT>
 __device__ __forceinline__ void load_x8(const void* base, int64_t elem, float (&x)[8]) {
     if constexpr (DT == 0) {  // f32

@@ -9,7 +9,8 @@ namespace uq {
 
 // Cache formats of the decode kernel template: the FP4 cache of this library
 // and the two plain comparison caches.
-enum KvFmt : int32_t { kFp4 = 0, kFp8 = 1, kBf16 = 2, kTq4 = 3 };
+// kFp4d64 / kFp4d256: the FP4 cache at head sizes 64 and 256 (kFp4 is 128).
+enum KvFmt : int32_t { kFp4 = 0, kFp8 = 1, kBf16 = 2, kTq4 = 3, kFp4d64 = 4, kFp4d256 = 5 };
 
 // Tables of the Ultra-TQ key codebook, built on the host from the 16 levels
 // rounded to BF16: the encoder's midpoints and the decoder's byte lookup
@@ -37,6 +38,7 @@ struct QuantizeParams {
     int32_t rotate_v;
     uint8_t* codes;
     uint8_t* scales;
+    int32_t head_dim;          // 64, 128 or 256
 };
 
 struct RefWriteParams {
@@ -88,6 +90,7 @@ struct DecodeParams {
     void* out;                 // [B][Hq][128]
     int32_t out_dtype;         // 0 f32, 1 bf16
     int32_t rotate_v;
+    int32_t head_dim;          // 64, 128 or 256 (FP4 cache; the others are 128)
     TqTables tq;               // Ultra-TQ cache only
     // cascade decode over a shared prefix (prefix_pages == nullptr: off).
     // Partial slots per (sequence, query head): the suffix_partitions of the

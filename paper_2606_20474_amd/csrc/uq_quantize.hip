@@ -21,20 +21,22 @@ __device__ __forceinline__ float quad_xor(float x) {
     return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), ctrl, 0xF, 0xF, true));
 }
 
-// The rotation of one 128-vector held by 4 lanes of a quad: lane L holds
-// channels 32j + 8L + i in x[j][i] (j = 0..3, i = 0..7).  The stages run in
-// the order of the format (widths 1, 2, 4, 8, 16, 32, 64): 1, 2, 4 inside a
-// lane over i, 8 and 16 across lanes L^1, L^2, 32 and 64 inside a lane over
-// j; each maps (a, b) to (a + b, a - b) in fp32 (the upper element of a
-// cross-lane pair takes fma(-1, b, a) = a - b, exactly rounded), then one
-// multiply by fl32(1/sqrt(128)).  The values equal those of wht128_x8
-// bit for bit.
-__device__ __forceinline__ void wht128_x32(float (&x)[4][8], int L) {
+// The rotation of one head vector of D = 32 NG channels held by 4 lanes of
+// a quad: lane L holds channels 32j + 8L + i in x[j][i] (j < NG, i < 8).
+// The stages run in the order of the format (widths 1, 2, 4, ..., D/2): 1,
+// 2, 4 inside a lane over i, 8 and 16 across lanes L^1, L^2, then 32, 64
+// (and 128 for D = 256) inside a lane over j; each maps (a, b) to
+// (a + b, a - b) in fp32 (the upper element of a cross-lane pair takes
+// fma(-1, b, a) = a - b, exactly rounded), then one multiply by
+// fl32(1/sqrt(D)).  The values equal those of the 16-lane form wht_x bit
+// for bit.
+template <int NG>
+__device__ __forceinline__ void wht_quad(float (&x)[NG][8], int L) {
 #pragma clang fp contract(off)
 #pragma unroll
     for (int h = 1; h < 8; h <<= 1) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < NG; ++j) {
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
                 if (i & h) continue;
@@ -47,17 +49,17 @@ __device__ __forceinline__ void wht128_x32(float (&x)[4][8], int L) {
     const float s1 = (L & 1) ? -1.0f : 1.0f;
     const float s2 = (L & 2) ? -1.0f : 1.0f;
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < NG; ++j)
 #pragma unroll
         for (int i = 0; i < 8; ++i) x[j][i] = __builtin_fmaf(s1, x[j][i], quad_xor<1>(x[j][i]));
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < NG; ++j)
 #pragma unroll
         for (int i = 0; i < 8; ++i) x[j][i] = __builtin_fmaf(s2, x[j][i], quad_xor<2>(x[j][i]));
 #pragma unroll
-    for (int h = 1; h < 4; h <<= 1) {
+    for (int h = 1; h < NG; h <<= 1) {
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
+        for (int j = 0; j < NG; ++j) {
             if (j & h) continue;
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
@@ -67,24 +69,27 @@ __device__ __forceinline__ void wht128_x32(float (&x)[4][8], int L) {
             }
         }
     }
-    const float r = inv_sqrt128();
+    const float r = inv_sqrt_d<32 * NG>();
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < NG; ++j)
 #pragma unroll
         for (int i = 0; i < 8; ++i) x[j][i] = x[j][i] * r;
 }
 
-// Quantise one 128-vector held by a quad (rotated first if `rotate`): per
+__device__ __forceinline__ void wht128_x32(float (&x)[4][8], int L) { wht_quad<4>(x, L); }
+
+// Quantise one head vector held by a quad (rotated first if `rotate`): per
 // 32-channel group j the UE8M0 exponent E_j of the group maximum, and the
 // E2M1 codes of the lane's 8 channels of the group in w[j] (channel order,
 // low nibble first) by the hardware conversion, which rounds x / 2^E_j to
 // the nearest E2M1 level with ties to the even code, saturates at 6 and
 // keeps the sign: the same codes as e2m1_code.
-__device__ __forceinline__ void quantize_x32(float (&x)[4][8], int L, float c, bool rotate, uint32_t (&w)[4],
-                                             int (&E)[4]) {
-    if (rotate) wht128_x32(x, L);
+template <int NG>
+__device__ __forceinline__ void quantize_xq(float (&x)[NG][8], int L, float c, bool rotate, uint32_t (&w)[NG],
+                                            int (&E)[NG]) {
+    if (rotate) wht_quad<NG>(x, L);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < NG; ++j) {
         float m = 0.0f;
 #pragma unroll
         for (int i = 0; i < 8; ++i) m = __builtin_fmaxf(m, __builtin_fabsf(x[j][i]));
@@ -101,14 +106,26 @@ __device__ __forceinline__ void quantize_x32(float (&x)[4][8], int L, float c, b
     }
 }
 
-// Quantize-on-write, 4 lanes (one quad) per (token, kv head) vector, 64
-// vectors per 256-thread block.  Lane L loads and keeps channels
-// 32j + 8L + i (16-byte loads, a quad covers 64 contiguous bytes per j), so
-// the two cross-lane stages of the rotation and the group maxima are DPP
-// quad permutes.  Stores: one codes dword per group for K and V, and the
-// scale bytes of group L for K and V.
-template <int DT>
+// Element j of a small register array at a lane-dependent index, by selects
+// (a dynamic index would put the array in scratch memory).
+template <int NG>
+__device__ __forceinline__ int pick(const int (&e)[NG], int j) {
+    int r = e[0];
+#pragma unroll
+    for (int k = 1; k < NG; ++k) r = j == k ? e[k] : r;
+    return r;
+}
+
+// Quantize-on-write, 4 lanes (one quad) per (token, kv head) vector of
+// D = 32 NG channels, 64 vectors per 256-thread block.  Lane L loads and
+// keeps channels 32j + 8L + i (16-byte loads, a quad covers 64 contiguous
+// bytes per j), so the two cross-lane stages of the rotation and the group
+// maxima are DPP quad permutes.  Stores: one codes dword per group for K and
+// V, and the scale bytes of groups L, L + 4, ... for K and V.  Tiles are
+// 8 D code bytes and D/2 scale bytes per (page, head, K|V).
+template <int DT, int NG>
 __global__ void __launch_bounds__(256) quantize_kv_kernel(QuantizeParams p) {
+    constexpr int D = 32 * NG;
     const int L = threadIdx.x & 3;
     const int64_t vec = int64_t(blockIdx.x) * 64 + (threadIdx.x >> 2);
     const int64_t nvec = p.num_tokens * p.num_kv_heads;
@@ -133,34 +150,38 @@ __global__ void __launch_bounds__(256) quantize_kv_kernel(QuantizeParams p) {
     }
     if (page < 0 || page >= p.num_pages) return;
 
-    const int64_t row = t * p.token_stride + int64_t(h) * kHeadDim + 8 * L;
-    float xk[4][8], xv[4][8];
+    const int64_t row = t * p.token_stride + int64_t(h) * D + 8 * L;
+    float xk[NG][8], xv[NG][8];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < NG; ++j) {
         load_x8<DT>(p.k, row + 32 * j, xk[j]);
         load_x8<DT>(p.v, row + 32 * j, xv[j]);
     }
-    uint32_t wk[4], wv[4];
-    int ek[4], ev[4];
-    quantize_x32(xk, L, p.c, true, wk, ek);
-    quantize_x32(xv, L, p.c, p.rotate_v != 0, wv, ev);
+    uint32_t wk[NG], wv[NG];
+    int ek[NG], ev[NG];
+    quantize_xq<NG>(xk, L, p.c, true, wk, ek);
+    quantize_xq<NG>(xv, L, p.c, p.rotate_v != 0, wv, ev);
 
-    const int64_t tile = (page * p.num_kv_heads + h) * 2;
-    uint8_t* kc = p.codes + tile * kTileCodes;
-    uint8_t* vc = kc + kTileCodes;
+    const int64_t ph = page * p.num_kv_heads + h;
+    uint8_t* kc = p.codes + ph * (16 * D);
+    uint8_t* vc = kc + 8 * D;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
+    for (int j = 0; j < NG; ++j) {
         // K tile [group][token][16 B]: channels 32j+8L.. are bytes 4L..4L+3 of the row
         *reinterpret_cast<uint32_t*>(kc + (j * kPage + off) * 16 + 4 * L) = wk[j];
         // V tile [token/4][channel/8][token%4][4 B]: channel block 4j+L
-        *reinterpret_cast<uint32_t*>(vc + ((off >> 2) * 16 + 4 * j + L) * 16 + (off & 3) * 4) = wv[j];
+        *reinterpret_cast<uint32_t*>(vc + ((off >> 2) * (D / 8) + 4 * j + L) * 16 + (off & 3) * 4) = wv[j];
     }
-    // scale bytes [K|V][group][token]: lane L writes group L
-    const int eks = L == 0 ? ek[0] : L == 1 ? ek[1] : L == 2 ? ek[2] : ek[3];
-    const int evs = L == 0 ? ev[0] : L == 1 ? ev[1] : L == 2 ? ev[2] : ev[3];
-    uint8_t* ks = p.scales + tile * kTileScales;
-    ks[L * kPage + off] = uint8_t(eks + 127);
-    ks[kTileScales + L * kPage + off] = uint8_t(evs + 127);
+    // scale bytes [K|V][group][token]: lane L writes groups L, L + 4, ...
+    uint8_t* ks = p.scales + ph * D;
+#pragma unroll
+    for (int q = 0; q < (NG + 3) / 4; ++q) {
+        const int j = L + 4 * q;
+        if (j < NG) {
+            ks[j * kPage + off] = uint8_t(pick<NG>(ek, j) + 127);
+            ks[D / 2 + j * kPage + off] = uint8_t(pick<NG>(ev, j) + 127);
+        }
+    }
 }
 
 // Round-trip error of the FP4 encoder for a list of constants c, the
@@ -307,15 +328,23 @@ __global__ void __launch_bounds__(256) prepare_query_kernel(const void* q, int64
     *reinterpret_cast<uint2*>(q8 + row * kHeadDim + 8 * lane16) = make_uint2(lo, hi);
 }
 
+template <int NG>
+static void launch_quantize_ng(const QuantizeParams& p, int dtype, const dim3& grid, hipStream_t stream) {
+    const dim3 block{256u};
+    if (dtype == 0) hipLaunchKernelGGL((quantize_kv_kernel<0, NG>), grid, block, 0, stream, p);
+    else if (dtype == 1) hipLaunchKernelGGL((quantize_kv_kernel<1, NG>), grid, block, 0, stream, p);
+    else hipLaunchKernelGGL((quantize_kv_kernel<2, NG>), grid, block, 0, stream, p);
+}
+
 hipError_t launch_quantize_kv(const QuantizeParams& p, int dtype, hipStream_t stream) {
     const int64_t nvec = p.num_tokens * p.num_kv_heads;
     const int64_t blocks = (nvec + 63) / 64;   // 64 quads per block
     if (blocks == 0) return hipSuccess;
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
-    const dim3 grid{unsigned(blocks)}, block{256u};
-    if (dtype == 0) hipLaunchKernelGGL(quantize_kv_kernel<0>, grid, block, 0, stream, p);
-    else if (dtype == 1) hipLaunchKernelGGL(quantize_kv_kernel<1>, grid, block, 0, stream, p);
-    else hipLaunchKernelGGL(quantize_kv_kernel<2>, grid, block, 0, stream, p);
+    const dim3 grid{unsigned(blocks)};
+    if (p.head_dim == 64) launch_quantize_ng<2>(p, dtype, grid, stream);
+    else if (p.head_dim == 256) launch_quantize_ng<8>(p, dtype, grid, stream);
+    else launch_quantize_ng<4>(p, dtype, grid, stream);
     return hipGetLastError();
 }
 

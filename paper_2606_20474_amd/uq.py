@@ -172,7 +172,8 @@ _DT = {torch.float32: UQ_F32, torch.bfloat16: UQ_BF16, torch.float16: UQ_F16, to
 
 @dataclass
 class CacheDesc:
-    """Python mirror of ``uq_cache_desc``."""
+    """Python mirror of ``uq_cache_desc`` (head_dim 64, 128 or 256; the step,
+    cascade and FP8-query calls take 128 only)."""
     num_kv_heads: int
     num_pages: int
     c: float = 0.156
@@ -186,10 +187,10 @@ class CacheDesc:
                              self.c, int(bool(self.rotate_v)))
 
     def codes_bytes(self):
-        return self.num_pages * self.num_kv_heads * 2 * TILE_CODES
+        return self.num_pages * self.num_kv_heads * 2 * 8 * self.head_dim
 
     def scales_bytes(self):
-        return self.num_pages * self.num_kv_heads * 2 * TILE_SCALES
+        return self.num_pages * self.num_kv_heads * 2 * (self.head_dim // 2)
 
     def alloc_pools(self, device="cuda", fill=None):
         codes = torch.empty(self.codes_bytes(), dtype=torch.uint8, device=device)
@@ -262,11 +263,11 @@ def decode_attention(desc: CacheDesc, q, codes, scales, page_table, context_lens
     """q: [B, Hq, 128] -> out [B, Hq, 128]."""
     B, Hq = q.shape[0], q.shape[1]
     if softmax_scale is None:
-        softmax_scale = HEAD_DIM ** -0.5
+        softmax_scale = desc.head_dim ** -0.5
     if workspace is None:
         workspace = alloc_workspace(desc, B, Hq, max_context, partition_tokens, q.device)
     if out is None:
-        out = torch.empty((B, Hq, HEAD_DIM), dtype=out_dtype, device=q.device)
+        out = torch.empty((B, Hq, desc.head_dim), dtype=out_dtype, device=q.device)
     d = desc.c_struct()
     qdt = _DT[q.dtype] if q_dtype is None else q_dtype
     st = lib.uq_decode_attention(ctypes.byref(d), _ptr(q), qdt, B, Hq, _ptr(codes), _ptr(scales), _ptr(page_table),
@@ -297,11 +298,11 @@ def decode_step(desc: CacheDesc, q, k_new, v_new, codes, scales, page_table, con
     last position, then decode attention; q: [B, Hq, 128] -> out."""
     B, Hq = q.shape[0], q.shape[1]
     if softmax_scale is None:
-        softmax_scale = HEAD_DIM ** -0.5
+        softmax_scale = desc.head_dim ** -0.5
     if workspace is None:
         workspace = alloc_workspace(desc, B, Hq, max_context, partition_tokens, q.device)
     if out is None:
-        out = torch.empty((B, Hq, HEAD_DIM), dtype=out_dtype, device=q.device)
+        out = torch.empty((B, Hq, desc.head_dim), dtype=out_dtype, device=q.device)
     d = desc.c_struct()
     qdt = _DT[q.dtype] if q_dtype is None else q_dtype
     fn = lib.uq_decode_step_partials if partials_only else lib.uq_decode_step

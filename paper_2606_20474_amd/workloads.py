@@ -55,7 +55,8 @@ class DecodeWorkload:
     rotate_v: bool = True
     k_outliers: np.ndarray = field(default=None)   # int64 [Hkv, 4]
     v_outliers: np.ndarray = field(default=None)
-    q: torch.Tensor = field(default=None)          # fp32 [B, Hq, 128] on the CPU
+    q: torch.Tensor = field(default=None)          # fp32 [B, Hq, head_dim] on the CPU
+    head_dim: int = HEAD_DIM
 
     @property
     def max_context(self) -> int:
@@ -73,8 +74,9 @@ class DecodeWorkload:
         return int(self.context_lens.astype(np.int64).sum())
 
     def kv_bytes_fp4(self) -> int:
-        """Logical KV bytes one decode step reads: 136 B per token and kv head."""
-        return self.total_tokens() * self.num_kv_heads * 136
+        """Logical KV bytes one decode step reads: 17 B per 32 channels of K
+        and of V per token and kv head (136 B at head size 128)."""
+        return self.total_tokens() * self.num_kv_heads * 17 * self.head_dim // 16
 
     # -- bulk data ---------------------------------------------------------
     def segments(self):
@@ -125,7 +127,7 @@ class DecodeWorkload:
         return pages * PAGE + pos % PAGE
 
     def kv(self, key: int, lo: int, hi: int, device="cpu", dtype=torch.float32):
-        """K, V [hi-lo, Hkv, 128] of one segment, regenerated from its own
+        """K, V [hi-lo, Hkv, head_dim] of one segment, regenerated from its own
         seed.  A sequence's stream (key >= 0) starts at the segment; the
         shared prefix (key -1) is always drawn whole and then sliced, so any
         part of it can be regenerated (a generator's leading values depend
@@ -137,8 +139,8 @@ class DecodeWorkload:
             n, skip = self.shared_prefix_tokens, lo
         else:
             n, skip = hi - lo, 0
-        k = torch.randn((n, self.num_kv_heads, HEAD_DIM), generator=g, device=device, dtype=torch.float32)
-        v = torch.randn((n, self.num_kv_heads, HEAD_DIM), generator=g, device=device, dtype=torch.float32)
+        k = torch.randn((n, self.num_kv_heads, self.head_dim), generator=g, device=device, dtype=torch.float32)
+        v = torch.randn((n, self.num_kv_heads, self.head_dim), generator=g, device=device, dtype=torch.float32)
         k, v = k[skip:skip + hi - lo], v[skip:skip + hi - lo]
         for h in range(self.num_kv_heads):
             k[:, h, torch.as_tensor(self.k_outliers[h], device=device)] *= OUTLIER_GAIN
@@ -147,15 +149,17 @@ class DecodeWorkload:
 
 
 def _meta(gen: torch.Generator, wl: DecodeWorkload):
-    wl.k_outliers = np.stack([torch.randperm(HEAD_DIM, generator=gen)[:OUTLIERS].numpy() for _ in range(wl.num_kv_heads)])
-    wl.v_outliers = np.stack([torch.randperm(HEAD_DIM, generator=gen)[:OUTLIERS].numpy() for _ in range(wl.num_kv_heads)])
-    wl.q = torch.randn((wl.batch, wl.num_q_heads, HEAD_DIM), generator=gen, dtype=torch.float32)
+    d = wl.head_dim
+    wl.k_outliers = np.stack([torch.randperm(d, generator=gen)[:OUTLIERS].numpy() for _ in range(wl.num_kv_heads)])
+    wl.v_outliers = np.stack([torch.randperm(d, generator=gen)[:OUTLIERS].numpy() for _ in range(wl.num_kv_heads)])
+    wl.q = torch.randn((wl.batch, wl.num_q_heads, d), generator=gen, dtype=torch.float32)
     return wl
 
 
 def custom(batch, num_q_heads, num_kv_heads, context_lens, seed=0, paging="random", spare_pages=3,
-           shared_prefix_tokens=0, partition_tokens=0, rotate_v=True, name="custom") -> DecodeWorkload:
-    """A decode workload of any shape: paging 'identity' or 'random'."""
+           shared_prefix_tokens=0, partition_tokens=0, rotate_v=True, name="custom", head_dim=HEAD_DIM) -> DecodeWorkload:
+    """A decode workload of any shape (head_dim 64, 128 or 256): paging
+    'identity' or 'random'."""
     ctx = np.asarray(context_lens, dtype=np.int32).reshape(batch)
     gen = torch.Generator().manual_seed(seed)
     pages_per = [(int(c) + PAGE - 1) // PAGE for c in ctx]
@@ -185,7 +189,7 @@ def custom(batch, num_q_heads, num_kv_heads, context_lens, seed=0, paging="rando
     wl = DecodeWorkload(name, batch, num_q_heads, num_kv_heads, ctx, pt, num_pages, seed,
                         shared_prefix_tokens=shared_prefix_tokens, partition_tokens=partition_tokens,
                         rotate_v=rotate_v, private_tail=tail if tail.any() else None,
-                        prefix_pages=np.asarray(perm[:shared], dtype=np.int64))
+                        prefix_pages=np.asarray(perm[:shared], dtype=np.int64), head_dim=head_dim)
     return _meta(gen, wl)
 
 
@@ -267,3 +271,12 @@ def key_rows(n: int, seed: int = 0) -> np.ndarray:
     k = rng.standard_normal((n, HEAD_DIM))
     k[:, rng.permutation(HEAD_DIM)[:OUTLIERS]] *= OUTLIER_GAIN
     return k.astype(np.float32)
+
+
+def gpt_oss_like(head_dim: int = 64) -> DecodeWorkload:
+    """A head-size-64 attention layer shaped like GPT-OSS-20B's (the model of
+    the paper's per-block ablation): 64 query heads, 8 KV heads, batch 32,
+    every context 32768, random pages; seed 5.  head_dim 256 gives the same
+    shape at head size 256 (seed 6)."""
+    return custom(32, 64, 8, [32768] * 32, seed=5 if head_dim == 64 else 6, paging="random", spare_pages=0,
+                  name=f"gpt-oss-like-hd{head_dim}-b32-ctx32k", head_dim=head_dim)

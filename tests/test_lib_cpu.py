@@ -58,7 +58,7 @@ def quantize(uq, d, num_tokens=4, stride=256, k=FAKE, pt=None, num_seqs=0, mpps=
 def test_quantize_validation(uq):
     E = uq
     assert quantize(uq, None) == E.UQ_ERR_INVALID_ARGUMENT
-    assert quantize(uq, desc(head_dim=64)) == E.UQ_ERR_UNSUPPORTED
+    assert quantize(uq, desc(head_dim=96)) == E.UQ_ERR_UNSUPPORTED
     assert quantize(uq, desc(page_size=32)) == E.UQ_ERR_UNSUPPORTED
     assert quantize(uq, desc(group_size=16)) == E.UQ_ERR_UNSUPPORTED
     assert quantize(uq, desc(c=0.0)) == E.UQ_ERR_INVALID_ARGUMENT
@@ -86,7 +86,7 @@ def decode(uq, d, q=FAKE, qdt=0, B=2, Hq=4, mpps=4, maxctx=64, scale=0.1, part=0
 def test_decode_validation(uq):
     E = uq
     assert decode(uq, None) == E.UQ_ERR_INVALID_ARGUMENT
-    assert decode(uq, desc(head_dim=256)) == E.UQ_ERR_UNSUPPORTED
+    assert decode(uq, desc(head_dim=96)) == E.UQ_ERR_UNSUPPORTED
     assert decode(uq, desc(), Hq=3) == E.UQ_ERR_INVALID_ARGUMENT               # Hq % Hkv
     assert decode(uq, desc(), Hq=34) == E.UQ_ERR_UNSUPPORTED                   # 17 query heads per kv head
     assert decode(uq, desc(), B=0) == E.UQ_ERR_INVALID_ARGUMENT
@@ -292,3 +292,30 @@ def test_tq4_codebook_validation(uq):
         assert lib.uq_ref_write_kv(ctypes.byref(d), FAKE, FAKE, 1, 4, 256, None, 0, 0, FAKE, FAKE, None) == \
             E.UQ_ERR_INVALID_ARGUMENT
     assert uq.RefCacheDesc(2, 10, "tq4").cache_bytes() == 10 * 2 * 2368
+
+
+def test_head_sizes_64_and_256(uq):
+    """Head sizes 64 and 256 pass validation for write and decode; the
+    decode step, cascade, the FP8-query form and uq_prepare_query are
+    head-size-128 calls (UNSUPPORTED otherwise).  Workspace rows hold d + 2
+    floats."""
+    E = uq
+    lib = uq.lib
+    for d in (64, 256):
+        # validation passes, then the launch fails for want of a GPU
+        assert quantize(uq, desc(head_dim=d), stride=2 * d) == E.UQ_ERR_HIP
+        assert quantize(uq, desc(head_dim=d), stride=2 * d - 8) == E.UQ_ERR_INVALID_ARGUMENT
+        assert decode(uq, desc(head_dim=d)) == E.UQ_ERR_HIP
+        assert decode(uq, desc(head_dim=d), qdt=3) == E.UQ_ERR_UNSUPPORTED
+        assert lib.uq_prepare_query(ctypes.byref(desc(head_dim=d)), FAKE, 0, 4, FAKE, None) == E.UQ_ERR_UNSUPPORTED
+        dd = desc(head_dim=d)
+        w = lib.uq_decode_workspace_bytes(ctypes.byref(dd), 2, 4, 64, 32)
+        w128 = lib.uq_decode_workspace_bytes(ctypes.byref(desc()), 2, 4, 64, 32)
+        assert w == 2 * 4 * 2 * (d + 2) * 4 and w128 == 2 * 4 * 2 * 130 * 4
+        from paper_2606_20474_amd.uq import uq_shared_prefix
+        sp = uq_shared_prefix(0x10000, 0x10000, 64, 0)
+        r = lib.uq_decode_cascade(ctypes.byref(dd), FAKE, 0, None, None, 0, 2, 4, FAKE, FAKE, FAKE, 4, FAKE, 64,
+                                  ctypes.byref(sp), 0.1, 0, FAKE, 1 << 30, FAKE, 0, None)
+        assert r == E.UQ_ERR_UNSUPPORTED
+    cd = uq.CacheDesc(num_kv_heads=2, num_pages=10, head_dim=64)
+    assert cd.codes_bytes() == 10 * 2 * 2 * 512 and cd.scales_bytes() == 10 * 2 * 2 * 32
