@@ -137,6 +137,7 @@ def timed(step, steps, warmup, stream):
     """Run `warmup` untimed steps, then `steps` timed ones; returns (ms per
     step over the whole timed region, mean ms of the decode launch between
     the events each step records)."""
+    import gc
     import torch
     for _ in range(warmup):
         step()
@@ -145,11 +146,18 @@ def timed(step, steps, warmup, stream):
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    t_start.record(stream)
-    for i in range(steps):
-        step(*evs[i])
-    t_end.record(stream)
-    torch.cuda.synchronize()
+    # no Python garbage collection while launching: a collection pause on the
+    # host leaves the GPU idle between launches and inflates the event times
+    gc.collect()
+    gc.disable()
+    try:
+        t_start.record(stream)
+        for i in range(steps):
+            step(*evs[i])
+        t_end.record(stream)
+        torch.cuda.synchronize()
+    finally:
+        gc.enable()
     return t_start.elapsed_time(t_end) / steps, float(np.mean([a.elapsed_time(b) for a, b in evs]))
 
 
