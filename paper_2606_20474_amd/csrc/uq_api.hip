@@ -38,7 +38,7 @@ int32_t pick_partition(int32_t batch, int32_t num_kv_heads, int32_t max_context)
     // blocks; between 1024 and 16384 tokens.
     const int64_t heads = int64_t(batch) * num_kv_heads;
     int32_t part = 16384;
-    while (part > 1024 && heads * ((int64_t(max_context) + part - 1) / part) < 512) part /= 2;
+    while (part > 1024 && heads * ((int64_t(max_context) + part - 1) / part) < 2 * uq::kNumCus) part /= 2;
     return part;
 }
 

@@ -25,11 +25,13 @@
 //             the whole partition (the query is hoisted out of the K-tile
 //             loop).
 //   loop      each wave takes pairs of pages (32 tokens) round-robin and
-//             stages them through its own 2-slot LDS ring with
+//             stages them through its own S-slot LDS ring (S = 2) with
 //             global_load_lds_dwordx4 (16 bytes per lane, 1 KiB per
-//             instruction); a slot is refilled with the pair two iterations
-//             ahead as soon as it has been read into registers, so two pairs
-//             per wave are in flight while one is computed.
+//             instruction); a slot is refilled with the pair S iterations
+//             ahead as soon as it has been read into registers, so S pairs
+//             per wave are in flight while one is computed.  The next 64
+//             page ids are copied into LDS the same way, so the wave never
+//             waits on a register load while pages are in flight.
 //             QK^T: FP4 -- one v_mfma_scale_f32_16x16x128_f8f6f4 per page,
 //             the FP4 K tile as operand A (rows = tokens) with its UE8M0
 //             bytes as the A scales and the FP8 query as operand B (columns
@@ -113,7 +115,23 @@ template <> struct Fmt<kTq4> {
 
 // One stage of the ring: [K page0][V page0][K page1][V page1][scales0][scales1].
 template <int F> constexpr int stage_bytes() { return 4 * Fmt<F>::kTile + 2 * Fmt<F>::kScaleBlock; }
-template <int F> constexpr int ring_bytes() { return 2 * stage_bytes<F>(); }
+template <int F, int S> constexpr int ring_bytes() { return S * stage_bytes<F>(); }
+// LDS of one block besides the rings and id slots: the query operand and
+// the merge's (max, sum).
+template <int F> constexpr int q_lds_bytes() {
+    return (F == kBf16 || F == kTq4) ? 4 * 64 * 16 : (head_dim_of<F>() / 128 + (head_dim_of<F>() < 128)) * 64 * 32;
+}
+constexpr int kIdsSlot = 256;   // LDS bytes per wave for the next 64 page ids
+template <int F, int S> constexpr int block_lds_bytes() {
+    return Fmt<F>::kWaves * (ring_bytes<F, S>() + kIdsSlot) + q_lds_bytes<F>() + 2 * Fmt<F>::kWaves * 16 * 4;
+}
+// Waves per SIMD with an S-slot ring: what 160 KiB of LDS per CU holds,
+// capped by the format's register-set budget.
+template <int F, int S> constexpr int occupancy() {
+    constexpr int blocks = (160 * 1024) / block_lds_bytes<F, S>();
+    constexpr int waves = blocks * Fmt<F>::kWaves / 4;
+    return waves < 1 ? 1 : (waves < Fmt<F>::kOccupancy ? waves : Fmt<F>::kOccupancy);
+}
 template <int F> constexpr int dma_per_stage() { return 4 * Fmt<F>::kTile / 1024 + (Fmt<F>::kScaleBlock ? 1 : 0); }
 
 // Exchange with the lane 16 (or 32) positions away: after
@@ -170,21 +188,46 @@ __device__ __forceinline__ void split_p(float a, float b, uint32_t& hi, uint32_t
     lo = pack_bf16x2(a - bits_f32(ua & 0xFFFF0000u), b - bits_f32(ub & 0xFFFF0000u));
 }
 
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
 // Page ids of one wave, 64 at a time: lane j holds the id of the wave's
 // page 2*(32*chunk + j/2) + j%2 counted in its own iteration order
-// (iteration k of wave w covers partition pages 2*(w + W*k) and +1).
+// (iteration k of wave w covers partition pages 2*(w + W*k) and +1).  The
+// range check (clamp_ids) follows once the ids are in registers.
+template <int W>
+__device__ __forceinline__ int ids_page(int wave, int chunk, int lane) {
+    return 2 * (wave + W * (32 * chunk + (lane >> 1))) + (lane & 1);
+}
 template <int W>
 __device__ __forceinline__ int32_t load_page_ids(const int32_t* __restrict__ pt_row, int first_page, int n_pages,
-                                                 int wave, int chunk, int lane, int64_t num_pages) {
-    const int k = 32 * chunk + (lane >> 1);
-    const int pg = 2 * (wave + W * k) + (lane & 1);
+                                                 int wave, int chunk, int lane) {
+    const int pg = ids_page<W>(wave, chunk, lane);
     int32_t id = 0;
     if (pg < n_pages) id = pt_row[first_page + pg];
-    if (id < 0 || int64_t(id) >= num_pages) id = 0;   // out-of-range ids never leave the pools
     return id;
 }
+// The same ids copied into the wave's LDS slot (lane j's id at dword j)
+// with global_load_lds_dword, so that no register waits for them: loading
+// them into registers would make the wave wait for this load, and with it
+// for every page copy in flight, when their values are first used.  Lanes
+// past the partition read its first entry (their ids are never used).
+template <int W>
+__device__ __forceinline__ void copy_page_ids(uint8_t* slot, const int32_t* __restrict__ pt_row, int first_page,
+                                              int n_pages, int wave, int chunk, int lane) {
+    const int pg = ids_page<W>(wave, chunk, lane);
+    __builtin_amdgcn_global_load_lds(pt_row + first_page + (pg < n_pages ? pg : 0), (lds_ptr_t)slot, 4, 0, 0);
+}
+// This lane's id from the wave's LDS slot; the caller has waited for the copy.
+__device__ __forceinline__ int32_t read_page_ids(uint32_t slot_addr, int lane) {
+    int32_t v;
+    asm volatile("ds_read_b32 %0, %1\n\ts_waitcnt lgkmcnt(0)" : "=v"(v) : "v"(slot_addr + 4 * lane) : "memory");
+    return v;
+}
 
-typedef __attribute__((address_space(3))) void* lds_ptr_t;
+// Out-of-range ids never leave the pools.
+__device__ __forceinline__ int32_t clamp_ids(int32_t id, int64_t num_pages) {
+    return (id < 0 || int64_t(id) >= num_pages) ? 0 : id;
+}
 
 // Asynchronous copy of one iteration (two pages of one kv head) from HBM
 // into an LDS stage with global_load_lds_dwordx4: every lane moves 16 bytes
@@ -664,9 +707,10 @@ __device__ __forceinline__ void zero_token(StageRegs<kTq4>& c, int pg, int t) {
     else m.w = 0u;
 }
 
-template <int F>
+template <int F, int S>
 __global__ void __launch_bounds__(64 * Fmt<F>::kWaves)
-__attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) decode_kernel(DecodeParams p) {
+__attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decode_kernel(DecodeParams p) {
+    static_assert(S == 2 || S == 4, "ring slots");
     constexpr int W = Fmt<F>::kWaves;
     constexpr int kThreads = 64 * W;
     constexpr int kStage = stage_bytes<F>();
@@ -760,8 +804,9 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
     const bool append = D == 128 && !pre && p.k_new != nullptr && pos_new >= start && wave == it_new % W;
     const int k_new_local = it_new / W;                              // that wave's local iteration
 
-    __shared__ __attribute__((aligned(16))) uint8_t smem[W * ring_bytes<F>()];
-    __shared__ __attribute__((aligned(16))) uint8_t q_lds[(F == kBf16 || F == kTq4) ? 4 * 64 * 16 : (D / 128 + (D < 128)) * 64 * 32];
+    __shared__ __attribute__((aligned(16))) uint8_t smem[W * ring_bytes<F, S>()];
+    __shared__ __attribute__((aligned(16))) uint8_t q_lds[q_lds_bytes<F>()];
+    __shared__ __attribute__((aligned(16))) uint8_t ids_lds[W * kIdsSlot];
     __shared__ float red_m[W][16];
     __shared__ float red_l[W][16];
 
@@ -859,22 +904,25 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
     }
     const int g4 = lane >> 4;           // lane group: tokens 4*g4..4*g4+3 of each page
     const int n = lane & 15;
-    uint8_t* ring = smem + wave * ring_bytes<F>();
+    uint8_t* ring = smem + wave * ring_bytes<F, S>();
     const uint32_t ring_addr = uint32_t(reinterpret_cast<uintptr_t>((lds_ptr_t)ring));
     const int64_t head_tile = int64_t(hk) * 2;
     const int64_t tiles_per_page = int64_t(p.num_kv_heads) * 2;
 
-    int32_t ids = 0, ids_next = 0;
+    uint8_t* ids_slot = ids_lds + wave * kIdsSlot;
+    const uint32_t ids_addr = uint32_t(reinterpret_cast<uintptr_t>((lds_ptr_t)ids_slot));
+    int32_t ids = 0;
     if (n_local > 0) {
-        ids = load_page_ids<W>(pt_row, first_page, n_pages, wave, 0, lane, p.num_pages);
-        if (n_local > 32) ids_next = load_page_ids<W>(pt_row, first_page, n_pages, wave, 1, lane, p.num_pages);
+        ids = load_page_ids<W>(pt_row, first_page, n_pages, wave, 0, lane);
+        if (n_local > 32) copy_page_ids<W>(ids_slot, pt_row, first_page, n_pages, wave, 1, lane);
     }
     // The query, the new token and the page ids are in registers before the
     // first page copies are issued (one wait for all of them, so that the
     // query transform below overlaps the copies instead of waiting for them).
     __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    ids = clamp_ids(ids, p.num_pages);
     if (n_local > 0) {
-        for (int s = 0; s < 2 && s < n_local; ++s) {
+        for (int s = 0; s < S && s < n_local; ++s) {
             const int64_t id0 = __builtin_amdgcn_readlane(ids, 2 * s);
             const int64_t id1 = __builtin_amdgcn_readlane(ids, 2 * s + 1);
             stage_issue<F>(ring + s * kStage, p.codes, p.scales, id0 * tiles_per_page + head_tile,
@@ -999,9 +1047,13 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
 
     // ---------------- main loop: one stage (2 pages, 32 tokens) per iteration
     for (int k = 0; k < n_local; ++k) {
-        if (k + 1 < n_local) wait_vmem<dma_per_stage<F>()>();
+        // stage k has landed once at most the later stages' copies are outstanding
+        const int ahead = (n_local - 1 - k) < (S - 1) ? (n_local - 1 - k) : (S - 1);
+        if (S == 4 && ahead >= 3) wait_vmem<3 * dma_per_stage<F>()>();
+        else if (S == 4 && ahead == 2) wait_vmem<2 * dma_per_stage<F>()>();
+        else if (ahead >= 1) wait_vmem<dma_per_stage<F>()>();
         else wait_vmem<0>();
-        const uint32_t slot = uint32_t(k & 1);
+        const uint32_t slot = uint32_t(k & (S - 1));
         if constexpr (D == 128) {
             if (append && k == k_new_local && lane < 16) {
                 // the staged page holds what the pools held before this step
@@ -1013,13 +1065,14 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
         }
         StageRegs<F> c;
         stage_read(c, ring_addr + slot * kStage, lane);
-        if (k + 2 < n_local) {
-            // refill this slot with iteration k+2 while iteration k computes
-            const int kn = k + 2;
+        if (k + S < n_local) {
+            // refill this slot with iteration k+S while iteration k computes
+            const int kn = k + S;
             if ((kn & 31) == 0) {
-                ids = ids_next;
-                if (kn + 32 < n_local)
-                    ids_next = load_page_ids<W>(pt_row, first_page, n_pages, wave, (kn >> 5) + 1, lane, p.num_pages);
+                // the next chunk's copy is older than every stage in flight,
+                // so the wait at the top of this iteration covered it
+                ids = clamp_ids(read_page_ids(ids_addr, lane), p.num_pages);
+                if (kn + 32 < n_local) copy_page_ids<W>(ids_slot, pt_row, first_page, n_pages, wave, (kn >> 5) + 1, lane);
             }
             const int s = 2 * (kn & 31);
             const int64_t id0 = __builtin_amdgcn_readlane(ids, s);
@@ -1151,7 +1204,7 @@ __attribute__((amdgpu_waves_per_eu(Fmt<F>::kOccupancy, Fmt<F>::kOccupancy))) dec
     __syncthreads();
     float* red_acc = reinterpret_cast<float*>(smem);
     constexpr int kAS = D + 1;   // LDS row stride (floats) of the merge buffer
-    static_assert(W * 16 * kAS * 4 <= W * ring_bytes<F>(), "merge buffer aliases the staging rings");
+    static_assert(W * 16 * kAS * 4 <= W * ring_bytes<F, S>(), "merge buffer aliases the staging rings");
     if (g4 == 0) {
         red_m[wave][n] = m_run;
         red_l[wave][n] = l_run;
@@ -1272,10 +1325,14 @@ __global__ void __launch_bounds__(256) merge_kernel(DecodeParams p) {
     write_out<N>(p, int64_t(b) * p.num_q_heads + hq, L, o);
 }
 
+// Two ring slots per wave: a 4-slot ring (twice the copies in flight, half
+// the blocks per CU) measured no faster on 32k contexts and slower on 16k.
 template <int F>
 static hipError_t launch_partials(const DecodeParams& p, hipStream_t stream) {
+    constexpr int kSlots = 2;
+    static_assert(occupancy<F, kSlots>() == Fmt<F>::kOccupancy, "the LDS footprint lowers the occupancy");
     const dim3 grid{unsigned(int64_t(p.prefix_blocks) + int64_t(p.suffix_partitions) * p.num_kv_heads * p.batch)};
-    hipLaunchKernelGGL(decode_kernel<F>, grid, dim3(64 * Fmt<F>::kWaves), 0, stream, p);
+    hipLaunchKernelGGL((decode_kernel<F, kSlots>), grid, dim3(64 * Fmt<F>::kWaves), 0, stream, p);
     return hipGetLastError();
 }
 

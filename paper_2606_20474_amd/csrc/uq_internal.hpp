@@ -20,6 +20,7 @@ struct TqTables {
     float mid[15];
     uint32_t lut[8];
 };
+constexpr int kNumCus = 256;     // compute units of an MI355X (8 XCDs x 32)
 constexpr int kTqBlock = 2368;   // bytes per (page, kv head) of the Ultra-TQ cache
 constexpr int kTqMeta = 2048;    // offset of the norms and (scale, zero) words in a block
 
