@@ -135,14 +135,19 @@ def alg_token_heads(wl, cascade):
 
 def timed(step, steps, warmup, stream):
     """Run `warmup` untimed steps, then `steps` timed ones; returns (ms per
-    step over the whole timed region, mean ms of the decode launch between
-    the events each step records)."""
+    step over the whole timed region, mean ms between the event pair each
+    step receives).  Every step hands its pair to uq.time_next_launch, so it
+    brackets the timed kernel itself (the decode partition kernel, or the
+    quantize-on-write kernel): its start and end, as rocprofv3 reports them."""
     import gc
     import torch
     for _ in range(warmup):
         step()
     torch.cuda.synchronize()
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for a, b in evs:   # create the HIP events
+        a.record(stream)
+        b.record(stream)
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
@@ -185,15 +190,13 @@ def comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, args, dev, stream, p
 
     def step(ev_a=None, ev_b=None):
         if ev_a is not None:
-            ev_a.record(stream)
+            uq.time_next_launch(ev_a, ev_b)
         if prefix is None:
             uq.ref_decode_step(desc, q, k_new, v_new, cache, pt, ctx, wl.max_context, scale, part, ws, out,
                                partials_only=True)
         else:
             uq.ref_decode_cascade(desc, q, cache, pt, ctx, wl.max_context, prefix, scale, part, ws, out,
                                   k_new=k_new, v_new=v_new, partials_only=True)
-        if ev_b is not None:
-            ev_b.record(stream)
         if prefix is None:
             uq.ref_decode_merge(desc, wl.batch, wl.num_q_heads, ctx, wl.max_context, part, ws, out)
         else:
@@ -228,17 +231,13 @@ def write_path(uq, args, dev, stream):
 
     def prefill(ev_a=None, ev_b=None):
         if ev_a is not None:
-            ev_a.record(stream)
+            uq.time_next_launch(ev_a, ev_b)
         uq.quantize_kv(desc, kp, vp, pslots, codes, scales)
-        if ev_b is not None:
-            ev_b.record(stream)
 
     def append(ev_a=None, ev_b=None):
         if ev_a is not None:
-            ev_a.record(stream)
+            uq.time_next_launch(ev_a, ev_b)
         uq.quantize_kv(desc, ka, va, aslots, codes, scales, page_table=pt)
-        if ev_b is not None:
-            ev_b.record(stream)
 
     n = max(args.steps, 10)
     _, pre_ms = timed(prefill, n, 3, stream)
@@ -325,7 +324,7 @@ def main():
             # head sizes 64 and 256: the write of the new tokens is its own launch
             uq.quantize_kv(desc, k_new, v_new, new_slots, codes, scales)
         if ev_a is not None:
-            ev_a.record(stream)
+            uq.time_next_launch(ev_a, ev_b)
         if D != 128:
             uq.decode_partials(desc, q, codes, scales, pt, ctx, wl.max_context, scale, part, ws, out)
         elif prefix is None:
@@ -334,8 +333,6 @@ def main():
         else:
             uq.decode_cascade(desc, q, codes, scales, pt, ctx, wl.max_context, prefix, scale, part, ws, out,
                               k_new=k_new, v_new=v_new, partials_only=True)
-        if ev_b is not None:
-            ev_b.record(stream)
         if prefix is None:
             uq.decode_merge(desc, wl.batch, wl.num_q_heads, ctx, wl.max_context, part, ws, out)
         else:

@@ -469,6 +469,25 @@ uq_status uq_ref_decode_merge(const uq_ref_cache_desc *desc, int32_t batch, int3
                               const void *workspace, size_t workspace_bytes, void *out, uq_dtype out_dtype,
                               void *stream);
 
+/* ------------------------------------------------------------------------
+ * Kernel timing (benchmarks).
+ *
+ * HIP events recorded on the stream around a call also count the command
+ * processor's dispatch and completion latency (a few microseconds).  After
+ * uq_time_next_launch(start, stop), the next launch of the decode partition
+ * kernel (by uq_decode_attention, uq_decode_partials,
+ * uq_decode_step(_partials), the cascade calls or their comparison-cache
+ * forms) or of the quantize-on-write kernel (uq_quantize_kv) made from the
+ * calling host thread is dispatched with hipExtLaunchKernel, which sets
+ * `start` and `stop` (hipEvent_t, created by the caller, not owned by the
+ * library) to that kernel's own start and end; hipEventElapsedTime(start,
+ * stop) is then the kernel's duration.  The setting is used by that one
+ * launch and then cleared (a call that fails its checks launches nothing
+ * and leaves it); NULL, NULL clears it.  Errors: INVALID_ARGUMENT when
+ * exactly one of the two is NULL.
+ * ---------------------------------------------------------------------- */
+uq_status uq_time_next_launch(void *start_event, void *stop_event);
+
 #ifdef __cplusplus
 }
 #endif

@@ -810,4 +810,10 @@ uq_status uq_ref_decode_cascade_merge(const uq_ref_cache_desc* desc, int32_t bat
     return from_hip(uq::launch_decode_merge(p, static_cast<hipStream_t>(stream)));
 }
 
+uq_status uq_time_next_launch(void* start_event, void* stop_event) {
+    if ((start_event == nullptr) != (stop_event == nullptr)) return UQ_ERR_INVALID_ARGUMENT;
+    uq::time_next_launch(static_cast<hipEvent_t>(start_event), static_cast<hipEvent_t>(stop_event));
+    return UQ_OK;
+}
+
 }  // extern "C"

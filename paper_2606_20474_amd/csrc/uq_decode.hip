@@ -1342,7 +1342,7 @@ static hipError_t launch_partials(const DecodeParams& p, hipStream_t stream) {
     constexpr int kSlots = 2;
     static_assert(occupancy<F, kSlots>() == Fmt<F>::kOccupancy, "the LDS footprint lowers the occupancy");
     const dim3 grid{unsigned(int64_t(p.prefix_blocks) + int64_t(p.suffix_partitions) * p.num_kv_heads * p.batch)};
-    hipLaunchKernelGGL((decode_kernel<F, kSlots>), grid, dim3(64 * Fmt<F>::kWaves), 0, stream, p);
+    launch_kernel(decode_kernel<F, kSlots>, grid, dim3(64 * Fmt<F>::kWaves), stream, p);
     return hipGetLastError();
 }
 

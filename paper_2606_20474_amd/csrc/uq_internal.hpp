@@ -2,6 +2,7 @@
 // the libuq translation units (not part of the public ABI).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -124,5 +125,24 @@ hipError_t launch_write_kv_ref(const RefWriteParams& p, int dtype, hipStream_t s
 hipError_t launch_prepare_query(const void* q, int dtype, int64_t rows, uint8_t* q8, hipStream_t stream);
 hipError_t launch_decode_partials(const DecodeParams& p, hipStream_t stream);
 hipError_t launch_decode_merge(const DecodeParams& p, hipStream_t stream);
+
+// Kernel timing: the next decode partition or quantize-on-write launch of
+// this host thread sets `start` and `stop` to its kernel's own start and
+// end (hipExtLaunchKernel), then the pair is forgotten.
+struct LaunchEvents {
+    hipEvent_t start = nullptr, stop = nullptr;
+};
+inline thread_local LaunchEvents g_launch_events;
+inline void time_next_launch(hipEvent_t start, hipEvent_t stop) { g_launch_events = LaunchEvents{start, stop}; }
+template <class Kernel, class... Args>
+inline void launch_kernel(Kernel kernel, const dim3& grid, const dim3& block, hipStream_t stream, Args... args) {
+    const LaunchEvents ev = g_launch_events;
+    if (ev.start != nullptr) {
+        g_launch_events = LaunchEvents{};
+        hipExtLaunchKernelGGL(kernel, grid, block, 0, stream, ev.start, ev.stop, 0, args...);
+    } else {
+        hipLaunchKernelGGL(kernel, grid, block, 0, stream, args...);
+    }
+}
 
 }  // namespace uq

@@ -331,9 +331,9 @@ __global__ void __launch_bounds__(256) prepare_query_kernel(const void* q, int64
 template <int NG>
 static void launch_quantize_ng(const QuantizeParams& p, int dtype, const dim3& grid, hipStream_t stream) {
     const dim3 block{256u};
-    if (dtype == 0) hipLaunchKernelGGL((quantize_kv_kernel<0, NG>), grid, block, 0, stream, p);
-    else if (dtype == 1) hipLaunchKernelGGL((quantize_kv_kernel<1, NG>), grid, block, 0, stream, p);
-    else hipLaunchKernelGGL((quantize_kv_kernel<2, NG>), grid, block, 0, stream, p);
+    if (dtype == 0) launch_kernel(quantize_kv_kernel<0, NG>, grid, block, stream, p);
+    else if (dtype == 1) launch_kernel(quantize_kv_kernel<1, NG>, grid, block, stream, p);
+    else launch_kernel(quantize_kv_kernel<2, NG>, grid, block, stream, p);
 }
 
 hipError_t launch_quantize_kv(const QuantizeParams& p, int dtype, hipStream_t stream) {

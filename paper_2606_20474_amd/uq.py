@@ -34,7 +34,7 @@ EXPORTS = (
     "uq_ref_decode_attention", "uq_ref_decode_partials", "uq_ref_decode_merge", "uq_ref_decode_step",
     "uq_ref_decode_step_partials", "uq_decode_cascade_workspace_bytes", "uq_decode_cascade",
     "uq_decode_cascade_partials", "uq_decode_cascade_merge", "uq_ref_decode_cascade",
-    "uq_ref_decode_cascade_partials", "uq_ref_decode_cascade_merge", "uq_quantize_error",
+    "uq_ref_decode_cascade_partials", "uq_ref_decode_cascade_merge", "uq_quantize_error", "uq_time_next_launch",
 )
 
 UQ_REF_FP8_E4M3, UQ_REF_BF16, UQ_REF_TQ4 = 1, 2, 3
@@ -95,6 +95,8 @@ def _load():
     L.uq_prepare_query.restype = i32
     L.uq_quantize_error.argtypes = [vp, i32, i64, i64, i32, i32, i32, vp, vp, vp]
     L.uq_quantize_error.restype = i32
+    L.uq_time_next_launch.argtypes = [vp, vp]
+    L.uq_time_next_launch.restype = i32
     L.uq_decode_workspace_bytes.argtypes = [D, i32, i32, i32, i32]
     L.uq_decode_workspace_bytes.restype = sz
     L.uq_default_partition.argtypes = [D, i32, i32, i32]
@@ -223,6 +225,20 @@ def prepare_query(desc: CacheDesc, q, out=None, stream=None):
     _check(lib.uq_prepare_query(ctypes.byref(d), _ptr(q), _DT[q.dtype], rows, _ptr(out), _stream(stream)),
            "uq_prepare_query")
     return out
+
+
+def time_next_launch(start, stop):
+    """The next decode partition or quantize-on-write launch of this thread
+    sets the torch CUDA events `start` and `stop` to its kernel's own start
+    and end (record them once beforehand, so that their HIP events exist);
+    None, None clears."""
+    if start is None and stop is None:
+        _check(lib.uq_time_next_launch(None, None), "uq_time_next_launch")
+        return
+    if not start.cuda_event or not stop.cuda_event:
+        raise ValueError("record the events once before passing them")
+    _check(lib.uq_time_next_launch(ctypes.c_void_p(start.cuda_event), ctypes.c_void_p(stop.cuda_event)),
+           "uq_time_next_launch")
 
 
 def quantize_error(x, c_values, rotate=True, pow2=True, sums=None, stream=None):

@@ -319,3 +319,11 @@ def test_head_sizes_64_and_256(uq):
         assert r == E.UQ_ERR_UNSUPPORTED
     cd = uq.CacheDesc(num_kv_heads=2, num_pages=10, head_dim=64)
     assert cd.codes_bytes() == 10 * 2 * 2 * 512 and cd.scales_bytes() == 10 * 2 * 2 * 32
+
+
+def test_time_next_launch_validation(uq):
+    """One event without the other is rejected; NULL, NULL clears (no HIP call)."""
+    lib = uq.lib
+    assert lib.uq_time_next_launch(FAKE, None) == uq.UQ_ERR_INVALID_ARGUMENT
+    assert lib.uq_time_next_launch(None, FAKE) == uq.UQ_ERR_INVALID_ARGUMENT
+    assert lib.uq_time_next_launch(None, None) == uq.UQ_OK
