@@ -147,7 +147,11 @@ uq_status uq_prepare_query(const uq_cache_desc *desc, const void *q, uq_dtype q_
 size_t uq_decode_workspace_bytes(const uq_cache_desc *desc, int32_t batch, int32_t num_q_heads,
                                  int32_t max_context, int32_t partition_tokens);
 
-/* Partition length (tokens) the library picks when partition_tokens == 0. */
+/* Partition length (tokens) the library picks when partition_tokens == 0:
+ * the longest (1024 .. 16384) that still gives the 256 compute units two
+ * blocks each.  A block serves one KV head, or two at head size 64 when the
+ * group size is at most 8 and num_kv_heads is even (the kernel then treats
+ * the pair as one 128-channel head with a block-diagonal query operand). */
 int32_t uq_default_partition(const uq_cache_desc *desc, int32_t batch, int32_t num_q_heads, int32_t max_context);
 
 /*

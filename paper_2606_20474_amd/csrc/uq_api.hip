@@ -32,6 +32,15 @@ uq_status require_128(const uq_cache_desc* d) { return d->head_dim == kHeadDim ?
 
 uq_status from_hip(hipError_t e) { return e == hipSuccess ? UQ_OK : UQ_ERR_HIP; }
 
+// Head size 64 runs two KV heads per block when the group size is at most 8
+// and the KV heads pair up: then the grid has one block per pair.
+bool paired_heads(const uq_cache_desc* desc, int32_t num_q_heads) {
+    return desc->head_dim == 64 && desc->num_kv_heads % 2 == 0 && num_q_heads <= 8 * desc->num_kv_heads;
+}
+int32_t block_heads(const uq_cache_desc* desc, int32_t num_q_heads) {
+    return paired_heads(desc, num_q_heads) ? desc->num_kv_heads / 2 : desc->num_kv_heads;
+}
+
 int32_t pick_partition(int32_t batch, int32_t num_kv_heads, int32_t max_context) {
     // The longest partition (fewest partials to merge, fewest per-block
     // prologues) that still gives every one of the 256 CUs at least two
@@ -74,7 +83,8 @@ uq_status make_decode_params(const uq_cache_desc* desc, const void* q, uq_dtype 
                              int32_t max_context, float softmax_scale, int32_t partition_tokens, void* workspace,
                              size_t workspace_bytes, void* out, uq_dtype out_dtype, uq::DecodeParams& p,
                              int64_t extra_slots = 0) {
-    const int32_t part = partition_tokens == 0 ? pick_partition(batch, desc->num_kv_heads, max_context) : partition_tokens;
+    const int32_t part = partition_tokens == 0 ? pick_partition(batch, block_heads(desc, num_q_heads), max_context)
+                                               : partition_tokens;
     const size_t need = workspace_for(batch, num_q_heads, max_context, part, extra_slots, desc->head_dim);
     if (workspace == nullptr) return UQ_ERR_INVALID_ARGUMENT;
     if (workspace_bytes < need) return UQ_ERR_WORKSPACE_TOO_SMALL;
@@ -113,7 +123,8 @@ uq_status make_decode_params(const uq_cache_desc* desc, const void* q, uq_dtype 
     p.out_dtype = out_dtype == UQ_F32 ? 0 : 1;
     p.rotate_v = desc->rotate_v != 0;
     p.head_dim = desc->head_dim;
-    p.kv_fmt = desc->head_dim == 64 ? uq::kFp4d64 : desc->head_dim == 256 ? uq::kFp4d256 : uq::kFp4;
+    p.kv_fmt = desc->head_dim == 64 ? (paired_heads(desc, num_q_heads) ? uq::kFp4d64x2 : uq::kFp4d64)
+               : desc->head_dim == 256 ? uq::kFp4d256 : uq::kFp4;
     p.out_scale = 1.0f;
     p.prefix_pages = nullptr;
     p.prefix_lens = nullptr;
@@ -350,13 +361,14 @@ uq_status uq_quantize_error(const void* x, uq_dtype dtype, int64_t rows, int64_t
 
 int32_t uq_default_partition(const uq_cache_desc* desc, int32_t batch, int32_t num_q_heads, int32_t max_context) {
     if (check_decode_common(desc, batch, num_q_heads, max_context, 0) != UQ_OK) return 0;
-    return pick_partition(batch, desc->num_kv_heads, max_context);
+    return pick_partition(batch, block_heads(desc, num_q_heads), max_context);
 }
 
 size_t uq_decode_workspace_bytes(const uq_cache_desc* desc, int32_t batch, int32_t num_q_heads, int32_t max_context,
                                  int32_t partition_tokens) {
     if (check_decode_common(desc, batch, num_q_heads, max_context, partition_tokens) != UQ_OK) return 0;
-    const int32_t part = partition_tokens == 0 ? pick_partition(batch, desc->num_kv_heads, max_context) : partition_tokens;
+    const int32_t part = partition_tokens == 0 ? pick_partition(batch, block_heads(desc, num_q_heads), max_context)
+                                               : partition_tokens;
     return workspace_for(batch, num_q_heads, max_context, part, 0, desc->head_dim);
 }
 

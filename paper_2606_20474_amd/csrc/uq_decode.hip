@@ -102,8 +102,28 @@ template <> struct Fmt<kFp4d256> {
     static constexpr int kWaves = 4;
     static constexpr int kOccupancy = 2;
 };
-template <int F> constexpr bool is_fp4() { return F == kFp4 || F == kFp4d64 || F == kFp4d256; }
-template <int F> constexpr int head_dim_of() { return F == kFp4d64 ? 64 : F == kFp4d256 ? 256 : 128; }
+// Head size 64, two KV heads A and B per block.  A stage holds them in the
+// layout of one 128-channel head: K tile = A's two channel groups then B's
+// (k 0..63 and 64..127 of the QK operand), V tile = per 4 tokens A's eight
+// 8-channel blocks then B's (channel blocks 0..7 and 8..15 of PV), scales
+// [K: A, B][V: A, B].  The query operand is block diagonal: columns 0..7
+// hold A's query heads on k 0..63, columns 8..15 B's on k 64..127, so the
+// scores of each column see only its own head's keys; of the PV output only
+// the tiles (A's channels, A's columns) and (B's, B's) are kept.  The block
+// then does the arithmetic of one head-size-128 block for two heads of 64.
+template <> struct Fmt<kFp4d64x2> {
+    static constexpr int kTile = 1024;
+    static constexpr int kScaleBlock = 2 * kTileScales;
+    static constexpr int kWaves = 4;
+    static constexpr int kOccupancy = 4;
+};
+template <int F> constexpr bool is_fp4() { return F == kFp4 || F == kFp4d64 || F == kFp4d256 || F == kFp4d64x2; }
+template <int F> constexpr int head_dim_of() {
+    return (F == kFp4d64 || F == kFp4d64x2) ? 64 : F == kFp4d256 ? 256 : 128;
+}
+// The register and operand formats: the paired head-size-64 stage is read
+// and computed as a head-size-128 FP4 stage.
+template <int F> constexpr int regs_fmt() { return F == kFp4d64x2 ? kFp4 : F; }
 // Ultra-TQ: per page 1 KiB of K indices, 1 KiB of V codes and 320 bytes of
 // norms and (scale, zero) words ("scale block").
 template <> struct Fmt<kTq4> {
@@ -250,6 +270,28 @@ __device__ __forceinline__ void stage_issue(uint8_t* stage, const uint8_t* __res
         if (lane < 40) {
             const uint8_t* m = lane < 20 ? b0 + kTqMeta + 16 * lane : b1 + kTqMeta + 16 * (lane - 20);
             __builtin_amdgcn_global_load_lds(m, (lds_ptr_t)(stage + 4096), 16, 0, 0);
+        }
+        return;
+    }
+    if constexpr (F == kFp4d64x2) {
+        // tile0/tile1: head A's K tile of each page in 512-byte tiles; the
+        // pool holds [K_A][V_A][K_B][V_B] (512 B each), the scale pool
+        // [K_A][V_A][K_B][V_B] (32 B each) per page and head pair
+        const int u = lane & 15, r = lane >> 4;
+        const int64_t ko = lane < 32 ? 16 * lane : 1024 + 16 * (lane - 32);
+        const int64_t vo = (u < 8 ? 512 : 1536) + 16 * (8 * r + (u & 7));
+        const uint8_t* b0 = codes + tile0 * 512;
+        const uint8_t* b1 = codes + tile1 * 512;
+        __builtin_amdgcn_global_load_lds(b0 + ko, (lds_ptr_t)stage, 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(b0 + vo, (lds_ptr_t)(stage + 1024), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(b1 + ko, (lds_ptr_t)(stage + 2048), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(b1 + vo, (lds_ptr_t)(stage + 3072), 16, 0, 0);
+        if (lane < 16) {
+            // 16-byte unit j of a page's 128-byte block: K_A K_A K_B K_B V_A V_A V_B V_B
+            const int j = lane & 7;
+            const int64_t so = (j < 4 ? 0 : 32) + ((j & 2) ? 64 : 0) + 16 * (j & 1);
+            const uint8_t* sc = scales + ((lane < 8 ? tile0 : tile1) >> 1) * 64 + so;
+            __builtin_amdgcn_global_load_lds(sc, (lds_ptr_t)(stage + 4096), 16, 0, 0);
         }
         return;
     }
@@ -717,7 +759,9 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
     constexpr int kQRounds = 256 / kThreads;   // 16 threads per query row, 16 rows
     constexpr int D = head_dim_of<F>();         // head size
     constexpr int N = D / 16;                   // channels per lane of a 16-lane row
-    constexpr int kAccTiles = D == 256 ? 16 : 8;   // PV output tiles of 16 channel blocks x 16 heads
+    constexpr bool kPair = F == kFp4d64x2;      // two kv heads of 64 per block
+    constexpr int DA = kPair ? 128 : D;         // channels of the accumulators
+    constexpr int kAccTiles = DA == 256 ? 16 : 8;   // PV output tiles of 16 channel blocks x 16 heads
     // Linear block order: kv head fastest, then sequence, then partition.
     // Workgroups go to the 8 XCDs round-robin by linear id, so this spreads
     // the work of every sequence evenly over the XCDs whatever the context
@@ -738,8 +782,9 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
     // MiniMax-like workload).
     const int lin = blockIdx.x;
     const bool cascade = p.prefix_pages != nullptr;
-    const int hk = lin % p.num_kv_heads;
-    const int row = lin / p.num_kv_heads;
+    const int units = kPair ? p.num_kv_heads / 2 : p.num_kv_heads;   // kv heads, or pairs of them
+    const int hk = lin % units;
+    const int row = lin / units;
     bool pre = false;
     int rest = row;
     if (cascade) {
@@ -777,11 +822,12 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
         if (start >= ctx) {
             // nothing of this sequence here; an empty context still gets its zero output
             if (ctx <= 0 && part == 0) {
-                for (int r = tid >> 4; r < G; r += kThreads / 16) {
+                // the block's query heads: G of kv head hk, or 2 G of the pair
+                for (int r = tid >> 4; r < (kPair ? 2 : 1) * G; r += kThreads / 16) {
                     float z[N];
 #pragma unroll
                     for (int i = 0; i < N; ++i) z[i] = 0.f;
-                    write_out<N>(p, int64_t(b) * p.num_q_heads + hk * G + r, tid & 15, z);
+                    write_out<N>(p, int64_t(b) * p.num_q_heads + (kPair ? 2 : 1) * hk * G + r, tid & 15, z);
                 }
             }
             return;
@@ -792,6 +838,12 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
     const bool in_place = !cascade && ctx <= p.partition_tokens;
     // query row r (0..15) of this block: valid, its sequence and query head
     auto row_of = [&](int r, int& rb, int& rhq) -> bool {
+        if constexpr (kPair) {
+            // rows 0..7: query heads of kv head 2 hk, rows 8..15: of 2 hk + 1
+            rb = b;
+            rhq = (2 * hk + (r >> 3)) * G + (r & 7);
+            return (r & 7) < G;
+        }
         if (pre) {
             const int f = 16 * chunk + r;
             rb = f / G;
@@ -916,7 +968,7 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
     const int n = lane & 15;
     uint8_t* ring = smem + wave * ring_bytes<F, S>();
     const uint32_t ring_addr = uint32_t(reinterpret_cast<uintptr_t>((lds_ptr_t)ring));
-    const int64_t head_tile = int64_t(hk) * 2;
+    const int64_t head_tile = int64_t(kPair ? 2 * hk : hk) * 2;   // K tile of the (first) kv head
     const int64_t tiles_per_page = int64_t(p.num_kv_heads) * 2;
 
     uint8_t* ids_slot = ids_lds + wave * kIdsSlot;
@@ -962,6 +1014,21 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
                 }
             }
             *reinterpret_cast<uint4*>(q_lds + ((qL >> 2) * 64 + (qL & 3) * 16 + qr) * 16) = w;
+        } else if constexpr (kPair) {
+            // rotated (64-point) and cast to FP8: rows 0..7 (head A) on k
+            // 0..63, rows 8..15 (head B) on k 64..127 of the B operand (layout
+            // below); the other half of each row stays zero
+            uint32_t wq = 0u;
+            if (qvalid) {
+                wht_x<N>(qx[h], qL);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) wq |= e4m3_byte(qx[h][j]) << (8 * j);
+            }
+            const int ch = N * qL + (qr >= 8 ? 64 : 0);
+            const int g = (ch & 63) >> 4;
+            const int e0 = (ch & 15) + (ch >= 64 ? 16 : 0);
+            *reinterpret_cast<uint32_t*>(q_lds + (g * 16 + qr) * 32 + e0) = wq;
+            if (qL < 4) *reinterpret_cast<uint4*>(q_lds + (qL * 16 + qr) * 32 + (qr >= 8 ? 0 : 16)) = uint4{0u, 0u, 0u, 0u};
         } else if constexpr (F == kFp4d64 || F == kFp4d256) {
             // rotated (D-point) and cast to FP8; the lane's N channels go to the
             // B operand of the 128-channel chunk they belong to (layout below)
@@ -1009,7 +1076,7 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
         }
     }
     __syncthreads();
-    QOperand<F> qop;
+    QOperand<regs_fmt<F>()> qop;
     if constexpr (F == kBf16 || F == kTq4) {
 #pragma unroll
         for (int st = 0; st < 4; ++st)
@@ -1073,7 +1140,7 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
                                pos_new & 15, lane, tok);
             }
         }
-        StageRegs<F> c;
+        StageRegs<regs_fmt<F>()> c;
         stage_read(c, ring_addr + slot * kStage, lane);
         if (k + S < n_local) {
             // refill this slot with iteration k+S while iteration k computes
@@ -1101,7 +1168,7 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
             x[4 + i] = s1[i];
         }
         uint32_t vs0 = 0, vs1 = 0;   // V scale bytes of the lane's 4 tokens per page (FP4)
-        if constexpr (F == kFp4) {
+        if constexpr (regs_fmt<F>() == kFp4) {
             vs0 = c.vs[0];
             vs1 = c.vs[1];
         }
@@ -1213,7 +1280,7 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
     const float l_run = acc_l[0];   // the column sum, in every lane of the column
     __syncthreads();
     float* red_acc = reinterpret_cast<float*>(smem);
-    constexpr int kAS = D + 1;   // LDS row stride (floats) of the merge buffer
+    constexpr int kAS = DA + 1;   // LDS row stride (floats) of the merge buffer
     static_assert(W * 16 * kAS * 4 <= W * ring_bytes<F, S>(), "merge buffer aliases the staging rings");
     if (g4 == 0) {
         red_m[wave][n] = m_run;
@@ -1227,7 +1294,7 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 // head size 64: rows of channel blocks 8..15 (g4 >= 2) do not exist
-                if (D != 64 || g4 < 2) red_acc[(wave * 16 + n) * kAS + 128 * bl + 32 * g4 + 8 * i + j] = acc[8 * bl + j][i];
+                if (DA != 64 || g4 < 2) red_acc[(wave * 16 + n) * kAS + 128 * bl + 32 * g4 + 8 * i + j] = acc[8 * bl + j][i];
             }
         }
     }
@@ -1249,12 +1316,13 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
             f[w] = __builtin_amdgcn_exp2f(red_m[w][r] - M);
             lsum += f[w] * red_l[w][r];
         }
+        const int c0 = (kPair && r >= 8) ? 64 : 0;   // head B's channels are 64..127 of the accumulators
         float o[N];
 #pragma unroll
         for (int cc = 0; cc < N; ++cc) {
             float s = 0.f;
 #pragma unroll
-            for (int w = 0; w < W; ++w) s += f[w] * red_acc[(w * 16 + r) * kAS + N * L + cc];
+            for (int w = 0; w < W; ++w) s += f[w] * red_acc[(w * 16 + r) * kAS + c0 + N * L + cc];
             o[cc] = s;
         }
         if (in_place) {
@@ -1341,7 +1409,8 @@ template <int F>
 static hipError_t launch_partials(const DecodeParams& p, hipStream_t stream) {
     constexpr int kSlots = 2;
     static_assert(occupancy<F, kSlots>() == Fmt<F>::kOccupancy, "the LDS footprint lowers the occupancy");
-    const dim3 grid{unsigned(int64_t(p.prefix_blocks) + int64_t(p.suffix_partitions) * p.num_kv_heads * p.batch)};
+    const int64_t units = F == kFp4d64x2 ? p.num_kv_heads / 2 : p.num_kv_heads;
+    const dim3 grid{unsigned(int64_t(p.prefix_blocks) + int64_t(p.suffix_partitions) * units * p.batch)};
     launch_kernel(decode_kernel<F, kSlots>, grid, dim3(64 * Fmt<F>::kWaves), stream, p);
     return hipGetLastError();
 }
@@ -1351,6 +1420,7 @@ hipError_t launch_decode_partials(const DecodeParams& p, hipStream_t stream) {
     if (p.kv_fmt == kBf16) return launch_partials<kBf16>(p, stream);
     if (p.kv_fmt == kTq4) return launch_partials<kTq4>(p, stream);
     if (p.kv_fmt == kFp4d64) return launch_partials<kFp4d64>(p, stream);
+    if (p.kv_fmt == kFp4d64x2) return launch_partials<kFp4d64x2>(p, stream);
     if (p.kv_fmt == kFp4d256) return launch_partials<kFp4d256>(p, stream);
     return launch_partials<kFp4>(p, stream);
 }

@@ -11,7 +11,9 @@ namespace uq {
 // Cache formats of the decode kernel template: the FP4 cache of this library
 // and the two plain comparison caches.
 // kFp4d64 / kFp4d256: the FP4 cache at head sizes 64 and 256 (kFp4 is 128).
-enum KvFmt : int32_t { kFp4 = 0, kFp8 = 1, kBf16 = 2, kTq4 = 3, kFp4d64 = 4, kFp4d256 = 5 };
+// kFp4d64x2: head size 64 with two KV heads per block, staged and computed as
+// one 128-channel head (group size at most 8, an even number of KV heads).
+enum KvFmt : int32_t { kFp4 = 0, kFp8 = 1, kBf16 = 2, kTq4 = 3, kFp4d64 = 4, kFp4d256 = 5, kFp4d64x2 = 6 };
 
 // Tables of the Ultra-TQ key codebook, built on the host from the 16 levels
 // rounded to BF16: the encoder's midpoints and the decoder's byte lookup

@@ -5,7 +5,8 @@ the oracle at the same head size.
     the oracle's, f32 and bf16 rows, rotate_v on and off, padding slots;
   * decode attention: max-abs 2e-3 and relative L2 1e-3 against the fp64
     oracle, ragged contexts with an empty one, partitions 0/32/256, group
-    sizes 6, 16 and 1, f32 and bf16 queries, a bf16 output, and a
+    sizes 6, 16 and 1 (at head size 64 both the one-head and the two-head
+    blocks), f32 and bf16 queries, a bf16 output, and a
     GPT-OSS-like layer (64 query heads, 8 KV heads, batch 32, context 32768)
     at full size on sampled sequences.
 """
@@ -114,6 +115,25 @@ def test_decode_group_sizes(uq, d, hq, hkv):
     ref = oracle.decode_attention(wl.q.numpy(), pools, wl.page_table, wl.context_lens, wl.num_kv_heads,
                                   1 / math.sqrt(d), True)
     check(out, ref, f"d={d} {hq}/{hkv}")
+
+
+@pytest.mark.parametrize("hq,hkv,ctx", [(32, 4, [40, 513, 0, 2000]), (2, 2, [700, 1, 95, 4096]),
+                                        (48, 8, [16, 17, 1000, 333])])
+def test_decode_paired_heads(uq, hq, hkv, ctx):
+    """Head size 64 with group size <= 8 and an even number of KV heads
+    runs two KV heads per block (block-diagonal query operand): group sizes
+    8, 1 and 6, an empty context, several partitions."""
+    dev = torch.device("cuda:0")
+    wl = workloads.custom(4, hq, hkv, ctx, seed=65, paging="random", head_dim=64)
+    desc, codes, scales, pools = both_caches(uq, wl, dev)
+    ref = oracle.decode_attention(wl.q.numpy(), pools, wl.page_table, wl.context_lens, wl.num_kv_heads,
+                                  1 / math.sqrt(64), True)
+    for partition in (0, 64, 512):
+        log(f"paired d=64 hq={hq} hkv={hkv} partition={partition}")
+        out = decode(uq, wl, desc, codes, scales, dev, partition)
+        if 0 in ctx:
+            assert np.all(out[ctx.index(0)] == 0)
+        check(out, ref, f"paired {hq}/{hkv} p{partition}")
 
 
 @pytest.mark.parametrize("d", [64, 256])
