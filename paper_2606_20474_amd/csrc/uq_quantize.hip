@@ -133,7 +133,18 @@ __global__ void __launch_bounds__(256) quantize_kv_kernel(QuantizeParams p) {
     const int64_t t = vec / p.num_kv_heads;
     const int h = int(vec - t * p.num_kv_heads);
 
-    int64_t slot = p.slot_mapping[t];
+    // The rows are loaded together with the slot, before the slot is known
+    // to be valid: the row loads then overlap the slot and page-table
+    // lookups instead of waiting behind them (a padding token's row is read
+    // for nothing).
+    const int64_t slot = p.slot_mapping[t];
+    const int64_t row = t * p.token_stride + int64_t(h) * D + 8 * L;
+    float xk[NG][8], xv[NG][8];
+#pragma unroll
+    for (int j = 0; j < NG; ++j) {
+        load_x8<DT>(p.k, row + 32 * j, xk[j]);
+        load_x8<DT>(p.v, row + 32 * j, xv[j]);
+    }
     if (slot < 0) return;
     int64_t page;
     int off;
@@ -150,13 +161,6 @@ __global__ void __launch_bounds__(256) quantize_kv_kernel(QuantizeParams p) {
     }
     if (page < 0 || page >= p.num_pages) return;
 
-    const int64_t row = t * p.token_stride + int64_t(h) * D + 8 * L;
-    float xk[NG][8], xv[NG][8];
-#pragma unroll
-    for (int j = 0; j < NG; ++j) {
-        load_x8<DT>(p.k, row + 32 * j, xk[j]);
-        load_x8<DT>(p.v, row + 32 * j, xv[j]);
-    }
     uint32_t wk[NG], wv[NG];
     int ek[NG], ev[NG];
     quantize_xq<NG>(xk, L, p.c, true, wk, ek);
