@@ -327,3 +327,26 @@ def test_time_next_launch_validation(uq):
     assert lib.uq_time_next_launch(FAKE, None) == uq.UQ_ERR_INVALID_ARGUMENT
     assert lib.uq_time_next_launch(None, FAKE) == uq.UQ_ERR_INVALID_ARGUMENT
     assert lib.uq_time_next_launch(None, None) == uq.UQ_OK
+
+
+def test_default_partition_counts_blocks(uq):
+    """The default partition is the longest (1024..16384) that still gives the
+    256 CUs two blocks each, counting one block per KV head, or per pair of
+    KV heads where head size 64 runs two per block (G <= 8, even KV heads)."""
+    from paper_2606_20474_amd.uq import CacheDesc
+
+    def pick(units, ctx):
+        part = 16384
+        while part > 1024 and units * -(-ctx // part) < 512:
+            part //= 2
+        return part
+
+    for hd, hkv, hq, B, ctx in [(128, 4, 64, 32, 32768), (128, 8, 64, 256, 131072), (128, 8, 48, 64, 131072),
+                                (64, 8, 64, 32, 32768), (64, 8, 128, 32, 32768), (64, 3, 24, 32, 32768),
+                                (256, 8, 64, 32, 32768), (64, 2, 2, 1, 4096)]:
+        d = CacheDesc(num_kv_heads=hkv, num_pages=16, head_dim=hd)
+        paired = hd == 64 and hkv % 2 == 0 and hq <= 8 * hkv
+        want = pick(B * (hkv // 2 if paired else hkv), ctx)
+        assert uq.default_partition(d, B, hq, ctx) == want, (hd, hkv, hq, B, ctx)
+        # the workspace follows the same pick
+        assert uq.workspace_bytes(d, B, hq, ctx, 0) == uq.workspace_bytes(d, B, hq, ctx, want)
