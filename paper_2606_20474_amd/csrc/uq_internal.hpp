@@ -104,7 +104,7 @@ struct DecodeParams {
     int32_t prefix_tokens;
     int32_t prefix_partition;      // prefix tokens per prefix block
     int32_t prefix_chunks;         // ceil(B * G / 16) column chunks per kv head
-    int32_t prefix_blocks;         // Hkv * prefix_chunks * prefix partitions, first in the grid
+    int32_t prefix_blocks;         // Hkv * prefix_chunks * prefix partitions, after the context blocks in the grid
     int32_t suffix_partitions;
 };
 
