@@ -80,12 +80,18 @@ def make_workload(name):
 
 
 def kernel_source_hash():
-    """sha256 of the decode kernel's sources; a profile taken on other sources is stale."""
+    """sha256 of the decode kernel's sources without comments and layout
+    (a change to a comment does not change the kernel); a profile taken on
+    other sources is stale."""
     import hashlib
+    import re
     h = hashlib.sha256()
     for name in ("uq_decode.hip", "uq_device.hpp"):
-        with open(os.path.join(ROOT, "paper_2606_20474_amd", "csrc", name), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(ROOT, "paper_2606_20474_amd", "csrc", name)) as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()
 
 

@@ -1,10 +1,12 @@
 // uq_decode.hip -- split-context decode attention over a paged KV cache
 // (paper, Algorithm 1, "Decode"; section "Kernel Implementation in vLLM").
 //
-// One kernel template serves three cache formats so that the comparison
+// One kernel template serves the cache formats so that the comparison
 // between them measures the format, not the kernel:
 //   kFp4   the UltraQuant cache: FP4 E2M1 codes + UE8M0 scales per 32
-//          channels, K (and V with rotate_v) Walsh-Hadamard rotated;
+//          channels, K (and V with rotate_v) Walsh-Hadamard rotated
+//          (kFp4d64x2, kFp4d64, kFp4d256: the same cache at head sizes 64
+//          and 256; kFp4d64x2 takes two KV heads per block);
 //   kFp8   a plain FP8 E4M3 cache with one scale per tensor;
 //   kBf16  a plain BF16 cache;
 //   kTq4   the Ultra-TQ codebook cache (rotated K as 4-bit indices into 16
@@ -15,8 +17,9 @@
 //          token's norm; V is decoded with one fused multiply-add per
 //          element into BF16.
 //
-// decode_kernel<F>: one block of Fmt<F>::kWaves waves per (partition, kv
-// head, sequence), in an XCD-aware linear order (kv head fastest).
+// decode_kernel<F, S>: one block of Fmt<F>::kWaves waves per (partition, kv
+// head, sequence), in an XCD-aware linear order (kv head fastest); S ring
+// slots per wave.
 //   prologue  the block loads its G query heads (G <= 16), rotates them
 //             with the in-register WHT butterfly and casts them to FP8
 //             E4M3 (FP4 cache), casts them to FP8 (FP8 cache) or to BF16
