@@ -21,7 +21,9 @@
  *    pointers on the current HIP device.  `stream` is a hipStream_t (NULL =
  *    the default stream).  Every call only enqueues work on `stream`; none
  *    synchronises.  The library allocates nothing and keeps no pointer after
- *    a call returns; the caller owns every buffer.  Calls are thread-safe.
+ *    a call returns (except the two events of uq_time_next_launch, held for
+ *    the calling thread's next launch); the caller owns every buffer.  Calls
+ *    are thread-safe.
  *  - Arguments are validated on the host before any HIP call: a failed
  *    check returns its status and enqueues nothing.  Device-resident
  *    indices (page ids, slots, context lengths) cannot be checked without a
