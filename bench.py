@@ -51,8 +51,8 @@ REF_SCALE = 0.3                 # per-tensor FP8 scale of the comparison cache (
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--workload", default="qwen3-235b-like",
                     choices=["qwen3-235b-like", "high-concurrency", "minimax-like", "tiny", "gpt-oss-like-hd64",
                              "gpt-oss-like-hd256"])
