@@ -36,7 +36,10 @@
  *    cascade decode, the pre-cast FP8 query, uq_prepare_query and the
  *    comparison caches are d = 128 calls (UNSUPPORTED for 64 and 256).
  *    Sizes written 128 below are d for head sizes 64 and 256.
- *  - Inputs must be finite.
+ *  - Inputs must be finite.  Attention stays finite and accurate for scores
+ *    (q.k * softmax_scale * log2 e) of any magnitude up to 1e30, as long as
+ *    the fp32 products themselves do not overflow; only tokens inside a
+ *    context are read, so every one of them must have been written.
  *
  * Cache format (the "pools")
  * --------------------------

@@ -1116,7 +1116,11 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
     const float sl2 = p.scale_log2;
     const uint32_t k23 = 23u;
     // finite start: a column with every score masked keeps exp2(-inf - m) = 0
-    float m_run = -1e30f;
+    constexpr float kNoMax = -1e30f;
+    float m_run = kNoMax;
+    // wave-uniform: some column's running max has magnitude 2^20 or more
+    // (then the exponents round the scaled score first; see below)
+    bool big_max = false;
     // running softmax sum per column, on the matrix unit: every row of
     // (all ones) x P is the column sum of P
     const v8bf ones = __builtin_bit_cast(v8bf, uint4{0x3F803F80u, 0x3F803F80u, 0x3F803F80u, 0x3F803F80u});
@@ -1204,7 +1208,9 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
         // ---- online softmax (log2 domain, m_run in scaled units), lazy rescale:
         // the running max of a column moves only when a score exceeds it by
         // more than kLazyRescale; a wave-wide vote skips the cross-lane maximum
-        // when no lane holds such a score (then no column would move)
+        // when no lane holds such a score (then no column would move).  m_run
+        // is a rounded scaled score, so every rounded scaled score is at most
+        // m_run + kLazyRescale (+ the rounding of that sum: 16 in all).
         float smax = x[0];
 #pragma unroll
         for (int i = 1; i < 8; ++i) smax = __builtin_fmaxf(smax, x[i]);
@@ -1217,10 +1223,23 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
                 for (int j = 0; j < kAccTiles; ++j) acc[j] *= alpha;
                 m_run = mloc;
             }
+            big_max = __builtin_amdgcn_ballot_w64(__builtin_fabsf(m_run) >= 0x1p20f && m_run != kNoMax) != 0;
         }
         float pr[8];
+        if (!big_max) {
+            // the fused form sees the exact product x * sl2, within 2^-4 of
+            // the rounded one below 2^20 (a column still at kNoMax has only
+            // masked scores)
 #pragma unroll
-        for (int i = 0; i < 8; ++i) pr[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(x[i], sl2, -m_run));
+            for (int i = 0; i < 8; ++i) pr[i] = __builtin_amdgcn_exp2f(__builtin_fmaf(x[i], sl2, -m_run));
+        } else {
+            // scores of 2^20 and more: the exact product can sit half an ulp
+            // (over 128 from 2^32 on) away from every float, so round the
+            // product first, as m_run was, and subtract (not fused)
+#pragma clang fp contract(off)
+#pragma unroll
+            for (int i = 0; i < 8; ++i) pr[i] = __builtin_amdgcn_exp2f(x[i] * sl2 - m_run);
+        }
         uint32_t phi[4], plo[4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) split_p(pr[2 * r], pr[2 * r + 1], phi[r], plo[r]);
