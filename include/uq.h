@@ -120,7 +120,9 @@ int32_t uq_version(void);
  *   page_table    : int32 [num_seqs][max_pages_per_seq] or NULL.
  *   k, v must be 16-byte aligned and token_stride a multiple of 16 bytes.
  *   kv_codes, kv_scales : the pools described above; only the slots named
- *                   by slot_mapping are written.
+ *                   by slot_mapping are written.  Two tokens of one call
+ *                   naming the same slot race: the slot's bytes are then
+ *                   unspecified (possibly a mix of both tokens).
  * Per token and head the K vector is always rotated, V only with rotate_v.
  * Codes and scale bytes are a pure function of the inputs and `c`.
  * Errors: INVALID_ARGUMENT for null k/v/slot_mapping/pools, num_tokens < 0,
