@@ -162,6 +162,68 @@ def _ptr(t):
     return None if t is None else ctypes.c_void_p(t.data_ptr())
 
 
+_ROWS = (torch.float32, torch.bfloat16, torch.float16)               # K/V and query rows
+_QUERY = _ROWS + (torch.uint8, torch.float8_e4m3fn)                    # ... or a pre-cast FP8 query
+_OUT = (torch.float32, torch.bfloat16)
+_I32 = (torch.int32,)
+_U8 = (torch.uint8,)
+
+
+def _need(t, name, dtypes, shape=None, min_numel=None, contiguous=True):
+    """The checks the C ABI cannot make, since it sees raw pointers only: a
+    HIP tensor on the current device, of one of `dtypes`, contiguous (unless
+    the caller checks strides itself), of `shape` (None matches any size)
+    and with at least `min_numel` elements.  Raises before anything is
+    enqueued."""
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name}: a torch.Tensor expected, got {type(t).__name__}")
+    if not t.is_cuda:
+        raise ValueError(f"{name}: a tensor on the GPU expected, got one on {t.device}")
+    if t.device.index != torch.cuda.current_device():
+        raise ValueError(f"{name}: on {t.device}, but the current device is cuda:{torch.cuda.current_device()}")
+    if t.dtype not in dtypes:
+        raise TypeError(f"{name}: dtype {t.dtype}, expected one of {[str(d) for d in dtypes]}")
+    if contiguous and not t.is_contiguous():
+        raise ValueError(f"{name}: a contiguous tensor expected")
+    if shape is not None and (t.dim() != len(shape) or any(w is not None and w != n for w, n in zip(shape, t.shape))):
+        raise ValueError(f"{name}: shape {tuple(t.shape)}, expected {tuple('*' if w is None else w for w in shape)}")
+    if min_numel is not None and t.numel() < min_numel:
+        raise ValueError(f"{name}: {t.numel()} elements, at least {min_numel} needed")
+    return t
+
+
+def _rows(k, v, num_kv_heads, head_dim, token_stride):
+    """K and V rows [T, Hkv, head_dim]: channels and heads contiguous, one
+    token stride for both; returns the token stride in elements."""
+    for t, name in ((k, "k"), (v, "v")):
+        _need(t, name, _ROWS, (None, num_kv_heads, head_dim), contiguous=False)
+        if t.stride(2) != 1 or t.stride(1) != head_dim:
+            raise ValueError(f"{name}: heads and channels of a token must be contiguous")
+    if v.shape[0] != k.shape[0] or v.dtype != k.dtype:
+        raise ValueError("k and v: the same number of tokens and dtype expected")
+    if token_stride is None:
+        token_stride = k.stride(0)
+    if k.shape[0] > 1 and (k.stride(0) != token_stride or v.stride(0) != token_stride):
+        raise ValueError(f"k and v: token stride {token_stride} expected, got {k.stride(0)} and {v.stride(0)}")
+    return token_stride
+
+
+def _table(page_table, context_lens, B):
+    """Page table int32 [>= B, max_pages_per_seq] and context lengths int32 [B]."""
+    _need(page_table, "page_table", _I32, (None, None))
+    if page_table.shape[0] < B:
+        raise ValueError(f"page_table: {page_table.shape[0]} rows for a batch of {B}")
+    _need(context_lens, "context_lens", _I32, (B,))
+
+
+def _q_out(q, out, head_dim):
+    _need(q, "q", _QUERY, (None, None, head_dim))
+    B, Hq = q.shape[0], q.shape[1]
+    if out is not None:
+        _need(out, "out", _OUT, (B, Hq, head_dim))
+    return B, Hq
+
+
 def _stream(stream=None):
     if stream is None:
         stream = torch.cuda.current_stream()
@@ -203,12 +265,20 @@ class CacheDesc:
         return codes, scales
 
 
+def _pools(desc: CacheDesc, codes, scales):
+    _need(codes, "codes", _U8, min_numel=desc.codes_bytes())
+    _need(scales, "scales", _U8, min_numel=desc.scales_bytes())
+
+
 def quantize_kv(desc: CacheDesc, k, v, slot_mapping, codes, scales, page_table=None, max_pages_per_seq=0,
                 token_stride=None, stream=None):
-    """k, v: [T, Hkv, 128] (or strided rows); slot_mapping int64 [T]."""
+    """k, v: [T, Hkv, head_dim] (or strided rows); slot_mapping int64 [T]."""
+    token_stride = _rows(k, v, desc.num_kv_heads, desc.head_dim, token_stride)
     T = k.shape[0]
-    if token_stride is None:
-        token_stride = k.stride(0)
+    _need(slot_mapping, "slot_mapping", (torch.int64,), (T,))
+    _pools(desc, codes, scales)
+    if page_table is not None:
+        _need(page_table, "page_table", _I32, (None, None))
     num_seqs = 0 if page_table is None else page_table.shape[0]
     mpps = 0 if page_table is None else (max_pages_per_seq or page_table.shape[1])
     d = desc.c_struct()
@@ -218,9 +288,13 @@ def quantize_kv(desc: CacheDesc, k, v, slot_mapping, codes, scales, page_table=N
 
 
 def prepare_query(desc: CacheDesc, q, out=None, stream=None):
+    _need(q, "q", _ROWS)
+    if q.numel() % HEAD_DIM:
+        raise ValueError(f"q: rows of {HEAD_DIM} channels expected")
     rows = q.numel() // HEAD_DIM
     if out is None:
         out = torch.empty(q.shape, dtype=torch.uint8, device=q.device)
+    _need(out, "out", (torch.uint8, torch.float8_e4m3fn), min_numel=q.numel())
     d = desc.c_struct()
     _check(lib.uq_prepare_query(ctypes.byref(d), _ptr(q), _DT[q.dtype], rows, _ptr(out), _stream(stream)),
            "uq_prepare_query")
@@ -246,12 +320,14 @@ def quantize_error(x, c_values, rotate=True, pow2=True, sums=None, stream=None):
     (last dimension contiguous), c_values float32 [n] on the device ->
     ``sums`` float64 [n, 2] (sum of squared errors, sum of squares),
     accumulated into ``sums`` if given, else into a new zeroed tensor."""
+    _need(x, "x", _ROWS, contiguous=False)
     rows = x.reshape(-1, HEAD_DIM) if x.dim() != 2 else x
     if rows.shape[-1] != HEAD_DIM or rows.stride(-1) != 1:
         raise ValueError("rows of 128 contiguous channels expected")
     c = c_values.to(device=x.device, dtype=torch.float32).contiguous()
     if sums is None:
         sums = torch.zeros((c.numel(), 2), dtype=torch.float64, device=x.device)
+    _need(sums, "sums", (torch.float64,), (c.numel(), 2))
     st = lib.uq_quantize_error(_ptr(rows), _DT[x.dtype], rows.shape[0], rows.stride(0), int(bool(rotate)),
                                int(bool(pow2)), c.numel(), _ptr(c), _ptr(sums), _stream(stream))
     _check(st, "uq_quantize_error")
@@ -276,12 +352,15 @@ def alloc_workspace(desc: CacheDesc, batch, num_q_heads, max_context, partition_
 def decode_attention(desc: CacheDesc, q, codes, scales, page_table, context_lens, max_context, softmax_scale=None,
                      partition_tokens=0, workspace=None, out=None, out_dtype=torch.float32, q_dtype=None,
                      stream=None):
-    """q: [B, Hq, 128] -> out [B, Hq, 128]."""
-    B, Hq = q.shape[0], q.shape[1]
+    """q: [B, Hq, head_dim] -> out [B, Hq, head_dim]."""
+    B, Hq = _q_out(q, out, desc.head_dim)
+    _pools(desc, codes, scales)
+    _table(page_table, context_lens, B)
     if softmax_scale is None:
         softmax_scale = desc.head_dim ** -0.5
     if workspace is None:
         workspace = alloc_workspace(desc, B, Hq, max_context, partition_tokens, q.device)
+    _need(workspace, "workspace", _U8)
     if out is None:
         out = torch.empty((B, Hq, desc.head_dim), dtype=out_dtype, device=q.device)
     d = desc.c_struct()
@@ -297,7 +376,10 @@ def decode_attention(desc: CacheDesc, q, codes, scales, page_table, context_lens
 def decode_partials(desc: CacheDesc, q, codes, scales, page_table, context_lens, max_context, softmax_scale,
                     partition_tokens, workspace, out, q_dtype=None, stream=None):
     """First launch of decode_attention (partition kernel)."""
-    B, Hq = q.shape[0], q.shape[1]
+    B, Hq = _q_out(q, out, desc.head_dim)
+    _pools(desc, codes, scales)
+    _table(page_table, context_lens, B)
+    _need(workspace, "workspace", _U8)
     d = desc.c_struct()
     qdt = _DT[q.dtype] if q_dtype is None else q_dtype
     st = lib.uq_decode_partials(ctypes.byref(d), _ptr(q), qdt, B, Hq, _ptr(codes), _ptr(scales), _ptr(page_table),
@@ -307,16 +389,26 @@ def decode_partials(desc: CacheDesc, q, codes, scales, page_table, context_lens,
     return out
 
 
+def _new_token(k_new, v_new, B, num_kv_heads):
+    """The decode step's new tokens: [B, Hkv, 128] each, contiguous, one dtype."""
+    _need(k_new, "k_new", _ROWS, (B, num_kv_heads, HEAD_DIM))
+    _need(v_new, "v_new", (k_new.dtype,), (B, num_kv_heads, HEAD_DIM))
+
+
 def decode_step(desc: CacheDesc, q, k_new, v_new, codes, scales, page_table, context_lens, max_context,
                 softmax_scale=None, partition_tokens=0, workspace=None, out=None, out_dtype=torch.float32,
                 q_dtype=None, stream=None, partials_only=False):
     """Write each sequence's new token (k_new, v_new: [B, Hkv, 128]) at its
     last position, then decode attention; q: [B, Hq, 128] -> out."""
-    B, Hq = q.shape[0], q.shape[1]
+    B, Hq = _q_out(q, out, desc.head_dim)
+    _pools(desc, codes, scales)
+    _table(page_table, context_lens, B)
+    _new_token(k_new, v_new, B, desc.num_kv_heads)
     if softmax_scale is None:
         softmax_scale = desc.head_dim ** -0.5
     if workspace is None:
         workspace = alloc_workspace(desc, B, Hq, max_context, partition_tokens, q.device)
+    _need(workspace, "workspace", _U8)
     if out is None:
         out = torch.empty((B, Hq, desc.head_dim), dtype=out_dtype, device=q.device)
     d = desc.c_struct()
@@ -332,6 +424,9 @@ def decode_step(desc: CacheDesc, q, k_new, v_new, codes, scales, page_table, con
 def decode_merge(desc: CacheDesc, batch, num_q_heads, context_lens, max_context, partition_tokens, workspace, out,
                  stream=None):
     """Second launch of decode_attention (merge of the partitions)."""
+    _need(context_lens, "context_lens", _I32, (batch,))
+    _need(workspace, "workspace", _U8)
+    _need(out, "out", _OUT, (batch, num_q_heads, desc.head_dim))
     d = desc.c_struct()
     st = lib.uq_decode_merge(ctypes.byref(d), batch, num_q_heads, _ptr(context_lens), max_context, partition_tokens,
                              _ptr(workspace), workspace.numel(), _ptr(out), _DT[out.dtype], _stream(stream))
@@ -385,11 +480,18 @@ class RefCacheDesc:
         return cache
 
 
+def _cache(desc: RefCacheDesc, cache):
+    _need(cache, "cache", _U8, min_numel=desc.cache_bytes())
+
+
 def ref_write_kv(desc: RefCacheDesc, k, v, slot_mapping, cache, page_table=None, max_pages_per_seq=0,
                  token_stride=None, stream=None):
+    token_stride = _rows(k, v, desc.num_kv_heads, desc.head_dim, token_stride)
     T = k.shape[0]
-    if token_stride is None:
-        token_stride = k.stride(0)
+    _need(slot_mapping, "slot_mapping", (torch.int64,), (T,))
+    _cache(desc, cache)
+    if page_table is not None:
+        _need(page_table, "page_table", _I32, (None, None))
     num_seqs = 0 if page_table is None else page_table.shape[0]
     mpps = 0 if page_table is None else (max_pages_per_seq or page_table.shape[1])
     d = desc.c_struct()
@@ -410,11 +512,14 @@ def ref_alloc_workspace(desc: RefCacheDesc, batch, num_q_heads, max_context, par
 
 def ref_decode_attention(desc: RefCacheDesc, q, cache, page_table, context_lens, max_context, softmax_scale=None,
                          partition_tokens=0, workspace=None, out=None, out_dtype=torch.float32, stream=None):
-    B, Hq = q.shape[0], q.shape[1]
+    B, Hq = _q_out(q, out, HEAD_DIM)
+    _cache(desc, cache)
+    _table(page_table, context_lens, B)
     if softmax_scale is None:
         softmax_scale = HEAD_DIM ** -0.5
     if workspace is None:
         workspace = ref_alloc_workspace(desc, B, Hq, max_context, partition_tokens, q.device)
+    _need(workspace, "workspace", _U8)
     if out is None:
         out = torch.empty((B, Hq, HEAD_DIM), dtype=out_dtype, device=q.device)
     d = desc.c_struct()
@@ -428,7 +533,10 @@ def ref_decode_attention(desc: RefCacheDesc, q, cache, page_table, context_lens,
 
 def ref_decode_partials(desc: RefCacheDesc, q, cache, page_table, context_lens, max_context, softmax_scale,
                         partition_tokens, workspace, out, stream=None):
-    B, Hq = q.shape[0], q.shape[1]
+    B, Hq = _q_out(q, out, HEAD_DIM)
+    _cache(desc, cache)
+    _table(page_table, context_lens, B)
+    _need(workspace, "workspace", _U8)
     d = desc.c_struct()
     st = lib.uq_ref_decode_partials(ctypes.byref(d), _ptr(q), _DT[q.dtype], B, Hq, _ptr(cache), _ptr(page_table),
                                     page_table.shape[1], _ptr(context_lens), max_context, softmax_scale,
@@ -440,6 +548,9 @@ def ref_decode_partials(desc: RefCacheDesc, q, cache, page_table, context_lens, 
 
 def ref_decode_merge(desc: RefCacheDesc, batch, num_q_heads, context_lens, max_context, partition_tokens, workspace,
                      out, stream=None):
+    _need(context_lens, "context_lens", _I32, (batch,))
+    _need(workspace, "workspace", _U8)
+    _need(out, "out", _OUT, (batch, num_q_heads, HEAD_DIM))
     d = desc.c_struct()
     st = lib.uq_ref_decode_merge(ctypes.byref(d), batch, num_q_heads, _ptr(context_lens), max_context,
                                  partition_tokens, _ptr(workspace), workspace.numel(), _ptr(out), _DT[out.dtype],
@@ -451,11 +562,15 @@ def ref_decode_merge(desc: RefCacheDesc, batch, num_q_heads, context_lens, max_c
 def ref_decode_step(desc: RefCacheDesc, q, k_new, v_new, cache, page_table, context_lens, max_context,
                     softmax_scale=None, partition_tokens=0, workspace=None, out=None, out_dtype=torch.float32,
                     stream=None, partials_only=False):
-    B, Hq = q.shape[0], q.shape[1]
+    B, Hq = _q_out(q, out, HEAD_DIM)
+    _cache(desc, cache)
+    _table(page_table, context_lens, B)
+    _new_token(k_new, v_new, B, desc.num_kv_heads)
     if softmax_scale is None:
         softmax_scale = HEAD_DIM ** -0.5
     if workspace is None:
         workspace = ref_alloc_workspace(desc, B, Hq, max_context, partition_tokens, q.device)
+    _need(workspace, "workspace", _U8)
     if out is None:
         out = torch.empty((B, Hq, HEAD_DIM), dtype=out_dtype, device=q.device)
     d = desc.c_struct()
@@ -490,14 +605,23 @@ def cascade_workspace_bytes(num_kv_heads, batch, num_q_heads, max_context, prefi
                                                      ctypes.byref(sp)))
 
 
+def _prefix(prefix: SharedPrefix, B):
+    _need(prefix.pages, "prefix.pages", _I32, (None,), min_numel=max(prefix.num_tokens, 0) // PAGE_SIZE)
+    _need(prefix.lens, "prefix.lens", _I32, (B,))
+
+
 def _cascade_common(q, k_new, v_new, max_context, num_kv_heads, prefix, softmax_scale, partition_tokens, workspace,
                     out, out_dtype):
-    B, Hq = q.shape[0], q.shape[1]
+    B, Hq = _q_out(q, out, HEAD_DIM)
+    _prefix(prefix, B)
+    if k_new is not None or v_new is not None:
+        _new_token(k_new, v_new, B, num_kv_heads)
     if softmax_scale is None:
         softmax_scale = HEAD_DIM ** -0.5
     if workspace is None:
         n = cascade_workspace_bytes(num_kv_heads, B, Hq, max_context, prefix, partition_tokens)
         workspace = torch.empty(n, dtype=torch.uint8, device=q.device)
+    _need(workspace, "workspace", _U8)
     if out is None:
         out = torch.empty((B, Hq, HEAD_DIM), dtype=out_dtype, device=q.device)
     ndt = UQ_F32 if k_new is None else _DT[k_new.dtype]
@@ -510,6 +634,8 @@ def decode_cascade(desc: CacheDesc, q, codes, scales, page_table, context_lens, 
     """Decode attention (or, with k_new/v_new, a decode step) with a shared prefix."""
     B, Hq, scale, workspace, out, ndt = _cascade_common(q, k_new, v_new, max_context, desc.num_kv_heads, prefix,
                                                         softmax_scale, partition_tokens, workspace, out, out_dtype)
+    _pools(desc, codes, scales)
+    _table(page_table, context_lens, B)
     d = desc.c_struct()
     sp = prefix.c_struct()
     fn = lib.uq_decode_cascade_partials if partials_only else lib.uq_decode_cascade
@@ -522,6 +648,10 @@ def decode_cascade(desc: CacheDesc, q, codes, scales, page_table, context_lens, 
 
 def decode_cascade_merge(desc: CacheDesc, batch, num_q_heads, context_lens, max_context, prefix: SharedPrefix,
                          partition_tokens, workspace, out, stream=None):
+    _need(context_lens, "context_lens", _I32, (batch,))
+    _prefix(prefix, batch)
+    _need(workspace, "workspace", _U8)
+    _need(out, "out", _OUT, (batch, num_q_heads, HEAD_DIM))
     d = desc.c_struct()
     sp = prefix.c_struct()
     st = lib.uq_decode_cascade_merge(ctypes.byref(d), batch, num_q_heads, _ptr(context_lens), max_context,
@@ -536,6 +666,8 @@ def ref_decode_cascade(desc: RefCacheDesc, q, cache, page_table, context_lens, m
                        k_new=None, v_new=None, stream=None, partials_only=False):
     B, Hq, scale, workspace, out, ndt = _cascade_common(q, k_new, v_new, max_context, desc.num_kv_heads, prefix,
                                                         softmax_scale, partition_tokens, workspace, out, out_dtype)
+    _cache(desc, cache)
+    _table(page_table, context_lens, B)
     d = desc.c_struct()
     sp = prefix.c_struct()
     fn = lib.uq_ref_decode_cascade_partials if partials_only else lib.uq_ref_decode_cascade
@@ -548,6 +680,10 @@ def ref_decode_cascade(desc: RefCacheDesc, q, cache, page_table, context_lens, m
 
 def ref_decode_cascade_merge(desc: RefCacheDesc, batch, num_q_heads, context_lens, max_context, prefix: SharedPrefix,
                              partition_tokens, workspace, out, stream=None):
+    _need(context_lens, "context_lens", _I32, (batch,))
+    _prefix(prefix, batch)
+    _need(workspace, "workspace", _U8)
+    _need(out, "out", _OUT, (batch, num_q_heads, HEAD_DIM))
     d = desc.c_struct()
     sp = prefix.c_struct()
     st = lib.uq_ref_decode_cascade_merge(ctypes.byref(d), batch, num_q_heads, _ptr(context_lens), max_context,
