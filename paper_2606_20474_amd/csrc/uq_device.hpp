@@ -6,7 +6,6 @@
 //                     section "Ultra-TurboQuant" and Algorithm 1).
 //  * ue8m0_exponent   E = round(log2(c*m)) from the fp32 bits (paper,
 //                     section "Constant-Optimized Scaling").
-//  * e2m1_code        nearest E2M1 level of x / 2^E, ties to the even code.
 //  * e4m3_byte        OCP e4m3fn, round to nearest even, saturating.
 //  * load_x8, encode_token, place_token, store_token
 //                     one token's K/V from the input rows into a cache tile.
@@ -131,17 +130,6 @@ __device__ __forceinline__ int ue8m0_exponent(float m, float c) {
     return E;
 }
 
-// Code of x on the E2M1 grid {0,.5,1,1.5,2,3,4,6} after division by 2^E:
-// the magnitude index counts the decision thresholds passed, strict at
-// thresholds whose lower neighbour has the even index and inclusive where
-// the upper neighbour has it (ties to even); |t| > 5 saturates to 6.  The
-// sign bit of x is kept.  x * 2^-E is exact (a power-of-two scaling).
-__device__ __forceinline__ uint32_t e2m1_code(float x, int E) {
-    const float a = __builtin_fabsf(__builtin_ldexpf(x, -E));
-    uint32_t k = (a > 0.25f) + (a >= 0.75f) + (a > 1.25f) + (a >= 1.75f) + (a > 2.5f) + (a >= 3.5f) + (a > 5.0f);
-    return k | ((f32_bits(x) >> 28) & 8u);
-}
-
 // OCP e4m3fn byte of x, round to nearest even, saturating to +-448.
 // Normal range: keep 3 fraction bits of the fp32 pattern with RNE (a carry
 // moves into the exponent by itself) and rebias 127 -> 7.  Below 2^-6 the
@@ -219,9 +207,15 @@ __device__ __forceinline__ uint32_t quantize_x8(float (&x)[8], int L, float c, b
     m = __builtin_fmaxf(m, __shfl_xor(m, 2, 16));
     const int E = ue8m0_exponent(m, c);
     scale_byte = uint32_t(E + 127);
-    uint32_t w = 0;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) w |= e2m1_code(x[i], E) << (4 * i);
+    // E2M1 codes of x / 2^E by the hardware conversion (nearest level, ties
+    // to the even code, saturating at 6, sign kept), channel order, low
+    // nibble first; 2^E exactly, subnormal for E = -127
+    const float sc = __builtin_ldexpf(1.0f, E);
+    uint32_t w = 0u;
+    w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, x[0], x[1], sc, 0);
+    w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, x[2], x[3], sc, 1);
+    w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, x[4], x[5], sc, 2);
+    w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(w, x[6], x[7], sc, 3);
     return w;
 }
 

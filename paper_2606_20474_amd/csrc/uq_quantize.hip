@@ -83,7 +83,8 @@ __device__ __forceinline__ void wht128_x32(float (&x)[4][8], int L) { wht_quad<4
 // E2M1 codes of the lane's 8 channels of the group in w[j] (channel order,
 // low nibble first) by the hardware conversion, which rounds x / 2^E_j to
 // the nearest E2M1 level with ties to the even code, saturates at 6 and
-// keeps the sign: the same codes as e2m1_code.
+// keeps the sign (checked against a threshold encoder over every tie, both
+// zeros, subnormal inputs and scales 2^-127 .. 2^127).
 template <int NG>
 __device__ __forceinline__ void quantize_xq(float (&x)[NG][8], int L, float c, bool rotate, uint32_t (&w)[NG],
                                             int (&E)[NG]) {
