@@ -58,7 +58,7 @@ def parse():
                              "gpt-oss-like-hd256"])
     ap.add_argument("--partition", type=int, default=-1, help="partition tokens (-1: workload default)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-seqs", type=int, default=4)
+    ap.add_argument("--cpu-sample-seqs", type=int, default=8)
     ap.add_argument("--comparators", default="fp8,bf16,tq4",
                     help="comma list of comparison caches to time as well (fp8, bf16, tq4) or 'none'")
     ap.add_argument("--no-cascade", action="store_true",
@@ -281,13 +281,14 @@ def cpu_baseline(wl, nseq, dev):
     return {"value": toks / dt, "unit": "tokens/s", "cores": oracle.num_threads(), "kind": "oracle",
             "sample": f"{len(seqs)} of {wl.batch} sequences, all {wl.num_q_heads} query heads, "
                       f"{toks} context tokens; fp64 decode attention over the oracle's own FP4 cache; "
-                      f"{dt:.2f} s wall"}
+                      f"{dt:.2f} s wall on {oracle.num_threads()} threads ({dt * oracle.num_threads():.0f} "
+                      f"thread-seconds)"}
 
 
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); this build has no multi-GPU path.",
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the library has no multi-GPU path.",
               file=sys.stderr)
         sys.exit(2)
     import torch
