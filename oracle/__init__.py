@@ -24,12 +24,21 @@ _lib = None
 
 
 def lib():
-    """Load ``liboracle.so``, compiling it first if it is not there."""
+    """Load ``liboracle.so``, compiling it first if it is not there.  The
+    environment variable UQ_ORACLE_LIB names another build of the same
+    source instead (the planted-mistake test loads deliberately broken
+    copies that way, in subprocesses of its own)."""
     global _lib
     if _lib is None:
-        if not os.path.exists(_build.LIB):
-            _build.build()
-        L = ctypes.CDLL(_build.LIB)
+        path = os.environ.get("UQ_ORACLE_LIB")
+        if path:
+            if not os.path.exists(path):
+                raise FileNotFoundError(f"UQ_ORACLE_LIB={path} does not exist")
+        else:
+            path = _build.LIB
+            if not os.path.exists(path):
+                _build.build()
+        L = ctypes.CDLL(path)
         vp, i64, i32, f32, f64 = ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_float, ctypes.c_double
         L.uqo_num_threads.restype = i32
         L.uqo_wht128_f32.argtypes = [vp, i64]

@@ -250,6 +250,25 @@ def test_e4m3_matches_torch_cast_in_range():
     assert np.array_equal(got, ref)
 
 
+def test_e4m3_midpoints_go_to_even_code():
+    """Every exact midpoint between adjacent finite E4M3 values (4
+    significant bits, so exact in fp32), both signs: round to nearest even
+    picks the neighbour with the even code, as torch's float8_e4m3fn cast
+    does."""
+    n = 0
+    for b in range(0x7E):
+        lo, hi = oracle.e4m3_value(b), oracle.e4m3_value(b + 1)
+        mid = np.float32((lo + hi) / 2)
+        assert float(mid) == (lo + hi) / 2
+        even = b if b % 2 == 0 else b + 1
+        for sign, x in ((0x00, mid), (0x80, -mid)):
+            got = oracle.e4m3_encode(x)
+            ref = int(torch.tensor([float(x)], dtype=torch.float32).to(torch.float8_e4m3fn).view(torch.uint8)[0])
+            assert got == (sign | even) == ref, (b, float(x), got, ref)
+            n += 1
+    assert n == 2 * 0x7E
+
+
 def test_e4m3_saturates():
     assert oracle.e4m3_encode(np.float32(1e4)) == 0x7E
     assert oracle.e4m3_encode(np.float32(-470.0)) == 0xFE
