@@ -1,11 +1,10 @@
 """Planted mistakes in the oracle, on the CPU: each plausible mistake below
 is written into a copy of oracle/uq_oracle.c, the copy is built with the
-oracle's own flags, and the oracle pins (tests/test_oracle_pins.py) run
+oracle's own flags, and every CPU pin of the oracle (PIN_FILES) runs
 against it in a subprocess (UQ_ORACLE_LIB).  Every mistake must make at
 least one pin fail, and the unchanged copy must pass them all, so the pins
 are shown to pin the oracle and not only to agree with it."""
 import os
-import shutil
 import subprocess
 import sys
 from concurrent.futures import ThreadPoolExecutor
@@ -35,7 +34,13 @@ MISTAKES = {
                              "const int hk = hq % num_kv_heads;\n            const int ctx = context_lens[b];")],
     "softmax scale dropped": [("s[j] = softmax_scale * dot;", "s[j] = dot;")],
     "output not rotated back": [("if (rotate_v) uqo_wht_f64(acc, o, d);", "if (0) uqo_wht_f64(acc, o, d);")],
+    "TQ4 key norm not square-rooted": [("const float n = sqrtf(part[0]);", "const float n = part[0];")],
+    "TQ4 value zero point not BF16": [("const float z = uqo_bf16_rne(mn);", "const float z = mn;")],
+    "TQ4 value grid of 16 steps": [("const float s = uqo_bf16_rne(d / 15.0f);", "const float s = uqo_bf16_rne(d / 16.0f);")],
+    "TQ4 V tokens reversed in a dword": [("4 * (t % 4) + (c % 8) / 2; }", "4 * (3 - t % 4) + (c % 8) / 2; }")],
 }
+# every CPU pin of the oracle
+PIN_FILES = ["test_oracle_pins.py", "test_oracle_headdim.py", "test_tq4_oracle.py", "test_calibration_cpu.py"]
 
 
 def run_pins(src_text, workdir, name):
@@ -48,8 +53,8 @@ def run_pins(src_text, workdir, name):
         f.write(src_text)
     lib = oracle_build.build(src=src, lib=os.path.join(d, "liboracle.so"))
     env = dict(os.environ, UQ_ORACLE_LIB=lib, OMP_NUM_THREADS="2")
-    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider",
-                        os.path.join(ROOT, "tests", "test_oracle_pins.py")],
+    r = subprocess.run([sys.executable, "-m", "pytest", "-x", "-q", "-p", "no:cacheprovider"] +
+                       [os.path.join(ROOT, "tests", f) for f in PIN_FILES],
                        cwd=ROOT, env=env, capture_output=True, text=True, timeout=600)
     return r.returncode, (r.stdout + r.stderr)[-600:]
 
