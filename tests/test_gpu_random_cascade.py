@@ -21,7 +21,7 @@ from paper_2606_20474_amd import workloads
 
 pytestmark = pytest.mark.gpu
 
-CASES = 16
+CASES = 32
 SCALE = 1 / math.sqrt(128)
 
 

@@ -14,7 +14,7 @@ from paper_2606_20474_amd import workloads
 
 pytestmark = pytest.mark.gpu
 
-CASES = 24
+CASES = 64
 
 
 def params(i):

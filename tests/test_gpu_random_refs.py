@@ -20,7 +20,7 @@ from test_gpu_ref_caches import MAX_ABS, REL_L2, attention, query_values, seq_va
 pytestmark = pytest.mark.gpu
 
 SCALE = 1 / math.sqrt(128)
-CASES = 8
+CASES = 16
 
 
 def params(fmt, i):

@@ -16,7 +16,7 @@ import oracle
 
 pytestmark = pytest.mark.gpu
 
-CASES = 16
+CASES = 32
 
 
 def params(i):
