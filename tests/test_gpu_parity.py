@@ -177,6 +177,47 @@ def test_prepare_query_bit_exact(uq):
         assert np.array_equal(got, ref), dt
 
 
+def e4m3_tie_rows():
+    """Query rows c * e_j whose rotation lands every channel on an exact
+    midpoint between two adjacent E4M3 values: the butterfly of c e_j is
+    +-c in every channel (additions of zeros are exact), then one fp32
+    multiply by fl32(1/sqrt(128)), so c is chosen with fl32(c * r) equal to
+    the midpoint.  One row per midpoint and sign, j varied so that the
+    Hadamard row's signs vary too.  Such a c exists for 96 of the 126
+    midpoints: where c = m / r has the larger exponent, consecutive products
+    fl32(c * r) lie about 1.4 ulp of m apart and can step over m."""
+    r = np.float32(1.0 / math.sqrt(128.0))
+    rows = []
+    for b in range(0x7E):
+        m = np.float32((oracle.e4m3_value(b) + oracle.e4m3_value(b + 1)) / 2)
+        c0 = np.float32(float(m) / float(r))
+        cands = [c0]
+        up = down = c0
+        for _ in range(8):
+            up = np.nextafter(up, np.float32(np.inf))
+            down = np.nextafter(down, np.float32(-np.inf))
+            cands += [up, down]
+        for c in cands:
+            if np.float32(c * r) == m:
+                for sign in (1, -1):
+                    row = np.zeros(128, np.float32)
+                    row[(b * 7 + (sign > 0)) % 128] = sign * c
+                    rows.append(row)
+                break
+    return np.stack(rows)
+
+
+def test_prepare_query_ties_go_to_even_code(uq):
+    q = e4m3_tie_rows()
+    assert len(q) == 2 * 96, len(q)
+    log(f"prepare_query: {len(q)} rows on exact E4M3 midpoints")
+    desc = uq.CacheDesc(num_kv_heads=1, num_pages=1)
+    got = uq.prepare_query(desc, torch.as_tensor(q, device=torch.device("cuda:0"))).cpu().numpy()
+    ref = oracle.prepare_query(q)
+    assert np.array_equal(got, ref)
+    assert np.all((got & 0x7F) % 2 == 0), "a tie rounded to an odd code"
+
+
 # --------------------------------------------------------------------------
 # decode attention
 # --------------------------------------------------------------------------
