@@ -177,6 +177,38 @@ def test_prepare_query_bit_exact(uq):
         assert np.array_equal(got, ref), dt
 
 
+def test_write_e2m1_ties_go_to_even_code(uq):
+    """V rows (rotate_v off, so V is encoded as given) whose groups hold
+    every E2M1 midpoint of the scaled grid: each group's first channel is
+    6 * 2^k, which sets E = k (fl32(0.156 * 6) rounds to exponent 0); the
+    others are +-{0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5} * 2^k, both zeros,
+    exact levels and values past 6 (at most 9, so that the group maximum
+    keeps E = k).  Every pool byte against the oracle."""
+    dev = torch.device("cuda:0")
+    ties = [0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0]
+    group = [6.0] + ties + [-t for t in ties] + [0.0, -0.0, 0.5, -0.5, -1.5, 4.0, -6.0, 7.5, -9.0, 3.0, -2.0, 1.0,
+                                                 0.2499, 0.7501, -5.0001, 4.9999, 2.0]
+    assert len(group) == 32
+    rows = []
+    for k in (-30, -8, 0, 7, 40):
+        for rot in range(4):   # the values move between channels, the anchor between groups
+            g = np.roll(np.array(group, np.float64) * 2.0 ** k, rot * 5)
+            rows.append(np.concatenate([np.roll(g, 3 * j) for j in range(4)]))
+    v = np.stack(rows).astype(np.float32)
+    assert np.all(np.isfinite(v))
+    T = len(v)
+    kv = torch.as_tensor(v).reshape(T, 1, 128)
+    slots = np.arange(T, dtype=np.int64)
+    pages = (T + 15) // 16
+    desc = uq.CacheDesc(num_kv_heads=1, num_pages=pages, rotate_v=False)
+    codes, scales = desc.alloc_pools(dev, fill=0x77)
+    uq.quantize_kv(desc, kv.to(dev), kv.to(dev), torch.as_tensor(slots, device=dev), codes, scales)
+    pools = oracle.alloc_pools(pages, 1, fill=0x77)
+    oracle.quantize_kv(kv.numpy(), kv.numpy(), slots, pages, rotate_v=False, pools=pools)
+    assert np.array_equal(scales.cpu().numpy(), pools[1])
+    assert np.array_equal(codes.cpu().numpy(), pools[0])
+
+
 def e4m3_tie_rows():
     """Query rows c * e_j whose rotation lands every channel on an exact
     midpoint between two adjacent E4M3 values: the butterfly of c e_j is
