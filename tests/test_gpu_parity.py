@@ -177,7 +177,9 @@ def test_prepare_query_bit_exact(uq):
         assert np.array_equal(got, ref), dt
 
 
-def test_write_e2m1_ties_go_to_even_code(uq):
+@pytest.mark.parametrize("d", [64, 128, 256])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_write_e2m1_ties_go_to_even_code(uq, d, dtype):
     """V rows (rotate_v off, so V is encoded as given) whose groups hold
     every E2M1 midpoint of the scaled grid: each group's first channel is
     6 * 2^k, which sets E = k (fl32(0.156 * 6) rounds to exponent 0); the
@@ -193,18 +195,18 @@ def test_write_e2m1_ties_go_to_even_code(uq):
     for k in (-30, -8, 0, 7, 40):
         for rot in range(4):   # the values move between channels, the anchor between groups
             g = np.roll(np.array(group, np.float64) * 2.0 ** k, rot * 5)
-            rows.append(np.concatenate([np.roll(g, 3 * j) for j in range(4)]))
+            rows.append(np.concatenate([np.roll(g, 3 * j) for j in range(d // 32)]))
     v = np.stack(rows).astype(np.float32)
     assert np.all(np.isfinite(v))
     T = len(v)
-    kv = torch.as_tensor(v).reshape(T, 1, 128)
+    kv = torch.as_tensor(v).reshape(T, 1, d).to(dtype)
     slots = np.arange(T, dtype=np.int64)
     pages = (T + 15) // 16
-    desc = uq.CacheDesc(num_kv_heads=1, num_pages=pages, rotate_v=False)
+    desc = uq.CacheDesc(num_kv_heads=1, num_pages=pages, rotate_v=False, head_dim=d)
     codes, scales = desc.alloc_pools(dev, fill=0x77)
     uq.quantize_kv(desc, kv.to(dev), kv.to(dev), torch.as_tensor(slots, device=dev), codes, scales)
-    pools = oracle.alloc_pools(pages, 1, fill=0x77)
-    oracle.quantize_kv(kv.numpy(), kv.numpy(), slots, pages, rotate_v=False, pools=pools)
+    pools = oracle.alloc_pools(pages, 1, fill=0x77, head_dim=d)
+    oracle.quantize_kv(kv.float().numpy(), kv.float().numpy(), slots, pages, rotate_v=False, pools=pools)
     assert np.array_equal(scales.cpu().numpy(), pools[1])
     assert np.array_equal(codes.cpu().numpy(), pools[0])
 
