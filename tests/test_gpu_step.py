@@ -107,6 +107,35 @@ def compare_step(uq, fmt, wl, dev, part, new_dtype=torch.float32):
     return out_one
 
 
+def test_step_encodes_e2m1_ties_like_the_write(uq):
+    """New V tokens (rotate_v off, so encoded as given) whose groups hold
+    every E2M1 midpoint at five exponents: the step's in-kernel encoder must
+    write the same bytes as uq_quantize_kv, whose ties are pinned against
+    the oracle."""
+    dev = torch.device("cuda:0")
+    ties = [0.25, 0.75, 1.25, 1.75, 2.5, 3.5, 5.0]
+    group = np.array([6.0] + ties + [-t for t in ties] + [0.0, -0.0, 0.5, -0.5, -1.5, 4.0, -6.0, 7.5, -9.0, 3.0,
+                                                          -2.0, 1.0, 0.2499, 0.7501, -5.0001, 4.9999, 2.0])
+    rows = [np.concatenate([np.roll(group * 2.0 ** k, 5 * r + 3 * j) for j in range(4)])
+            for k in (-30, -8, 0, 7, 40) for r in range(4)]
+    B = len(rows)
+    wl = workloads.custom(B, 8, 1, [1 + 37 * i for i in range(B)], seed=91, paging="random", rotate_v=False)
+    q = wl.q.to(dev)
+    pt = torch.as_tensor(wl.page_table, device=dev)
+    ctx = torch.as_tensor(wl.context_lens, device=dev)
+    v_new = torch.as_tensor(np.stack(rows).astype(np.float32)).reshape(B, 1, 128).to(dev)
+    k_new = torch.randn((B, 1, 128), generator=torch.Generator(device=dev).manual_seed(92), device=dev)
+    two = Cache(uq, "fp4", wl, dev)
+    two.write(k_new, v_new, last_slots(wl, dev))
+    out_two = two.attend(q, pt, ctx, 64)
+    one = Cache(uq, "fp4", wl, dev)
+    out_one = one.step(q, k_new, v_new, pt, ctx, 64)
+    torch.cuda.synchronize()
+    for a, b in zip(one.bytes(), two.bytes()):
+        assert np.array_equal(a, b), "pools differ"
+    assert torch.equal(out_one, out_two)
+
+
 @pytest.mark.parametrize("fmt", ["fp4", "fp8", "bf16", "tq4"])
 @pytest.mark.parametrize("partition", [0, 32, 64, 256])
 def test_step_equals_write_then_decode(uq, fmt, partition):
