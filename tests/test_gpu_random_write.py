@@ -63,7 +63,8 @@ def test_random_write(uq, i):
 
     # slots: unique physical targets, some padding and some out of range
     if p["paged"]:
-        S, P = int(rng.integers(1, 5)), max(1, num_pages // 5)
+        S = min(int(rng.integers(1, 5)), num_pages)
+        P = max(1, min(num_pages // 5, num_pages // S))   # S * P <= num_pages
         page_table = rng.permutation(num_pages)[:S * P].reshape(S, P).astype(np.int32)
         logical = rng.permutation(S * P * 16)[:T] if T <= S * P * 16 else None
         if logical is None:
