@@ -216,6 +216,23 @@ def _table(page_table, context_lens, B):
     _need(context_lens, "context_lens", _I32, (B,))
 
 
+def _write_table(page_table, max_pages_per_seq):
+    """Page table of a write (int32 [num_seqs, width]) and the row length
+    the kernel indexes it with: 0 selects the width; an explicit value must
+    lie in 1..width, since the kernel reads page_table[seq * mpps + page]
+    and a longer row would read past the tensor.  Returns (num_seqs, mpps),
+    (0, 0) without a table."""
+    if page_table is None:
+        return 0, 0
+    if isinstance(page_table, torch.Tensor) and page_table.dim() == 2:
+        width = page_table.shape[1]
+        mpps = max_pages_per_seq or width
+        if not 1 <= mpps <= width:
+            raise ValueError(f"max_pages_per_seq: {mpps}, expected 1..{width} (the page table's row length)")
+    _need(page_table, "page_table", _I32, (None, None))
+    return page_table.shape[0], max_pages_per_seq or page_table.shape[1]
+
+
 def _q_out(q, out, head_dim):
     _need(q, "q", _QUERY, (None, None, head_dim))
     B, Hq = q.shape[0], q.shape[1]
@@ -273,14 +290,11 @@ def _pools(desc: CacheDesc, codes, scales):
 def quantize_kv(desc: CacheDesc, k, v, slot_mapping, codes, scales, page_table=None, max_pages_per_seq=0,
                 token_stride=None, stream=None):
     """k, v: [T, Hkv, head_dim] (or strided rows); slot_mapping int64 [T]."""
+    num_seqs, mpps = _write_table(page_table, max_pages_per_seq)
     token_stride = _rows(k, v, desc.num_kv_heads, desc.head_dim, token_stride)
     T = k.shape[0]
     _need(slot_mapping, "slot_mapping", (torch.int64,), (T,))
     _pools(desc, codes, scales)
-    if page_table is not None:
-        _need(page_table, "page_table", _I32, (None, None))
-    num_seqs = 0 if page_table is None else page_table.shape[0]
-    mpps = 0 if page_table is None else (max_pages_per_seq or page_table.shape[1])
     d = desc.c_struct()
     st = lib.uq_quantize_kv(ctypes.byref(d), _ptr(k), _ptr(v), _DT[k.dtype], T, token_stride, _ptr(page_table),
                             num_seqs, mpps, _ptr(slot_mapping), _ptr(codes), _ptr(scales), _stream(stream))
@@ -486,14 +500,11 @@ def _cache(desc: RefCacheDesc, cache):
 
 def ref_write_kv(desc: RefCacheDesc, k, v, slot_mapping, cache, page_table=None, max_pages_per_seq=0,
                  token_stride=None, stream=None):
+    num_seqs, mpps = _write_table(page_table, max_pages_per_seq)
     token_stride = _rows(k, v, desc.num_kv_heads, desc.head_dim, token_stride)
     T = k.shape[0]
     _need(slot_mapping, "slot_mapping", (torch.int64,), (T,))
     _cache(desc, cache)
-    if page_table is not None:
-        _need(page_table, "page_table", _I32, (None, None))
-    num_seqs = 0 if page_table is None else page_table.shape[0]
-    mpps = 0 if page_table is None else (max_pages_per_seq or page_table.shape[1])
     d = desc.c_struct()
     st = lib.uq_ref_write_kv(ctypes.byref(d), _ptr(k), _ptr(v), _DT[k.dtype], T, token_stride, _ptr(page_table),
                              num_seqs, mpps, _ptr(slot_mapping), _ptr(cache), _stream(stream))

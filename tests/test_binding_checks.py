@@ -103,3 +103,22 @@ def test_ref_cache_too_small(dev):
     k = torch.zeros((4, 2, 128), device=dev)
     with pytest.raises(ValueError):
         uq.ref_write_kv(r, k, k, torch.arange(4, device=dev), cache[:-1])
+
+
+def test_write_page_table_row_length_is_bounded():
+    """An explicit max_pages_per_seq longer than the page table's rows would
+    make the write kernels read past the table: the binding refuses it
+    before any other check (no GPU needed); 0 takes the row length."""
+    pt = torch.zeros(2, 4, dtype=torch.int32)
+    for bad in (5, 100, -1):
+        with pytest.raises(ValueError, match="max_pages_per_seq"):
+            uq._write_table(pt, bad)
+    d = uq.CacheDesc(num_kv_heads=2, num_pages=4)
+    r = uq.RefCacheDesc(num_kv_heads=2, num_pages=4, fmt="fp8")
+    k = torch.zeros(3, 2, 128)
+    slots = torch.zeros(3, dtype=torch.int64)
+    u8 = torch.zeros(1 << 16, dtype=torch.uint8)
+    with pytest.raises(ValueError, match="max_pages_per_seq"):
+        uq.quantize_kv(d, k, k, slots, u8, u8, page_table=pt, max_pages_per_seq=5)
+    with pytest.raises(ValueError, match="max_pages_per_seq"):
+        uq.ref_write_kv(r, k, k, slots, u8, page_table=pt, max_pages_per_seq=5)
