@@ -65,6 +65,9 @@ def parse():
                     help="workloads with a shared prefix: read it per sequence instead of once per kv head")
     ap.add_argument("--no-write-path", action="store_true",
                     help="skip the quantize-on-write measurement (65536-token bf16 prefill + 256 appends)")
+    ap.add_argument("--no-flush", action="store_true",
+                    help="time the FP4 decode kernel back to back only (no 1 GiB write between launches)")
+    ap.add_argument("--no-probes", action="store_true", help="skip the achievable-bandwidth probes")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one device-to-device copy of this many MiB before the timed steps; its "
                          "FETCH_SIZE/WRITE_SIZE counters calibrate the HBM-traffic counters")
@@ -139,19 +142,33 @@ def alg_token_heads(wl, cascade):
     return (own + wl.shared_prefix_tokens) * wl.num_kv_heads
 
 
-def timed(step, steps, warmup, stream):
+FLUSH_BYTES = 1 << 30   # written and read between flushed steps: 4x the 256 MB last-level cache
+
+
+def timed(step, steps, warmup, stream, flush=None):
     """Run `warmup` untimed steps, then `steps` timed ones; returns (ms per
-    step over the whole timed region, mean ms between the event pair each
-    step receives).  Every step hands its pair to uq.time_next_launch, so it
-    brackets the timed kernel itself (the decode partition kernel, or the
-    quantize-on-write kernel): its start and end, as rocprofv3 reports them."""
+    step, mean ms between the event pair each step hands to
+    uq.time_next_launch, which brackets the timed kernel itself: the decode
+    partition kernel, a probe or the quantize-on-write kernel, start to end,
+    as rocprofv3 reports it).
+
+    Without `flush` the steps run back to back and the step time is the
+    whole timed region over `steps`.  With `flush` (a callable that writes
+    FLUSH_BYTES of device memory), every timed step is preceded by that
+    write and read, outside its events, so that no step finds the previous
+    one's bytes in L2 or the last-level cache; the step time is then the mean
+    over steps of an event pair recorded on the stream around the step's
+    launches."""
     import gc
     import torch
     for _ in range(warmup):
+        if flush is not None:
+            flush()
         step()
     torch.cuda.synchronize()
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
-    for a, b in evs:   # create the HIP events
+    around = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for a, b in evs + around:   # create the HIP events
         a.record(stream)
         b.record(stream)
     t_start = torch.cuda.Event(enable_timing=True)
@@ -164,15 +181,43 @@ def timed(step, steps, warmup, stream):
     try:
         t_start.record(stream)
         for i in range(steps):
+            if flush is not None:
+                flush()
+                around[i][0].record(stream)
             step(*evs[i])
+            if flush is not None:
+                around[i][1].record(stream)
         t_end.record(stream)
         torch.cuda.synchronize()
     finally:
         gc.enable()
-    return t_start.elapsed_time(t_end) / steps, float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    kernel_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
+    if flush is None:
+        return t_start.elapsed_time(t_end) / steps, kernel_ms
+    return float(np.mean([a.elapsed_time(b) for a, b in around])), kernel_ms
 
 
-def comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, args, dev, stream, prefix=None):
+def make_flush(dev):
+    """1 GiB written, then read back (uq_probe_stream_read): the write evicts
+    the workload's lines from L2 and the last-level cache, the read evicts
+    the write's dirty lines in turn, so that their write-back to HBM happens
+    here and not inside the next timed kernel (a write alone left up to
+    256 MB of dirty lines behind and added ~60 us of write-back traffic to
+    the next launch)."""
+    import torch
+    from paper_2606_20474_amd import uq
+    buf = torch.empty(FLUSH_BYTES, dtype=torch.uint8, device=dev)
+    sink = torch.empty(uq.PROBE_STREAM_BLOCKS, dtype=torch.int32, device=dev)
+    state = {"i": 0}
+
+    def flush():
+        state["i"] += 1
+        buf.fill_(state["i"] & 0xFF)
+        uq.probe_stream_read(buf, sink)
+    return flush
+
+
+def comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, args, dev, stream, flush, prefix=None):
     """The same step (uq_ref_decode_step: the new token of every sequence
     written by the partition launch, then the merge) over a comparison cache
     holding the same K/V: plain FP8 or BF16, or the Ultra-TQ codebook cache
@@ -209,16 +254,20 @@ def comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, args, dev, stream, p
             uq.ref_decode_cascade_merge(desc, wl.batch, wl.num_q_heads, ctx, wl.max_context, prefix, part, ws, out)
 
     ms_step, dec_ms = timed(step, args.steps, args.warmup, stream)
+    f_step, f_dec = timed(step, args.steps, args.warmup, stream, flush=flush)
     nbytes = alg_token_heads(wl, prefix is not None) * REF_BYTES_PER_TOKEN_HEAD[fmt]
     del cache, ws, out
     torch.cuda.empty_cache()
     return {"tokens_per_s": wl.total_tokens() / (ms_step * 1e-3), "ms_per_step": ms_step,
             "decode_kernel_ms": dec_ms, "bytes_per_token_head": REF_BYTES_PER_TOKEN_HEAD[fmt],
             "kv_gbs": nbytes / (dec_ms * 1e-3) / 1e9, "kv_frac": nbytes / (dec_ms * 1e-3) / 1e9 / HBM_PEAK_GBS,
+            "flushed": {"tokens_per_s": wl.total_tokens() / (f_step * 1e-3), "ms_per_step": f_step,
+                        "decode_kernel_ms": f_dec, "kv_gbs": nbytes / (f_dec * 1e-3) / 1e9,
+                        "kv_frac": nbytes / (f_dec * 1e-3) / 1e9 / HBM_PEAK_GBS},
             "traffic": profiled_traffic(wl.name, fmt)}
 
 
-def write_path(uq, args, dev, stream):
+def write_path(uq, args, dev, stream, flush):
     """Quantize-on-write (Algorithm 1, Write) on its own: a 65536-token bf16
     prefill of 8 KV heads into random pages, and a 1-token append for each of
     256 sequences through a page table. Algorithmic bytes of the prefill:
@@ -246,7 +295,8 @@ def write_path(uq, args, dev, stream):
         uq.quantize_kv(desc, ka, va, aslots, codes, scales, page_table=pt)
 
     n = max(args.steps, 10)
-    _, pre_ms = timed(prefill, n, 3, stream)
+    _, pre_ms = timed(prefill, n, 3, stream, flush=flush)
+    _, pre_ms_b2b = timed(prefill, n, 3, stream)
     _, app_ms = timed(append, n, 3, stream)
     rd = 2 * kp.numel() * kp.element_size()
     wr = ww.prefill_tokens * ww.num_kv_heads * KV_BYTES_PER_TOKEN_HEAD
@@ -254,7 +304,46 @@ def write_path(uq, args, dev, stream):
     return {"prefill_tokens": ww.prefill_tokens, "num_kv_heads": ww.num_kv_heads, "in_dtype": "bf16",
             "prefill_us": pre_ms * 1e3, "prefill_tokens_per_s": ww.prefill_tokens / (pre_ms * 1e-3),
             "prefill_bytes": rd + wr, "prefill_gbs": gbs, "prefill_frac": gbs / HBM_PEAK_GBS,
-            "append_seqs": ww.append_seqs, "append_us": app_ms * 1e3}
+            "prefill_us_back_to_back": pre_ms_b2b * 1e3, "append_seqs": ww.append_seqs, "append_us": app_ms * 1e3,
+            "timing": "prefill: kernel events, 1 GiB written and read back before every launch; append: back to back"}
+
+
+def achievable(uq, wl, desc, codes, scales, pt, ctx, part, alg_bytes, args, dev, stream, flush):
+    """What this GPU delivers to the decode kernel's reads, timed like the
+    kernel (flushed, kernel events): a plain stream of the launch's
+    algorithmic bytes and of 4 GiB (uq_probe_stream_read), and the decode
+    kernel's own page gather of this workload without its arithmetic
+    (uq_probe_page_gather: same grid, page walk, copies and LDS reads)."""
+    import torch
+    n = max(20, args.steps // 4)
+    res = {}
+    for name, nbytes in (("stream_same_bytes", alg_bytes), ("stream_4gib", 4 << 30)):
+        buf = torch.zeros((nbytes + 15) // 16 * 16, dtype=torch.uint8, device=dev)
+        sink = torch.empty(uq.PROBE_STREAM_BLOCKS, dtype=torch.int32, device=dev)
+
+        def probe(ev_a=None, ev_b=None):
+            if ev_a is not None:
+                uq.time_next_launch(ev_a, ev_b)
+            uq.probe_stream_read(buf, sink)
+        _, ms = timed(probe, n, 3, stream, flush=flush)
+        res[f"{name}_gbs"] = buf.numel() / (ms * 1e-3) / 1e9
+        res[f"{name}_bytes"] = buf.numel()
+        del buf, sink
+        torch.cuda.empty_cache()
+    if wl.head_dim == 128 and not wl.shared_prefix_tokens:
+        sink = torch.empty(4 * max(1, -(-wl.max_context // part)) * wl.num_kv_heads * wl.batch, dtype=torch.int32,
+                           device=dev)
+
+        def gather(ev_a=None, ev_b=None):
+            if ev_a is not None:
+                uq.time_next_launch(ev_a, ev_b)
+            uq.probe_page_gather(desc, wl.num_q_heads, codes, scales, pt, ctx, wl.max_context, part, sink)
+        _, ms = timed(gather, n, 3, stream, flush=flush)
+        res["page_gather_gbs"] = alg_bytes / (ms * 1e-3) / 1e9
+        res["page_gather_ms"] = ms
+    else:
+        res["page_gather_gbs"] = None   # the probe covers the plain head-size-128 grid
+    return res
 
 
 def cpu_baseline(wl, nseq, dev):
@@ -352,13 +441,20 @@ def main():
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-    ms_step, dec_ms = timed(step, args.steps, args.warmup, stream)
+    flush = make_flush(dev)
+    ms_step, dec_ms_b2b = timed(step, args.steps, args.warmup, stream)
+    if args.no_flush:
+        f_step, dec_ms = ms_step, dec_ms_b2b
+    else:
+        f_step, dec_ms = timed(step, args.steps, args.warmup, stream, flush=flush)
 
     tokens = wl.total_tokens()
     kv_bytes = wl.kv_bytes_fp4()            # logical: every sequence's whole context
     alg_tokens = alg_token_heads(wl, prefix is not None) // wl.num_kv_heads
     alg_bytes = alg_tokens * wl.num_kv_heads * (KV_BYTES_PER_TOKEN_HEAD * D // 128)
     achieved = alg_bytes / (dec_ms * 1e-3) / 1e9
+    ach = None if args.no_probes else achievable(uq, wl, desc, codes, scales, pt, ctx, part, alg_bytes, args, dev,
+                                                 stream, flush)
     result = {
         "metric": "decode-attention KV tokens/s and achieved HBM GB/s (% of peak) at 32k context",
         "value": tokens / (ms_step * 1e-3),
@@ -380,8 +476,19 @@ def main():
         "hbm_frac_step": kv_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBS,
         "roofline": {"bound": "hbm", "kernel": "decode_kernel", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": profiled_traffic(wl.name),
-                     "launch_ms": dec_ms, "bytes_per_launch": alg_bytes, "logical_bytes_per_launch": kv_bytes},
+                     "launch_ms": dec_ms, "bytes_per_launch": alg_bytes, "logical_bytes_per_launch": kv_bytes,
+                     "timing": "kernel events (uq_time_next_launch), 1 GiB written and read back before every launch"
+                               + (" (not: --no-flush)" if args.no_flush else ""),
+                     "launch_ms_back_to_back": dec_ms_b2b,
+                     "achieved_back_to_back": alg_bytes / (dec_ms_b2b * 1e-3) / 1e9},
+        "flushed": {"ms_per_step": f_step, "tokens_per_s": tokens / (f_step * 1e-3),
+                    "step_timing": "event pair around the step's launches, 1 GiB written and read back before every step"},
     }
+    if ach is not None:
+        result["achievable"] = ach
+        if ach.get("page_gather_gbs"):
+            result["roofline"]["achievable_gbs"] = ach["page_gather_gbs"]
+            result["roofline"]["frac_of_achievable"] = achieved / ach["page_gather_gbs"]
     # the comparison caches exist at head size 128
     fmts = [f for f in args.comparators.split(",") if f and f != "none"] if D == 128 else []
     if fmts:
@@ -389,11 +496,14 @@ def main():
         for fmt in fmts:
             if fmt not in REF_BYTES_PER_TOKEN_HEAD:
                 sys.exit(f"unknown comparator {fmt!r}")
-            comp[f"{fmt}_kv"] = comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, args, dev, stream, prefix)
+            comp[f"{fmt}_kv"] = comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, args, dev, stream, flush,
+                                           prefix)
             comp[f"fp4_over_{fmt}_tokens_per_s"] = result["value"] / comp[f"{fmt}_kv"]["tokens_per_s"]
+            comp[f"fp4_over_{fmt}_tokens_per_s_flushed"] = (result["flushed"]["tokens_per_s"]
+                                                           / comp[f"{fmt}_kv"]["flushed"]["tokens_per_s"])
         result["comparators"] = comp
     if not args.no_write_path:
-        result["write_path"] = write_path(uq, args, dev, stream)
+        result["write_path"] = write_path(uq, args, dev, stream, flush)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample_seqs, dev)
     print(json.dumps(result), flush=True)

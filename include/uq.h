@@ -481,6 +481,61 @@ uq_status uq_ref_decode_merge(const uq_ref_cache_desc *desc, int32_t batch, int3
                               void *stream);
 
 /* ------------------------------------------------------------------------
+ * Measurement probes (diagnostics, not part of the method; section
+ * "Kernel-Level Roofline Analysis" measures against the HBM roof, and these
+ * give the share of it this GPU actually delivers to the access patterns of
+ * this library, and the arithmetic of its matrix instructions).
+ *
+ * uq_probe_stream_read -- read `bytes` of device memory at `buf` once
+ *   (16-byte loads, a grid-stride pass of UQ_PROBE_STREAM_BLOCKS blocks),
+ *   XOR-folding them into one checksum word per block in `sink`.  Its kernel
+ *   time is the time a plain stream of that many bytes takes.
+ *   buf 16-byte aligned, bytes > 0 and a multiple of 16; sink: at least
+ *   UQ_PROBE_STREAM_BLOCKS uint32 words of device memory.
+ *   Errors: INVALID_ARGUMENT otherwise.
+ *
+ * uq_probe_page_gather -- the FP4 decode kernel's memory traffic alone:
+ *   the grid of uq_decode_attention for these arguments (one block of 4
+ *   waves per (partition, kv head, sequence)), the same page walk through
+ *   page_table, page-id copies and 2-slot LDS ring filled by the same copy
+ *   instructions, every staged byte read back into registers, and no
+ *   arithmetic beyond an XOR checksum (one uint32 per wave in `sink`).
+ *   Arguments as uq_decode_attention (head size 128); sink_words >= 4 x
+ *   partitions x num_kv_heads x batch, partitions = ceil(max_context /
+ *   partition), the partition being partition_tokens or, for 0, the
+ *   library's default for the shape; sink 16-byte aligned.
+ *   Errors: those of uq_decode_attention's argument checks;
+ *   WORKSPACE_TOO_SMALL for a short sink; UNSUPPORTED for head sizes other
+ *   than 128.
+ *
+ * uq_probe_mfma -- n independent one-wave products D = A x B of one matrix
+ *   instruction on given operand bytes, in the instruction's lane layout:
+ *   a, b: [n][64 lanes][32 bytes] (an FP4 operand uses the first 16 bytes of
+ *   a lane: 32 E2M1 codes, k order = nibble order, low nibble first; a BF16
+ *   operand the first 16: 8 values); scale_a, scale_b: [n][64] UE8M0 bytes,
+ *   lane 16 j + i scaling row (A) or column (B) i over k-block j of 32;
+ *   d: [n][64][4] floats, lane l element r = D[4 (l / 16) + r][l % 16].
+ *   kind 0: v_mfma_scale_f32_16x16x128_f8f6f4 with A FP4 E2M1, B FP8 E4M3
+ *   (the QK^T instruction of the decode kernel); kind 1: the same with A and
+ *   B FP8 E4M3 (the FP8-KV comparator's); kind 2:
+ *   v_mfma_f32_16x16x32_bf16 (scales unused, may be NULL); kind 3: the
+ *   scaled instruction with A FP8 E4M3, B FP4 E2M1.  Lane l of an operand
+ *   holds row (A) or column (B) l % 16; k = 32 (l / 16) + e for FP4 element
+ *   e; for FP8 bytes 0..15 are k = 16 (l / 16) + e, bytes 16..31 are k = 64
+ *   + 16 (l / 16) + e - 16; for BF16 k = 8 (l / 16) + e.
+ *   Errors: INVALID_ARGUMENT for null or misaligned pointers, n < 1 or
+ *   n > 65535, an unknown kind.
+ * ---------------------------------------------------------------------- */
+#define UQ_PROBE_STREAM_BLOCKS 2048
+uq_status uq_probe_stream_read(const void *buf, size_t bytes, uint32_t *sink, void *stream);
+uq_status uq_probe_page_gather(const uq_cache_desc *desc, int32_t batch, int32_t num_q_heads,
+                               const uint8_t *kv_codes, const uint8_t *kv_scales, const int32_t *page_table,
+                               int32_t max_pages_per_seq, const int32_t *context_lens, int32_t max_context,
+                               int32_t partition_tokens, uint32_t *sink, size_t sink_words, void *stream);
+uq_status uq_probe_mfma(int32_t kind, const void *a, const void *b, const uint8_t *scale_a, const uint8_t *scale_b,
+                        int32_t n, float *d, void *stream);
+
+/* ------------------------------------------------------------------------
  * Kernel timing (benchmarks).
  *
  * HIP events recorded on the stream around a call also count the command
@@ -488,8 +543,9 @@ uq_status uq_ref_decode_merge(const uq_ref_cache_desc *desc, int32_t batch, int3
  * uq_time_next_launch(start, stop), the next launch of the decode partition
  * kernel (by uq_decode_attention, uq_decode_partials,
  * uq_decode_step(_partials), the cascade calls or their comparison-cache
- * forms) or of the quantize-on-write kernel (uq_quantize_kv) made from the
- * calling host thread is dispatched with hipExtLaunchKernel, which sets
+ * forms), of the quantize-on-write kernel (uq_quantize_kv) or of a bandwidth
+ * probe (uq_probe_stream_read, uq_probe_page_gather) made from the calling
+ * host thread is dispatched with hipExtLaunchKernel, which sets
  * `start` and `stop` (hipEvent_t, created by the caller, not owned by the
  * library) to that kernel's own start and end; hipEventElapsedTime(start,
  * stop) is then the kernel's duration.  The setting is used by that one

@@ -7,7 +7,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libuq.so")
-SOURCES = ["uq_api.hip", "uq_quantize.hip", "uq_decode.hip"]
+SOURCES = ["uq_api.hip", "uq_quantize.hip", "uq_decode.hip", "uq_probe.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

@@ -822,6 +822,40 @@ uq_status uq_ref_decode_cascade_merge(const uq_ref_cache_desc* desc, int32_t bat
     return from_hip(uq::launch_decode_merge(p, static_cast<hipStream_t>(stream)));
 }
 
+uq_status uq_probe_stream_read(const void* buf, size_t bytes, uint32_t* sink, void* stream) {
+    if (buf == nullptr || sink == nullptr || bytes == 0 || bytes % 16 != 0) return UQ_ERR_INVALID_ARGUMENT;
+    if (!aligned16(buf) || (reinterpret_cast<uintptr_t>(sink) & 3u) != 0) return UQ_ERR_INVALID_ARGUMENT;
+    return from_hip(uq::launch_stream_read_probe(buf, int64_t(bytes / 16), sink, UQ_PROBE_STREAM_BLOCKS,
+                                                 static_cast<hipStream_t>(stream)));
+}
+
+uq_status uq_probe_page_gather(const uq_cache_desc* desc, int32_t batch, int32_t num_q_heads, const uint8_t* kv_codes,
+                               const uint8_t* kv_scales, const int32_t* page_table, int32_t max_pages_per_seq,
+                               const int32_t* context_lens, int32_t max_context, int32_t partition_tokens,
+                               uint32_t* sink, size_t sink_words, void* stream) {
+    // the decode call's own checks (the sink stands in for the query, the
+    // output and the workspace, which the probe does not touch)
+    uq::DecodeParams p;
+    const size_t ws = uq_decode_workspace_bytes(desc, batch, num_q_heads, max_context, partition_tokens);
+    uq_status s = decode_setup(desc, sink, UQ_F32, batch, num_q_heads, kv_codes, kv_scales, page_table,
+                               max_pages_per_seq, context_lens, max_context, 1.0f, partition_tokens, sink, ws, sink,
+                               UQ_F32, p);
+    if (s != UQ_OK) return s;
+    if (desc->head_dim != kHeadDim) return UQ_ERR_UNSUPPORTED;
+    const size_t need = size_t(4) * size_t(p.num_partitions) * size_t(p.num_kv_heads) * size_t(batch);
+    if (sink_words < need) return UQ_ERR_WORKSPACE_TOO_SMALL;
+    return from_hip(uq::launch_gather_probe(p, sink, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uq_probe_mfma(int32_t kind, const void* a, const void* b, const uint8_t* scale_a, const uint8_t* scale_b,
+                        int32_t n, float* d, void* stream) {
+    if (kind < 0 || kind > 3 || n < 1 || n > 65535) return UQ_ERR_INVALID_ARGUMENT;
+    if (a == nullptr || b == nullptr || d == nullptr) return UQ_ERR_INVALID_ARGUMENT;
+    if (kind != 2 && (scale_a == nullptr || scale_b == nullptr)) return UQ_ERR_INVALID_ARGUMENT;
+    if (!aligned16(a) || !aligned16(b) || !aligned16(d)) return UQ_ERR_INVALID_ARGUMENT;
+    return from_hip(uq::launch_mfma_probe(kind, a, b, scale_a, scale_b, n, d, static_cast<hipStream_t>(stream)));
+}
+
 uq_status uq_time_next_launch(void* start_event, void* stop_event) {
     if ((start_event == nullptr) != (stop_event == nullptr)) return UQ_ERR_INVALID_ARGUMENT;
     uq::time_next_launch(static_cast<hipEvent_t>(start_event), static_cast<hipEvent_t>(stop_event));

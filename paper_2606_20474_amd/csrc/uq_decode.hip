@@ -1425,6 +1425,89 @@ __global__ void __launch_bounds__(256) merge_kernel(DecodeParams p) {
     write_out<N>(p, int64_t(b) * p.num_q_heads + hq, L, o);
 }
 
+// Bandwidth probe of the FP4 decode kernel's page gather: the same grid
+// (one block of 4 waves per (partition, kv head, sequence), kv head fastest),
+// the same page walk, page-id chunks and 2-slot LDS ring filled by the same
+// global_load_lds_dwordx4 copies, and every staged byte read back into
+// registers as the decode kernel reads it, but no arithmetic on it beyond an
+// XOR into a checksum (one word per wave in `sink`).  Its time is the time
+// the decode kernel's memory traffic alone takes on this GPU.
+__global__ void __launch_bounds__(256) gather_probe_kernel(DecodeParams p, uint32_t* __restrict__ sink) {
+    constexpr int W = 4, S = 2;
+    constexpr int kStage = stage_bytes<kFp4>();
+    const int lin = blockIdx.x;
+    const int hk = lin % p.num_kv_heads;
+    const int row = lin / p.num_kv_heads;
+    const int b = row % p.batch;
+    const int part = row / p.batch;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    int ctx = p.context_lens[b];
+    ctx = ctx < p.max_context ? ctx : p.max_context;
+    const int start = part * p.partition_tokens;
+    const int end = (start + p.partition_tokens) < ctx ? (start + p.partition_tokens) : ctx;
+    __shared__ __attribute__((aligned(16))) uint8_t smem[W * ring_bytes<kFp4, S>()];
+    __shared__ __attribute__((aligned(16))) uint8_t ids_lds[W * kIdsSlot];
+    uint32_t acc = 0u;
+    const int n_pages = start < end ? (end - start + 15) >> 4 : 0;
+    const int n_iter = (n_pages + 1) >> 1;
+    const int n_local = wave < n_iter ? (n_iter - wave + W - 1) / W : 0;
+    if (n_local > 0) {
+        const int first_page = start >> 4;
+        const int32_t* pt_row = p.page_table + int64_t(b) * p.max_pages_per_seq;
+        uint8_t* ring = smem + wave * ring_bytes<kFp4, S>();
+        const uint32_t ring_addr = uint32_t(reinterpret_cast<uintptr_t>((lds_ptr_t)ring));
+        uint8_t* ids_slot = ids_lds + wave * kIdsSlot;
+        const uint32_t ids_addr = uint32_t(reinterpret_cast<uintptr_t>((lds_ptr_t)ids_slot));
+        const int64_t head_tile = int64_t(hk) * 2;
+        const int64_t tiles_per_page = int64_t(p.num_kv_heads) * 2;
+        int32_t ids = load_page_ids<W>(pt_row, first_page, n_pages, wave, 0, lane);
+        if (n_local > 32) copy_page_ids<W>(ids_slot, pt_row, first_page, n_pages, wave, 1, lane);
+        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+        ids = clamp_ids(ids, p.num_pages);
+        for (int s = 0; s < S && s < n_local; ++s) {
+            const int64_t id0 = __builtin_amdgcn_readlane(ids, 2 * s);
+            const int64_t id1 = __builtin_amdgcn_readlane(ids, 2 * s + 1);
+            stage_issue<kFp4>(ring + s * kStage, p.codes, p.scales, id0 * tiles_per_page + head_tile,
+                              id1 * tiles_per_page + head_tile, lane);
+        }
+        for (int k = 0; k < n_local; ++k) {
+            if (k + 1 < n_local) wait_vmem<dma_per_stage<kFp4>()>();
+            else wait_vmem<0>();
+            const uint32_t slot = uint32_t(k & (S - 1));
+            StageRegs<kFp4> c;
+            stage_read(c, ring_addr + slot * kStage, lane);
+            if (k + S < n_local) {
+                const int kn = k + S;
+                if ((kn & 31) == 0) {
+                    ids = clamp_ids(read_page_ids(ids_addr, lane), p.num_pages);
+                    if (kn + 32 < n_local)
+                        copy_page_ids<W>(ids_slot, pt_row, first_page, n_pages, wave, (kn >> 5) + 1, lane);
+                }
+                const int s2 = 2 * (kn & 31);
+                const int64_t id0 = __builtin_amdgcn_readlane(ids, s2);
+                const int64_t id1 = __builtin_amdgcn_readlane(ids, s2 + 1);
+                stage_issue<kFp4>(ring + slot * kStage, p.codes, p.scales, id0 * tiles_per_page + head_tile,
+                                  id1 * tiles_per_page + head_tile, lane);
+            }
+#pragma unroll
+            for (int pg = 0; pg < 2; ++pg)
+                acc ^= c.k[pg].x ^ c.k[pg].y ^ c.k[pg].z ^ c.k[pg].w ^ c.v[pg].x ^ c.v[pg].y ^ c.v[pg].z ^
+                       c.v[pg].w ^ c.ks[pg] ^ c.vs[pg];
+        }
+    }
+#pragma unroll
+    for (int s = 1; s < 64; s <<= 1) acc ^= uint32_t(__shfl_xor(int(acc), s));
+    if (lane == 0) sink[int64_t(lin) * W + wave] = acc;
+}
+
+hipError_t launch_gather_probe(const DecodeParams& p, uint32_t* sink, hipStream_t stream) {
+    const dim3 grid{unsigned(int64_t(p.num_partitions) * p.num_kv_heads * p.batch)};
+    launch_kernel(gather_probe_kernel, grid, dim3(256), stream, p, sink);
+    return hipGetLastError();
+}
+
 // Two ring slots per wave: a 4-slot ring (twice the copies in flight, half
 // the blocks per CU) measured no faster on 32k contexts and slower on 16k.
 template <int F>

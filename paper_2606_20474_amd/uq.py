@@ -19,6 +19,8 @@ LIB_PATH = os.path.join(_PKG, "libuq.so")
 
 UQ_OK, UQ_ERR_INVALID_ARGUMENT, UQ_ERR_UNSUPPORTED, UQ_ERR_WORKSPACE_TOO_SMALL, UQ_ERR_HIP = range(5)
 UQ_F32, UQ_BF16, UQ_F16, UQ_FP8_E4M3 = range(4)
+PROBE_STREAM_BLOCKS = 2048         # UQ_PROBE_STREAM_BLOCKS
+PROBE_MFMA_FP4_FP8, PROBE_MFMA_FP8_FP8, PROBE_MFMA_BF16, PROBE_MFMA_FP8_FP4 = range(4)
 
 HEAD_DIM = 128
 PAGE_SIZE = 16
@@ -35,6 +37,7 @@ EXPORTS = (
     "uq_ref_decode_step_partials", "uq_decode_cascade_workspace_bytes", "uq_decode_cascade",
     "uq_decode_cascade_partials", "uq_decode_cascade_merge", "uq_ref_decode_cascade",
     "uq_ref_decode_cascade_partials", "uq_ref_decode_cascade_merge", "uq_quantize_error", "uq_time_next_launch",
+    "uq_probe_stream_read", "uq_probe_page_gather", "uq_probe_mfma",
 )
 
 UQ_REF_FP8_E4M3, UQ_REF_BF16, UQ_REF_TQ4 = 1, 2, 3
@@ -107,6 +110,12 @@ def _load():
     L.uq_decode_partials.restype = i32
     L.uq_decode_merge.argtypes = [D, i32, i32, vp, i32, i32, vp, sz, vp, i32, vp]
     L.uq_decode_merge.restype = i32
+    L.uq_probe_stream_read.argtypes = [vp, sz, vp, vp]
+    L.uq_probe_stream_read.restype = i32
+    L.uq_probe_page_gather.argtypes = [D, i32, i32, vp, vp, vp, i32, vp, i32, i32, vp, sz, vp]
+    L.uq_probe_page_gather.restype = i32
+    L.uq_probe_mfma.argtypes = [i32, vp, vp, vp, vp, i32, vp, vp]
+    L.uq_probe_mfma.restype = i32
     for name in ("uq_decode_step", "uq_decode_step_partials"):
         fn = getattr(L, name)
         fn.argtypes = [D, vp, i32, vp, vp, i32, i32, i32, vp, vp, vp, i32, vp, i32, f32, i32, vp, sz, vp, i32, vp]
@@ -702,3 +711,53 @@ def ref_decode_cascade_merge(desc: RefCacheDesc, batch, num_q_heads, context_len
                                          _ptr(out), _DT[out.dtype], _stream(stream))
     _check(st, "uq_ref_decode_cascade_merge")
     return out
+
+
+# ---------------------------------------------------------------------------
+# Measurement probes
+
+
+def probe_stream_read(buf, sink=None, stream=None):
+    """Read every byte of the uint8 tensor ``buf`` once (a plain stream);
+    returns the per-block checksum words (int32 [PROBE_STREAM_BLOCKS])."""
+    _need(buf, "buf", _U8)
+    if sink is None:
+        sink = torch.empty(PROBE_STREAM_BLOCKS, dtype=torch.int32, device=buf.device)
+    _need(sink, "sink", (torch.int32,), min_numel=PROBE_STREAM_BLOCKS)
+    _check(lib.uq_probe_stream_read(_ptr(buf), buf.numel(), _ptr(sink), _stream(stream)), "uq_probe_stream_read")
+    return sink
+
+
+def probe_page_gather(desc: CacheDesc, num_q_heads, codes, scales, page_table, context_lens, max_context,
+                      partition_tokens=0, sink=None, stream=None):
+    """The FP4 decode kernel's page gather without its arithmetic, for the
+    same arguments; returns the per-wave checksum words."""
+    B = context_lens.shape[0]
+    _pools(desc, codes, scales)
+    _table(page_table, context_lens, B)
+    part = partition_tokens or default_partition(desc, B, num_q_heads, max_context)
+    nwords = 4 * max(1, -(-max_context // part)) * desc.num_kv_heads * B
+    if sink is None:
+        sink = torch.empty(nwords, dtype=torch.int32, device=codes.device)
+    _need(sink, "sink", (torch.int32,), min_numel=nwords)
+    d = desc.c_struct()
+    st = lib.uq_probe_page_gather(ctypes.byref(d), B, num_q_heads, _ptr(codes), _ptr(scales), _ptr(page_table),
+                                  page_table.shape[1], _ptr(context_lens), max_context, partition_tokens, _ptr(sink),
+                                  sink.numel(), _stream(stream))
+    _check(st, "uq_probe_page_gather")
+    return sink
+
+
+def probe_mfma(kind, a, b, scale_a=None, scale_b=None, stream=None):
+    """n one-wave matrix products: a, b uint8 [n, 64, 32] in the lane layout,
+    scale_a, scale_b uint8 [n, 64] (kinds 0, 1, 3) -> float32 [n, 64, 4]."""
+    n = a.shape[0]
+    _need(a, "a", _U8, (n, 64, 32))
+    _need(b, "b", _U8, (n, 64, 32))
+    if kind != PROBE_MFMA_BF16:
+        _need(scale_a, "scale_a", _U8, (n, 64))
+        _need(scale_b, "scale_b", _U8, (n, 64))
+    d = torch.empty((n, 64, 4), dtype=torch.float32, device=a.device)
+    _check(lib.uq_probe_mfma(kind, _ptr(a), _ptr(b), _ptr(scale_a), _ptr(scale_b), n, _ptr(d), _stream(stream)),
+           "uq_probe_mfma")
+    return d

@@ -350,3 +350,35 @@ def test_default_partition_counts_blocks(uq):
         assert uq.default_partition(d, B, hq, ctx) == want, (hd, hkv, hq, B, ctx)
         # the workspace follows the same pick
         assert uq.workspace_bytes(d, B, hq, ctx, 0) == uq.workspace_bytes(d, B, hq, ctx, want)
+
+
+def test_probe_validation(uq):
+    """The measurement probes check their arguments before any HIP call."""
+    E = uq
+    L = uq.lib
+    assert L.uq_probe_stream_read(None, 1 << 20, FAKE, None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert L.uq_probe_stream_read(FAKE, 0, FAKE, None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert L.uq_probe_stream_read(FAKE, 1000, FAKE, None) == E.UQ_ERR_INVALID_ARGUMENT       # not 16-byte words
+    assert L.uq_probe_stream_read(ctypes.c_void_p(0x10008), 1 << 20, FAKE, None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert L.uq_probe_stream_read(FAKE, 1 << 20, None, None) == E.UQ_ERR_INVALID_ARGUMENT
+
+    def gather(d, B=2, Hq=4, mpps=4, maxctx=64, part=32, sink_words=1 << 20, pt=FAKE):
+        return L.uq_probe_page_gather(ctypes.byref(d), B, Hq, FAKE, FAKE, pt, mpps, FAKE, maxctx, part, FAKE,
+                                      sink_words, None)
+    assert gather(desc(head_dim=96)) == E.UQ_ERR_UNSUPPORTED
+    assert gather(desc(head_dim=64)) == E.UQ_ERR_UNSUPPORTED
+    assert gather(desc(), Hq=3) == E.UQ_ERR_INVALID_ARGUMENT
+    assert gather(desc(), maxctx=65) == E.UQ_ERR_INVALID_ARGUMENT
+    assert gather(desc(), pt=None) == E.UQ_ERR_INVALID_ARGUMENT
+    # 2 partitions x 2 kv heads x 2 sequences x 4 waves = 32 words
+    assert gather(desc(), sink_words=31) == E.UQ_ERR_WORKSPACE_TOO_SMALL
+
+    def mfma(kind=0, a=FAKE, b=FAKE, sa=FAKE, sb=FAKE, n=1, d=FAKE):
+        return L.uq_probe_mfma(kind, a, b, sa, sb, n, d, None)
+    assert mfma(kind=4) == E.UQ_ERR_INVALID_ARGUMENT
+    assert mfma(kind=-1) == E.UQ_ERR_INVALID_ARGUMENT
+    assert mfma(n=0) == E.UQ_ERR_INVALID_ARGUMENT
+    assert mfma(n=65536) == E.UQ_ERR_INVALID_ARGUMENT
+    assert mfma(a=None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert mfma(sa=None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert mfma(d=ctypes.c_void_p(0x10004)) == E.UQ_ERR_INVALID_ARGUMENT
