@@ -481,6 +481,35 @@ uq_status uq_ref_decode_merge(const uq_ref_cache_desc *desc, int32_t batch, int3
                               void *stream);
 
 /* ------------------------------------------------------------------------
+ * uq_decode_attention_noalloc -- uq_decode_attention for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc.  The partition partials go to a device
+ * array the library holds for the life of the process (one per GPU, made at
+ * module load; UQ_NOALLOC_SCRATCH_BYTES bytes) instead of a caller's
+ * workspace.  The call makes no hipMalloc, hipFree or other allocating
+ * call: its first call on a device looks the array's address up once
+ * (hipGetSymbolAddress) with that device current.
+ *   Arguments, layouts, launches, numerics and errors are those of
+ *   uq_decode_attention without the workspace pair: the output is the same,
+ *   bit for bit, for the same arguments.  The stream must belong to the
+ *   current device.
+ *   WORKSPACE_TOO_SMALL when the call needs more than the array holds, i.e.
+ *   uq_decode_workspace_bytes(desc, batch, num_q_heads, max_context,
+ *   partition_tokens) > UQ_NOALLOC_SCRATCH_BYTES (checked on the host before
+ *   anything is enqueued); UQ_ERR_HIP if the address lookup fails.
+ *   Every call on a GPU shares that GPU's array: calls that overlap on one GPU
+ *   (other streams, other host threads) race and must be serialised by the
+ *   caller.  Nothing in the array needs to start at zero: every partial the
+ *   merge reads is written by the same call first.
+ * ---------------------------------------------------------------------- */
+#define UQ_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+uq_status uq_decode_attention_noalloc(const uq_cache_desc *desc, const void *q, uq_dtype q_dtype, int32_t batch,
+                                      int32_t num_q_heads, const uint8_t *kv_codes, const uint8_t *kv_scales,
+                                      const int32_t *page_table, int32_t max_pages_per_seq,
+                                      const int32_t *context_lens, int32_t max_context, float softmax_scale,
+                                      int32_t partition_tokens, void *out, uq_dtype out_dtype, void *stream);
+
+/* ------------------------------------------------------------------------
  * Measurement probes (diagnostics, not part of the method; section
  * "Kernel-Level Roofline Analysis" measures against the HBM roof, and these
  * give the share of it this GPU actually delivers to the access patterns of

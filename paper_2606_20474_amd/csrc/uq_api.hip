@@ -1,7 +1,9 @@
 // uq_api.hip -- the C ABI of libuq (declared in include/uq.h): argument
 // validation on the host, launch configuration, workspace sizing.
+#include <atomic>
 #include <cstring>
 #include <math.h>
+#include <mutex>
 #include <stdint.h>
 
 #include "uq.h"
@@ -272,6 +274,37 @@ int64_t ref_tile_bytes(const uq_ref_cache_desc* d) {
     return d->format == UQ_REF_FP8_E4M3 ? 2048 : d->format == UQ_REF_TQ4 ? uq::kTqBlock / 2 : 4096;
 }
 
+}  // namespace
+
+// The partials of uq_decode_attention_noalloc: one array per GPU, placed by
+// the module loader, never allocated by a call.  In host code `scratch` is a
+// host-side stand-in for the symbol, not a device address: only the address
+// hipGetSymbolAddress returns for the current device is ever passed to a
+// kernel.
+static __device__ __align__(256) uint8_t scratch[UQ_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_ptr[kMaxDevices];
+std::mutex g_scratch_mutex;
+
+// The array's address on the current device, looked up once per device.
+uq_status scratch_of_current_device(void** ptr) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0) return UQ_ERR_HIP;
+    if (dev >= kMaxDevices) return UQ_ERR_UNSUPPORTED;
+    void* p = g_scratch_ptr[dev].load(std::memory_order_acquire);
+    if (p == nullptr) {
+        std::lock_guard<std::mutex> lock(g_scratch_mutex);
+        p = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+        if (p == nullptr) {
+            if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return UQ_ERR_HIP;
+            g_scratch_ptr[dev].store(p, std::memory_order_release);
+        }
+    }
+    *ptr = p;
+    return UQ_OK;
+}
 }  // namespace
 
 extern "C" {
@@ -819,6 +852,33 @@ uq_status uq_ref_decode_cascade_merge(const uq_ref_cache_desc* desc, int32_t bat
     if (s != UQ_OK) return s;
     p.kv_fmt = ref_fmt(desc);
     if (desc->format == UQ_REF_FP8_E4M3) p.out_scale = desc->v_scale;
+    return from_hip(uq::launch_decode_merge(p, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uq_decode_attention_noalloc(const uq_cache_desc* desc, const void* q, uq_dtype q_dtype, int32_t batch,
+                                      int32_t num_q_heads, const uint8_t* kv_codes, const uint8_t* kv_scales,
+                                      const int32_t* page_table, int32_t max_pages_per_seq,
+                                      const int32_t* context_lens, int32_t max_context, float softmax_scale,
+                                      int32_t partition_tokens, void* out, uq_dtype out_dtype, void* stream) {
+    // every host-side check of uq_decode_attention, the size bound included
+    // (WORKSPACE_TOO_SMALL), before the first HIP call: an aligned stand-in
+    // address takes the array's place until its device address is known
+    uq::DecodeParams p;
+    void* const stand_in = reinterpret_cast<void*>(uintptr_t(256));
+    uq_status s = decode_setup(desc, q, q_dtype, batch, num_q_heads, kv_codes, kv_scales, page_table,
+                               max_pages_per_seq, context_lens, max_context, softmax_scale, partition_tokens,
+                               stand_in, UQ_NOALLOC_SCRATCH_BYTES, out, out_dtype, p);
+    if (s != UQ_OK) return s;
+    void* base = nullptr;
+    s = scratch_of_current_device(&base);
+    if (s != UQ_OK) return s;
+    // the same parameter block with the array's device address
+    s = decode_setup(desc, q, q_dtype, batch, num_q_heads, kv_codes, kv_scales, page_table, max_pages_per_seq,
+                     context_lens, max_context, softmax_scale, partition_tokens, base, UQ_NOALLOC_SCRATCH_BYTES, out,
+                     out_dtype, p);
+    if (s != UQ_OK) return s;
+    s = from_hip(uq::launch_decode_partials(p, static_cast<hipStream_t>(stream)));
+    if (s != UQ_OK) return s;
     return from_hip(uq::launch_decode_merge(p, static_cast<hipStream_t>(stream)));
 }
 

@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(_PKG, "libuq.so")
 
 UQ_OK, UQ_ERR_INVALID_ARGUMENT, UQ_ERR_UNSUPPORTED, UQ_ERR_WORKSPACE_TOO_SMALL, UQ_ERR_HIP = range(5)
 UQ_F32, UQ_BF16, UQ_F16, UQ_FP8_E4M3 = range(4)
+NOALLOC_SCRATCH_BYTES = 32 << 20   # UQ_NOALLOC_SCRATCH_BYTES
 PROBE_STREAM_BLOCKS = 2048         # UQ_PROBE_STREAM_BLOCKS
 PROBE_MFMA_FP4_FP8, PROBE_MFMA_FP8_FP8, PROBE_MFMA_BF16, PROBE_MFMA_FP8_FP4 = range(4)
 
@@ -37,7 +38,7 @@ EXPORTS = (
     "uq_ref_decode_step_partials", "uq_decode_cascade_workspace_bytes", "uq_decode_cascade",
     "uq_decode_cascade_partials", "uq_decode_cascade_merge", "uq_ref_decode_cascade",
     "uq_ref_decode_cascade_partials", "uq_ref_decode_cascade_merge", "uq_quantize_error", "uq_time_next_launch",
-    "uq_probe_stream_read", "uq_probe_page_gather", "uq_probe_mfma",
+    "uq_decode_attention_noalloc", "uq_probe_stream_read", "uq_probe_page_gather", "uq_probe_mfma",
 )
 
 UQ_REF_FP8_E4M3, UQ_REF_BF16, UQ_REF_TQ4 = 1, 2, 3
@@ -110,6 +111,8 @@ def _load():
     L.uq_decode_partials.restype = i32
     L.uq_decode_merge.argtypes = [D, i32, i32, vp, i32, i32, vp, sz, vp, i32, vp]
     L.uq_decode_merge.restype = i32
+    L.uq_decode_attention_noalloc.argtypes = [D, vp, i32, i32, i32, vp, vp, vp, i32, vp, i32, f32, i32, vp, i32, vp]
+    L.uq_decode_attention_noalloc.restype = i32
     L.uq_probe_stream_read.argtypes = [vp, sz, vp, vp]
     L.uq_probe_stream_read.restype = i32
     L.uq_probe_page_gather.argtypes = [D, i32, i32, vp, vp, vp, i32, vp, i32, i32, vp, sz, vp]
@@ -393,6 +396,25 @@ def decode_attention(desc: CacheDesc, q, codes, scales, page_table, context_lens
                                  partition_tokens, _ptr(workspace), workspace.numel(), _ptr(out), _DT[out.dtype],
                                  _stream(stream))
     _check(st, "uq_decode_attention")
+    return out
+
+
+def decode_attention_noalloc(desc: CacheDesc, q, codes, scales, page_table, context_lens, max_context, out,
+                             softmax_scale=None, partition_tokens=0, q_dtype=None, stream=None):
+    """decode_attention with its partials in the library's own device array
+    (no workspace, nothing allocated by the call); ``out`` [B, Hq, head_dim]
+    is the caller's."""
+    B, Hq = _q_out(q, out, desc.head_dim)
+    _pools(desc, codes, scales)
+    _table(page_table, context_lens, B)
+    if softmax_scale is None:
+        softmax_scale = desc.head_dim ** -0.5
+    d = desc.c_struct()
+    qdt = _DT[q.dtype] if q_dtype is None else q_dtype
+    st = lib.uq_decode_attention_noalloc(ctypes.byref(d), _ptr(q), qdt, B, Hq, _ptr(codes), _ptr(scales),
+                                         _ptr(page_table), page_table.shape[1], _ptr(context_lens), max_context,
+                                         softmax_scale, partition_tokens, _ptr(out), _DT[out.dtype], _stream(stream))
+    _check(st, "uq_decode_attention_noalloc")
     return out
 
 

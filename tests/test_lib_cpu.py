@@ -110,6 +110,40 @@ def test_decode_validation(uq):
     assert decode(uq, big, B=65535, Hq=65535, part=32, wsb=1 << 62) == E.UQ_ERR_UNSUPPORTED
 
 
+def decode_noalloc(uq, d, q=FAKE, qdt=0, B=2, Hq=4, mpps=4, maxctx=64, scale=0.1, part=0, out=FAKE, odt=0, ctx=FAKE,
+                   pt=FAKE):
+    return uq.lib.uq_decode_attention_noalloc(ctypes.byref(d) if d is not None else None, q, qdt, B, Hq, FAKE, FAKE,
+                                              pt, mpps, ctx, maxctx, scale, part, out, odt, None)
+
+
+def test_decode_noalloc_validation(uq):
+    """The no-allocation decode makes uq_decode_attention's host checks, and
+    refuses a call whose partials exceed its device array, before any HIP
+    call (so before it looks the array up)."""
+    E = uq
+    assert decode_noalloc(uq, None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert decode_noalloc(uq, desc(head_dim=96)) == E.UQ_ERR_UNSUPPORTED
+    assert decode_noalloc(uq, desc(), Hq=3) == E.UQ_ERR_INVALID_ARGUMENT
+    assert decode_noalloc(uq, desc(), maxctx=65) == E.UQ_ERR_INVALID_ARGUMENT
+    assert decode_noalloc(uq, desc(), part=48) == E.UQ_ERR_INVALID_ARGUMENT
+    assert decode_noalloc(uq, desc(), q=None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert decode_noalloc(uq, desc(), out=None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert decode_noalloc(uq, desc(), odt=3) == E.UQ_ERR_UNSUPPORTED
+    # 256 sequences x 64 query heads x 32 partitions of 4096 tokens (128k
+    # contexts): 273 MB of partials, beyond the array
+    from paper_2606_20474_amd.uq import CacheDesc
+    big = desc(num_kv_heads=8, num_pages=1 << 21)
+    need = uq.workspace_bytes(CacheDesc(num_kv_heads=8, num_pages=1 << 21), 256, 64, 131072, 4096)
+    assert need > uq.NOALLOC_SCRATCH_BYTES
+    assert decode_noalloc(uq, big, B=256, Hq=64, mpps=8192, maxctx=131072, part=4096) == E.UQ_ERR_WORKSPACE_TOO_SMALL
+    # the Qwen3-235B-like layer's partials (4.3 MB at the default partition) fit
+    qwen = CacheDesc(num_kv_heads=4, num_pages=65536)
+    assert uq.workspace_bytes(qwen, 32, 64, 32768, 0) <= uq.NOALLOC_SCRATCH_BYTES
+    text = open(os.path.join(ROOT, "include", "uq.h")).read()
+    assert re.search(r"#define UQ_NOALLOC_SCRATCH_BYTES \(\(size_t\)32 << 20\)", text)
+    assert uq.NOALLOC_SCRATCH_BYTES == 32 << 20
+
+
 def test_workspace_and_partition_sizes(uq):
     from paper_2606_20474_amd.uq import CacheDesc
     d = CacheDesc(num_kv_heads=4, num_pages=65536)
