@@ -359,13 +359,15 @@ uq_status uq_decode_cascade_merge(const uq_cache_desc *desc, int32_t batch, int3
  *
  * TQ4 is the codebook encoding UltraQuant replaces (appendix "Calibrated LUT
  * int4 KV Encoding (Ultra-TQ)", its algorithm): K is rotated by the same
- * R as the FP4 cache, its fp32 norm n is stored per token and each rotated
- * channel x is coded to the nearest of the 16 codebook levels c_j (rounded
- * to BF16) as the number of midpoints m_j = (c_j + c_{j+1}) / 2 with
- * x > m_j * n (fp32); the decoded key is n * c[idx].  The norm is the
- * fp32 square root of a fused multiply-add sum in a fixed order (per 8
- * channels in channel order, then a pairwise tree over the 16 slices), so
- * the codes are reproducible.  V is not rotated: per 32-channel group,
+ * R as the FP4 cache, its norm n (the l2 norm of the rotated fp32 key,
+ * rounded once to fp32) is stored per token and each rotated channel x is
+ * coded to the index of the codebook level c_j (rounded to BF16) nearest to
+ * x / n, ties to the lower index: the number of midpoints m_j = (c_j +
+ * c_{j+1}) / 2 with x > m_j n, compared exactly (index 0 when n = 0); the
+ * decoded key is n * c[idx].  A codebook must be 16 finite, strictly
+ * ascending values whose adjacent BF16 levels lie within 2^44 of each other
+ * (so that each m_j is exact in fp64), else INVALID_ARGUMENT.  V is not
+ * rotated: per 32-channel group,
  * z = bf16(min), s = bf16(max(max - z, 0) / 15), code = clamp(rint((x - z)
  * / s), 0, 15) (0 when s = 0), decoded as bf16(fma(s, code, z)).  Decode
  * attention rotates the query and rounds it to BF16.  The block of one

@@ -75,6 +75,10 @@ def lib():
         L.uqo_bf16_rne.argtypes = [f32]
         L.uqo_bf16_rne.restype = f32
         L.uqo_tq4_encode_vector.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp]
+        L.uqo_tq4_norm.argtypes = [vp]
+        L.uqo_tq4_norm.restype = ctypes.c_float
+        L.uqo_tq4_index.argtypes = [ctypes.c_float, ctypes.c_float, vp]
+        L.uqo_tq4_index.restype = i32
         L.uqo_tq4_write.argtypes = [vp, vp, i64, i32, i64, vp, i64, vp, vp]
         L.uqo_tq4_write.restype = i64
         L.uqo_tq4_load.argtypes = [vp, i32, i64, i32, i32, vp, vp, vp, vp, vp]
@@ -278,6 +282,17 @@ def _levels(levels):
 
 def bf16_rne(x):
     return float(lib().uqo_bf16_rne(float(np.float32(x))))
+
+
+def tq4_norm(x):
+    """Reading T2: the l2 norm of the fp32 vector x [128], rounded once to fp32."""
+    x = _f32(x).reshape(HEAD_DIM)
+    return float(lib().uqo_tq4_norm(_ptr(x)))
+
+
+def tq4_index(x, n, levels):
+    """Reading T3: index of the BF16 level nearest to x / n (ties to the lower)."""
+    return int(lib().uqo_tq4_index(float(np.float32(x)), float(np.float32(n)), _ptr(_levels(levels))))
 
 
 def tq4_encode_vector(k, v, levels):

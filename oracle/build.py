@@ -14,7 +14,7 @@ LIB = os.path.join(HERE, "liboracle.so")
 def build(verbose: bool = False, src: str = SRC, lib: str = LIB) -> str:
     """Compile `src` (default: the oracle) into the shared library `lib`."""
     cmd = ["gcc", "-O2", "-std=gnu11", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
-           "-Wall", "-Wextra", "-shared", "-fPIC", src, "-o", lib + ".tmp", "-lm"]
+           "-Wall", "-Wextra", "-shared", "-fPIC", src, "-o", lib + ".tmp", "-lquadmath", "-lm"]
     if verbose:
         print(" ".join(cmd))
     subprocess.run(cmd, check=True)

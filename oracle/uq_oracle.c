@@ -45,11 +45,14 @@
  *      keys only; rotate_v = 0 is that mode).  With rotate_v the attention
  *      output is mapped back by R (R is symmetric and orthonormal).
  *
- * Built with: gcc -O2 -std=c11 -fopenmp -ffp-contract=off -shared -fPIC
- * (no -ffast-math: fp32 results must follow IEEE round-to-nearest-even).
+ * Built with: gcc -O2 -std=gnu11 -fopenmp -ffp-contract=off -shared -fPIC
+ * -lquadmath (no -ffast-math: fp32 results must follow IEEE
+ * round-to-nearest-even; binary128 gives the Ultra-TQ norm and index their
+ * exact reference values).
  */
 #include <math.h>
 #include <omp.h>
+#include <quadmath.h>
 #include <stdint.h>
 #include <stdlib.h>
 #include <string.h>
@@ -447,16 +450,18 @@ void uqo_quantize_error(const float *x, int64_t rows, int rotate, int pow2, int 
 /*   T1 K is rotated by R, V is not.  K's block is the whole head vector    */
 /*      (the production per-token l2 norm); V's blocks are the 32-channel  */
 /*      groups.                                                             */
-/*   T2 the norm n is fp32: per 8-channel slice s (channels 8s..8s+7) a     */
-/*      fused multiply-add chain p_s = fma(x, x, p_s) in channel order,     */
-/*      then the pairwise tree ((p0+p1)+(p2+p3))+... over the 16 slices,    */
-/*      then a correctly rounded sqrtf.  Codes are decided from n, so this  */
-/*      order is part of the format.                                        */
+/*   T2 the norm n is the l2 norm of the fp32 rotated key, rounded once to  */
+/*      fp32: the squares (exact) are summed in binary128 -- exactly, when  */
+/*      the key's nonzero magnitudes lie within 2^29 of each other, else to */
+/*      113 bits -- and the square root is taken in binary128, then rounded */
+/*      to fp32 (nearest even).                                             */
 /*   T3 the 16 levels are used as BF16 (round to nearest even), the matrix  */
-/*      operand type; the K index is the number of midpoints m_j =          */
-/*      fl32((c_j + c_{j+1}) / 2) with x > fl32(m_j * n) (nearest level of  */
-/*      x / n, ties to the lower one).  The dequantised key is n * c[idx],  */
-/*      exact.                                                              */
+/*      operand type; the K index is that of the level nearest to x / n,    */
+/*      ties to the lower one, i.e. the number of midpoints                 */
+/*      m_j = (c_j + c_{j+1}) / 2 below x / n, each comparison x > m_j n    */
+/*      made exactly (binary128, where m_j and m_j n are exact).  A zero    */
+/*      key (n = 0) has index 0 in every channel.  The dequantised key is   */
+/*      n * c[idx], exact.                                                  */
 /*   T4 V per group: zero z = bf16(min), scale s = bf16(max(max - z, 0) /  */
 /*      15) (fp32 subtract and divide), code = clamp(rint((x - z) / s),    */
 /*      0, 15), or 0 when s = 0; the dequantised value is                  */
@@ -486,36 +491,39 @@ float uqo_bf16_rne(float x) {
     return f32_of_bits(u & 0xFFFF0000u);
 }
 
-static void tq_tables(const float *levels, float lv[16], float mid[15]) {
+/* The 16 levels as BF16 and their 15 midpoints (exact in binary128). */
+static void tq_tables(const float *levels, float lv[16], __float128 mid[15]) {
     for (int j = 0; j < 16; ++j) lv[j] = uqo_bf16_rne(levels[j]);
-    for (int j = 0; j < 15; ++j) mid[j] = (lv[j] + lv[j + 1]) * 0.5f;
+    for (int j = 0; j < 15; ++j) mid[j] = ((__float128)lv[j] + (__float128)lv[j + 1]) / 2;
+}
+
+/* Reading T2: fl32(sqrt(sum of x_i^2)). */
+float uqo_tq4_norm(const float x[UQO_D]) {
+    __float128 s = 0;
+    for (int c = 0; c < UQO_D; ++c) s += (__float128)x[c] * (__float128)x[c];
+    return (float)sqrtq(s);
+}
+
+/* Reading T3: index of the level nearest to x / n (ties to the lower). */
+int uqo_tq4_index(float x, float n, const float *levels) {
+    float lv[16];
+    __float128 mid[15];
+    tq_tables(levels, lv, mid);
+    if (!(n > 0.0f)) return 0;
+    int idx = 0;
+    for (int j = 0; j < 15; ++j) idx += (__float128)x > mid[j] * (__float128)n;
+    return idx;
 }
 
 /* Encode one token's K and V (128 channels each) per readings T1-T4. */
 void uqo_tq4_encode_vector(const float *k_in, const float *v, const float *levels, uint8_t kidx[UQO_D], float *norm,
                            uint8_t vcode[UQO_D], float s_out[UQO_NGROUP], float z_out[UQO_NGROUP]) {
-    float lv[16], mid[15];
-    tq_tables(levels, lv, mid);
     float x[UQO_D];
     memcpy(x, k_in, sizeof(x));
     uqo_wht128_f32(x, 1);
-    float part[16];
-    for (int sl = 0; sl < 16; ++sl) {
-        float p = 0.0f;
-        for (int i = 0; i < 8; ++i) p = fmaf(x[8 * sl + i], x[8 * sl + i], p);
-        part[sl] = p;
-    }
-    for (int w = 16; w > 1; w /= 2)
-        for (int i = 0; i < w / 2; ++i) part[i] = part[2 * i] + part[2 * i + 1];
-    const float n = sqrtf(part[0]);
+    const float n = uqo_tq4_norm(x);
     *norm = n;
-    float thr[15];
-    for (int j = 0; j < 15; ++j) thr[j] = mid[j] * n;
-    for (int c = 0; c < UQO_D; ++c) {
-        int idx = 0;
-        for (int j = 0; j < 15; ++j) idx += x[c] > thr[j];
-        kidx[c] = (uint8_t)idx;
-    }
+    for (int c = 0; c < UQO_D; ++c) kidx[c] = (uint8_t)uqo_tq4_index(x[c], n, levels);
     for (int g = 0; g < UQO_NGROUP; ++g) {
         const float *vg = v + g * UQO_GROUP;
         float mn = vg[0], mx = vg[0];
@@ -604,7 +612,8 @@ void uqo_tq4_load(const uint8_t *cache, int num_kv_heads, int64_t page, int head
  * (the rotated key), V = bf16(fma(s, code, z)). */
 void uqo_tq4_dequant(const uint8_t *cache, int num_kv_heads, int64_t page, int head, int t, const float *levels,
                      double kout[UQO_D], double vout[UQO_D]) {
-    float lv[16], mid[15];
+    float lv[16];
+    __float128 mid[15];
     tq_tables(levels, lv, mid);
     uint8_t kidx[UQO_D], vcode[UQO_D];
     float n, s[UQO_NGROUP], z[UQO_NGROUP];

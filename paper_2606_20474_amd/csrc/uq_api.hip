@@ -209,7 +209,7 @@ float bf16_nearest(float x) {
 }
 
 // The Ultra-TQ codebook tables: levels rounded to BF16 (finite, strictly
-// ascending), the encoder's midpoints (c_j + c_{j+1}) / 2 in fp32 and the
+// ascending), the encoder's midpoints (c_j + c_{j+1}) / 2 in fp64 and the
 // decoder's byte tables.  False for an unusable codebook.
 bool tq_tables(const float* cb, uq::TqTables& t) {
     if (cb == nullptr) return false;
@@ -221,7 +221,13 @@ bool tq_tables(const float* cb, uq::TqTables& t) {
     }
     for (int j = 0; j < 15; ++j)
         if (!(lv[j] < lv[j + 1])) return false;
-    for (int j = 0; j < 15; ++j) t.mid[j] = (lv[j] + lv[j + 1]) * 0.5f;
+    for (int j = 0; j < 15; ++j) {
+        // the midpoint must be exact in fp64 (adjacent levels within 2^44 of
+        // each other): the encoder decides x > m_j n by the sign of an fma
+        const double a = lv[j], b = lv[j + 1], s = a + b;
+        if (s - a != b || s - b != a) return false;
+        t.mid[j] = s * 0.5;
+    }
     for (int w = 0; w < 4; ++w) {
         uint32_t hi = 0, lo = 0;
         for (int b = 0; b < 4; ++b) {

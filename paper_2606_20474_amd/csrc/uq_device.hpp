@@ -237,34 +237,80 @@ __device__ __forceinline__ float bf16_round(float x) {
     return bits_f32(__builtin_bit_cast(uint32_t, h) << 16);
 }
 
+// s + e = a + b exactly (Knuth's two-sum).
+__device__ __forceinline__ void two_sum(double a, double b, double& s, double& e) {
+#pragma clang fp contract(off)
+    s = a + b;
+    const double bb = s - a;
+    e = (a - (s - bb)) + (b - bb);
+}
+// (sh, sl) = (ah, al) + (bh, bl) in double-double arithmetic (about 106
+// significant bits), operands in a fixed order.
+__device__ __forceinline__ void dd_add(double ah, double al, double bh, double bl, double& sh, double& sl) {
+#pragma clang fp contract(off)
+    double s, e;
+    two_sum(ah, bh, s, e);
+    e += al + bl;
+    sh = s + e;
+    sl = e - (sh - s);
+}
+
+// The l2 norm of a 128-vector held 8 channels per lane by 16 lanes, rounded
+// once to fp32: the squares (exact in fp64) are summed in double-double
+// arithmetic (exact while the magnitudes lie within about 2^25 of each
+// other), the square root is taken in fp64 and refined by one Newton step
+// on the double-double sum, then rounded to fp32.  Every lane gets the same
+// bits: each butterfly step adds the lower lane's partial first.
+__device__ __forceinline__ float exact_norm128(const float (&x)[8], int lane16) {
+#pragma clang fp contract(off)
+    double h = double(x[0]) * double(x[0]), l = 0.0;
+#pragma unroll
+    for (int i = 1; i < 8; ++i) dd_add(h, l, double(x[i]) * double(x[i]), 0.0, h, l);
+#pragma unroll
+    for (int s = 1; s < 16; s <<= 1) {
+        const double oh = __shfl_xor(h, s, 16), ol = __shfl_xor(l, s, 16);
+        if (lane16 & s) dd_add(oh, ol, h, l, h, l);
+        else dd_add(h, l, oh, ol, h, l);
+    }
+    if (!(h > 0.0)) return 0.0f;
+    // sqrt(h + l) = r + c to about 2^-100 relative (c: one Newton step)
+    const double r = __builtin_sqrt(h);
+    const double c = (__builtin_fma(-r, r, h) + l) / (2.0 * r);
+    double rh, rl;
+    two_sum(r, c, rh, rl);
+    const float f = float(rh);
+    // rh exactly halfway between f and its neighbour g (the rounding went to
+    // the even one) while the remainder rl lies beyond it: the norm is
+    // nearer to g
+    const double d = rh - double(f);
+    if (rl != 0.0 && d != 0.0 && (rl > 0.0) == (d > 0.0) && f > 0.0f && f < 0x1p127f) {
+        const float g = bits_f32(f32_bits(f) + (d > 0.0 ? 1u : 0xFFFFFFFFu));   // f > 0: the next float up / down
+        if (__builtin_fabs(d) == 0.5 * __builtin_fabs(double(g) - double(f))) return g;
+    }
+    return f;
+}
+
 // Ultra-TQ encoding of the 8 channels this lane holds (all 16 lanes of the
-// vector take part).  K: rotated; the fp32 norm is a fused multiply-add
-// chain over the lane's channels in order, then a pairwise tree over the 16
-// lanes (each butterfly step adds the same two values in every lane, so all
-// lanes hold the same bits), then a correctly rounded square root; index =
-// number of midpoints m_j with x > m_j * n.  V: per 32-channel group (4
+// vector take part).  K: rotated; n = the l2 norm rounded once to fp32
+// (exact_norm128); index = that of the level nearest to x / n, ties to the
+// lower one: the number of midpoints m_j (exact doubles) with x > m_j n,
+// each decided by the sign of fma(-m_j, n, x) in fp64, which is the sign of
+// the exact x - m_j n (index 0 when n = 0).  V: per 32-channel group (4
 // lanes) zero = bf16(min), scale = bf16(max(max - zero, 0) / 15), code =
 // clamp(rint((x - zero) / scale), 0, 15).
 __device__ __forceinline__ void tq4_encode(float (&xk)[8], const float (&xv)[8], int lane16, const TqTables& tq,
                                            TokenBits<kTq4>& t) {
     wht128_x8(xk, lane16);
-    float p = 0.0f;
-#pragma unroll
-    for (int i = 0; i < 8; ++i) p = __builtin_fmaf(xk[i], xk[i], p);
-    p += __shfl_xor(p, 1, 16);
-    p += __shfl_xor(p, 2, 16);
-    p += __shfl_xor(p, 4, 16);
-    p += __shfl_xor(p, 8, 16);
-    const float n = __builtin_sqrtf(p);
-    float thr[15];
-#pragma unroll
-    for (int j = 0; j < 15; ++j) thr[j] = tq.mid[j] * n;
+    const float n = exact_norm128(xk, lane16);
+    const double nd = n;
     uint32_t wk = 0;
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
         uint32_t idx = 0;
+        if (n > 0.0f) {
 #pragma unroll
-        for (int j = 0; j < 15; ++j) idx += xk[i] > thr[j] ? 1u : 0u;
+            for (int j = 0; j < 15; ++j) idx += __builtin_fma(-tq.mid[j], nd, double(xk[i])) > 0.0 ? 1u : 0u;
+        }
         wk |= idx << (4 * i);
     }
     float mn = xv[0], mx = xv[0];

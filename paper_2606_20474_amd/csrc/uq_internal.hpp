@@ -16,11 +16,11 @@ namespace uq {
 enum KvFmt : int32_t { kFp4 = 0, kFp8 = 1, kBf16 = 2, kTq4 = 3, kFp4d64 = 4, kFp4d256 = 5, kFp4d64x2 = 6 };
 
 // Tables of the Ultra-TQ key codebook, built on the host from the 16 levels
-// rounded to BF16: the encoder's midpoints and the decoder's byte lookup
-// (lut[0..3]: high bytes of the BF16 levels, four per dword in level order;
-// lut[4..7]: low bytes).
+// rounded to BF16: the encoder's midpoints (c_j + c_{j+1}) / 2, exact in
+// fp64, and the decoder's byte lookup (lut[0..3]: high bytes of the BF16
+// levels, four per dword in level order; lut[4..7]: low bytes).
 struct TqTables {
-    float mid[15];
+    double mid[15];
     uint32_t lut[8];
 };
 constexpr int kNumCus = 256;     // compute units of an MI355X (8 XCDs x 32)

@@ -34,7 +34,10 @@ MISTAKES = {
                              "const int hk = hq % num_kv_heads;\n            const int ctx = context_lens[b];")],
     "softmax scale dropped": [("s[j] = softmax_scale * dot;", "s[j] = dot;")],
     "output not rotated back": [("if (rotate_v) uqo_wht_f64(acc, o, d);", "if (0) uqo_wht_f64(acc, o, d);")],
-    "TQ4 key norm not square-rooted": [("const float n = sqrtf(part[0]);", "const float n = part[0];")],
+    "TQ4 key norm not square-rooted": [("return (float)sqrtq(s);", "return (float)s;")],
+    "TQ4 key norm from fp32 squares": [("s += (__float128)x[c] * (__float128)x[c];", "s += (__float128)(x[c] * x[c]);")],
+    "TQ4 key index ties to the upper level": [("idx += (__float128)x > mid[j] * (__float128)n;",
+                                               "idx += (__float128)x >= mid[j] * (__float128)n;")],
     "TQ4 value zero point not BF16": [("const float z = uqo_bf16_rne(mn);", "const float z = mn;")],
     "TQ4 value grid of 16 steps": [("const float s = uqo_bf16_rne(d / 15.0f);", "const float s = uqo_bf16_rne(d / 16.0f);")],
     "TQ4 V tokens reversed in a dword": [("4 * (t % 4) + (c % 8) / 2; }", "4 * (3 - t % 4) + (c % 8) / 2; }")],

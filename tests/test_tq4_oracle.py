@@ -4,11 +4,13 @@ times a per-token norm, values as 4-bit uniform codes with a (scale, zero)
 per 32-channel group; readings T1-T5 in oracle/uq_oracle.c).
 
 Each pin checks the oracle against something other than its own formula:
-torch's BF16 cast, a brute-force nearest-level search, numpy's norm, the
-codebook's design MSE, exact uniform grids, hand-derived layout offsets
+torch's BF16 cast, exact rational arithmetic (the norm rounded once, an
+exhaustive nearest-level search with exact ties), the codebook's design MSE, exact uniform grids, hand-derived layout offsets
 (tests/golden/tq4_layout.txt), scipy's softmax and invariants.
 """
+import math
 import os
+from fractions import Fraction
 
 import numpy as np
 import pytest
@@ -36,26 +38,98 @@ def test_bf16_rounding_matches_torch():
     assert np.array_equal(got, bf16(x))
 
 
-def test_norm_is_the_l2_norm_of_the_rotated_key():
-    for _ in range(300):
-        k = (RNG.standard_normal(128) * RNG.uniform(0.01, 100)).astype(np.float32)
-        _, n, _, _, _ = oracle.tq4_encode_vector(k, k, CB)
-        ref = np.linalg.norm(oracle.wht128_f32(k).astype(np.float64))
-        assert abs(n - ref) <= 2 * np.spacing(np.float32(ref)), (n, ref)
+def rn32_sqrt(S):
+    """sqrt of the non-negative dyadic rational S rounded once to fp32
+    (nearest, ties to even), by exact integer square roots."""
+    if S == 0:
+        return 0.0
+    e = math.floor(math.log2(float(S)) / 2)
+    while Fraction(2) ** (2 * e) > S:
+        e -= 1
+    while Fraction(2) ** (2 * e + 2) <= S:
+        e += 1
+    # 2^e <= sqrt(S) < 2^(e+1); scale so that sqrt(N) carries 23 + 40 bits
+    # below 2^e and N is an integer
+    t = 23 - e + 40
+    t = max(t, (S.denominator.bit_length() + 1) // 2)
+    N = S * 4 ** t
+    assert N.denominator == 1
+    N = N.numerator
+    r = math.isqrt(N)
+    exact = r * r == N
+    shift = t - (23 - e)
+    q, rem = divmod(r, 1 << shift)
+    half = 1 << (shift - 1)
+    if rem > half or (rem == half and not exact) or (rem == half and exact and q & 1):
+        q += 1
+    return float(q * Fraction(2) ** (e - 23))
+
+
+def exact_norm(x):
+    return rn32_sqrt(sum(Fraction(float(v)) ** 2 for v in x))
+
+
+def test_norm_is_the_l2_norm_rounded_once():
+    """Reading T2 against exact rational arithmetic: fl32(sqrt(sum x_i^2))."""
+    for i in range(300):
+        x = (RNG.standard_normal(128) * 10.0 ** RNG.uniform(-6, 6)).astype(np.float32)
+        if i % 3 == 0:
+            x[RNG.integers(0, 128, 4)] *= np.float32(2.0 ** 20)      # outliers: squares spanning 2^40+
+        assert oracle.tq4_norm(x) == exact_norm(x), i
+
+
+def test_norm_ties_and_near_ties():
+    """Sums of squares that are the square of an fp32 midpoint: the exact
+    tie goes to the even neighbour; a tiny extra square moves it up."""
+    x = np.zeros(128, np.float32)
+    x[:6] = [2.0 ** 24, 5792, 84, 10, 3, 2]          # (2^24)^2 + 2^25 + 1 = (2^24 + 1)^2
+    assert sum(Fraction(int(v)) ** 2 for v in x) == (2 ** 24 + 1) ** 2
+    assert oracle.tq4_norm(x) == exact_norm(x) == 2.0 ** 24
+    x[6] = 2.0 ** -20
+    assert oracle.tq4_norm(x) == exact_norm(x) == 2.0 ** 24 + 2
+    x = np.zeros(128, np.float32)
+    x[:2] = [3.0, 4.0]
+    assert oracle.tq4_norm(x) == 5.0
+    assert oracle.tq4_norm(np.zeros(128, np.float32)) == 0.0
+
+
+def nearest_level(x, n, lv):
+    """Brute force: the index of the level nearest to x / n, exactly, ties to
+    the lower index."""
+    u = Fraction(float(x)) / Fraction(float(n))
+    d = [abs(u - Fraction(float(c))) for c in lv]
+    return min(range(16), key=lambda j: (d[j], j))
 
 
 def test_key_index_is_the_nearest_level():
-    lv = bf16(CB).astype(np.float64)
-    mid = (lv[1:] + lv[:-1]) / 2
-    bad = 0
-    for _ in range(300):
+    """Reading T3 against an exact brute-force search, every channel of
+    random rotated keys, no value left out."""
+    lv = bf16(CB)
+    for _ in range(60):
         k = RNG.standard_normal(128).astype(np.float32)
         kidx, n, _, _, _ = oracle.tq4_encode_vector(k, k, CB)
-        u = oracle.wht128_f32(k).astype(np.float64) / n
-        near = np.argmin(np.abs(u[:, None] - lv[None, :]), axis=1)
-        boundary = np.min(np.abs(u[:, None] - mid[None, :]), axis=1) < 1e-6
-        bad += int(np.sum((near != kidx) & ~boundary))
-    assert bad == 0
+        x = oracle.wht128_f32(k)
+        assert n == exact_norm(x)
+        for c in range(128):
+            assert kidx[c] == nearest_level(x[c], n, lv), (c, x[c], n)
+
+
+def test_key_index_ties_go_to_the_lower_level():
+    """x / n exactly on a midpoint (n a power of two, the midpoint of two
+    BF16 levels times n exact in fp32) takes the lower index; the fp32
+    neighbours on either side take the nearer level."""
+    lv = bf16(CB)
+    for n in (0.5, 1.0, 8.0, 2.0 ** -10):
+        for j in range(15):
+            m = (Fraction(float(lv[j])) + Fraction(float(lv[j + 1]))) / 2 * Fraction(n)
+            x = np.float32(float(m))
+            assert Fraction(float(x)) == m
+            assert oracle.tq4_index(x, n, CB) == j == nearest_level(x, n, lv)
+            up = np.nextafter(x, np.float32(np.inf))
+            dn = np.nextafter(x, np.float32(-np.inf))
+            assert oracle.tq4_index(up, n, CB) == j + 1 == nearest_level(up, n, lv)
+            assert oracle.tq4_index(dn, n, CB) == j == nearest_level(dn, n, lv)
+    assert oracle.tq4_index(0.3, 0.0, CB) == 0          # zero key: index 0
 
 
 def test_key_error_is_the_codebook_design_error():
