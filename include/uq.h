@@ -73,7 +73,17 @@
 extern "C" {
 #endif
 
-typedef enum uq_status {
+/* The enumerations are 32-bit integers on both sides of the ABI; a C caller
+ * may pass any int32_t value (out-of-range values are rejected, and
+ * uq_status_string names them UQ_ERR_UNKNOWN), so C++ gives them that
+ * underlying type explicitly. */
+#ifdef __cplusplus
+#define UQ_ENUM_BASE : int32_t
+#else
+#define UQ_ENUM_BASE
+#endif
+
+typedef enum uq_status UQ_ENUM_BASE {
     UQ_OK = 0,
     UQ_ERR_INVALID_ARGUMENT = 1,   /* null pointer, negative size, inconsistent shape */
     UQ_ERR_UNSUPPORTED = 2,        /* valid request outside the supported shapes */
@@ -81,7 +91,7 @@ typedef enum uq_status {
     UQ_ERR_HIP = 4                 /* a HIP launch failed (hipGetLastError) */
 } uq_status;
 
-typedef enum uq_dtype {
+typedef enum uq_dtype UQ_ENUM_BASE {
     UQ_F32 = 0,
     UQ_BF16 = 1,
     UQ_F16 = 2,
@@ -381,7 +391,7 @@ uq_status uq_decode_cascade_merge(const uq_cache_desc *desc, int32_t batch, int3
  *                 group g at 2112 + 16 * (4 * (t/4) + g) + 4 * (t%4).
  * ---------------------------------------------------------------------- */
 
-typedef enum uq_ref_format {
+typedef enum uq_ref_format UQ_ENUM_BASE {
     UQ_REF_FP8_E4M3 = 1, /* OCP E4M3 (no infinities), one scale per tensor */
     UQ_REF_BF16 = 2,
     UQ_REF_TQ4 = 3       /* the Ultra-TQ codebook cache (see below) */

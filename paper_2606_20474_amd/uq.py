@@ -15,7 +15,9 @@ from dataclasses import dataclass
 import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libuq.so")
+# UQ_LIB names another build of the same sources (the CPU sanitizer test
+# loads a host-sanitised build that way, in a subprocess of its own)
+LIB_PATH = os.environ.get("UQ_LIB") or os.path.join(_PKG, "libuq.so")
 
 UQ_OK, UQ_ERR_INVALID_ARGUMENT, UQ_ERR_UNSUPPORTED, UQ_ERR_WORKSPACE_TOO_SMALL, UQ_ERR_HIP = range(5)
 UQ_F32, UQ_BF16, UQ_F16, UQ_FP8_E4M3 = range(4)
