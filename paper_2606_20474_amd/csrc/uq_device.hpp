@@ -130,6 +130,21 @@ __device__ __forceinline__ int ue8m0_exponent(float m, float c) {
     return E;
 }
 
+// The same rule as the UE8M0 byte E + 127, by integer arithmetic on the
+// bits u of y = fl32(c * m): for a normal y, adding 2^23 - 0x3504F4 carries
+// into the exponent field exactly when the fraction is >= 0x3504F4, so the
+// byte is the exponent field of the sum (clamped to 254: E <= 127, also for
+// y = +inf); a subnormal y gives E = -126 when y >= sqrt(2) 2^-127 (fraction
+// >= 0x5A827A), else E <= -127 (clamped): byte 1 or 0; y = 0 gives byte 0.
+// Equal to ue8m0_exponent(m, c) + 127 for every m >= 0 (m is a running
+// maximum of magnitudes, never negative or NaN).
+__device__ __forceinline__ uint32_t ue8m0_byte(float m, float c) {
+#pragma clang fp contract(off)
+    const uint32_t u = f32_bits(c * m);
+    const uint32_t b = __builtin_elementwise_min((u + 0x4AFB0Cu) >> 23, 254u);
+    return u < 0x800000u ? (u >= 0x5A827Au ? 1u : 0u) : b;
+}
+
 // OCP e4m3fn byte of x, round to nearest even, saturating to +-448.
 // Normal range: keep 3 fraction bits of the fp32 pattern with RNE (a carry
 // moves into the exponent by itself) and rebias 127 -> 7.  Below 2^-6 the

@@ -21,17 +21,38 @@ __device__ __forceinline__ float quad_xor(float x) {
     return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, x), ctrl, 0xF, 0xF, true));
 }
 
-// The rotation of one head vector of D = 32 NG channels held by 4 lanes of
-// a quad: lane L holds channels 32j + 8L + i in x[j][i] (j < NG, i < 8).
-// The stages run in the order of the format (widths 1, 2, 4, ..., D/2): 1,
-// 2, 4 inside a lane over i, 8 and 16 across lanes L^1, L^2, then 32, 64
-// (and 128 for D = 256) inside a lane over j; each maps (a, b) to
-// (a + b, a - b) in fp32 (the upper element of a cross-lane pair takes
-// fma(-1, b, a) = a - b, exactly rounded), then one multiply by
-// fl32(1/sqrt(D)).  The values equal those of the 16-lane form wht_x bit
-// for bit.
+// One cross-lane butterfly stage for the 8 values of a lane, partner L^S:
+// y <- dpp(y) * t + y, one v_fmac_f32 per value with the partner lane's
+// value as a DPP (quad_perm) operand (the compiler does not fold the DPP move
+// into this tied instruction itself).  s_nop 1 first: a DPP read needs two
+// wait states after a VALU write of its register, and inside the block no
+// register is read after it is written.  All 64 lanes are active.
+#define UQ_FMAC_DPP(P, i) "v_fmac_f32_dpp %" #i ", %" #i ", %8 quad_perm:" P " row_mask:0xf bank_mask:0xf bound_ctrl:1\n\t"
+#define UQ_FMAC_DPP8(P)                                                                                          \
+    "s_nop 1\n\t" UQ_FMAC_DPP(P, 0) UQ_FMAC_DPP(P, 1) UQ_FMAC_DPP(P, 2) UQ_FMAC_DPP(P, 3) UQ_FMAC_DPP(P, 4)      \
+        UQ_FMAC_DPP(P, 5) UQ_FMAC_DPP(P, 6) UQ_FMAC_DPP(P, 7)
+template <int S>
+__device__ __forceinline__ void quad_stage8(float (&y)[8], float t) {
+    if constexpr (S == 1) {
+        asm volatile(UQ_FMAC_DPP8("[1,0,3,2]")
+                     : "+v"(y[0]), "+v"(y[1]), "+v"(y[2]), "+v"(y[3]), "+v"(y[4]), "+v"(y[5]), "+v"(y[6]), "+v"(y[7])
+                     : "v"(t));
+    } else {
+        asm volatile(UQ_FMAC_DPP8("[2,3,0,1]")
+                     : "+v"(y[0]), "+v"(y[1]), "+v"(y[2]), "+v"(y[3]), "+v"(y[4]), "+v"(y[5]), "+v"(y[6]), "+v"(y[7])
+                     : "v"(t));
+    }
+}
+#undef UQ_FMAC_DPP8
+#undef UQ_FMAC_DPP
+
+// The rotation in its plain form: each cross-lane stage moves the partner's
+// value (DPP) and combines it with one fma, fma(s, x, o) = x + o or o - x.
+// wht_quad below gives the same values with one instruction per value and
+// stage, except for the signs of exact zeros when the input vector is all
+// zero; quantize_xq falls back to this form for such vectors.
 template <int NG>
-__device__ __forceinline__ void wht_quad(float (&x)[NG][8], int L) {
+__device__ __forceinline__ void wht_quad_plain(float (&x)[NG][8], int L) {
 #pragma clang fp contract(off)
 #pragma unroll
     for (int h = 1; h < 8; h <<= 1) {
@@ -76,28 +97,111 @@ __device__ __forceinline__ void wht_quad(float (&x)[NG][8], int L) {
         for (int i = 0; i < 8; ++i) x[j][i] = x[j][i] * r;
 }
 
+// The rotation of one head vector of D = 32 NG channels held by 4 lanes of
+// a quad: lane L holds channels 32j + 8L + i in x[j][i] (j < NG, i < 8).
+// The stages run in the order of the format (widths 1, 2, 4, ..., D/2): 1,
+// 2, 4 inside a lane over i, 8 and 16 across lanes L^1, L^2, then 32, 64
+// (and 128 for D = 256) inside a lane over j; each maps (a, b) to
+// (a + b, a - b) in fp32, then one multiply by fl32(1/sqrt(D)).  The values
+// equal those of the 16-lane form wht_x bit for bit.
+//
+// The two cross-lane stages take one instruction per value,
+// v_fmac_f32 with the partner's value as a DPP operand: y <- dpp(y) * t + y
+// with t = +-1 per lane.  The upper lane of a pair needs o - x but a single
+// form gives it x - o, so it keeps the negated value (every fp32 rounding is
+// symmetric under negation) and its sign sigma is tracked: t1 = sigma after
+// the first stage, and since both lanes of a second-stage pair carry the
+// same sigma, t2 makes the second stage right up to sign too; the final
+// multiply by sigma * fl32(1/sqrt(D)) (exact) restores every value.
+// Negation symmetry fails at exact zeros only: an exact cancellation gives
+// +0 whatever the signs.  The reference form yields -0 only from a subtree
+// of zeros, and every output depends on all inputs, so for an input that is
+// not all zero every zero output is +0: the final step is fma(y, sigma r,
+// +0), which keeps every nonzero result (and the sign of an underflow) and
+// turns every exact zero into +0.  An all-zero input is left to
+// wht_quad_plain.
+template <int NG>
+__device__ __forceinline__ void wht_quad(float (&x)[NG][8], int L) {
+#pragma clang fp contract(off)
+#pragma unroll
+    for (int h = 1; h < 8; h <<= 1) {
+#pragma unroll
+        for (int j = 0; j < NG; ++j) {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                if (i & h) continue;
+                const float a = x[j][i], b = x[j][i + h];
+                x[j][i] = a + b;
+                x[j][i + h] = a - b;
+            }
+        }
+    }
+    const float t1 = (L & 1) ? -1.0f : 1.0f;
+    const float t2 = (L & 2) ? -1.0f : 1.0f;
+#pragma unroll
+    for (int j = 0; j < NG; ++j) quad_stage8<1>(x[j], t1);
+#pragma unroll
+    for (int j = 0; j < NG; ++j) quad_stage8<2>(x[j], t2);
+#pragma unroll
+    for (int h = 1; h < NG; h <<= 1) {
+#pragma unroll
+        for (int j = 0; j < NG; ++j) {
+            if (j & h) continue;
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+                const float a = x[j][i], b = x[j + h][i];
+                x[j][i] = a + b;
+                x[j + h][i] = a - b;
+            }
+        }
+    }
+    const float r = inv_sqrt_d<32 * NG>() * (t1 * t2);
+#pragma unroll
+    for (int j = 0; j < NG; ++j)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) x[j][i] = __builtin_fmaf(x[j][i], r, 0.0f);
+}
+
 __device__ __forceinline__ void wht128_x32(float (&x)[4][8], int L) { wht_quad<4>(x, L); }
 
 // Quantise one head vector held by a quad (rotated first if `rotate`): per
-// 32-channel group j the UE8M0 exponent E_j of the group maximum, and the
-// E2M1 codes of the lane's 8 channels of the group in w[j] (channel order,
-// low nibble first) by the hardware conversion, which rounds x / 2^E_j to
-// the nearest E2M1 level with ties to the even code, saturates at 6 and
-// keeps the sign (checked against a threshold encoder over every tie, both
-// zeros, subnormal inputs and scales 2^-127 .. 2^127).
-template <int NG>
+// 32-channel group j the UE8M0 byte b_j = E_j + 127 of the group maximum
+// (ue8m0_byte), and the E2M1 codes of the lane's 8 channels of the group in
+// w[j] (channel order, low nibble first) by the hardware conversion, which
+// rounds x / 2^E_j to the nearest E2M1 level with ties to the even code,
+// saturates at 6 and keeps the sign (checked against a threshold encoder
+// over every tie, both zeros, subnormal inputs and scales 2^-127 .. 2^127).
+// `src` and `row` locate the vector's input (rows of dtype DT) for the
+// all-zero case.
+template <int DT, int NG>
 __device__ __forceinline__ void quantize_xq(float (&x)[NG][8], int L, float c, bool rotate, uint32_t (&w)[NG],
-                                            int (&E)[NG]) {
+                                            uint32_t (&byte)[NG], const void* src, int64_t row) {
     if (rotate) wht_quad<NG>(x, L);
+    float m[NG];
+    float mall = 0.0f;
 #pragma unroll
     for (int j = 0; j < NG; ++j) {
-        float m = 0.0f;
+        // group maximum of |x|: three-input maxima, then the quad
+        float mj = __builtin_fmaxf(__builtin_fmaxf(__builtin_fabsf(x[j][0]), __builtin_fabsf(x[j][1])),
+                                   __builtin_fabsf(x[j][2]));
+        mj = __builtin_fmaxf(__builtin_fmaxf(mj, __builtin_fabsf(x[j][3])), __builtin_fabsf(x[j][4]));
+        mj = __builtin_fmaxf(__builtin_fmaxf(mj, __builtin_fabsf(x[j][5])), __builtin_fabsf(x[j][6]));
+        mj = __builtin_fmaxf(mj, __builtin_fabsf(x[j][7]));
+        mj = __builtin_fmaxf(mj, quad_xor<1>(mj));
+        m[j] = __builtin_fmaxf(mj, quad_xor<2>(mj));
+        mall = __builtin_fmaxf(mall, m[j]);
+    }
+    // every rotated value zero (quad-uniform): the signs of the zeros, which
+    // the codes keep, come from the plain form of the rotation
+    if (rotate && __builtin_amdgcn_ballot_w64(mall == 0.0f) != 0 && mall == 0.0f) {
 #pragma unroll
-        for (int i = 0; i < 8; ++i) m = __builtin_fmaxf(m, __builtin_fabsf(x[j][i]));
-        m = __builtin_fmaxf(m, quad_xor<1>(m));
-        m = __builtin_fmaxf(m, quad_xor<2>(m));
-        E[j] = ue8m0_exponent(m, c);
-        const float sc = __builtin_ldexpf(1.0f, E[j]);   // 2^E exactly (subnormal for E = -127)
+        for (int j = 0; j < NG; ++j) load_x8<DT>(src, row + 32 * j, x[j]);
+        wht_quad_plain<NG>(x, L);
+    }
+#pragma unroll
+    for (int j = 0; j < NG; ++j) {
+        byte[j] = ue8m0_byte(m[j], c);
+        const float sc = __builtin_ldexpf(1.0f, int(byte[j]) - 127);   // 2^E exactly (subnormal for E = -127)
         uint32_t v = 0u;
         v = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(v, x[j][0], x[j][1], sc, 0);
         v = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(v, x[j][2], x[j][3], sc, 1);
@@ -110,29 +214,30 @@ __device__ __forceinline__ void quantize_xq(float (&x)[NG][8], int L, float c, b
 // Element j of a small register array at a lane-dependent index, by selects
 // (a dynamic index would put the array in scratch memory).
 template <int NG>
-__device__ __forceinline__ int pick(const int (&e)[NG], int j) {
-    int r = e[0];
+__device__ __forceinline__ uint32_t pick(const uint32_t (&e)[NG], int j) {
+    uint32_t r = e[0];
 #pragma unroll
     for (int k = 1; k < NG; ++k) r = j == k ? e[k] : r;
     return r;
 }
 
 // Quantize-on-write, 4 lanes (one quad) per (token, kv head) vector of
-// D = 32 NG channels, 64 vectors per 256-thread block.  Lane L loads and
-// keeps channels 32j + 8L + i (16-byte loads, a quad covers 64 contiguous
-// bytes per j), so the two cross-lane stages of the rotation and the group
-// maxima are DPP quad permutes.  Stores: one codes dword per group for K and
-// V, and the scale bytes of groups L, L + 4, ... for K and V.  Tiles are
-// 8 D code bytes and D/2 scale bytes per (page, head, K|V).
+// D = 32 NG channels, 64 tokens of one kv head per 256-thread block; the
+// linear grid runs kv head fastest, so consecutive blocks read the 64 tokens'
+// whole rows together, and a block writes whole (page, head) tiles when its
+// tokens fill pages.  Lane L loads and keeps channels 32j + 8L + i (16-byte
+// loads, a quad covers 64 contiguous bytes per j), so the two cross-lane
+// stages of the rotation and the group maxima are DPP quad permutes.
+// Stores: one codes dword per group for K and V, and the scale bytes of
+// groups L, L + 4, ... for K and V.  Tiles are 8 D code bytes and D/2 scale
+// bytes per (page, head, K|V).
 template <int DT, int NG>
 __global__ void __launch_bounds__(256) quantize_kv_kernel(QuantizeParams p) {
     constexpr int D = 32 * NG;
     const int L = threadIdx.x & 3;
-    const int64_t vec = int64_t(blockIdx.x) * 64 + (threadIdx.x >> 2);
-    const int64_t nvec = p.num_tokens * p.num_kv_heads;
-    if (vec >= nvec) return;   // whole quads leave together
-    const int64_t t = vec / p.num_kv_heads;
-    const int h = int(vec - t * p.num_kv_heads);
+    const int h = int(blockIdx.x % unsigned(p.num_kv_heads));              // block-uniform (scalar)
+    const int64_t t = int64_t(blockIdx.x / unsigned(p.num_kv_heads)) * 64 + (threadIdx.x >> 2);
+    if (t >= p.num_tokens) return;   // whole quads leave together
 
     // The rows are loaded together with the slot, before the slot is known
     // to be valid: the row loads then overlap the slot and page-table
@@ -157,15 +262,14 @@ __global__ void __launch_bounds__(256) quantize_kv_kernel(QuantizeParams p) {
         page = p.page_table[seq * p.max_pages_per_seq + pos / kPage];
         off = int(pos % kPage);
     } else {
-        page = slot / kPage;
-        off = int(slot % kPage);
+        page = slot >> 4;
+        off = int(slot & (kPage - 1));
     }
     if (page < 0 || page >= p.num_pages) return;
 
-    uint32_t wk[NG], wv[NG];
-    int ek[NG], ev[NG];
-    quantize_xq<NG>(xk, L, p.c, true, wk, ek);
-    quantize_xq<NG>(xv, L, p.c, p.rotate_v != 0, wv, ev);
+    uint32_t wk[NG], wv[NG], bk[NG], bv[NG];
+    quantize_xq<DT, NG>(xk, L, p.c, true, wk, bk, p.k, row);
+    quantize_xq<DT, NG>(xv, L, p.c, p.rotate_v != 0, wv, bv, p.v, row);
 
     const int64_t ph = page * p.num_kv_heads + h;
     uint8_t* kc = p.codes + ph * (16 * D);
@@ -183,8 +287,8 @@ __global__ void __launch_bounds__(256) quantize_kv_kernel(QuantizeParams p) {
     for (int q = 0; q < (NG + 3) / 4; ++q) {
         const int j = L + 4 * q;
         if (j < NG) {
-            ks[j * kPage + off] = uint8_t(pick<NG>(ek, j) + 127);
-            ks[D / 2 + j * kPage + off] = uint8_t(pick<NG>(ev, j) + 127);
+            ks[j * kPage + off] = uint8_t(pick<NG>(bk, j));
+            ks[D / 2 + j * kPage + off] = uint8_t(pick<NG>(bv, j));
         }
     }
 }
@@ -245,7 +349,7 @@ __global__ void __launch_bounds__(256) quantize_error_kernel(ErrorParams p) {
                 if (!(m[j] > 0.0f)) continue;   // an all-zero group decodes exactly
                 if (p.pow2) {
                     // The cache encoder itself: scale operand 2^E, decode by the same scale.
-                    const float sc = __builtin_ldexpf(1.0f, ue8m0_exponent(m[j], c));
+                    const float sc = __builtin_ldexpf(1.0f, int(ue8m0_byte(m[j], c)) - 127);
 #pragma unroll
                     for (int i = 0; i < 8; i += 2) {
                         const uint32_t w = __builtin_amdgcn_cvt_scalef32_pk_fp4_f32(0u, x[j][i], x[j][i + 1], sc, 0);
@@ -342,8 +446,8 @@ static void launch_quantize_ng(const QuantizeParams& p, int dtype, const dim3& g
 }
 
 hipError_t launch_quantize_kv(const QuantizeParams& p, int dtype, hipStream_t stream) {
-    const int64_t nvec = p.num_tokens * p.num_kv_heads;
-    const int64_t blocks = (nvec + 63) / 64;   // 64 quads per block
+    // 64 tokens of one kv head per block, kv head fastest
+    const int64_t blocks = (p.num_tokens + 63) / 64 * p.num_kv_heads;
     if (blocks == 0) return hipSuccess;
     if (blocks > 0x7FFFFFFF) return hipErrorInvalidValue;
     const dim3 grid{unsigned(blocks)};
