@@ -493,6 +493,26 @@ uq_status uq_ref_decode_merge(const uq_ref_cache_desc *desc, int32_t batch, int3
                               void *stream);
 
 /* ------------------------------------------------------------------------
+ * uq_decode_attention_scaled_pv -- uq_decode_attention with PV on the
+ * block-scaled matrix instruction (Algorithm 1, Decode, "PV via FP4/scale
+ * path"; section "UltraQuant Kernel Ladder"): a prototype kept for
+ * measurement against the default BF16 PV path.  QK^T and the softmax are
+ * the default kernel's; PV runs on v_mfma_scale_f32_16x16x128_f8f6f4 with
+ * the raw E2M1 V codes as one operand and P, scaled per (token, channel
+ * group) by V's UE8M0 scale and split into four FP8 terms, as the other
+ * (the instruction's scales are per 32-token block and cannot carry V's
+ * per-token scales).  Head size 128 only; V scale bytes up to 135
+ * (|V| < 6 * 2^8) keep the FP8 terms in range.  Arguments, outputs and
+ * errors as uq_decode_attention, plus UNSUPPORTED for other head sizes.
+ * ---------------------------------------------------------------------- */
+uq_status uq_decode_attention_scaled_pv(const uq_cache_desc *desc, const void *q, uq_dtype q_dtype, int32_t batch,
+                                        int32_t num_q_heads, const uint8_t *kv_codes, const uint8_t *kv_scales,
+                                        const int32_t *page_table, int32_t max_pages_per_seq,
+                                        const int32_t *context_lens, int32_t max_context, float softmax_scale,
+                                        int32_t partition_tokens, void *workspace, size_t workspace_bytes, void *out,
+                                        uq_dtype out_dtype, void *stream);
+
+/* ------------------------------------------------------------------------
  * uq_decode_attention_noalloc -- uq_decode_attention for callers that cannot
  * allocate device memory: code under HIP graph capture, tight serving loops,
  * harnesses that forbid hipMalloc.  The partition partials go to a device

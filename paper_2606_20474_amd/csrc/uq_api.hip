@@ -456,6 +456,23 @@ uq_status uq_decode_attention(const uq_cache_desc* desc, const void* q, uq_dtype
     return from_hip(uq::launch_decode_merge(p, static_cast<hipStream_t>(stream)));
 }
 
+uq_status uq_decode_attention_scaled_pv(const uq_cache_desc* desc, const void* q, uq_dtype q_dtype, int32_t batch,
+                                        int32_t num_q_heads, const uint8_t* kv_codes, const uint8_t* kv_scales,
+                                        const int32_t* page_table, int32_t max_pages_per_seq,
+                                        const int32_t* context_lens, int32_t max_context, float softmax_scale,
+                                        int32_t partition_tokens, void* workspace, size_t workspace_bytes, void* out,
+                                        uq_dtype out_dtype, void* stream) {
+    uq::DecodeParams p;
+    uq_status s = decode_setup(desc, q, q_dtype, batch, num_q_heads, kv_codes, kv_scales, page_table,
+                               max_pages_per_seq, context_lens, max_context, softmax_scale, partition_tokens, workspace,
+                               workspace_bytes, out, out_dtype, p);
+    if (s != UQ_OK) return s;
+    if (desc->head_dim != kHeadDim) return UQ_ERR_UNSUPPORTED;
+    s = from_hip(uq::launch_decode_partials_mxpv(p, static_cast<hipStream_t>(stream)));
+    if (s != UQ_OK) return s;
+    return from_hip(uq::launch_decode_merge(p, static_cast<hipStream_t>(stream)));
+}
+
 uq_status uq_decode_partials(const uq_cache_desc* desc, const void* q, uq_dtype q_dtype, int32_t batch,
                              int32_t num_q_heads, const uint8_t* kv_codes, const uint8_t* kv_scales,
                              const int32_t* page_table, int32_t max_pages_per_seq, const int32_t* context_lens,

@@ -1363,6 +1363,425 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
     }
 }
 
+// ---------------------------------------------------------------------------
+// Prototype: PV on the block-scaled matrix instruction (FP4 cache, head size
+// 128, plain decode).  QK^T and the online softmax are those of
+// decode_kernel<kFp4>; PV runs on v_mfma_scale_f32_16x16x128_f8f6f4 with the
+// raw E2M1 V codes as operand A (rows = 16 channels of a tile, k = tokens,
+// scale byte 127) and P as operand B in FP8.  V's UE8M0 scale varies per
+// (token, 32-channel group) along the contraction, which the instruction's
+// per-(row, 32-k block) scales cannot carry, so it goes into P: per channel
+// group g, P'_g = P * 2^(E_V(token, g) - 127), split into four FP8 terms
+// t_k = fp8(r_k), r_{k+1} = (r_k - t_k) * 16, whose B scale bytes 127 - 4k undo
+// the shifts (about 16 significant bits of P', as the BF16 hi + lo split of
+// the BF16 path).  The running maximum moves eagerly, so that P <= 1 and
+// P' <= 2^(E_V - 127) stays within FP8's 448.  K = 128 is filled with the 128 tokens of 4 consecutive
+// iterations of the wave: the B lane (column n, group g4) puts its own 8 P
+// values of iteration u into bytes 8u .. 8u + 7 (no exchange between lanes),
+// and the matching A rows come from ds_read_b64_tr_b4: each iteration the
+// V codes are written to a per-wave area as 8-byte rows (16 channels of one
+// token), and a transposed read gives lane r of a 16-lane group channel r of
+// the 16 tokens its group addressed.
+template <int U> struct MxPvSlots {};
+
+// Stage registers of the prototype: K as decode_kernel<kFp4>, V codes, and
+// the V scale bytes of the lane's 4 tokens of each page for all 4 groups.
+struct MxPvStage {
+    uint4 k[2], v[2];
+    uint32_t ks[2];
+    uint32_t vs[2][4];   // [page][group]: bytes = tokens 4 g4 .. 4 g4 + 3
+};
+
+__device__ __forceinline__ void mxpv_stage_read(MxPvStage& r, uint32_t stage_addr, int lane) {
+    const uint32_t ac = stage_addr + 16 * lane;
+    const uint32_t ak = stage_addr + lane;
+    const uint32_t av = stage_addr + 4096 + kTileScales + 4 * (lane >> 4);
+    asm volatile(
+        "ds_read_b128 %0, %14\n\t"
+        "ds_read_b128 %1, %14 offset:1024\n\t"
+        "ds_read_b128 %2, %14 offset:2048\n\t"
+        "ds_read_b128 %3, %14 offset:3072\n\t"
+        "ds_read_u8 %4, %15 offset:4096\n\t"
+        "ds_read_u8 %5, %15 offset:4224\n\t"
+        "ds_read_b32 %6, %16\n\t"
+        "ds_read_b32 %7, %16 offset:16\n\t"
+        "ds_read_b32 %8, %16 offset:32\n\t"
+        "ds_read_b32 %9, %16 offset:48\n\t"
+        "ds_read_b32 %10, %16 offset:128\n\t"
+        "ds_read_b32 %11, %16 offset:144\n\t"
+        "ds_read_b32 %12, %16 offset:160\n\t"
+        "ds_read_b32 %13, %16 offset:176\n\t"
+        "s_waitcnt lgkmcnt(0)"
+        : "=&v"(r.k[0]), "=&v"(r.v[0]), "=&v"(r.k[1]), "=&v"(r.v[1]), "=&v"(r.ks[0]), "=&v"(r.ks[1]),
+          "=&v"(r.vs[0][0]), "=&v"(r.vs[0][1]), "=&v"(r.vs[0][2]), "=&v"(r.vs[0][3]), "=&v"(r.vs[1][0]),
+          "=&v"(r.vs[1][1]), "=&v"(r.vs[1][2]), "=&v"(r.vs[1][3])
+        : "v"(ac), "v"(ak), "v"(av)
+        : "memory");
+}
+
+typedef int v2i_t __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) v2i_t* lds_v2i_ptr;
+typedef short v2s_t __attribute__((ext_vector_type(2)));
+
+// Four FP8 E4M3 bytes of r0..r3 (round to nearest even).
+__device__ __forceinline__ uint32_t fp8x4(float r0, float r1, float r2, float r3) {
+    v2s_t w = {0, 0};
+    w = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(w, r0, r1, 1.0f, false);
+    w = __builtin_amdgcn_cvt_scalef32_pk_fp8_f32(w, r2, r3, 1.0f, true);
+    return __builtin_bit_cast(uint32_t, w);
+}
+
+__global__ void __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(2, 2))) decode_kernel_mxpv(DecodeParams p) {
+    constexpr int W = 4, S = 2;
+    constexpr int kStage = stage_bytes<kFp4>();
+    constexpr int kRows = 2 * 8 * 16 * 8;   // per wave: [page][tile][token][8 B]
+    const int lin = blockIdx.x;
+    const int hk = lin % p.num_kv_heads;
+    const int row = lin / p.num_kv_heads;
+    const int b = row % p.batch;
+    const int part = row / p.batch;
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int G = p.group;
+    int ctx = p.context_lens[b];
+    ctx = ctx < p.max_context ? ctx : p.max_context;
+    const int start = part * p.partition_tokens;
+    if (start >= ctx) {
+        if (ctx <= 0 && part == 0) {
+            for (int r = tid >> 4; r < G; r += 16) {
+                float z[8];
+#pragma unroll
+                for (int i = 0; i < 8; ++i) z[i] = 0.f;
+                write_out<8>(p, int64_t(b) * p.num_q_heads + hk * G + r, tid & 15, z);
+            }
+        }
+        return;
+    }
+    const int end = (start + p.partition_tokens) < ctx ? (start + p.partition_tokens) : ctx;
+    const bool in_place = ctx <= p.partition_tokens;
+
+    __shared__ __attribute__((aligned(16))) uint8_t smem[W * ring_bytes<kFp4, S>()];
+    __shared__ __attribute__((aligned(16))) uint8_t q_lds[q_lds_bytes<kFp4>()];
+    __shared__ __attribute__((aligned(16))) uint8_t ids_lds[W * kIdsSlot];
+    __shared__ __attribute__((aligned(16))) uint8_t rows_lds[W * kRows];
+    __shared__ float red_m[W][16];
+    __shared__ float red_l[W][16];
+
+    // ---- query: as decode_kernel<kFp4> (rotate, FP8 cast, B-operand order)
+    {
+        const int qr = tid >> 4, qL = tid & 15;
+        float qx[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) qx[i] = 0.f;
+        uint32_t lo = 0u, hi = 0u;
+        if (qr < G) {
+            const int64_t elem = (int64_t(b) * p.num_q_heads + hk * G + qr) * kHeadDim + 8 * qL;
+            if (p.q_dtype == 3) {
+                const uint2 w = *reinterpret_cast<const uint2*>(static_cast<const uint8_t*>(p.q) + elem);
+                lo = w.x;
+                hi = w.y;
+            } else {
+                if (p.q_dtype == 0) load_x8<0>(p.q, elem, qx);
+                else if (p.q_dtype == 1) load_x8<1>(p.q, elem, qx);
+                else load_x8<2>(p.q, elem, qx);
+                wht128_x8(qx, qL);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    lo |= e4m3_byte(qx[i]) << (8 * i);
+                    hi |= e4m3_byte(qx[i + 4]) << (8 * i);
+                }
+            }
+        }
+        const int ch = 8 * qL;
+        const int g = (ch & 63) >> 4;
+        const int e0 = (ch & 15) + (ch >= 64 ? 16 : 0);
+        *reinterpret_cast<uint2*>(q_lds + (g * 16 + qr) * 32 + e0) = make_uint2(lo, hi);
+    }
+
+    const int first_page = start >> 4;
+    const int n_pages = (end - start + 15) >> 4;
+    const int n_iter = (n_pages + 1) >> 1;
+    const int n_local = wave < n_iter ? (n_iter - wave + W - 1) / W : 0;
+    const int32_t* pt_row = p.page_table + int64_t(b) * p.max_pages_per_seq;
+    const int g4 = lane >> 4;
+    const int n = lane & 15;
+    uint8_t* ring = smem + wave * ring_bytes<kFp4, S>();
+    const uint32_t ring_addr = uint32_t(reinterpret_cast<uintptr_t>((lds_ptr_t)ring));
+    const int64_t head_tile = int64_t(hk) * 2;
+    const int64_t tiles_per_page = int64_t(p.num_kv_heads) * 2;
+    uint8_t* ids_slot = ids_lds + wave * kIdsSlot;
+    const uint32_t ids_addr = uint32_t(reinterpret_cast<uintptr_t>((lds_ptr_t)ids_slot));
+    int32_t ids = 0;
+    if (n_local > 0) {
+        ids = load_page_ids<W>(pt_row, first_page, n_pages, wave, 0, lane);
+        if (n_local > 32) copy_page_ids<W>(ids_slot, pt_row, first_page, n_pages, wave, 1, lane);
+    }
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
+    ids = clamp_ids(ids, p.num_pages);
+    for (int s2 = 0; s2 < S && s2 < n_local; ++s2) {
+        const int64_t id0 = __builtin_amdgcn_readlane(ids, 2 * s2);
+        const int64_t id1 = __builtin_amdgcn_readlane(ids, 2 * s2 + 1);
+        stage_issue<kFp4>(ring + s2 * kStage, p.codes, p.scales, id0 * tiles_per_page + head_tile,
+                          id1 * tiles_per_page + head_tile, lane);
+    }
+    __syncthreads();
+    QOperand<kFp4> qop;
+    {
+        const uint4* src = reinterpret_cast<const uint4*>(q_lds + lane * 32);
+        const uint4 a = src[0], c = src[1];
+        qop.q = v8i{int(a.x), int(a.y), int(a.z), int(a.w), int(c.x), int(c.y), int(c.z), int(c.w)};
+    }
+
+    // rows area of this wave: row (page, tile, token) at ((page * 8 + tile) * 16 + token) * 8
+    uint8_t* rows = rows_lds + wave * kRows;
+    const uint32_t rows_addr = uint32_t(reinterpret_cast<uintptr_t>((lds_ptr_t)rows));
+    // this lane's writes: token 4 g4 + t of page pg, channels 8n..8n+7 -> tile n/2, byte (n%2)*4
+    const uint32_t wr_addr = rows_addr + ((n >> 1) * 16 + 4 * g4) * 8 + (n & 1) * 4;
+    // this lane's transposed-read row (row index n of its 16-lane group): nibble n of the result is
+    // k-slot q = n (n < 8) or 16 + n - 8 of its 32-slot k-block half; page (n / 4) % 2, token offset
+    // 8 (g4 % 2) + 4 (n / 8) + n % 4
+    const uint32_t rd_addr =
+        rows_addr + (((n >> 2) & 1) * 8 * 16 + (8 * (g4 & 1) + 4 * (n >> 3) + (n & 3))) * 8;
+
+    const float sl2 = p.scale_log2;
+    constexpr float kNoMax = -1e30f;
+    float m_run = kNoMax;
+    bool big_max = false;
+    float l_lane = 0.f;     // this lane's share of its column's softmax sum
+    v4f acc[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[j] = v4f{0.f, 0.f, 0.f, 0.f};
+    uint32_t av[8][4];      // FP4 A operands of the 8 channel tiles (32 tokens x 16 channels per lane group)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) av[j][0] = av[j][1] = av[j][2] = av[j][3] = 0u;
+    float pv[32];           // P of the super-iteration, index 8 u + 4 page + i
+    uint32_t ev[4][8];      // V scale bytes, [group][2 u + page], byte i = token 4 g4 + i
+    const uint32_t k23 = 23u;
+
+    for (int ks = 0; ks < n_local; ks += 4) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            const int k = ks + u;
+            if (k >= n_local) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) pv[8 * u + i] = 0.f;
+#pragma unroll
+                for (int g = 0; g < 4; ++g) ev[g][2 * u] = ev[g][2 * u + 1] = 0u;
+                continue;
+            }
+            const int ahead = (n_local - 1 - k) < (S - 1) ? (n_local - 1 - k) : (S - 1);
+            if (ahead >= 1) wait_vmem<dma_per_stage<kFp4>()>();
+            else wait_vmem<0>();
+            const uint32_t slot = uint32_t(k & (S - 1));
+            MxPvStage c;
+            mxpv_stage_read(c, ring_addr + slot * kStage, lane);
+            if (k + S < n_local) {
+                const int kn = k + S;
+                if ((kn & 31) == 0) {
+                    ids = clamp_ids(read_page_ids(ids_addr, lane), p.num_pages);
+                    if (kn + 32 < n_local)
+                        copy_page_ids<W>(ids_slot, pt_row, first_page, n_pages, wave, (kn >> 5) + 1, lane);
+                }
+                const int s2 = 2 * (kn & 31);
+                const int64_t id0 = __builtin_amdgcn_readlane(ids, s2);
+                const int64_t id1 = __builtin_amdgcn_readlane(ids, s2 + 1);
+                stage_issue<kFp4>(ring + slot * kStage, p.codes, p.scales, id0 * tiles_per_page + head_tile,
+                                  id1 * tiles_per_page + head_tile, lane);
+            }
+            // V codes -> rows area (8-byte rows: 16 channels of one token), then the transposed reads
+#pragma unroll
+            for (int pg = 0; pg < 2; ++pg)
+#pragma unroll
+                for (int t = 0; t < 4; ++t) {
+                    const uint32_t a = wr_addr + pg * 8 * 16 * 8 + t * 8;
+                    const uint32_t w = dword(c.v[pg], t);
+                    asm volatile("ds_write_b32 %0, %1" ::"v"(a), "v"(w) : "memory");
+                }
+            asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+            // lanes of k-block j take this iteration's tokens when j / 2 == u / 2, into dwords u % 2
+            // and 2 + u % 2 of their A operands
+            const bool take = (g4 >> 1) == (u >> 1);
+#pragma unroll
+            for (int tile = 0; tile < 8; ++tile) {
+                const v2i_t r = __builtin_amdgcn_ds_read_tr4_b64_v2i32((lds_v2i_ptr)(uintptr_t)(rd_addr + tile * 128));
+                if (take) {
+                    av[tile][u & 1] = uint32_t(r.x);
+                    av[tile][2 + (u & 1)] = uint32_t(r.y);
+                }
+            }
+
+            // ---- QK^T and the online softmax as decode_kernel<kFp4>
+            const v8i a0 = {int(c.k[0].x), int(c.k[0].y), int(c.k[0].z), int(c.k[0].w), 0, 0, 0, 0};
+            const v8i a1 = {int(c.k[1].x), int(c.k[1].y), int(c.k[1].z), int(c.k[1].w), 0, 0, 0, 0};
+            const v4f zero = {0.f, 0.f, 0.f, 0.f};
+            const v4f s0 = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a0, qop.q, zero, 4, 0, 0, int(c.ks[0]), 0, 127);
+            const v4f s1 = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a1, qop.q, zero, 4, 0, 0, int(c.ks[1]), 0, 127);
+            float x[8];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                x[i] = s0[i];
+                x[4 + i] = s1[i];
+            }
+            const int it = wave + W * k;
+            const int tok0 = start + 32 * it + 4 * g4;
+#pragma unroll
+            for (int g = 0; g < 4; ++g) {
+                ev[g][2 * u] = c.vs[0][g];
+                ev[g][2 * u + 1] = c.vs[1][g];
+            }
+            if (__builtin_amdgcn_ballot_w64(start + 32 * it + 32 > end) != 0) {
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    if (tok0 + i >= end) {
+                        x[i] = -__builtin_inff();
+#pragma unroll
+                        for (int g = 0; g < 4; ++g) ev[g][2 * u] &= ~(0xFFu << (8 * i));
+                    }
+                    if (tok0 + 16 + i >= end) {
+                        x[4 + i] = -__builtin_inff();
+#pragma unroll
+                        for (int g = 0; g < 4; ++g) ev[g][2 * u + 1] &= ~(0xFFu << (8 * i));
+                    }
+                }
+            }
+            float smax = x[0];
+#pragma unroll
+            for (int i = 1; i < 8; ++i) smax = __builtin_fmaxf(smax, x[i]);
+            // eager rescale (no lazy threshold): P <= 1, so P * 2^(E_V - 127) stays in the FP8 range
+            if (__builtin_amdgcn_ballot_w64(smax * sl2 > m_run) != 0) {
+                const float mloc = max_across_groups(smax) * sl2;
+                if (mloc > m_run) {
+                    const float alpha = __builtin_amdgcn_exp2f(m_run - mloc);
+                    l_lane *= alpha;
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) acc[j] *= alpha;
+#pragma unroll
+                    for (int e = 0; e < 8 * u; ++e) pv[e] *= alpha;   // pending P of this super-iteration
+                    m_run = mloc;
+                }
+                big_max = __builtin_amdgcn_ballot_w64(__builtin_fabsf(m_run) >= 0x1p20f && m_run != kNoMax) != 0;
+            }
+            if (!big_max) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) pv[8 * u + i] = __builtin_amdgcn_exp2f(__builtin_fmaf(x[i], sl2, -m_run));
+            } else {
+#pragma clang fp contract(off)
+#pragma unroll
+                for (int i = 0; i < 8; ++i) pv[8 * u + i] = __builtin_amdgcn_exp2f(x[i] * sl2 - m_run);
+            }
+#pragma unroll
+            for (int i = 0; i < 8; ++i) l_lane += pv[8 * u + i];
+        }
+
+        // ---- PV over the super-iteration's 128 tokens, channel group by channel group
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+            float r[32];
+#pragma unroll
+            for (int w = 0; w < 8; ++w) {
+                r[4 * w + 0] = pv[4 * w + 0] * byte_scale0(ev[g][w], k23);
+                r[4 * w + 1] = pv[4 * w + 1] * byte_scale1(ev[g][w], k23);
+                r[4 * w + 2] = pv[4 * w + 2] * byte_scale2(ev[g][w], k23);
+                r[4 * w + 3] = pv[4 * w + 3] * byte_scale3(ev[g][w], k23);
+            }
+#pragma unroll
+            for (int term = 0; term < 4; ++term) {
+                uint32_t bw[8];
+#pragma unroll
+                for (int w = 0; w < 8; ++w) bw[w] = fp8x4(r[4 * w], r[4 * w + 1], r[4 * w + 2], r[4 * w + 3]);
+                if (term < 3) {
+#pragma unroll
+                    for (int w = 0; w < 8; ++w) {
+                        const v2s_t lo = __builtin_bit_cast(v2s_t, bw[w]);
+                        const v2f b0 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(bw[w], 16.0f, false);
+                        const v2f b1 = __builtin_amdgcn_cvt_scalef32_pk_f32_fp8(bw[w], 16.0f, true);
+                        (void)lo;
+                        r[4 * w + 0] = __builtin_fmaf(r[4 * w + 0], 16.0f, -b0[0]);
+                        r[4 * w + 1] = __builtin_fmaf(r[4 * w + 1], 16.0f, -b0[1]);
+                        r[4 * w + 2] = __builtin_fmaf(r[4 * w + 2], 16.0f, -b1[0]);
+                        r[4 * w + 3] = __builtin_fmaf(r[4 * w + 3], 16.0f, -b1[1]);
+                    }
+                }
+                const v8i bop = {int(bw[0]), int(bw[1]), int(bw[2]), int(bw[3]), int(bw[4]), int(bw[5]), int(bw[6]),
+                                 int(bw[7])};
+#pragma unroll
+                for (int tt = 0; tt < 2; ++tt) {
+                    const int tile = 2 * g + tt;
+                    const v8i aop = {int(av[tile][0]), int(av[tile][1]), int(av[tile][2]), int(av[tile][3]), 0, 0, 0, 0};
+                    acc[tile] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(aop, bop, acc[tile], 4, 0, 0, 127, 0,
+                                                                                 127 - 4 * term);
+                }
+            }
+        }
+    }
+
+    // ---- merge the waves through LDS (the rings are free now)
+    float l_run;
+    {
+        float a = l_lane, bb = l_lane;
+        swap16(a, bb);
+        const float s1 = a + bb;
+        float c2 = s1, d2 = s1;
+        swap32(c2, d2);
+        l_run = c2 + d2;
+    }
+    __syncthreads();
+    float* red_acc = reinterpret_cast<float*>(smem);
+    constexpr int kAS = 129;
+    if (g4 == 0) {
+        red_m[wave][n] = m_run;
+        red_l[wave][n] = l_run;
+    }
+    // acc[tile][i] of lane (n, g4) is O^T[channel 16 tile + 4 g4 + i][head n]
+#pragma unroll
+    for (int tile = 0; tile < 8; ++tile)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) red_acc[(wave * 16 + n) * kAS + 16 * tile + 4 * g4 + i] = acc[tile][i];
+    __syncthreads();
+    {
+        const int r = tid >> 4;
+        const int L = tid & 15;
+        if (r < G) {
+            float M = red_m[0][r];
+#pragma unroll
+            for (int w = 1; w < W; ++w) M = __builtin_fmaxf(M, red_m[w][r]);
+            float f[W];
+            float lsum = 0.f;
+#pragma unroll
+            for (int w = 0; w < W; ++w) {
+                f[w] = __builtin_amdgcn_exp2f(red_m[w][r] - M);
+                lsum += f[w] * red_l[w][r];
+            }
+            float o[8];
+#pragma unroll
+            for (int cc = 0; cc < 8; ++cc) {
+                float sacc = 0.f;
+#pragma unroll
+                for (int w = 0; w < W; ++w) sacc += f[w] * red_acc[(w * 16 + r) * kAS + 8 * L + cc];
+                o[cc] = sacc;
+            }
+            const int hq = hk * G + r;
+            if (in_place) {
+                finish_row<8>(p, o, lsum, L);
+                write_out<8>(p, int64_t(b) * p.num_q_heads + hq, L, o);
+            } else {
+                const int64_t prow = (int64_t(b) * p.num_q_heads + hq) * p.num_partitions + part;
+                float4* dst = reinterpret_cast<float4*>(p.part_acc + prow * 128 + 8 * L);
+                dst[0] = make_float4(o[0], o[1], o[2], o[3]);
+                dst[1] = make_float4(o[4], o[5], o[6], o[7]);
+                if (L == 0) *reinterpret_cast<float2*>(p.part_ml + prow * 2) = make_float2(M, lsum);
+            }
+        }
+    }
+}
+
+hipError_t launch_decode_partials_mxpv(const DecodeParams& p, hipStream_t stream) {
+    const dim3 grid{unsigned(int64_t(p.suffix_partitions) * p.num_kv_heads * p.batch)};
+    launch_kernel(decode_kernel_mxpv, grid, dim3(256), stream, p);
+    return hipGetLastError();
+}
+
 // Merge the partitions of every (sequence, query head) with more than one:
 // online over the partitions (loads independent of the running state, so
 // they overlap), then finish the row.  One 16-lane row per query head.

@@ -127,6 +127,7 @@ hipError_t launch_write_kv_ref(const RefWriteParams& p, int dtype, hipStream_t s
 hipError_t launch_prepare_query(const void* q, int dtype, int64_t rows, uint8_t* q8, hipStream_t stream);
 hipError_t launch_decode_partials(const DecodeParams& p, hipStream_t stream);
 hipError_t launch_decode_merge(const DecodeParams& p, hipStream_t stream);
+hipError_t launch_decode_partials_mxpv(const DecodeParams& p, hipStream_t stream);
 // measurement probes
 hipError_t launch_gather_probe(const DecodeParams& p, uint32_t* sink, hipStream_t stream);
 hipError_t launch_stream_read_probe(const void* buf, int64_t n16, uint32_t* sink, int blocks, hipStream_t stream);

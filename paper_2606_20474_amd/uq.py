@@ -40,7 +40,7 @@ EXPORTS = (
     "uq_ref_decode_step_partials", "uq_decode_cascade_workspace_bytes", "uq_decode_cascade",
     "uq_decode_cascade_partials", "uq_decode_cascade_merge", "uq_ref_decode_cascade",
     "uq_ref_decode_cascade_partials", "uq_ref_decode_cascade_merge", "uq_quantize_error", "uq_time_next_launch",
-    "uq_decode_attention_noalloc", "uq_probe_stream_read", "uq_probe_page_gather", "uq_probe_mfma",
+    "uq_decode_attention_noalloc", "uq_decode_attention_scaled_pv", "uq_probe_stream_read", "uq_probe_page_gather", "uq_probe_mfma",
 )
 
 UQ_REF_FP8_E4M3, UQ_REF_BF16, UQ_REF_TQ4 = 1, 2, 3
@@ -113,6 +113,9 @@ def _load():
     L.uq_decode_partials.restype = i32
     L.uq_decode_merge.argtypes = [D, i32, i32, vp, i32, i32, vp, sz, vp, i32, vp]
     L.uq_decode_merge.restype = i32
+    L.uq_decode_attention_scaled_pv.argtypes = [D, vp, i32, i32, i32, vp, vp, vp, i32, vp, i32, f32, i32, vp, sz, vp,
+                                                i32, vp]
+    L.uq_decode_attention_scaled_pv.restype = i32
     L.uq_decode_attention_noalloc.argtypes = [D, vp, i32, i32, i32, vp, vp, vp, i32, vp, i32, f32, i32, vp, i32, vp]
     L.uq_decode_attention_noalloc.restype = i32
     L.uq_probe_stream_read.argtypes = [vp, sz, vp, vp]
@@ -398,6 +401,31 @@ def decode_attention(desc: CacheDesc, q, codes, scales, page_table, context_lens
                                  partition_tokens, _ptr(workspace), workspace.numel(), _ptr(out), _DT[out.dtype],
                                  _stream(stream))
     _check(st, "uq_decode_attention")
+    return out
+
+
+def decode_attention_scaled_pv(desc: CacheDesc, q, codes, scales, page_table, context_lens, max_context,
+                               softmax_scale=None, partition_tokens=0, workspace=None, out=None,
+                               out_dtype=torch.float32, q_dtype=None, stream=None):
+    """decode_attention with PV on the block-scaled matrix instruction (the
+    prototype of include/uq.h; head size 128)."""
+    B, Hq = _q_out(q, out, desc.head_dim)
+    _pools(desc, codes, scales)
+    _table(page_table, context_lens, B)
+    if softmax_scale is None:
+        softmax_scale = desc.head_dim ** -0.5
+    if workspace is None:
+        workspace = alloc_workspace(desc, B, Hq, max_context, partition_tokens, q.device)
+    _need(workspace, "workspace", _U8)
+    if out is None:
+        out = torch.empty((B, Hq, desc.head_dim), dtype=out_dtype, device=q.device)
+    d = desc.c_struct()
+    qdt = _DT[q.dtype] if q_dtype is None else q_dtype
+    st = lib.uq_decode_attention_scaled_pv(ctypes.byref(d), _ptr(q), qdt, B, Hq, _ptr(codes), _ptr(scales),
+                                           _ptr(page_table), page_table.shape[1], _ptr(context_lens), max_context,
+                                           softmax_scale, partition_tokens, _ptr(workspace), workspace.numel(),
+                                           _ptr(out), _DT[out.dtype], _stream(stream))
+    _check(st, "uq_decode_attention_scaled_pv")
     return out
 
 
