@@ -68,10 +68,17 @@ def parse():
     ap.add_argument("--no-flush", action="store_true",
                     help="time the FP4 decode kernel back to back only (no 1 GiB write between launches)")
     ap.add_argument("--no-probes", action="store_true", help="skip the achievable-bandwidth probes")
+    ap.add_argument("--no-scaled-pv", action="store_true",
+                    help="skip the A/B of PV on the block-scaled instruction (head size 128 only)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="run one device-to-device copy of this many MiB before the timed steps; its "
                          "FETCH_SIZE/WRITE_SIZE counters calibrate the HBM-traffic counters")
     return ap.parse_args()
+
+
+def progress(msg):
+    """One line on stderr per finished stage (stdout carries only the JSON line)."""
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
 def make_workload(name):
@@ -346,6 +353,31 @@ def achievable(uq, wl, desc, codes, scales, pt, ctx, part, alg_bytes, args, dev,
     return res
 
 
+def scaled_pv_ab(uq, wl, desc, codes, scales, q, pt, ctx, part, args, dev, stream, flush):
+    """A/B of PV on the block-scaled FP4 x FP8 instruction
+    (uq_decode_attention_scaled_pv) against the default BF16 PV
+    (uq_decode_attention), both reading every sequence's whole context
+    (no cascade, no fused write), kernel events on the partials launch,
+    flushed like the headline kernel."""
+    import torch
+    ws = uq.alloc_workspace(desc, wl.batch, wl.num_q_heads, wl.max_context, part, dev)
+    out = torch.empty((wl.batch, wl.num_q_heads, 128), dtype=torch.float32, device=dev)
+    nbytes = wl.total_tokens() * wl.num_kv_heads * KV_BYTES_PER_TOKEN_HEAD
+    n = max(20, args.steps // 4)
+    res = {"kv_bytes_per_launch": nbytes}
+    for name, fn in (("bf16_pv", uq.decode_attention), ("scaled_pv", uq.decode_attention_scaled_pv)):
+        def step(ev_a=None, ev_b=None, fn=fn):
+            if ev_a is not None:
+                uq.time_next_launch(ev_a, ev_b)
+            fn(desc, q, codes, scales, pt, ctx, wl.max_context, 1 / math.sqrt(128), part, workspace=ws, out=out)
+        st, k = timed(step, n, 3, stream, flush=None if args.no_flush else flush)
+        res[name] = {"kernel_ms": k, "kernel_gbs": nbytes / (k * 1e-3) / 1e9, "ms_per_step": st}
+    res["scaled_over_bf16_kernel_ms"] = res["scaled_pv"]["kernel_ms"] / res["bf16_pv"]["kernel_ms"]
+    del ws, out
+    torch.cuda.empty_cache()
+    return res
+
+
 def cpu_baseline(wl, nseq, dev):
     """The oracle on `nseq` sequences of the workload (all their query heads,
     full contexts), timed on the host; KV tokens/s."""
@@ -390,6 +422,7 @@ def main():
     desc = uq.CacheDesc(num_kv_heads=wl.num_kv_heads, num_pages=wl.num_pages, rotate_v=wl.rotate_v, head_dim=D)
     codes, scales = desc.alloc_pools(dev)
     fill_cache(uq, wl, desc, codes, scales, dev)
+    progress(f"{wl.name}: FP4 cache written")
     if part == 0:
         part = uq.default_partition(desc, wl.batch, wl.num_q_heads, wl.max_context)
 
@@ -447,6 +480,7 @@ def main():
         f_step, dec_ms = ms_step, dec_ms_b2b
     else:
         f_step, dec_ms = timed(step, args.steps, args.warmup, stream, flush=flush)
+    progress(f"FP4 step timed: {ms_step * 1e3:.1f} us back to back, {f_step * 1e3:.1f} us flushed")
 
     tokens = wl.total_tokens()
     kv_bytes = wl.kv_bytes_fp4()            # logical: every sequence's whole context
@@ -455,6 +489,8 @@ def main():
     achieved = alg_bytes / (dec_ms * 1e-3) / 1e9
     ach = None if args.no_probes else achievable(uq, wl, desc, codes, scales, pt, ctx, part, alg_bytes, args, dev,
                                                  stream, flush)
+    if ach is not None:
+        progress("bandwidth probes timed")
     result = {
         "metric": "decode-attention KV tokens/s and achieved HBM GB/s (% of peak) at 32k context",
         "value": tokens / (ms_step * 1e-3),
@@ -498,12 +534,18 @@ def main():
                 sys.exit(f"unknown comparator {fmt!r}")
             comp[f"{fmt}_kv"] = comparator(uq, fmt, wl, part, q, pt, ctx, k_new, v_new, args, dev, stream, flush,
                                            prefix)
+            progress(f"{fmt} comparator timed")
             comp[f"fp4_over_{fmt}_tokens_per_s"] = result["value"] / comp[f"{fmt}_kv"]["tokens_per_s"]
             comp[f"fp4_over_{fmt}_tokens_per_s_flushed"] = (result["flushed"]["tokens_per_s"]
                                                            / comp[f"{fmt}_kv"]["flushed"]["tokens_per_s"])
         result["comparators"] = comp
+    if D == 128 and not args.no_scaled_pv:
+        result["scaled_pv_ab"] = scaled_pv_ab(uq, wl, desc, codes, scales, q, pt, ctx, part, args, dev, stream,
+                                              flush)
+        progress("scaled-PV A/B timed")
     if not args.no_write_path:
         result["write_path"] = write_path(uq, args, dev, stream, flush)
+        progress("write path timed")
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, args.cpu_sample_seqs, dev)
     print(json.dumps(result), flush=True)
