@@ -135,6 +135,8 @@ uq_status make_decode_params(const uq_cache_desc* desc, const void* q, uq_dtype 
     p.prefix_chunks = 0;
     p.prefix_blocks = 0;
     p.suffix_partitions = int32_t(np_ctx);
+    p.allow_wave_parts = 1;
+    p.wave_parts = 0;
     return UQ_OK;
 }
 
@@ -468,6 +470,7 @@ uq_status uq_decode_attention_scaled_pv(const uq_cache_desc* desc, const void* q
                                workspace_bytes, out, out_dtype, p);
     if (s != UQ_OK) return s;
     if (desc->head_dim != kHeadDim) return UQ_ERR_UNSUPPORTED;
+    p.allow_wave_parts = 0;   // the prototype's grid is one block per partition
     s = from_hip(uq::launch_decode_partials_mxpv(p, static_cast<hipStream_t>(stream)));
     if (s != UQ_OK) return s;
     return from_hip(uq::launch_decode_merge(p, static_cast<hipStream_t>(stream)));

@@ -752,10 +752,11 @@ __device__ __forceinline__ void zero_token(StageRegs<kTq4>& c, int pg, int t) {
     else m.w = 0u;
 }
 
-template <int F, int S>
+template <int F, int S, bool WP>
 __global__ void __launch_bounds__(64 * Fmt<F>::kWaves)
 __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decode_kernel(DecodeParams p) {
     static_assert(S == 2 || S == 4, "ring slots");
+    static_assert(!WP || (head_dim_of<F>() == 128 && F != kFp4d64x2), "one wave per partition: head size 128");
     constexpr int W = Fmt<F>::kWaves;
     constexpr int kThreads = 64 * W;
     constexpr int kStage = stage_bytes<F>();
@@ -783,8 +784,16 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
     // fill the CUs that the ragged context blocks leave idle at the end
     // (first, or spread through the grid, measured 8-16 % slower on the
     // MiniMax-like workload).
+    //
+    // WP (one wave per partition): block `rest / batch` of a (kv head,
+    // sequence) takes partitions W * (rest / batch) + wave, one per wave.
+    // Each wave streams its whole partition through its own ring and writes
+    // its own partial, so a block's query prologue serves W partitions and
+    // no wave waits for another at the end (with 4096-token partitions the
+    // block-per-partition grid spent about 8 % of the kernel on its block
+    // prologues and LDS merges).
     const int lin = blockIdx.x;
-    const bool cascade = p.prefix_pages != nullptr;
+    const bool cascade = !WP && p.prefix_pages != nullptr;
     const int units = kPair ? p.num_kv_heads / 2 : p.num_kv_heads;   // kv heads, or pairs of them
     const int hk = lin % units;
     const int row = lin / units;
@@ -798,14 +807,16 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
     const int nb = pre ? p.prefix_chunks : p.batch;
     const int b = pre ? 0 : rest % nb;                                 // sequence (context blocks)
     const int chunk = pre ? rest % nb : 0;                             // column chunk (prefix blocks)
-    const int part = rest / nb;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave-uniform: scalar control flow
+    const int first_part = WP ? (rest / nb) * W : rest / nb;           // the block's (first) partition
+    const int part = WP ? first_part + wave : first_part;
     const int G = p.group;
     const int BG = p.batch * G;
 
     int start, end, ctx = 0;
+    bool idle = false;   // WP: this wave's partition starts past the context
     if (pre) {
         start = part * p.prefix_partition;
         end = (start + p.prefix_partition) < p.prefix_tokens ? (start + p.prefix_partition) : p.prefix_tokens;
@@ -822,9 +833,9 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
             if (start + p.partition_tokens <= pl) return;              // wholly inside the prefix
             start = start > pl ? start : pl;
         }
-        if (start >= ctx) {
+        if ((WP ? first_part * p.partition_tokens : start) >= ctx) {
             // nothing of this sequence here; an empty context still gets its zero output
-            if (ctx <= 0 && part == 0) {
+            if (ctx <= 0 && first_part == 0) {
                 // the block's query heads: G of kv head hk, or 2 G of the pair
                 for (int r = tid >> 4; r < (kPair ? 2 : 1) * G; r += kThreads / 16) {
                     float z[N];
@@ -836,9 +847,16 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
             return;
         }
         end = (part * p.partition_tokens + p.partition_tokens) < ctx ? (part * p.partition_tokens + p.partition_tokens) : ctx;
+        if (WP && start >= ctx) {
+            // a later wave of the block past a short context: no pages and
+            // no partial, but it still takes part in the query prologue
+            idle = true;
+            start = end = ctx;
+        }
     }
-    // a single partition holding the whole context is finished in place
-    const bool in_place = !cascade && ctx <= p.partition_tokens;
+    // a single partition holding the whole context is finished in place (the
+    // one-wave-per-partition grid leaves every row to the merge kernel)
+    const bool in_place = !WP && !cascade && ctx <= p.partition_tokens;
     // query row r (0..15) of this block: valid, its sequence and query head
     auto row_of = [&](int r, int& rb, int& rhq) -> bool {
         if constexpr (kPair) {
@@ -866,8 +884,9 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
     const int pos_new = ctx - 1;
     const int it_new = (pos_new - start) >> 5;                       // iteration holding the token
     // (the step is a head-size-128 call)
-    const bool append = D == 128 && !pre && p.k_new != nullptr && pos_new >= start && wave == it_new % W;
-    const int k_new_local = it_new / W;                              // that wave's local iteration
+    const bool append = D == 128 && !pre && p.k_new != nullptr && pos_new >= start && pos_new < end &&
+                        (WP || wave == it_new % W);
+    const int k_new_local = WP ? it_new : it_new / W;                // that wave's local iteration
 
     __shared__ __attribute__((aligned(16))) uint8_t smem[W * ring_bytes<F, S>()];
     __shared__ __attribute__((aligned(16))) uint8_t q_lds[q_lds_bytes<F>()];
@@ -950,7 +969,11 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
     const int first_page = start >> 4;
     const int n_pages = (end - start + 15) >> 4;
     const int n_iter = (n_pages + 1) >> 1;
-    const int n_local = wave < n_iter ? (n_iter - wave + W - 1) / W : 0;
+    const int n_local = WP ? n_iter : wave < n_iter ? (n_iter - wave + W - 1) / W : 0;
+    // page-walk order: iteration k of the wave covers partition pages
+    // 2 * (woff + ws * k) and + 1
+    constexpr int ws = WP ? 1 : W;
+    const int woff = WP ? 0 : wave;
     const int32_t* pt_row = pre ? p.prefix_pages : p.page_table + int64_t(b) * p.max_pages_per_seq;
     // prefix blocks: this lane's column attends to the first `lim` prefix tokens
     int lim = end;
@@ -978,8 +1001,8 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
     const uint32_t ids_addr = uint32_t(reinterpret_cast<uintptr_t>((lds_ptr_t)ids_slot));
     int32_t ids = 0;
     if (n_local > 0) {
-        ids = load_page_ids<W>(pt_row, first_page, n_pages, wave, 0, lane);
-        if (n_local > 32) copy_page_ids<W>(ids_slot, pt_row, first_page, n_pages, wave, 1, lane);
+        ids = load_page_ids<ws>(pt_row, first_page, n_pages, woff, 0, lane);
+        if (n_local > 32) copy_page_ids<ws>(ids_slot, pt_row, first_page, n_pages, woff, 1, lane);
     }
     // The query, the new token and the page ids are in registers before the
     // first page copies are issued (one wait for all of them, so that the
@@ -1156,7 +1179,7 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
                 // the next chunk's copy is older than every stage in flight,
                 // so the wait at the top of this iteration covered it
                 ids = clamp_ids(read_page_ids(ids_addr, lane), p.num_pages);
-                if (kn + 32 < n_local) copy_page_ids<W>(ids_slot, pt_row, first_page, n_pages, wave, (kn >> 5) + 1, lane);
+                if (kn + 32 < n_local) copy_page_ids<ws>(ids_slot, pt_row, first_page, n_pages, woff, (kn >> 5) + 1, lane);
             }
             const int s = 2 * (kn & 31);
             const int64_t id0 = __builtin_amdgcn_readlane(ids, s);
@@ -1179,7 +1202,7 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
             vs0 = c.vs[0];
             vs1 = c.vs[1];
         }
-        const int it = wave + W * k;
+        const int it = woff + ws * k;
         const int tok0 = start + 32 * it + 4 * g4;   // token of x[0]; x[4] is tok0 + 16
         if (__builtin_amdgcn_ballot_w64(start + 32 * it + 32 > lim) != 0) {
             // scores past the column's last token (the partition end, or a
@@ -1298,8 +1321,25 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
         }
     }
 
-    // ---------------- merge the waves through LDS (the rings are free now)
     const float l_run = acc_l[0];   // the column sum, in every lane of the column
+    if constexpr (WP) {
+        // the wave's partial straight from its registers: lane (n, g4) holds
+        // channels 32 g4 .. 32 g4 + 31 of column n (acc[j][i] is channel
+        // 32 g4 + 8 i + j)
+        int rb, hq;
+        if (idle || !row_of(n, rb, hq)) return;
+        const int64_t prow = (int64_t(rb) * p.num_q_heads + hq) * p.num_partitions + part;
+        float4* dst = reinterpret_cast<float4*>(p.part_acc + prow * D + 32 * g4);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            dst[2 * i] = make_float4(acc[0][i], acc[1][i], acc[2][i], acc[3][i]);
+            dst[2 * i + 1] = make_float4(acc[4][i], acc[5][i], acc[6][i], acc[7][i]);
+        }
+        if (g4 == 0) *reinterpret_cast<float2*>(p.part_ml + prow * 2) = make_float2(m_run, l_run);
+        return;
+    }
+
+    // ---------------- merge the waves through LDS (the rings are free now)
     __syncthreads();
     float* red_acc = reinterpret_cast<float*>(smem);
     constexpr int kAS = DA + 1;   // LDS row stride (floats) of the merge buffer
@@ -1808,7 +1848,7 @@ __global__ void __launch_bounds__(256) merge_kernel(DecodeParams p) {
         first = pl / p.partition_tokens;
         nq = (pl + p.prefix_partition - 1) / p.prefix_partition;
         if (np - first + nq <= 0) return;   // empty context: written by the decode kernel
-    } else if (np <= 1) {
+    } else if (np == 0 || (np == 1 && !p.wave_parts)) {
         return;                             // finished by the decode kernel
     }
     const int hq = hk * p.group + r;
@@ -1850,7 +1890,9 @@ __global__ void __launch_bounds__(256) merge_kernel(DecodeParams p) {
 // global_load_lds_dwordx4 copies, and every staged byte read back into
 // registers as the decode kernel reads it, but no arithmetic on it beyond an
 // XOR into a checksum (one word per wave in `sink`).  Its time is the time
-// the decode kernel's memory traffic alone takes on this GPU.
+// the decode kernel's memory traffic alone takes on this GPU.  WP: the
+// one-wave-per-partition grid of the decode kernel.
+template <bool WP>
 __global__ void __launch_bounds__(256) gather_probe_kernel(DecodeParams p, uint32_t* __restrict__ sink) {
     constexpr int W = 4, S = 2;
     constexpr int kStage = stage_bytes<kFp4>();
@@ -1858,10 +1900,12 @@ __global__ void __launch_bounds__(256) gather_probe_kernel(DecodeParams p, uint3
     const int hk = lin % p.num_kv_heads;
     const int row = lin / p.num_kv_heads;
     const int b = row % p.batch;
-    const int part = row / p.batch;
     const int tid = threadIdx.x;
     const int lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int part = WP ? (row / p.batch) * W + wave : row / p.batch;
+    constexpr int ws = WP ? 1 : W;
+    const int woff = WP ? 0 : wave;
     int ctx = p.context_lens[b];
     ctx = ctx < p.max_context ? ctx : p.max_context;
     const int start = part * p.partition_tokens;
@@ -1871,7 +1915,7 @@ __global__ void __launch_bounds__(256) gather_probe_kernel(DecodeParams p, uint3
     uint32_t acc = 0u;
     const int n_pages = start < end ? (end - start + 15) >> 4 : 0;
     const int n_iter = (n_pages + 1) >> 1;
-    const int n_local = wave < n_iter ? (n_iter - wave + W - 1) / W : 0;
+    const int n_local = WP ? n_iter : wave < n_iter ? (n_iter - wave + W - 1) / W : 0;
     if (n_local > 0) {
         const int first_page = start >> 4;
         const int32_t* pt_row = p.page_table + int64_t(b) * p.max_pages_per_seq;
@@ -1881,8 +1925,8 @@ __global__ void __launch_bounds__(256) gather_probe_kernel(DecodeParams p, uint3
         const uint32_t ids_addr = uint32_t(reinterpret_cast<uintptr_t>((lds_ptr_t)ids_slot));
         const int64_t head_tile = int64_t(hk) * 2;
         const int64_t tiles_per_page = int64_t(p.num_kv_heads) * 2;
-        int32_t ids = load_page_ids<W>(pt_row, first_page, n_pages, wave, 0, lane);
-        if (n_local > 32) copy_page_ids<W>(ids_slot, pt_row, first_page, n_pages, wave, 1, lane);
+        int32_t ids = load_page_ids<ws>(pt_row, first_page, n_pages, woff, 0, lane);
+        if (n_local > 32) copy_page_ids<ws>(ids_slot, pt_row, first_page, n_pages, woff, 1, lane);
         __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
         ids = clamp_ids(ids, p.num_pages);
         for (int s = 0; s < S && s < n_local; ++s) {
@@ -1902,7 +1946,7 @@ __global__ void __launch_bounds__(256) gather_probe_kernel(DecodeParams p, uint3
                 if ((kn & 31) == 0) {
                     ids = clamp_ids(read_page_ids(ids_addr, lane), p.num_pages);
                     if (kn + 32 < n_local)
-                        copy_page_ids<W>(ids_slot, pt_row, first_page, n_pages, wave, (kn >> 5) + 1, lane);
+                        copy_page_ids<ws>(ids_slot, pt_row, first_page, n_pages, woff, (kn >> 5) + 1, lane);
                 }
                 const int s2 = 2 * (kn & 31);
                 const int64_t id0 = __builtin_amdgcn_readlane(ids, s2);
@@ -1921,10 +1965,40 @@ __global__ void __launch_bounds__(256) gather_probe_kernel(DecodeParams p, uint3
     if (lane == 0) sink[int64_t(lin) * W + wave] = acc;
 }
 
+static bool choose_wave_parts(const DecodeParams& p);
+
 hipError_t launch_gather_probe(const DecodeParams& p, uint32_t* sink, hipStream_t stream) {
-    const dim3 grid{unsigned(int64_t(p.num_partitions) * p.num_kv_heads * p.batch)};
-    launch_kernel(gather_probe_kernel, grid, dim3(256), stream, p, sink);
+    // the grid the FP4 decode kernel takes for the same parameters
+    if (choose_wave_parts(p)) {
+        const dim3 grid{unsigned(int64_t((p.num_partitions + 3) / 4) * p.num_kv_heads * p.batch)};
+        launch_kernel(gather_probe_kernel<true>, grid, dim3(256), stream, p, sink);
+    } else {
+        const dim3 grid{unsigned(int64_t(p.num_partitions) * p.num_kv_heads * p.batch)};
+        launch_kernel(gather_probe_kernel<false>, grid, dim3(256), stream, p, sink);
+    }
     return hipGetLastError();
+}
+
+// The grid of a partition launch: one wave per partition when there are
+// enough partitions for W per block and enough such blocks to give every CU
+// several (8 per CU: two full rounds at 4 blocks per CU), head size 128, no
+// cascade; else one block per partition.  The merge launch makes the same
+// choice from the same parameters.
+static int waves_of(int32_t kv_fmt) {
+    switch (kv_fmt) {
+        case kFp8: return Fmt<kFp8>::kWaves;
+        case kBf16: return Fmt<kBf16>::kWaves;
+        case kTq4: return Fmt<kTq4>::kWaves;
+        default: return Fmt<kFp4>::kWaves;
+    }
+}
+static bool choose_wave_parts(const DecodeParams& p) {
+    if (!p.allow_wave_parts || p.prefix_pages != nullptr || p.head_dim != kHeadDim) return false;
+    if (p.kv_fmt != kFp4 && p.kv_fmt != kFp8 && p.kv_fmt != kBf16 && p.kv_fmt != kTq4) return false;
+    const int W = waves_of(p.kv_fmt);
+    if (p.num_partitions < W) return false;
+    const int64_t blocks = int64_t(p.batch) * p.num_kv_heads * ((p.num_partitions + W - 1) / W);
+    return blocks >= 8 * kNumCus;
 }
 
 // Two ring slots per wave: a 4-slot ring (twice the copies in flight, half
@@ -1934,8 +2008,19 @@ static hipError_t launch_partials(const DecodeParams& p, hipStream_t stream) {
     constexpr int kSlots = 2;
     static_assert(occupancy<F, kSlots>() == Fmt<F>::kOccupancy, "the LDS footprint lowers the occupancy");
     const int64_t units = F == kFp4d64x2 ? p.num_kv_heads / 2 : p.num_kv_heads;
+    constexpr bool kWaveOk = head_dim_of<F>() == 128 && F != kFp4d64x2;
+    if constexpr (kWaveOk) {
+        if (choose_wave_parts(p)) {
+            DecodeParams pw = p;
+            pw.wave_parts = 1;
+            constexpr int W = Fmt<F>::kWaves;
+            const dim3 grid{unsigned(int64_t((p.num_partitions + W - 1) / W) * units * p.batch)};
+            launch_kernel(decode_kernel<F, kSlots, true>, grid, dim3(64 * W), stream, pw);
+            return hipGetLastError();
+        }
+    }
     const dim3 grid{unsigned(int64_t(p.prefix_blocks) + int64_t(p.suffix_partitions) * units * p.batch)};
-    launch_kernel(decode_kernel<F, kSlots>, grid, dim3(64 * Fmt<F>::kWaves), stream, p);
+    launch_kernel(decode_kernel<F, kSlots, false>, grid, dim3(64 * Fmt<F>::kWaves), stream, p);
     return hipGetLastError();
 }
 
@@ -1951,10 +2036,12 @@ hipError_t launch_decode_partials(const DecodeParams& p, hipStream_t stream) {
 
 hipError_t launch_decode_merge(const DecodeParams& p, hipStream_t stream) {
     if (p.num_partitions <= 1 && p.prefix_pages == nullptr) return hipSuccess;   // every sequence was finished in place
+    DecodeParams pm = p;
+    pm.wave_parts = choose_wave_parts(p) ? 1 : 0;
     const dim3 grid{unsigned(p.num_kv_heads), unsigned(p.batch)};
-    if (p.head_dim == 64) hipLaunchKernelGGL(merge_kernel<64>, grid, dim3(256), 0, stream, p);
-    else if (p.head_dim == 256) hipLaunchKernelGGL(merge_kernel<256>, grid, dim3(256), 0, stream, p);
-    else hipLaunchKernelGGL(merge_kernel<128>, grid, dim3(256), 0, stream, p);
+    if (p.head_dim == 64) hipLaunchKernelGGL(merge_kernel<64>, grid, dim3(256), 0, stream, pm);
+    else if (p.head_dim == 256) hipLaunchKernelGGL(merge_kernel<256>, grid, dim3(256), 0, stream, pm);
+    else hipLaunchKernelGGL(merge_kernel<128>, grid, dim3(256), 0, stream, pm);
     return hipGetLastError();
 }
 

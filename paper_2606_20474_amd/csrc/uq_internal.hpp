@@ -106,6 +106,13 @@ struct DecodeParams {
     int32_t prefix_chunks;         // ceil(B * G / 16) column chunks per kv head
     int32_t prefix_blocks;         // Hkv * prefix_chunks * prefix partitions, after the context blocks in the grid
     int32_t suffix_partitions;
+    // grid shape of the partition launch: 0 one block per partition (its
+    // waves share the partition's pages and merge through LDS), 1 one wave
+    // per partition (a block takes kWaves consecutive partitions of one
+    // sequence and kv head; every wave writes its own partial, and the merge
+    // finishes every row).  Chosen by the launchers when allow_wave_parts.
+    int32_t allow_wave_parts;
+    int32_t wave_parts;
 };
 
 constexpr int kMaxErrorConstants = 256;   // constants per uq_quantize_error call
