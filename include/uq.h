@@ -175,7 +175,13 @@ int32_t uq_default_partition(const uq_cache_desc *desc, int32_t batch, int32_t n
  * uq_decode_attention -- decode attention over the FP4 cache (Algorithm 1,
  * "Decode"), one new query token per sequence: one launch of the partition
  * kernel, plus one launch of the merge kernel when a context can span more
- * than one partition (max_context > partition).
+ * than one partition (max_context > partition).  The partition kernel runs
+ * one block of 4 waves per (partition, kv head, sequence), the waves sharing
+ * the partition's pages, or -- when the launch has at least 2048 blocks of
+ * 4 partitions each (head size 128, no shared prefix) -- one wave per
+ * partition, a block taking 4 consecutive partitions of one sequence and kv
+ * head.  The partitions and the result do not depend on the grid beyond
+ * rounding.
  *   q             : [batch][num_q_heads][128].  F32/BF16/F16: rotated and
  *                   cast to FP8 inside the call.  FP8_E4M3: already
  *                   prepared by uq_prepare_query.
@@ -210,11 +216,12 @@ uq_status uq_decode_attention(const uq_cache_desc *desc, const void *q, uq_dtype
 
 /*
  * The two launches of uq_decode_attention, for callers that time or overlap
- * them.  uq_decode_partials runs the partition kernel: it writes the final
- * output of every sequence whose context fits one partition and a partial
+ * them.  uq_decode_partials runs the partition kernel: it writes a partial
  * (running max, running sum, 128 accumulators per query head) of every
- * other partition into the workspace.  uq_decode_merge merges those
- * partials into `out` (a no-op when max_context <= partition).  Called back
+ * partition into the workspace, except that on the block-per-partition grid
+ * a sequence whose context fits one partition gets its final output
+ * instead.  uq_decode_merge merges the partials into `out` (a no-op when
+ * max_context <= partition).  Called back
  * to back on one stream with the same arguments they are exactly
  * uq_decode_attention; the arguments, validation and errors are the same.
  */
