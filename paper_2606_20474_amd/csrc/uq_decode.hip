@@ -816,7 +816,6 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
     const int BG = p.batch * G;
 
     int start, end, ctx = 0;
-    bool idle = false;   // WP: this wave's partition starts past the context
     if (pre) {
         start = part * p.prefix_partition;
         end = (start + p.prefix_partition) < p.prefix_tokens ? (start + p.prefix_partition) : p.prefix_tokens;
@@ -848,15 +847,14 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
         }
         end = (part * p.partition_tokens + p.partition_tokens) < ctx ? (part * p.partition_tokens + p.partition_tokens) : ctx;
         if (WP && start >= ctx) {
-            // a later wave of the block past a short context: no pages and
-            // no partial, but it still takes part in the query prologue
-            idle = true;
+            // a later wave of the block past a short context: no pages, but
+            // it still takes part in the query prologue and the block merge
             start = end = ctx;
         }
     }
-    // a single partition holding the whole context is finished in place (the
-    // one-wave-per-partition grid leaves every row to the merge kernel)
-    const bool in_place = !WP && !cascade && ctx <= p.partition_tokens;
+    // a context held by this block alone is finished in place: one partition,
+    // or the W partitions of the first block of the wave grid
+    const bool in_place = !cascade && ctx <= (WP ? W : 1) * p.partition_tokens;
     // query row r (0..15) of this block: valid, its sequence and query head
     auto row_of = [&](int r, int& rb, int& rhq) -> bool {
         if constexpr (kPair) {
@@ -1322,24 +1320,9 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
     }
 
     const float l_run = acc_l[0];   // the column sum, in every lane of the column
-    if constexpr (WP) {
-        // the wave's partial straight from its registers: lane (n, g4) holds
-        // channels 32 g4 .. 32 g4 + 31 of column n (acc[j][i] is channel
-        // 32 g4 + 8 i + j)
-        int rb, hq;
-        if (idle || !row_of(n, rb, hq)) return;
-        const int64_t prow = (int64_t(rb) * p.num_q_heads + hq) * p.num_partitions + part;
-        float4* dst = reinterpret_cast<float4*>(p.part_acc + prow * D + 32 * g4);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            dst[2 * i] = make_float4(acc[0][i], acc[1][i], acc[2][i], acc[3][i]);
-            dst[2 * i + 1] = make_float4(acc[4][i], acc[5][i], acc[6][i], acc[7][i]);
-        }
-        if (g4 == 0) *reinterpret_cast<float2*>(p.part_ml + prow * 2) = make_float2(m_run, l_run);
-        return;
-    }
-
-    // ---------------- merge the waves through LDS (the rings are free now)
+    // ---------------- merge the waves through LDS (the rings are free now).
+    // WP: the block's W partitions (an idle wave holds m = kNoMax, l = 0 and
+    // zero accumulators, so its weight is 0) into one partial per block.
     __syncthreads();
     float* red_acc = reinterpret_cast<float*>(smem);
     constexpr int kAS = DA + 1;   // LDS row stride (floats) of the merge buffer
@@ -1393,7 +1376,8 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
             write_out<N>(p, int64_t(rb) * p.num_q_heads + hq, L, o);
         } else {
             // several partitions: publish this one for the merge kernel
-            const int slot = pre ? p.suffix_partitions + part : part;
+            // the wave grid: one slot per block of W partitions
+            const int slot = pre ? p.suffix_partitions + part : WP ? first_part / W : part;
             const int64_t prow = (int64_t(rb) * p.num_q_heads + hq) * p.num_partitions + slot;
             float4* dst = reinterpret_cast<float4*>(p.part_acc + prow * D + N * L);
 #pragma unroll
@@ -1838,7 +1822,7 @@ __global__ void __launch_bounds__(256) merge_kernel(DecodeParams p) {
     if (r >= p.group) return;   // whole 16-lane rows leave together
     int ctx = p.context_lens[b];
     ctx = ctx < p.max_context ? ctx : p.max_context;
-    const int np = ctx > 0 ? (ctx + p.partition_tokens - 1) / p.partition_tokens : 0;
+    int np = ctx > 0 ? (ctx + p.partition_tokens - 1) / p.partition_tokens : 0;
     int first = 0, nq = 0;
     if (p.prefix_pages != nullptr) {
         int pl = p.prefix_lens[b];
@@ -1848,8 +1832,10 @@ __global__ void __launch_bounds__(256) merge_kernel(DecodeParams p) {
         first = pl / p.partition_tokens;
         nq = (pl + p.prefix_partition - 1) / p.prefix_partition;
         if (np - first + nq <= 0) return;   // empty context: written by the decode kernel
-    } else if (np == 0 || (np == 1 && !p.wave_parts)) {
-        return;                             // finished by the decode kernel
+    } else {
+        // the wave grid reduces W partitions per block into one slot
+        if (p.wave_parts > 1) np = (np + p.wave_parts - 1) / p.wave_parts;
+        if (np <= 1) return;                // finished by the decode kernel
     }
     const int hq = hk * p.group + r;
     const int64_t row0 = (int64_t(b) * p.num_q_heads + hq) * p.num_partitions;
@@ -2012,8 +1998,8 @@ static hipError_t launch_partials(const DecodeParams& p, hipStream_t stream) {
     if constexpr (kWaveOk) {
         if (choose_wave_parts(p)) {
             DecodeParams pw = p;
-            pw.wave_parts = 1;
             constexpr int W = Fmt<F>::kWaves;
+            pw.wave_parts = W;
             const dim3 grid{unsigned(int64_t((p.num_partitions + W - 1) / W) * units * p.batch)};
             launch_kernel(decode_kernel<F, kSlots, true>, grid, dim3(64 * W), stream, pw);
             return hipGetLastError();
@@ -2037,7 +2023,7 @@ hipError_t launch_decode_partials(const DecodeParams& p, hipStream_t stream) {
 hipError_t launch_decode_merge(const DecodeParams& p, hipStream_t stream) {
     if (p.num_partitions <= 1 && p.prefix_pages == nullptr) return hipSuccess;   // every sequence was finished in place
     DecodeParams pm = p;
-    pm.wave_parts = choose_wave_parts(p) ? 1 : 0;
+    pm.wave_parts = choose_wave_parts(p) ? waves_of(p.kv_fmt) : 0;
     const dim3 grid{unsigned(p.num_kv_heads), unsigned(p.batch)};
     if (p.head_dim == 64) hipLaunchKernelGGL(merge_kernel<64>, grid, dim3(256), 0, stream, pm);
     else if (p.head_dim == 256) hipLaunchKernelGGL(merge_kernel<256>, grid, dim3(256), 0, stream, pm);

@@ -107,10 +107,11 @@ struct DecodeParams {
     int32_t prefix_blocks;         // Hkv * prefix_chunks * prefix partitions, after the context blocks in the grid
     int32_t suffix_partitions;
     // grid shape of the partition launch: 0 one block per partition (its
-    // waves share the partition's pages and merge through LDS), 1 one wave
-    // per partition (a block takes kWaves consecutive partitions of one
-    // sequence and kv head; every wave writes its own partial, and the merge
-    // finishes every row).  Chosen by the launchers when allow_wave_parts.
+    // waves share the partition's pages and merge through LDS); W > 1 one
+    // wave per partition, a block taking W consecutive partitions of one
+    // sequence and kv head and reducing them through LDS into one partial
+    // slot (slot = first partition / W).  Chosen by the launchers when
+    // allow_wave_parts.
     int32_t allow_wave_parts;
     int32_t wave_parts;
 };
