@@ -180,8 +180,8 @@ int32_t uq_default_partition(const uq_cache_desc *desc, int32_t batch, int32_t n
  * the partition's pages, or -- when the launch has at least 2048 blocks of
  * 4 partitions each (head size 128, no shared prefix) -- one wave per
  * partition, a block taking 4 consecutive partitions of one sequence and kv
- * head.  The partitions and the result do not depend on the grid beyond
- * rounding.
+ * head and reducing their partials into one before the merge.  The result
+ * does not depend on the grid beyond rounding.
  *   q             : [batch][num_q_heads][128].  F32/BF16/F16: rotated and
  *                   cast to FP8 inside the call.  FP8_E4M3: already
  *                   prepared by uq_prepare_query.
@@ -216,12 +216,11 @@ uq_status uq_decode_attention(const uq_cache_desc *desc, const void *q, uq_dtype
 
 /*
  * The two launches of uq_decode_attention, for callers that time or overlap
- * them.  uq_decode_partials runs the partition kernel: it writes a partial
- * (running max, running sum, 128 accumulators per query head) of every
- * partition into the workspace, except that on the block-per-partition grid
- * a sequence whose context fits one partition gets its final output
- * instead.  uq_decode_merge merges the partials into `out` (a no-op when
- * max_context <= partition).  Called back
+ * them.  uq_decode_partials runs the partition kernel: each block writes
+ * a partial (running max, running sum, 128 accumulators per query head) of
+ * its partition (its 4 partitions on the wave grid) into the workspace, or
+ * the final output when it holds the whole context.  uq_decode_merge
+ * merges the partials into `out` (a no-op when max_context <= partition).  Called back
  * to back on one stream with the same arguments they are exactly
  * uq_decode_attention; the arguments, validation and errors are the same.
  */
