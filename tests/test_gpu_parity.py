@@ -335,7 +335,8 @@ def test_decode_minimax_full_size_sampled(uq):
 
 def test_decode_high_concurrency_sampled(uq):
     """B=256, Hq=64, Hkv=8, every context 131072 (36.5 GB of FP4 KV),
-    partitions of 4096: one sequence against the oracle."""
+    partitions of 4096 (the one-wave-per-partition grid, as the benchmark
+    runs it): the first, last and two other sequences against the oracle."""
     dev = torch.device("cuda:0")
     wl = workloads.high_concurrency()
     log("decode high-concurrency full size")
@@ -343,7 +344,7 @@ def test_decode_high_concurrency_sampled(uq):
     out = run_decode(uq, wl, desc, codes, scales, dev)
     del codes, scales
     torch.cuda.empty_cache()
-    seqs = [201]
+    seqs = [0, 77, 201, 255]
     pools, ptc = oracle_cache(wl, seqs, dev)
     ref = oracle.decode_attention(wl.q.numpy()[seqs], pools, ptc, wl.context_lens[seqs], wl.num_kv_heads,
                                   1 / math.sqrt(128), True)
