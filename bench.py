@@ -308,11 +308,24 @@ def write_path(uq, args, dev, stream, flush):
     rd = 2 * kp.numel() * kp.element_size()
     wr = ww.prefill_tokens * ww.num_kv_heads * KV_BYTES_PER_TOKEN_HEAD
     gbs = (rd + wr) / (pre_ms * 1e-3) / 1e9
+    # what this GPU moves for reads plus writes: torch's device-to-device
+    # copy of 512 MiB, timed like the prefill (event pair around the launch,
+    # after the flush); a reference point, not the roof the fraction uses
+    src = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    dst = torch.empty_like(src)
+
+    def copy(ev_a=None, ev_b=None):
+        dst.copy_(src)
+    copy_ms, _ = timed(copy, max(10, n // 4), 2, stream, flush=flush)
+    copy_gbs = 2 * src.numel() / (copy_ms * 1e-3) / 1e9
+    del src, dst
     return {"prefill_tokens": ww.prefill_tokens, "num_kv_heads": ww.num_kv_heads, "in_dtype": "bf16",
             "prefill_us": pre_ms * 1e3, "prefill_tokens_per_s": ww.prefill_tokens / (pre_ms * 1e-3),
             "prefill_bytes": rd + wr, "prefill_gbs": gbs, "prefill_frac": gbs / HBM_PEAK_GBS,
             "prefill_us_back_to_back": pre_ms_b2b * 1e3, "append_seqs": ww.append_seqs, "append_us": app_ms * 1e3,
-            "timing": "prefill: kernel events, 1 GiB written and read back before every launch; append: back to back"}
+            "copy_gbs": copy_gbs, "prefill_frac_of_copy": gbs / copy_gbs,
+            "timing": "prefill and copy: 1 GiB written and read back before every launch, prefill by kernel events, "
+                      "copy by an event pair around it; append: back to back"}
 
 
 def achievable(uq, wl, desc, codes, scales, pt, ctx, part, alg_bytes, args, dev, stream, flush):
