@@ -192,7 +192,7 @@ int32_t uq_default_partition(const uq_cache_desc *desc, int32_t batch, int32_t n
  *                   device read.  Lengths above it are clamped to it.
  *   softmax_scale : multiplies q.k (usually 1/sqrt(128)); finite and > 0.
  *   partition_tokens : context tokens per split-context partition, a
- *                   multiple of 32, or 0 for the default.
+ *                   multiple of 16 (whole pages), or 0 for the default.
  *   workspace     : >= uq_decode_workspace_bytes(...) bytes of device
  *                   memory, 16-byte aligned, no initial contents required.
  *                   Calls that share a workspace must not run concurrently.
@@ -202,7 +202,7 @@ int32_t uq_default_partition(const uq_cache_desc *desc, int32_t batch, int32_t n
  * Query head h reads kv head h / (num_q_heads / num_kv_heads).
  * Errors: INVALID_ARGUMENT for null pointers, batch/num_q_heads < 1,
  * num_q_heads % num_kv_heads != 0, max_context < 0 or above
- * max_pages_per_seq * 16, partition_tokens not a multiple of 32, a
+ * max_pages_per_seq * 16, partition_tokens not a multiple of 16, a
  * non-finite or non-positive softmax_scale, misaligned q/pools/workspace/out; UNSUPPORTED
  * for more than 16 query heads per kv head or unsupported dtypes;
  * WORKSPACE_TOO_SMALL.
@@ -509,7 +509,8 @@ uq_status uq_ref_decode_merge(const uq_ref_cache_desc *desc, int32_t batch, int3
  * (the instruction's scales are per 32-token block and cannot carry V's
  * per-token scales).  Head size 128 only; V scale bytes up to 135
  * (|V| < 6 * 2^8) keep the FP8 terms in range.  Arguments, outputs and
- * errors as uq_decode_attention, plus UNSUPPORTED for other head sizes.
+ * errors as uq_decode_attention, plus UNSUPPORTED for other head sizes and
+ * INVALID_ARGUMENT for a partition_tokens that is not a multiple of 32.
  * ---------------------------------------------------------------------- */
 uq_status uq_decode_attention_scaled_pv(const uq_cache_desc *desc, const void *q, uq_dtype q_dtype, int32_t batch,
                                         int32_t num_q_heads, const uint8_t *kv_codes, const uint8_t *kv_scales,

@@ -59,7 +59,7 @@ uq_status check_decode_common(const uq_cache_desc* desc, int32_t batch, int32_t 
     if (s != UQ_OK) return s;
     if (batch < 1 || num_q_heads < 1 || max_context < 0 || partition_tokens < 0) return UQ_ERR_INVALID_ARGUMENT;
     if (num_q_heads % desc->num_kv_heads != 0) return UQ_ERR_INVALID_ARGUMENT;
-    if (partition_tokens % 32 != 0) return UQ_ERR_INVALID_ARGUMENT;
+    if (partition_tokens % 16 != 0) return UQ_ERR_INVALID_ARGUMENT;   // partitions are whole pages
     if (num_q_heads / desc->num_kv_heads > kMaxGroup) return UQ_ERR_UNSUPPORTED;
     if (batch > 65535 || desc->num_kv_heads > 65535) return UQ_ERR_UNSUPPORTED;
     return UQ_OK;
@@ -470,6 +470,7 @@ uq_status uq_decode_attention_scaled_pv(const uq_cache_desc* desc, const void* q
                                workspace_bytes, out, out_dtype, p);
     if (s != UQ_OK) return s;
     if (desc->head_dim != kHeadDim) return UQ_ERR_UNSUPPORTED;
+    if (p.partition_tokens % 32 != 0) return UQ_ERR_INVALID_ARGUMENT;   // whole page pairs only
     p.allow_wave_parts = 0;   // the prototype's grid is one block per partition
     s = from_hip(uq::launch_decode_partials_mxpv(p, static_cast<hipStream_t>(stream)));
     if (s != UQ_OK) return s;

@@ -78,7 +78,7 @@ def small(hq=12, hkv=2, seed=31):
                             shared_prefix_tokens=96)
 
 
-@pytest.mark.parametrize("partition,prefix_partition", [(0, 0), (32, 32), (64, 64), (256, 32)])
+@pytest.mark.parametrize("partition,prefix_partition", [(0, 0), (32, 32), (48, 32), (64, 64), (256, 32)])
 def test_cascade_against_oracle(uq, partition, prefix_partition):
     dev = torch.device("cuda:0")
     wl = small()

@@ -4,7 +4,7 @@ the oracle at the same head size.
   * quantize-on-write: every pool byte (pre-filled with a canary) equal to
     the oracle's, f32 and bf16 rows, rotate_v on and off, padding slots;
   * decode attention: max-abs 2e-3 and relative L2 1e-3 against the fp64
-    oracle, ragged contexts with an empty one, partitions 0/32/256, group
+    oracle, ragged contexts with an empty one, partitions 0/32/48/256, group
     sizes 6, 16 and 1 (at head size 64 both the one-head and the two-head
     blocks), f32 and bf16 queries, a bf16 output, and a
     GPT-OSS-like layer (64 query heads, 8 KV heads, batch 32, context 32768)
@@ -89,7 +89,7 @@ def test_write_bit_exact(uq, d, dtype, rotate_v):
 
 
 @pytest.mark.parametrize("d", [64, 256])
-@pytest.mark.parametrize("partition", [0, 32, 256])
+@pytest.mark.parametrize("partition", [0, 32, 48, 256])
 @pytest.mark.parametrize("rotate_v", [True, False])
 def test_decode_ragged(uq, d, partition, rotate_v):
     dev = torch.device("cuda:0")

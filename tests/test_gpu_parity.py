@@ -265,7 +265,7 @@ def tiny_case(uq):
     return wl, desc, codes, scales, ref
 
 
-@pytest.mark.parametrize("partition", [0, 32, 256, 1024, 4096])
+@pytest.mark.parametrize("partition", [0, 16, 32, 48, 80, 256, 1024, 4096])
 def test_decode_tiny_partitions(uq, tiny_case, partition):
     wl, desc, codes, scales, ref = tiny_case
     log(f"decode tiny partition={partition}")

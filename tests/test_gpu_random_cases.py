@@ -27,7 +27,7 @@ def params(i):
            for _ in range(b)]
     if max(ctx) == 0:
         ctx[0] = 5
-    part = int(rng.choice([0, 32, 64, 96, 256, 1024]))
+    part = int(rng.choice([0, 16, 32, 48, 64, 96, 256, 1024]))
     q_dt = [torch.float32, torch.bfloat16, torch.float16][int(rng.integers(0, 3))]
     row_dt = [torch.float32, torch.bfloat16, torch.float16][int(rng.integers(0, 3))]
     paging = "identity" if rng.random() < 0.3 else "random"

@@ -220,7 +220,7 @@ def test_ref_write_fp8_saturates_and_skips(uq):
 
 
 @pytest.mark.parametrize("fmt", ["fp8", "bf16"])
-@pytest.mark.parametrize("partition", [0, 64, 32])
+@pytest.mark.parametrize("partition", [0, 64, 32, 48])
 def test_ref_decode_ragged(uq, fmt, partition):
     """Ragged contexts around page, stage and partition edges, an empty
     context, GQA group 8."""

@@ -137,7 +137,7 @@ def test_step_encodes_e2m1_ties_like_the_write(uq):
 
 
 @pytest.mark.parametrize("fmt", ["fp4", "fp8", "bf16", "tq4"])
-@pytest.mark.parametrize("partition", [0, 32, 64, 256])
+@pytest.mark.parametrize("partition", [0, 32, 48, 64, 256])
 def test_step_equals_write_then_decode(uq, fmt, partition):
     dev = torch.device("cuda:0")
     wl = workloads.custom(8, 16, 2, CTX, seed=21, paging="random")

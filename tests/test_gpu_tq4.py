@@ -96,7 +96,7 @@ def test_write_matches_oracle(uq, dtype, which):
     assert diff.size == 0, f"{diff.size} bytes differ, first at {diff[:8]}"
 
 
-@pytest.mark.parametrize("partition", [0, 32, 64, 256])
+@pytest.mark.parametrize("partition", [0, 32, 48, 64, 256])
 def test_decode_against_oracle(uq, partition):
     dev = torch.device("cuda:0")
     wl = workloads.custom(6, 12, 2, [1, 17, 100, 257, 1000, 0], seed=52, paging="random")

@@ -133,7 +133,7 @@ def test_fp4_decode_against_oracle(uq, rotate_v):
     pt = torch.as_tensor(wl.page_table, device=dev)
     ctx = torch.as_tensor(wl.context_lens, device=dev)
     outs = {}
-    for part in (WAVE_PART, BLOCK_PART):
+    for part in (WAVE_PART, BLOCK_PART, 16, 48):
         out = uq.decode_attention(desc, wl.q.to(dev), codes, scales, pt, ctx, wl.max_context, SCALE, part)
         torch.cuda.synchronize()
         outs[part] = out.cpu().numpy().astype(np.float64)

@@ -92,7 +92,7 @@ def test_decode_validation(uq):
     assert decode(uq, desc(), B=0) == E.UQ_ERR_INVALID_ARGUMENT
     assert decode(uq, desc(), maxctx=65) == E.UQ_ERR_INVALID_ARGUMENT          # > max_pages_per_seq * 16
     assert decode(uq, desc(), maxctx=-1) == E.UQ_ERR_INVALID_ARGUMENT
-    assert decode(uq, desc(), part=48) == E.UQ_ERR_INVALID_ARGUMENT            # not a multiple of 32
+    assert decode(uq, desc(), part=40) == E.UQ_ERR_INVALID_ARGUMENT            # not whole pages (16 tokens)
     assert decode(uq, desc(), scale=float("inf")) == E.UQ_ERR_INVALID_ARGUMENT
     assert decode(uq, desc(), scale=0.0) == E.UQ_ERR_INVALID_ARGUMENT
     assert decode(uq, desc(), scale=-0.1) == E.UQ_ERR_INVALID_ARGUMENT
@@ -116,6 +116,18 @@ def decode_noalloc(uq, d, q=FAKE, qdt=0, B=2, Hq=4, mpps=4, maxctx=64, scale=0.1
                                               pt, mpps, ctx, maxctx, scale, part, out, odt, None)
 
 
+def test_scaled_pv_validation(uq):
+    """The prototype takes the decode call's checks, head size 128 only and
+    partitions of whole page pairs (32 tokens)."""
+    E = uq
+    def call(d, part=0):
+        return uq.lib.uq_decode_attention_scaled_pv(ctypes.byref(d), FAKE, 0, 2, 4, FAKE, FAKE, FAKE, 4, FAKE, 64,
+                                                    0.1, part, FAKE, 1 << 30, FAKE, 0, None)
+    assert call(desc(), part=40) == E.UQ_ERR_INVALID_ARGUMENT
+    assert call(desc(), part=48) == E.UQ_ERR_INVALID_ARGUMENT
+    assert call(desc(head_dim=64)) == E.UQ_ERR_UNSUPPORTED
+
+
 def test_decode_noalloc_validation(uq):
     """The no-allocation decode makes uq_decode_attention's host checks, and
     refuses a call whose partials exceed its device array, before any HIP
@@ -125,7 +137,7 @@ def test_decode_noalloc_validation(uq):
     assert decode_noalloc(uq, desc(head_dim=96)) == E.UQ_ERR_UNSUPPORTED
     assert decode_noalloc(uq, desc(), Hq=3) == E.UQ_ERR_INVALID_ARGUMENT
     assert decode_noalloc(uq, desc(), maxctx=65) == E.UQ_ERR_INVALID_ARGUMENT
-    assert decode_noalloc(uq, desc(), part=48) == E.UQ_ERR_INVALID_ARGUMENT
+    assert decode_noalloc(uq, desc(), part=40) == E.UQ_ERR_INVALID_ARGUMENT
     assert decode_noalloc(uq, desc(), q=None) == E.UQ_ERR_INVALID_ARGUMENT
     assert decode_noalloc(uq, desc(), out=None) == E.UQ_ERR_INVALID_ARGUMENT
     assert decode_noalloc(uq, desc(), odt=3) == E.UQ_ERR_UNSUPPORTED
@@ -204,7 +216,7 @@ def test_ref_cache_sizes_and_validation(uq):
     assert rdecode(rdesc(), qdt=3) == E.UQ_ERR_UNSUPPORTED          # the query is never pre-cast here
     assert rdecode(rdesc(), Hq=3) == E.UQ_ERR_INVALID_ARGUMENT
     assert rdecode(rdesc(), maxctx=65) == E.UQ_ERR_INVALID_ARGUMENT
-    assert rdecode(rdesc(), part=16) == E.UQ_ERR_INVALID_ARGUMENT
+    assert rdecode(rdesc(), part=24) == E.UQ_ERR_INVALID_ARGUMENT   # not whole pages
     assert rdecode(rdesc(), scale=0.0) == E.UQ_ERR_INVALID_ARGUMENT
     assert rdecode(rdesc(), wsb=16) == E.UQ_ERR_WORKSPACE_TOO_SMALL
     assert rdecode(rdesc(format=5)) == E.UQ_ERR_UNSUPPORTED
