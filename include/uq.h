@@ -331,7 +331,7 @@ size_t uq_decode_cascade_workspace_bytes(int32_t num_kv_heads, int32_t batch, in
  * step is written at position len_b - 1, which lies after lens[b].
  * Arguments, output and errors are those of uq_decode_step, plus
  * INVALID_ARGUMENT for a NULL prefix, pages or lens, a num_tokens that is not
- * a positive multiple of 16, a partition_tokens that is not a multiple of 32,
+ * a positive multiple of 16, a prefix partition_tokens that is not a multiple of 32,
  * or only one of k_new, v_new.  uq_decode_cascade_partials is its first
  * launch and uq_decode_cascade_merge (with the same prefix and partition)
  * its second.
