@@ -787,11 +787,11 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
     //
     // WP (one wave per partition): block `rest / batch` of a (kv head,
     // sequence) takes partitions W * (rest / batch) + wave, one per wave.
-    // Each wave streams its whole partition through its own ring and writes
-    // its own partial, so a block's query prologue serves W partitions and
-    // no wave waits for another at the end (with 4096-token partitions the
-    // block-per-partition grid spent about 8 % of the kernel on its block
-    // prologues and LDS merges).
+    // Each wave streams its whole partition through its own ring; the block
+    // then merges its W partials through LDS and writes one, so a block's
+    // query prologue and partial write serve W partitions (on 4096-token
+    // partitions of 128k contexts: 6.13 ms against 6.73 ms for one block
+    // per partition).
     const int lin = blockIdx.x;
     const bool cascade = !WP && p.prefix_pages != nullptr;
     const int units = kPair ? p.num_kv_heads / 2 : p.num_kv_heads;   // kv heads, or pairs of them
