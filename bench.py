@@ -52,7 +52,9 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
+    # after an idle spell the first ~100 launches (about 12 ms of steps) run
+    # up to 5 % slower while the GPU leaves its idle state
+    ap.add_argument("--warmup", type=int, default=200)
     ap.add_argument("--workload", default="qwen3-235b-like",
                     choices=["qwen3-235b-like", "high-concurrency", "minimax-like", "tiny", "gpt-oss-like-hd64",
                              "gpt-oss-like-hd256"])
@@ -153,26 +155,24 @@ FLUSH_BYTES = 1 << 30   # written and read between flushed steps: 4x the 256 MB 
 
 
 def timed(step, steps, warmup, stream, flush=None):
-    """Run `warmup` untimed steps, then `steps` timed ones; returns (ms per
-    step, mean ms between the event pair each step hands to
+    """Run `warmup` untimed steps, then `steps` timed ones twice; returns (ms
+    per step, mean ms between the event pair each step hands to
     uq.time_next_launch, which brackets the timed kernel itself: the decode
     partition kernel, a probe or the quantize-on-write kernel, start to end,
     as rocprofv3 reports it).
 
-    Without `flush` the steps run back to back and the step time is the
-    whole timed region over `steps`.  With `flush` (a callable that writes
-    FLUSH_BYTES of device memory), every timed step is preceded by that
-    write and read, outside its events, so that no step finds the previous
-    one's bytes in L2 or the last-level cache; the step time is then the mean
-    over steps of an event pair recorded on the stream around the step's
-    launches."""
+    The step time comes from the first pass, whose launches carry no kernel
+    events (a launch that records its own start and end events costs the
+    step about 4 us); the kernel time from the second, the same steps with
+    the events.  Without `flush` the steps run back to back and the step
+    time is the whole timed region over `steps`.  With `flush` (a callable
+    that writes FLUSH_BYTES of device memory), every timed step is preceded
+    by that write and read, outside its events, so that no step finds the
+    previous one's bytes in L2 or the last-level cache; the step time is then
+    the mean over steps of an event pair recorded on the stream around the
+    step's launches."""
     import gc
     import torch
-    for _ in range(warmup):
-        if flush is not None:
-            flush()
-        step()
-    torch.cuda.synchronize()
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     around = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     for a, b in evs + around:   # create the HIP events
@@ -181,27 +181,42 @@ def timed(step, steps, warmup, stream, flush=None):
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
-    # no Python garbage collection while launching: a collection pause on the
-    # host leaves the GPU idle between launches and inflates the event times
+    # no Python garbage collection from the warmup to the end: a collection
+    # pause on the host leaves the GPU idle, and after an idle spell its
+    # first launches run slower (the warmup covers the start of the run)
     gc.collect()
     gc.disable()
-    try:
+
+    def one_pass(kernel_events):
         t_start.record(stream)
         for i in range(steps):
             if flush is not None:
                 flush()
                 around[i][0].record(stream)
-            step(*evs[i])
+            if kernel_events:
+                step(*evs[i])
+            else:
+                step()
             if flush is not None:
                 around[i][1].record(stream)
         t_end.record(stream)
         torch.cuda.synchronize()
+        if flush is None:
+            return t_start.elapsed_time(t_end) / steps
+        return float(np.mean([a.elapsed_time(b) for a, b in around]))
+
+    try:
+        for _ in range(warmup):
+            if flush is not None:
+                flush()
+            step()
+        torch.cuda.synchronize()
+        step_ms = one_pass(False)
+        one_pass(True)
     finally:
         gc.enable()
     kernel_ms = float(np.mean([a.elapsed_time(b) for a, b in evs]))
-    if flush is None:
-        return t_start.elapsed_time(t_end) / steps, kernel_ms
-    return float(np.mean([a.elapsed_time(b) for a, b in around])), kernel_ms
+    return step_ms, kernel_ms
 
 
 def make_flush(dev):
