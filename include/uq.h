@@ -319,8 +319,11 @@ typedef struct uq_shared_prefix {
     int32_t partition_tokens; /* prefix tokens per prefix block, a multiple of 32, or 0 for the default */
 } uq_shared_prefix;
 
-/* Workspace of the cascade calls (FP4 and comparison caches); 0 for invalid
- * arguments. */
+/* Workspace of the cascade calls (FP4 and comparison caches): the partial
+ * rows of the context and prefix partitions (rounded up to 16 bytes), then
+ * the dispatch list of the partition kernel, 16 bytes per (context
+ * partition, sequence) and per (chunk of 16 query columns, prefix
+ * partition); 0 for invalid arguments. */
 size_t uq_decode_cascade_workspace_bytes(int32_t num_kv_heads, int32_t batch, int32_t num_q_heads,
                                          int32_t max_context, int32_t partition_tokens,
                                          const uq_shared_prefix *prefix);
@@ -333,8 +336,12 @@ size_t uq_decode_cascade_workspace_bytes(int32_t num_kv_heads, int32_t batch, in
  * INVALID_ARGUMENT for a NULL prefix, pages or lens, a num_tokens that is not
  * a positive multiple of 16, a prefix partition_tokens that is not a multiple of 32,
  * or only one of k_new, v_new.  uq_decode_cascade_partials is its first
- * launch and uq_decode_cascade_merge (with the same prefix and partition)
- * its second.
+ * part and uq_decode_cascade_merge (with the same prefix and partition)
+ * its second.  The first part is two launches: a one-block kernel lists the
+ * (context partition, sequence) rows in the workspace, the ones with the
+ * most tokens first, then the prefix rows, and the partition kernel's
+ * blocks take their rows from that list, so that the longest blocks start
+ * first and short ones fill the end; the order changes no result.
  */
 uq_status uq_decode_cascade(const uq_cache_desc *desc, const void *q, uq_dtype q_dtype, const void *k_new,
                             const void *v_new, uq_dtype new_dtype, int32_t batch, int32_t num_q_heads,

@@ -71,14 +71,22 @@ int64_t num_partitions(int32_t max_context, int32_t part) {
     return max_context > 0 ? (int64_t(max_context) + part - 1) / part : 1;
 }
 
-size_t workspace_for(int32_t batch, int32_t num_q_heads, int32_t max_context, int32_t part, int64_t extra_slots = 0,
-                     int32_t head_dim = kHeadDim) {
-    return align16(size_t(batch) * size_t(num_q_heads) * size_t(num_partitions(max_context, part) + extra_slots) *
-                   size_t(head_dim + 2) * sizeof(float));
+// Workspace of a decode call: the partial rows (accumulators, then the
+// (max, sum) pairs); a cascade call (extra_slots > 0: its prefix
+// partitions) adds its row list, 16 bytes per context row (partition,
+// sequence) and per prefix row (column chunk, prefix partition).
+size_t workspace_for(int32_t batch, int32_t num_q_heads, int32_t num_kv_heads, int32_t max_context, int32_t part,
+                     int64_t extra_slots = 0, int32_t head_dim = kHeadDim) {
+    const int64_t np_ctx = num_partitions(max_context, part);
+    const size_t rows = align16(size_t(batch) * size_t(num_q_heads) * size_t(np_ctx + extra_slots) *
+                                size_t(head_dim + 2) * sizeof(float));
+    if (extra_slots <= 0) return rows;
+    const int64_t chunks = (int64_t(batch) * (num_q_heads / num_kv_heads) + 15) / 16;
+    return rows + size_t(np_ctx * batch + chunks * extra_slots) * 16;
 }
 
 // Fill the parameter block of the decode launches.  Workspace: the partial
-// accumulators, then the (max, sum) pairs.
+// accumulators, then the (max, sum) pairs, then (cascade) the row list.
 uq_status make_decode_params(const uq_cache_desc* desc, const void* q, uq_dtype q_dtype, int32_t batch,
                              int32_t num_q_heads, const uint8_t* kv_codes, const uint8_t* kv_scales,
                              const int32_t* page_table, int32_t max_pages_per_seq, const int32_t* context_lens,
@@ -87,7 +95,8 @@ uq_status make_decode_params(const uq_cache_desc* desc, const void* q, uq_dtype 
                              int64_t extra_slots = 0) {
     const int32_t part = partition_tokens == 0 ? pick_partition(batch, block_heads(desc, num_q_heads), max_context)
                                                : partition_tokens;
-    const size_t need = workspace_for(batch, num_q_heads, max_context, part, extra_slots, desc->head_dim);
+    const size_t need =
+        workspace_for(batch, num_q_heads, desc->num_kv_heads, max_context, part, extra_slots, desc->head_dim);
     if (workspace == nullptr) return UQ_ERR_INVALID_ARGUMENT;
     if (workspace_bytes < need) return UQ_ERR_WORKSPACE_TOO_SMALL;
     if (!aligned16(workspace)) return UQ_ERR_INVALID_ARGUMENT;
@@ -119,8 +128,10 @@ uq_status make_decode_params(const uq_cache_desc* desc, const void* q, uq_dtype 
     p.num_partitions = int32_t(np);
     char* ws = static_cast<char*>(workspace);
     const size_t acc_bytes = size_t(batch) * num_q_heads * size_t(np) * size_t(desc->head_dim) * sizeof(float);
+    const size_t ml_bytes = size_t(batch) * num_q_heads * size_t(np) * 2 * sizeof(float);
     p.part_acc = reinterpret_cast<float*>(ws);
     p.part_ml = reinterpret_cast<float*>(ws + acc_bytes);
+    p.cascade_rows = extra_slots > 0 ? reinterpret_cast<int4*>(ws + align16(acc_bytes + ml_bytes)) : nullptr;
     p.out = out;
     p.out_dtype = out_dtype == UQ_F32 ? 0 : 1;
     p.rotate_v = desc->rotate_v != 0;
@@ -410,7 +421,7 @@ size_t uq_decode_workspace_bytes(const uq_cache_desc* desc, int32_t batch, int32
     if (check_decode_common(desc, batch, num_q_heads, max_context, partition_tokens) != UQ_OK) return 0;
     const int32_t part = partition_tokens == 0 ? pick_partition(batch, block_heads(desc, num_q_heads), max_context)
                                                : partition_tokens;
-    return workspace_for(batch, num_q_heads, max_context, part, 0, desc->head_dim);
+    return workspace_for(batch, num_q_heads, desc->num_kv_heads, max_context, part, 0, desc->head_dim);
 }
 
 // Shared set-up of the decode entry points: validation and the parameter block.
@@ -719,7 +730,7 @@ size_t uq_decode_cascade_workspace_bytes(int32_t num_kv_heads, int32_t batch, in
     d.rotate_v = 0;
     if (check_decode_common(&d, batch, num_q_heads, max_context, partition_tokens) != UQ_OK) return 0;
     const int32_t part = partition_tokens == 0 ? pick_partition(batch, num_kv_heads, max_context) : partition_tokens;
-    return workspace_for(batch, num_q_heads, max_context, part,
+    return workspace_for(batch, num_q_heads, num_kv_heads, max_context, part,
                          prefix_slots(prefix, num_kv_heads, batch, group_of(num_q_heads, num_kv_heads)));
 }
 

@@ -774,8 +774,14 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
     // sequences would idle), and it keeps one kv head on the same XCDs, whose
     // L2 then serves pages that several sequences share.
     //
-    // Cascade decode adds prefix blocks after the context blocks: one per (kv
-    // head, chunk of 16 query columns, prefix partition), same order.  A
+    // Cascade decode takes its rows from a list that cascade_rows_kernel
+    // writes: the context rows (partition, sequence) sorted by tokens,
+    // longest first, then the prefix rows, then the rows without work.  With
+    // the partition-major order the full partitions of the longest contexts
+    // were dispatched last and ran alone at the end (the MiniMax-like
+    // layer's last 60 µs), and the blocks without work went out before the
+    // prefix blocks.  A prefix row is one (chunk of 16 query columns, prefix
+    // partition), kv head fastest as for the context rows.  A
     // prefix block's columns are (sequence, query head) pairs f = 16 * chunk
     // + column of the flattened batch (b = f / G, head hk * G + f % G), and it
     // reads the shared prefix pages once for all of them.  Prefix blocks are
@@ -799,10 +805,17 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
     const int row = lin / units;
     bool pre = false;
     int rest = row;
+    int row_ctx = 0, row_pl = 0;   // a cascade context row's length and prefix tokens
     if (cascade) {
+        // the row list: context rows with the most tokens first, then the
+        // prefix rows, then rows without work
+        const int4 rec = p.cascade_rows[row];
+        if (rec.x < 0) return;                                // no work left for this block
         const int context_rows = p.suffix_partitions * p.batch;
-        pre = row >= context_rows;                            // block-uniform
-        rest = pre ? row - context_rows : row;
+        pre = rec.x >= context_rows;                          // block-uniform
+        rest = pre ? rec.x - context_rows : rec.x;
+        row_ctx = rec.y;
+        row_pl = rec.z;
     }
     const int nb = pre ? p.prefix_chunks : p.batch;
     const int b = pre ? 0 : rest % nb;                                 // sequence (context blocks)
@@ -820,15 +833,16 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
         start = part * p.prefix_partition;
         end = (start + p.prefix_partition) < p.prefix_tokens ? (start + p.prefix_partition) : p.prefix_tokens;
     } else {
-        ctx = p.context_lens[b];
-        ctx = ctx < p.max_context ? ctx : p.max_context;
+        if (cascade) {
+            ctx = row_ctx;
+        } else {
+            ctx = p.context_lens[b];
+            ctx = ctx < p.max_context ? ctx : p.max_context;
+        }
         start = part * p.partition_tokens;
         if (cascade) {
             // the context blocks start after the tokens the prefix blocks serve
-            int pl = p.prefix_lens[b];
-            pl = pl < p.prefix_tokens ? pl : p.prefix_tokens;
-            pl = pl < ctx - 1 ? pl : ctx - 1;
-            pl = pl > 0 ? (pl & ~15) : 0;
+            const int pl = row_pl;
             if (start + p.partition_tokens <= pl) return;              // wholly inside the prefix
             start = start > pl ? start : pl;
         }
@@ -1951,6 +1965,77 @@ __global__ void __launch_bounds__(256) gather_probe_kernel(DecodeParams p, uint3
     if (lane == 0) sink[int64_t(lin) * W + wave] = acc;
 }
 
+// The rows of a cascade launch in dispatch order (one block).  The tokens
+// of context row (part, b) are those of its partition after the prefix's
+// tokens and before the context end, as the decode kernel computes them.
+// A counting sort over 1024 classes of tokens / partition_tokens puts the
+// context rows with the most tokens first (rows of one class in any order:
+// each row is computed and stored the same way whichever block takes it); a
+// row without tokens stays in the list only as the zero output of an empty
+// context (partition 0).  The prefix rows follow (records R + j), then -1
+// for the rest.
+__global__ void __launch_bounds__(1024) cascade_rows_kernel(DecodeParams p) {
+    constexpr int kClasses = 1024;
+    __shared__ int hist[kClasses];
+    __shared__ int total;
+    const int R = p.suffix_partitions * p.batch;
+    const int P = p.partition_tokens;
+    const int tid = threadIdx.x;
+    hist[tid] = 0;
+    __syncthreads();
+    // tokens of row r, or -1 when the row has nothing to do
+    auto row_tokens = [&](int r, int& ctx, int& pl) -> int {
+        const int b = r % p.batch, part = r / p.batch;
+        ctx = p.context_lens[b];
+        ctx = ctx < p.max_context ? ctx : p.max_context;
+        pl = p.prefix_lens[b];
+        pl = pl < p.prefix_tokens ? pl : p.prefix_tokens;
+        pl = pl < ctx - 1 ? pl : ctx - 1;
+        pl = pl > 0 ? (pl & ~15) : 0;
+        const int s0 = part * P;
+        if (s0 + P <= pl) return -1;
+        const int start = s0 > pl ? s0 : pl;
+        if (start >= ctx) return (ctx <= 0 && part == 0) ? 0 : -1;
+        const int end = s0 + P < ctx ? s0 + P : ctx;
+        return end - start;
+    };
+    // class 0: a whole partition; kClasses - 1: the fewest tokens
+    auto class_of = [&](int t) {
+        const int c = int(int64_t(P - t) * (kClasses - 1) / P);
+        return c < 0 ? 0 : (c > kClasses - 1 ? kClasses - 1 : c);
+    };
+    for (int r = tid; r < R; r += kClasses) {
+        int ctx, pl;
+        const int t = row_tokens(r, ctx, pl);
+        if (t >= 0) atomicAdd(&hist[class_of(t)], 1);
+    }
+    __syncthreads();
+    // prefix sum of the class counts (Hillis-Steele over the 1024 threads)
+    const int count = hist[tid];
+    int v = count;
+    for (int d = 1; d < kClasses; d <<= 1) {
+        __syncthreads();
+        hist[tid] = v;
+        __syncthreads();
+        if (tid >= d) v += hist[tid - d];
+    }
+    __syncthreads();
+    if (tid == kClasses - 1) total = v;
+    hist[tid] = v - count;   // the first list position of the class
+    __syncthreads();
+    for (int r = tid; r < R; r += kClasses) {
+        int ctx, pl;
+        const int t = row_tokens(r, ctx, pl);
+        if (t >= 0) {
+            const int pos = atomicAdd(&hist[class_of(t)], 1);
+            p.cascade_rows[pos] = make_int4(r, ctx, pl, 0);
+        }
+    }
+    const int PR = p.prefix_blocks / p.num_kv_heads;
+    for (int j = tid; j < PR; j += kClasses) p.cascade_rows[total + j] = make_int4(R + j, 0, 0, 0);
+    for (int i = total + PR + tid; i < R + PR; i += kClasses) p.cascade_rows[i] = make_int4(-1, 0, 0, 0);
+}
+
 static bool choose_wave_parts(const DecodeParams& p);
 
 hipError_t launch_gather_probe(const DecodeParams& p, uint32_t* sink, hipStream_t stream) {
@@ -2004,6 +2089,10 @@ static hipError_t launch_partials(const DecodeParams& p, hipStream_t stream) {
             launch_kernel(decode_kernel<F, kSlots, true>, grid, dim3(64 * W), stream, pw);
             return hipGetLastError();
         }
+    }
+    if (p.prefix_pages != nullptr) {
+        // the cascade's row list first (a plain launch: the timing hook is the partition kernel's)
+        hipLaunchKernelGGL(cascade_rows_kernel, dim3(1), dim3(1024), 0, stream, p);
     }
     const dim3 grid{unsigned(int64_t(p.prefix_blocks) + int64_t(p.suffix_partitions) * units * p.batch)};
     launch_kernel(decode_kernel<F, kSlots, false>, grid, dim3(64 * Fmt<F>::kWaves), stream, p);

@@ -106,6 +106,11 @@ struct DecodeParams {
     int32_t prefix_chunks;         // ceil(B * G / 16) column chunks per kv head
     int32_t prefix_blocks;         // Hkv * prefix_chunks * prefix partitions, after the context blocks in the grid
     int32_t suffix_partitions;
+    // the rows of a cascade launch in dispatch order, written by
+    // cascade_rows_kernel before the partition launch: context rows {part *
+    // B + b, context length, tokens the prefix serves, 0}, longest first,
+    // then prefix rows {suffix_partitions * B + j, 0, 0, 0}, then -1
+    int4* cascade_rows;            // [suffix_partitions * B + prefix_blocks / Hkv]
     // grid shape of the partition launch: 0 one block per partition (its
     // waves share the partition's pages and merge through LDS); W > 1 one
     // wave per partition, a block taking W consecutive partitions of one

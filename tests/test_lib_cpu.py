@@ -284,7 +284,10 @@ def test_cascade_validation(uq):
     # 64 context tokens in partitions of 32 -> 2 slots, plus 2 prefix partitions of 32
     plain = uq.workspace_bytes(__import__("paper_2606_20474_amd.uq", fromlist=["CacheDesc"]).CacheDesc(2, 10), 2, 4,
                                64, 32)
-    assert lib.uq_decode_cascade_workspace_bytes(2, 2, 4, 64, 32, ctypes.byref(sp)) == plain * 2
+    # twice the partial rows, then the dispatch list: 16 bytes per context row
+    # (2 partitions x 2 sequences) and per prefix row (1 column chunk x 2
+    # prefix partitions)
+    assert lib.uq_decode_cascade_workspace_bytes(2, 2, 4, 64, 32, ctypes.byref(sp)) == plain * 2 + (4 + 2) * 16
     assert lib.uq_decode_cascade_workspace_bytes(2, 2, 3, 64, 32, ctypes.byref(sp)) == 0
     r = lib.uq_ref_decode_cascade(ctypes.byref(rdesc()), FAKE, 0, None, None, 0, 2, 4, FAKE, FAKE, 4, FAKE, 64,
                                   None, 0.1, 0, FAKE, 1 << 30, FAKE, 0, None)
