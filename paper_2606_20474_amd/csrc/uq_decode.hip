@@ -30,9 +30,11 @@
 //   loop      each wave takes pairs of pages (32 tokens) round-robin and
 //             stages them through its own S-slot LDS ring (S = 2) with
 //             global_load_lds_dwordx4 (16 bytes per lane, 1 KiB per
-//             instruction); a slot is refilled with the pair S iterations
-//             ahead as soon as it has been read into registers, so S pairs
-//             per wave are in flight while one is computed.  The next 64
+//             instruction; non-temporal for the pages of one sequence,
+//             default policy for shared-prefix pages); a slot is refilled
+//             with the pair S iterations ahead as soon as it has been read
+//             into registers, so S pairs per wave are in flight while one
+//             is computed.  The next 64
 //             page ids are copied into LDS the same way, so the wave never
 //             waits on a register load while pages are in flight.
 //             QK^T: FP4 -- one v_mfma_scale_f32_16x16x128_f8f6f4 per page,
@@ -252,12 +254,23 @@ __device__ __forceinline__ int32_t clamp_ids(int32_t id, int64_t num_pages) {
     return (id < 0 || int64_t(id) >= num_pages) ? 0 : id;
 }
 
+// Cache policy bits of the page copies (the aux operand of
+// global_load_lds): kPageStream sets nt, the non-temporal (streaming)
+// policy, for pages that one block reads once; kPageShared keeps the
+// default policy for the shared-prefix pages, which the column chunks of a
+// prefix partition read again from L2.  On the Qwen3-like layer (570 MB of
+// pages per call) the streaming policy takes the FP4 decode kernel from
+// 106.5 to 93.1 us and its page-gather probe from 99 to 88 us (sc0/sc1 on
+// top of nt change nothing).
+constexpr int kPageStream = 2;   // nt
+constexpr int kPageShared = 0;
+
 // Asynchronous copy of one iteration (two pages of one kv head) from HBM
 // into an LDS stage with global_load_lds_dwordx4: every lane moves 16 bytes
 // and the hardware places lane i's bytes at dst + 16 i, so each 1 KiB chunk
 // of a tile lands in lane order.  The FP4 scale blocks of both pages
-// (2 x 128 bytes) are moved by lanes 0..15.
-template <int F>
+// (2 x 128 bytes) are moved by lanes 0..15.  AUX: the cache policy bits.
+template <int F, int AUX = kPageStream>
 __device__ __forceinline__ void stage_issue(uint8_t* stage, const uint8_t* __restrict__ codes,
                                             const uint8_t* __restrict__ scales, int64_t tile0, int64_t tile1,
                                             int lane) {
@@ -266,13 +279,13 @@ __device__ __forceinline__ void stage_issue(uint8_t* stage, const uint8_t* __res
         // metadata (lanes 0..19 page 0, lanes 20..39 page 1)
         const uint8_t* b0 = codes + (tile0 >> 1) * kTqBlock;
         const uint8_t* b1 = codes + (tile1 >> 1) * kTqBlock;
-        __builtin_amdgcn_global_load_lds(b0 + 16 * lane, (lds_ptr_t)stage, 16, 0, 0);
-        __builtin_amdgcn_global_load_lds(b0 + 1024 + 16 * lane, (lds_ptr_t)(stage + 1024), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds(b1 + 16 * lane, (lds_ptr_t)(stage + 2048), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds(b1 + 1024 + 16 * lane, (lds_ptr_t)(stage + 3072), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(b0 + 16 * lane, (lds_ptr_t)stage, 16, 0, AUX);
+        __builtin_amdgcn_global_load_lds(b0 + 1024 + 16 * lane, (lds_ptr_t)(stage + 1024), 16, 0, AUX);
+        __builtin_amdgcn_global_load_lds(b1 + 16 * lane, (lds_ptr_t)(stage + 2048), 16, 0, AUX);
+        __builtin_amdgcn_global_load_lds(b1 + 1024 + 16 * lane, (lds_ptr_t)(stage + 3072), 16, 0, AUX);
         if (lane < 40) {
             const uint8_t* m = lane < 20 ? b0 + kTqMeta + 16 * lane : b1 + kTqMeta + 16 * (lane - 20);
-            __builtin_amdgcn_global_load_lds(m, (lds_ptr_t)(stage + 4096), 16, 0, 0);
+            __builtin_amdgcn_global_load_lds(m, (lds_ptr_t)(stage + 4096), 16, 0, AUX);
         }
         return;
     }
@@ -285,16 +298,16 @@ __device__ __forceinline__ void stage_issue(uint8_t* stage, const uint8_t* __res
         const int64_t vo = (u < 8 ? 512 : 1536) + 16 * (8 * r + (u & 7));
         const uint8_t* b0 = codes + tile0 * 512;
         const uint8_t* b1 = codes + tile1 * 512;
-        __builtin_amdgcn_global_load_lds(b0 + ko, (lds_ptr_t)stage, 16, 0, 0);
-        __builtin_amdgcn_global_load_lds(b0 + vo, (lds_ptr_t)(stage + 1024), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds(b1 + ko, (lds_ptr_t)(stage + 2048), 16, 0, 0);
-        __builtin_amdgcn_global_load_lds(b1 + vo, (lds_ptr_t)(stage + 3072), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(b0 + ko, (lds_ptr_t)stage, 16, 0, AUX);
+        __builtin_amdgcn_global_load_lds(b0 + vo, (lds_ptr_t)(stage + 1024), 16, 0, AUX);
+        __builtin_amdgcn_global_load_lds(b1 + ko, (lds_ptr_t)(stage + 2048), 16, 0, AUX);
+        __builtin_amdgcn_global_load_lds(b1 + vo, (lds_ptr_t)(stage + 3072), 16, 0, AUX);
         if (lane < 16) {
             // 16-byte unit j of a page's 128-byte block: K_A K_A K_B K_B V_A V_A V_B V_B
             const int j = lane & 7;
             const int64_t so = (j < 4 ? 0 : 32) + ((j & 2) ? 64 : 0) + 16 * (j & 1);
             const uint8_t* sc = scales + ((lane < 8 ? tile0 : tile1) >> 1) * 64 + so;
-            __builtin_amdgcn_global_load_lds(sc, (lds_ptr_t)(stage + 4096), 16, 0, 0);
+            __builtin_amdgcn_global_load_lds(sc, (lds_ptr_t)(stage + 4096), 16, 0, AUX);
         }
         return;
     }
@@ -303,11 +316,11 @@ __device__ __forceinline__ void stage_issue(uint8_t* stage, const uint8_t* __res
     const uint8_t* k1 = codes + tile1 * T + 16 * lane;
 #pragma unroll
     for (int c = 0; c < 2 * T; c += 1024) {
-        __builtin_amdgcn_global_load_lds(k0 + c, (lds_ptr_t)(stage + c), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(k0 + c, (lds_ptr_t)(stage + c), 16, 0, AUX);
     }
 #pragma unroll
     for (int c = 0; c < 2 * T; c += 1024) {
-        __builtin_amdgcn_global_load_lds(k1 + c, (lds_ptr_t)(stage + 2 * T + c), 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(k1 + c, (lds_ptr_t)(stage + 2 * T + c), 16, 0, AUX);
     }
     if constexpr (Fmt<F>::kScaleBlock != 0) {
         // both pages' scale blocks (K then V scales, kScaleBlock bytes per page)
@@ -315,7 +328,7 @@ __device__ __forceinline__ void stage_issue(uint8_t* stage, const uint8_t* __res
         if (lane < SB / 8) {
             const int64_t t = lane < SB / 16 ? tile0 : tile1;
             const uint8_t* sc = scales + (t >> 1) * SB + 16 * (lane % (SB / 16));
-            __builtin_amdgcn_global_load_lds(sc, (lds_ptr_t)(stage + 4 * T), 16, 0, 0);
+            __builtin_amdgcn_global_load_lds(sc, (lds_ptr_t)(stage + 4 * T), 16, 0, AUX);
         }
     }
 }
@@ -1025,8 +1038,12 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
         for (int s = 0; s < S && s < n_local; ++s) {
             const int64_t id0 = __builtin_amdgcn_readlane(ids, 2 * s);
             const int64_t id1 = __builtin_amdgcn_readlane(ids, 2 * s + 1);
-            stage_issue<F>(ring + s * kStage, p.codes, p.scales, id0 * tiles_per_page + head_tile,
-                           id1 * tiles_per_page + head_tile, lane);
+            if (pre)
+                stage_issue<F, kPageShared>(ring + s * kStage, p.codes, p.scales, id0 * tiles_per_page + head_tile,
+                                            id1 * tiles_per_page + head_tile, lane);
+            else
+                stage_issue<F, kPageStream>(ring + s * kStage, p.codes, p.scales, id0 * tiles_per_page + head_tile,
+                                            id1 * tiles_per_page + head_tile, lane);
         }
     }
 
@@ -1196,8 +1213,12 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
             const int s = 2 * (kn & 31);
             const int64_t id0 = __builtin_amdgcn_readlane(ids, s);
             const int64_t id1 = __builtin_amdgcn_readlane(ids, s + 1);
-            stage_issue<F>(ring + slot * kStage, p.codes, p.scales, id0 * tiles_per_page + head_tile,
-                           id1 * tiles_per_page + head_tile, lane);
+            if (pre)
+                stage_issue<F, kPageShared>(ring + slot * kStage, p.codes, p.scales, id0 * tiles_per_page + head_tile,
+                                            id1 * tiles_per_page + head_tile, lane);
+            else
+                stage_issue<F, kPageStream>(ring + slot * kStage, p.codes, p.scales,
+                                            id0 * tiles_per_page + head_tile, id1 * tiles_per_page + head_tile, lane);
         }
 
         // ---- QK^T: raw scores (the softmax scale is applied in the exponent)
