@@ -562,9 +562,10 @@ uq_status uq_decode_attention_noalloc(const uq_cache_desc *desc, const void *q, 
  * this library, and the arithmetic of its matrix instructions).
  *
  * uq_probe_stream_read -- read `bytes` of device memory at `buf` once
- *   (16-byte loads, a grid-stride pass of UQ_PROBE_STREAM_BLOCKS blocks),
- *   XOR-folding them into one checksum word per block in `sink`.  Its kernel
- *   time is the time a plain stream of that many bytes takes.
+ *   (UQ_PROBE_STREAM_BLOCKS blocks, each streaming its own contiguous share
+ *   with non-temporal 16-byte loads), XOR-folding them into one checksum
+ *   word per block in `sink`.  Its kernel time is the time a plain stream
+ *   of that many bytes takes.
  *   buf 16-byte aligned, bytes > 0 and a multiple of 16; sink: at least
  *   UQ_PROBE_STREAM_BLOCKS uint32 words of device memory.
  *   Errors: INVALID_ARGUMENT otherwise.
