@@ -343,7 +343,7 @@ def write_path(uq, args, dev, stream, flush):
                       "copy by an event pair around it; append: back to back"}
 
 
-def achievable(uq, wl, desc, codes, scales, pt, ctx, part, alg_bytes, args, dev, stream, flush):
+def achievable(uq, wl, desc, codes, scales, pt, ctx, part, alg_bytes, args, dev, stream, flush, prefix=None):
     """What this GPU delivers to the decode kernel's reads, timed like the
     kernel (flushed, kernel events): a plain stream of the launch's
     algorithmic bytes and of 4 GiB (uq_probe_stream_read), and the decode
@@ -365,7 +365,9 @@ def achievable(uq, wl, desc, codes, scales, pt, ctx, part, alg_bytes, args, dev,
         res[f"{name}_bytes"] = buf.numel()
         del buf, sink
         torch.cuda.empty_cache()
-    if wl.head_dim == 128 and not wl.shared_prefix_tokens:
+    # the decode kernel's own grid as a probe: plain (any head size) or the
+    # cascade's, as the timed step runs it
+    if prefix is None:
         sink = torch.empty(4 * max(1, -(-wl.max_context // part)) * wl.num_kv_heads * wl.batch, dtype=torch.int32,
                            device=dev)
 
@@ -373,11 +375,20 @@ def achievable(uq, wl, desc, codes, scales, pt, ctx, part, alg_bytes, args, dev,
             if ev_a is not None:
                 uq.time_next_launch(ev_a, ev_b)
             uq.probe_page_gather(desc, wl.num_q_heads, codes, scales, pt, ctx, wl.max_context, part, sink)
-        _, ms = timed(gather, n, 3, stream, flush=flush)
-        res["page_gather_gbs"] = alg_bytes / (ms * 1e-3) / 1e9
-        res["page_gather_ms"] = ms
     else:
-        res["page_gather_gbs"] = None   # the probe covers the plain head-size-128 grid
+        pws = torch.empty(uq.cascade_workspace_bytes(wl.num_kv_heads, wl.batch, wl.num_q_heads, wl.max_context,
+                                                     prefix, part), dtype=torch.uint8, device=dev)
+        sink = uq.probe_page_gather_cascade(desc, wl.num_q_heads, codes, scales, pt, ctx, wl.max_context, prefix,
+                                            part, pws)
+
+        def gather(ev_a=None, ev_b=None):
+            if ev_a is not None:
+                uq.time_next_launch(ev_a, ev_b)
+            uq.probe_page_gather_cascade(desc, wl.num_q_heads, codes, scales, pt, ctx, wl.max_context, prefix, part,
+                                         pws, sink)
+    _, ms = timed(gather, n, 3, stream, flush=flush)
+    res["page_gather_gbs"] = alg_bytes / (ms * 1e-3) / 1e9
+    res["page_gather_ms"] = ms
     return res
 
 
@@ -516,7 +527,7 @@ def main():
     alg_bytes = alg_tokens * wl.num_kv_heads * (KV_BYTES_PER_TOKEN_HEAD * D // 128)
     achieved = alg_bytes / (dec_ms * 1e-3) / 1e9
     ach = None if args.no_probes else achievable(uq, wl, desc, codes, scales, pt, ctx, part, alg_bytes, args, dev,
-                                                 stream, flush)
+                                                 stream, flush, prefix)
     if ach is not None:
         progress("bandwidth probes timed")
     result = {

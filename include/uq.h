@@ -571,18 +571,32 @@ uq_status uq_decode_attention_noalloc(const uq_cache_desc *desc, const void *q, 
  *   Errors: INVALID_ARGUMENT otherwise.
  *
  * uq_probe_page_gather -- the FP4 decode kernel's memory traffic alone:
- *   the grid of uq_decode_attention for these arguments (one block of 4
- *   waves per (partition, kv head, sequence)), the same page walk through
- *   page_table, page-id copies and 2-slot LDS ring filled by the same copy
- *   instructions, every staged byte read back into registers, and no
- *   arithmetic beyond an XOR checksum (one uint32 per wave in `sink`).
- *   Arguments as uq_decode_attention (head size 128); sink_words >= 4 x
- *   partitions x num_kv_heads x batch, partitions = ceil(max_context /
+ *   the partition launch of uq_decode_attention for these arguments, run
+ *   as a probe: its grid (one block per partition, or one wave per
+ *   partition on the grid the library picks for many partitions; head
+ *   sizes 64, 128 and 256), page walk through page_table, page-id copies
+ *   and 2-slot LDS ring filled by the same copy instructions with the same
+ *   cache policy, every staged byte read back into registers, and no query
+ *   prologue, arithmetic or partial rows: each wave writes one uint32 XOR
+ *   checksum of what it staged to sink[4 * block + wave] (0 for a wave
+ *   without pages).  Arguments as uq_decode_attention; sink_words >= 4 x
+ *   partitions x num_kv_heads x batch (partitions = ceil(max_context /
  *   partition), the partition being partition_tokens or, for 0, the
- *   library's default for the shape; sink 16-byte aligned.
+ *   library's default for the shape) always suffices: 4 words per block of
+ *   the launch are written; sink 16-byte aligned.
  *   Errors: those of uq_decode_attention's argument checks;
- *   WORKSPACE_TOO_SMALL for a short sink; UNSUPPORTED for head sizes other
- *   than 128.
+ *   WORKSPACE_TOO_SMALL for a short sink.
+ *
+ * uq_probe_page_gather_cascade -- the same probe of uq_decode_cascade's
+ *   partition launch: the row list is written to `workspace` (sized as for
+ *   uq_decode_cascade) and the context and shared-prefix blocks stage their
+ *   pages as the cascade kernel does (the prefix pages with the default
+ *   cache policy).  sink_words >= 4 x (context blocks + prefix blocks),
+ *   context blocks = partitions x num_kv_heads x batch, prefix blocks =
+ *   num_kv_heads x ceil(batch x group / 16) x prefix partitions; rows
+ *   without work leave their 4 words 0.  Errors: those of
+ *   uq_decode_cascade's argument checks; WORKSPACE_TOO_SMALL for a short
+ *   sink.
  *
  * uq_probe_mfma -- n independent one-wave products D = A x B of one matrix
  *   instruction on given operand bytes, in the instruction's lane layout:
@@ -608,6 +622,11 @@ uq_status uq_probe_page_gather(const uq_cache_desc *desc, int32_t batch, int32_t
                                const uint8_t *kv_codes, const uint8_t *kv_scales, const int32_t *page_table,
                                int32_t max_pages_per_seq, const int32_t *context_lens, int32_t max_context,
                                int32_t partition_tokens, uint32_t *sink, size_t sink_words, void *stream);
+uq_status uq_probe_page_gather_cascade(const uq_cache_desc *desc, int32_t batch, int32_t num_q_heads,
+                                       const uint8_t *kv_codes, const uint8_t *kv_scales, const int32_t *page_table,
+                                       int32_t max_pages_per_seq, const int32_t *context_lens, int32_t max_context,
+                                       const uq_shared_prefix *prefix, int32_t partition_tokens, void *workspace,
+                                       size_t workspace_bytes, uint32_t *sink, size_t sink_words, void *stream);
 uq_status uq_probe_mfma(int32_t kind, const void *a, const void *b, const uint8_t *scale_a, const uint8_t *scale_b,
                         int32_t n, float *d, void *stream);
 
@@ -620,7 +639,7 @@ uq_status uq_probe_mfma(int32_t kind, const void *a, const void *b, const uint8_
  * kernel (by uq_decode_attention, uq_decode_partials,
  * uq_decode_step(_partials), the cascade calls or their comparison-cache
  * forms), of the quantize-on-write kernel (uq_quantize_kv) or of a bandwidth
- * probe (uq_probe_stream_read, uq_probe_page_gather) made from the calling
+ * probe (uq_probe_stream_read, uq_probe_page_gather(_cascade)) made from the calling
  * host thread is dispatched with hipExtLaunchKernel, which sets
  * `start` and `stop` (hipEvent_t, created by the caller, not owned by the
  * library) to that kernel's own start and end; hipEventElapsedTime(start,

@@ -148,6 +148,7 @@ uq_status make_decode_params(const uq_cache_desc* desc, const void* q, uq_dtype 
     p.suffix_partitions = int32_t(np_ctx);
     p.allow_wave_parts = 1;
     p.wave_parts = 0;
+    p.probe_sink = nullptr;
     return UQ_OK;
 }
 
@@ -939,9 +940,24 @@ uq_status uq_probe_page_gather(const uq_cache_desc* desc, int32_t batch, int32_t
                                max_pages_per_seq, context_lens, max_context, 1.0f, partition_tokens, sink, ws, sink,
                                UQ_F32, p);
     if (s != UQ_OK) return s;
-    if (desc->head_dim != kHeadDim) return UQ_ERR_UNSUPPORTED;
-    const size_t need = size_t(4) * size_t(p.num_partitions) * size_t(p.num_kv_heads) * size_t(batch);
-    if (sink_words < need) return UQ_ERR_WORKSPACE_TOO_SMALL;
+    if (sink_words < size_t(4) * size_t(uq::partition_blocks(p))) return UQ_ERR_WORKSPACE_TOO_SMALL;
+    return from_hip(uq::launch_gather_probe(p, sink, static_cast<hipStream_t>(stream)));
+}
+
+uq_status uq_probe_page_gather_cascade(const uq_cache_desc* desc, int32_t batch, int32_t num_q_heads,
+                                       const uint8_t* kv_codes, const uint8_t* kv_scales, const int32_t* page_table,
+                                       int32_t max_pages_per_seq, const int32_t* context_lens, int32_t max_context,
+                                       const uq_shared_prefix* prefix, int32_t partition_tokens, void* workspace,
+                                       size_t workspace_bytes, uint32_t* sink, size_t sink_words, void* stream) {
+    // the cascade call's own checks (the sink stands in for the query and the
+    // output; the workspace receives the row list)
+    uq::DecodeParams p;
+    uq_status s = cascade_setup(desc, sink, UQ_F32, nullptr, nullptr, UQ_F32, batch, num_q_heads,
+                                const_cast<uint8_t*>(kv_codes), const_cast<uint8_t*>(kv_scales), page_table,
+                                max_pages_per_seq, context_lens, max_context, prefix, 1.0f, partition_tokens, workspace,
+                                workspace_bytes, sink, UQ_F32, p);
+    if (s != UQ_OK) return s;
+    if (sink_words < size_t(4) * size_t(uq::partition_blocks(p))) return UQ_ERR_WORKSPACE_TOO_SMALL;
     return from_hip(uq::launch_gather_probe(p, sink, static_cast<hipStream_t>(stream)));
 }
 

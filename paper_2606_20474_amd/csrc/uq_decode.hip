@@ -765,10 +765,24 @@ __device__ __forceinline__ void zero_token(StageRegs<kTq4>& c, int pg, int t) {
     else m.w = 0u;
 }
 
-template <int F, int S, bool WP>
+// XOR of every 32-bit word of a stage's registers (the page-gather probe's
+// checksum).
+template <class R>
+__device__ __forceinline__ uint32_t fold_words(const R& r) {
+    static_assert(sizeof(R) % 4 == 0, "register words");
+    struct Words { uint32_t w[sizeof(R) / 4]; };
+    const Words x = __builtin_bit_cast(Words, r);
+    uint32_t a = 0u;
+#pragma unroll
+    for (int i = 0; i < int(sizeof(R) / 4); ++i) a ^= x.w[i];
+    return a;
+}
+
+template <int F, int S, bool WP, bool PROBE = false>
 __global__ void __launch_bounds__(64 * Fmt<F>::kWaves)
 __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decode_kernel(DecodeParams p) {
     static_assert(S == 2 || S == 4, "ring slots");
+    static_assert(!PROBE || is_fp4<F>(), "the page-gather probe follows the FP4 kernels");
     static_assert(!WP || (head_dim_of<F>() == 128 && F != kFp4d64x2), "one wave per partition: head size 128");
     constexpr int W = Fmt<F>::kWaves;
     constexpr int kThreads = 64 * W;
@@ -812,6 +826,13 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
     // partitions of 128k contexts: 6.13 ms against 6.73 ms for one block
     // per partition).
     const int lin = blockIdx.x;
+    // PROBE: the page-gather probe -- this grid, page walk, page-id copies,
+    // ring copies and LDS reads, with the query prologue, the arithmetic and
+    // the epilogue left out; each wave writes one XOR checksum of what it
+    // staged to probe_sink[block * W + wave] (0 for a wave without pages).
+    if constexpr (PROBE) {
+        if ((threadIdx.x & 63) == 0) p.probe_sink[int64_t(lin) * W + (threadIdx.x >> 6)] = 0u;
+    }
     const bool cascade = !WP && p.prefix_pages != nullptr;
     const int units = kPair ? p.num_kv_heads / 2 : p.num_kv_heads;   // kv heads, or pairs of them
     const int hk = lin % units;
@@ -861,7 +882,7 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
         }
         if ((WP ? first_part * p.partition_tokens : start) >= ctx) {
             // nothing of this sequence here; an empty context still gets its zero output
-            if (ctx <= 0 && first_part == 0) {
+            if (!PROBE && ctx <= 0 && first_part == 0) {
                 // the block's query heads: G of kv head hk, or 2 G of the pair
                 for (int r = tid >> 4; r < (kPair ? 2 : 1) * G; r += kThreads / 16) {
                     float z[N];
@@ -909,7 +930,7 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
     const int pos_new = ctx - 1;
     const int it_new = (pos_new - start) >> 5;                       // iteration holding the token
     // (the step is a head-size-128 call)
-    const bool append = D == 128 && !pre && p.k_new != nullptr && pos_new >= start && pos_new < end &&
+    const bool append = !PROBE && D == 128 && !pre && p.k_new != nullptr && pos_new >= start && pos_new < end &&
                         (WP || wave == it_new % W);
     const int k_new_local = WP ? it_new : it_new / W;                // that wave's local iteration
 
@@ -933,7 +954,7 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
         int rb, rhq;
         if constexpr (D != 128) {
             // head sizes 64 and 256: an F32, BF16 or F16 query, N channels per thread
-            if (qr < 16 && row_of(qr, rb, rhq)) {
+            if (!PROBE && qr < 16 && row_of(qr, rb, rhq)) {
                 const int64_t elem = (int64_t(rb) * p.num_q_heads + rhq) * D + N * qL;
                 float (&x)[N] = qx[h];
                 if constexpr (N == 4) {
@@ -956,7 +977,7 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
                 }
             }
         } else {
-          if (qr < 16 && row_of(qr, rb, rhq)) {
+          if (!PROBE && qr < 16 && row_of(qr, rb, rhq)) {
             const int64_t elem = (int64_t(rb) * p.num_q_heads + rhq) * kHeadDim + 8 * qL;
             if (p.q_dtype == 3) {
                 const uint2 w = *reinterpret_cast<const uint2*>(static_cast<const uint8_t*>(p.q) + elem);
@@ -1049,7 +1070,7 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
 
     // ---------------- query prologue: transform and store in B-operand order
 #pragma unroll
-    for (int h = 0; h < kQRounds; ++h) {
+    for (int h = 0; h < (PROBE ? 0 : kQRounds); ++h) {
         const int qr = (tid >> 4) + h * (kThreads / 16);
         const int qL = tid & 15;
         int rb, rhq;
@@ -1130,7 +1151,7 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
             *reinterpret_cast<uint2*>(q_lds + (g * 16 + qr) * 32 + e0) = make_uint2(lo, hi);
         }
     }
-    __syncthreads();
+    if constexpr (!PROBE) __syncthreads();
     QOperand<regs_fmt<F>()> qop;
     if constexpr (F == kBf16 || F == kTq4) {
 #pragma unroll
@@ -1181,6 +1202,7 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
 #pragma unroll
     for (int j = 0; j < kAccTiles; ++j) acc[j] = v4f{0.f, 0.f, 0.f, 0.f};
 
+    uint32_t chk = 0u;   // PROBE: XOR of every staged word
     // ---------------- main loop: one stage (2 pages, 32 tokens) per iteration
     for (int k = 0; k < n_local; ++k) {
         // stage k has landed once at most the later stages' copies are outstanding
@@ -1219,6 +1241,11 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
             else
                 stage_issue<F, kPageStream>(ring + slot * kStage, p.codes, p.scales,
                                             id0 * tiles_per_page + head_tile, id1 * tiles_per_page + head_tile, lane);
+        }
+
+        if constexpr (PROBE) {
+            chk ^= fold_words(c);
+            continue;
         }
 
         // ---- QK^T: raw scores (the softmax scale is applied in the exponent)
@@ -1354,6 +1381,12 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
         }
     }
 
+    if constexpr (PROBE) {
+#pragma unroll
+        for (int s = 1; s < 64; s <<= 1) chk ^= uint32_t(__shfl_xor(int(chk), s));
+        if (lane == 0) p.probe_sink[int64_t(lin) * W + wave] = chk;
+        return;
+    }
     const float l_run = acc_l[0];   // the column sum, in every lane of the column
     // ---------------- merge the waves through LDS (the rings are free now).
     // WP: the block's W partitions (an idle wave holds m = kNoMax, l = 0 and
@@ -1905,87 +1938,6 @@ __global__ void __launch_bounds__(256) merge_kernel(DecodeParams p) {
     write_out<N>(p, int64_t(b) * p.num_q_heads + hq, L, o);
 }
 
-// Bandwidth probe of the FP4 decode kernel's page gather: the same grid
-// (one block of 4 waves per (partition, kv head, sequence), kv head fastest),
-// the same page walk, page-id chunks and 2-slot LDS ring filled by the same
-// global_load_lds_dwordx4 copies, and every staged byte read back into
-// registers as the decode kernel reads it, but no arithmetic on it beyond an
-// XOR into a checksum (one word per wave in `sink`).  Its time is the time
-// the decode kernel's memory traffic alone takes on this GPU.  WP: the
-// one-wave-per-partition grid of the decode kernel.
-template <bool WP>
-__global__ void __launch_bounds__(256) gather_probe_kernel(DecodeParams p, uint32_t* __restrict__ sink) {
-    constexpr int W = 4, S = 2;
-    constexpr int kStage = stage_bytes<kFp4>();
-    const int lin = blockIdx.x;
-    const int hk = lin % p.num_kv_heads;
-    const int row = lin / p.num_kv_heads;
-    const int b = row % p.batch;
-    const int tid = threadIdx.x;
-    const int lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int part = WP ? (row / p.batch) * W + wave : row / p.batch;
-    constexpr int ws = WP ? 1 : W;
-    const int woff = WP ? 0 : wave;
-    int ctx = p.context_lens[b];
-    ctx = ctx < p.max_context ? ctx : p.max_context;
-    const int start = part * p.partition_tokens;
-    const int end = (start + p.partition_tokens) < ctx ? (start + p.partition_tokens) : ctx;
-    __shared__ __attribute__((aligned(16))) uint8_t smem[W * ring_bytes<kFp4, S>()];
-    __shared__ __attribute__((aligned(16))) uint8_t ids_lds[W * kIdsSlot];
-    uint32_t acc = 0u;
-    const int n_pages = start < end ? (end - start + 15) >> 4 : 0;
-    const int n_iter = (n_pages + 1) >> 1;
-    const int n_local = WP ? n_iter : wave < n_iter ? (n_iter - wave + W - 1) / W : 0;
-    if (n_local > 0) {
-        const int first_page = start >> 4;
-        const int32_t* pt_row = p.page_table + int64_t(b) * p.max_pages_per_seq;
-        uint8_t* ring = smem + wave * ring_bytes<kFp4, S>();
-        const uint32_t ring_addr = uint32_t(reinterpret_cast<uintptr_t>((lds_ptr_t)ring));
-        uint8_t* ids_slot = ids_lds + wave * kIdsSlot;
-        const uint32_t ids_addr = uint32_t(reinterpret_cast<uintptr_t>((lds_ptr_t)ids_slot));
-        const int64_t head_tile = int64_t(hk) * 2;
-        const int64_t tiles_per_page = int64_t(p.num_kv_heads) * 2;
-        int32_t ids = load_page_ids<ws>(pt_row, first_page, n_pages, woff, 0, lane);
-        if (n_local > 32) copy_page_ids<ws>(ids_slot, pt_row, first_page, n_pages, woff, 1, lane);
-        __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
-        ids = clamp_ids(ids, p.num_pages);
-        for (int s = 0; s < S && s < n_local; ++s) {
-            const int64_t id0 = __builtin_amdgcn_readlane(ids, 2 * s);
-            const int64_t id1 = __builtin_amdgcn_readlane(ids, 2 * s + 1);
-            stage_issue<kFp4>(ring + s * kStage, p.codes, p.scales, id0 * tiles_per_page + head_tile,
-                              id1 * tiles_per_page + head_tile, lane);
-        }
-        for (int k = 0; k < n_local; ++k) {
-            if (k + 1 < n_local) wait_vmem<dma_per_stage<kFp4>()>();
-            else wait_vmem<0>();
-            const uint32_t slot = uint32_t(k & (S - 1));
-            StageRegs<kFp4> c;
-            stage_read(c, ring_addr + slot * kStage, lane);
-            if (k + S < n_local) {
-                const int kn = k + S;
-                if ((kn & 31) == 0) {
-                    ids = clamp_ids(read_page_ids(ids_addr, lane), p.num_pages);
-                    if (kn + 32 < n_local)
-                        copy_page_ids<ws>(ids_slot, pt_row, first_page, n_pages, woff, (kn >> 5) + 1, lane);
-                }
-                const int s2 = 2 * (kn & 31);
-                const int64_t id0 = __builtin_amdgcn_readlane(ids, s2);
-                const int64_t id1 = __builtin_amdgcn_readlane(ids, s2 + 1);
-                stage_issue<kFp4>(ring + slot * kStage, p.codes, p.scales, id0 * tiles_per_page + head_tile,
-                                  id1 * tiles_per_page + head_tile, lane);
-            }
-#pragma unroll
-            for (int pg = 0; pg < 2; ++pg)
-                acc ^= c.k[pg].x ^ c.k[pg].y ^ c.k[pg].z ^ c.k[pg].w ^ c.v[pg].x ^ c.v[pg].y ^ c.v[pg].z ^
-                       c.v[pg].w ^ c.ks[pg] ^ c.vs[pg];
-        }
-    }
-#pragma unroll
-    for (int s = 1; s < 64; s <<= 1) acc ^= uint32_t(__shfl_xor(int(acc), s));
-    if (lane == 0) sink[int64_t(lin) * W + wave] = acc;
-}
-
 // The rows of a cascade launch in dispatch order (one block).  The tokens
 // of context row (part, b) are those of its partition after the prefix's
 // tokens and before the context end, as the decode kernel computes them.
@@ -2057,20 +2009,6 @@ __global__ void __launch_bounds__(1024) cascade_rows_kernel(DecodeParams p) {
     for (int i = total + PR + tid; i < R + PR; i += kClasses) p.cascade_rows[i] = make_int4(-1, 0, 0, 0);
 }
 
-static bool choose_wave_parts(const DecodeParams& p);
-
-hipError_t launch_gather_probe(const DecodeParams& p, uint32_t* sink, hipStream_t stream) {
-    // the grid the FP4 decode kernel takes for the same parameters
-    if (choose_wave_parts(p)) {
-        const dim3 grid{unsigned(int64_t((p.num_partitions + 3) / 4) * p.num_kv_heads * p.batch)};
-        launch_kernel(gather_probe_kernel<true>, grid, dim3(256), stream, p, sink);
-    } else {
-        const dim3 grid{unsigned(int64_t(p.num_partitions) * p.num_kv_heads * p.batch)};
-        launch_kernel(gather_probe_kernel<false>, grid, dim3(256), stream, p, sink);
-    }
-    return hipGetLastError();
-}
-
 // The grid of a partition launch: one wave per partition when there are
 // enough partitions for W per block and enough such blocks to give every CU
 // several (8 per CU: two full rounds at 4 blocks per CU), head size 128, no
@@ -2094,8 +2032,10 @@ static bool choose_wave_parts(const DecodeParams& p) {
 }
 
 // Two ring slots per wave: a 4-slot ring (twice the copies in flight, half
-// the blocks per CU) measured no faster on 32k contexts and slower on 16k.
-template <int F>
+// the blocks per CU) measured no faster on 32k contexts and slower on 16k,
+// also with the streaming page copies. PROBE: the same grid with the
+// page-gather probe of the kernel (FP4 formats).
+template <int F, bool PROBE = false>
 static hipError_t launch_partials(const DecodeParams& p, hipStream_t stream) {
     constexpr int kSlots = 2;
     static_assert(occupancy<F, kSlots>() == Fmt<F>::kOccupancy, "the LDS footprint lowers the occupancy");
@@ -2107,7 +2047,7 @@ static hipError_t launch_partials(const DecodeParams& p, hipStream_t stream) {
             constexpr int W = Fmt<F>::kWaves;
             pw.wave_parts = W;
             const dim3 grid{unsigned(int64_t((p.num_partitions + W - 1) / W) * units * p.batch)};
-            launch_kernel(decode_kernel<F, kSlots, true>, grid, dim3(64 * W), stream, pw);
+            launch_kernel(decode_kernel<F, kSlots, true, PROBE>, grid, dim3(64 * W), stream, pw);
             return hipGetLastError();
         }
     }
@@ -2116,8 +2056,24 @@ static hipError_t launch_partials(const DecodeParams& p, hipStream_t stream) {
         hipLaunchKernelGGL(cascade_rows_kernel, dim3(1), dim3(1024), 0, stream, p);
     }
     const dim3 grid{unsigned(int64_t(p.prefix_blocks) + int64_t(p.suffix_partitions) * units * p.batch)};
-    launch_kernel(decode_kernel<F, kSlots, false>, grid, dim3(64 * Fmt<F>::kWaves), stream, p);
+    launch_kernel(decode_kernel<F, kSlots, false, PROBE>, grid, dim3(64 * Fmt<F>::kWaves), stream, p);
     return hipGetLastError();
+}
+
+int64_t partition_blocks(const DecodeParams& p) {
+    const int64_t units = p.kv_fmt == kFp4d64x2 ? p.num_kv_heads / 2 : p.num_kv_heads;
+    if (choose_wave_parts(p)) return int64_t((p.num_partitions + 3) / 4) * units * p.batch;
+    return int64_t(p.prefix_blocks) + int64_t(p.suffix_partitions) * units * p.batch;
+}
+
+hipError_t launch_gather_probe(const DecodeParams& p, uint32_t* sink, hipStream_t stream) {
+    DecodeParams pp = p;
+    pp.probe_sink = sink;
+    if (p.kv_fmt == kFp4d64) return launch_partials<kFp4d64, true>(pp, stream);
+    if (p.kv_fmt == kFp4d64x2) return launch_partials<kFp4d64x2, true>(pp, stream);
+    if (p.kv_fmt == kFp4d256) return launch_partials<kFp4d256, true>(pp, stream);
+    if (p.kv_fmt == kFp4) return launch_partials<kFp4, true>(pp, stream);
+    return hipErrorInvalidValue;
 }
 
 hipError_t launch_decode_partials(const DecodeParams& p, hipStream_t stream) {

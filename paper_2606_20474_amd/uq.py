@@ -40,7 +40,8 @@ EXPORTS = (
     "uq_ref_decode_step_partials", "uq_decode_cascade_workspace_bytes", "uq_decode_cascade",
     "uq_decode_cascade_partials", "uq_decode_cascade_merge", "uq_ref_decode_cascade",
     "uq_ref_decode_cascade_partials", "uq_ref_decode_cascade_merge", "uq_quantize_error", "uq_time_next_launch",
-    "uq_decode_attention_noalloc", "uq_decode_attention_scaled_pv", "uq_probe_stream_read", "uq_probe_page_gather", "uq_probe_mfma",
+    "uq_decode_attention_noalloc", "uq_decode_attention_scaled_pv", "uq_probe_stream_read", "uq_probe_page_gather",
+    "uq_probe_page_gather_cascade", "uq_probe_mfma",
 )
 
 UQ_REF_FP8_E4M3, UQ_REF_BF16, UQ_REF_TQ4 = 1, 2, 3
@@ -122,6 +123,8 @@ def _load():
     L.uq_probe_stream_read.restype = i32
     L.uq_probe_page_gather.argtypes = [D, i32, i32, vp, vp, vp, i32, vp, i32, i32, vp, sz, vp]
     L.uq_probe_page_gather.restype = i32
+    L.uq_probe_page_gather_cascade.argtypes = [D, i32, i32, vp, vp, vp, i32, vp, i32, vp, i32, vp, sz, vp, sz, vp]
+    L.uq_probe_page_gather_cascade.restype = i32
     L.uq_probe_mfma.argtypes = [i32, vp, vp, vp, vp, i32, vp, vp]
     L.uq_probe_mfma.restype = i32
     for name in ("uq_decode_step", "uq_decode_step_partials"):
@@ -783,7 +786,9 @@ def probe_stream_read(buf, sink=None, stream=None):
 def probe_page_gather(desc: CacheDesc, num_q_heads, codes, scales, page_table, context_lens, max_context,
                       partition_tokens=0, sink=None, stream=None):
     """The FP4 decode kernel's page gather without its arithmetic, for the
-    same arguments; returns the per-wave checksum words."""
+    same arguments (head sizes 64, 128, 256); returns the per-wave checksum
+    words (4 per block of the launch; an allocated sink holds the bound
+    4 x partitions x kv heads x batch)."""
     B = context_lens.shape[0]
     _pools(desc, codes, scales)
     _table(page_table, context_lens, B)
@@ -797,6 +802,37 @@ def probe_page_gather(desc: CacheDesc, num_q_heads, codes, scales, page_table, c
                                   page_table.shape[1], _ptr(context_lens), max_context, partition_tokens, _ptr(sink),
                                   sink.numel(), _stream(stream))
     _check(st, "uq_probe_page_gather")
+    return sink
+
+
+def probe_page_gather_cascade(desc: CacheDesc, num_q_heads, codes, scales, page_table, context_lens, max_context,
+                              prefix: SharedPrefix, partition_tokens=0, workspace=None, sink=None, stream=None):
+    """The cascade decode kernel's page gather without its arithmetic, for
+    the same arguments; returns the per-wave checksum words. An allocated
+    sink holds an upper bound of the launch's blocks: the context blocks and
+    Hkv x ceil(B G / 16) x ceil(prefix tokens / 32) prefix blocks."""
+    B = context_lens.shape[0]
+    _pools(desc, codes, scales)
+    _table(page_table, context_lens, B)
+    _prefix(prefix, B)
+    if workspace is None:
+        n = cascade_workspace_bytes(desc.num_kv_heads, B, num_q_heads, max_context, prefix, partition_tokens)
+        workspace = torch.empty(n, dtype=torch.uint8, device=codes.device)
+    _need(workspace, "workspace", _U8)
+    part = partition_tokens or default_partition(desc, B, num_q_heads, max_context)
+    G = num_q_heads // desc.num_kv_heads
+    blocks = (max(1, -(-max_context // part)) * desc.num_kv_heads * B
+              + desc.num_kv_heads * -(-B * G // 16) * max(1, -(-prefix.num_tokens // 32)))
+    if sink is None:
+        sink = torch.empty(4 * blocks, dtype=torch.int32, device=codes.device)
+    _need(sink, "sink", (torch.int32,), min_numel=1)
+    d = desc.c_struct()
+    sp = prefix.c_struct()
+    st = lib.uq_probe_page_gather_cascade(ctypes.byref(d), B, num_q_heads, _ptr(codes), _ptr(scales),
+                                          _ptr(page_table), page_table.shape[1], _ptr(context_lens), max_context,
+                                          ctypes.byref(sp), partition_tokens, _ptr(workspace), workspace.numel(),
+                                          _ptr(sink), sink.numel(), _stream(stream))
+    _check(st, "uq_probe_page_gather_cascade")
     return sink
 
 

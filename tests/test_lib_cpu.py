@@ -415,12 +415,31 @@ def test_probe_validation(uq):
         return L.uq_probe_page_gather(ctypes.byref(d), B, Hq, FAKE, FAKE, pt, mpps, FAKE, maxctx, part, FAKE,
                                       sink_words, None)
     assert gather(desc(head_dim=96)) == E.UQ_ERR_UNSUPPORTED
-    assert gather(desc(head_dim=64)) == E.UQ_ERR_UNSUPPORTED
     assert gather(desc(), Hq=3) == E.UQ_ERR_INVALID_ARGUMENT
     assert gather(desc(), maxctx=65) == E.UQ_ERR_INVALID_ARGUMENT
     assert gather(desc(), pt=None) == E.UQ_ERR_INVALID_ARGUMENT
     # 2 partitions x 2 kv heads x 2 sequences x 4 waves = 32 words
     assert gather(desc(), sink_words=31) == E.UQ_ERR_WORKSPACE_TOO_SMALL
+    # head size 64 at group size 2: two kv heads per block, 16 words; a
+    # valid call reaches the launch (a HIP error without a GPU)
+    assert gather(desc(head_dim=64), sink_words=15) == E.UQ_ERR_WORKSPACE_TOO_SMALL
+    assert gather(desc(head_dim=64), sink_words=16) == E.UQ_ERR_HIP
+
+    from paper_2606_20474_amd.uq import uq_shared_prefix
+
+    def cgather(sp, head_dim=128, sink_words=1 << 20, wsb=1 << 30):
+        return L.uq_probe_page_gather_cascade(ctypes.byref(desc(head_dim=head_dim)), 2, 4, FAKE, FAKE, FAKE, 4, FAKE,
+                                              64, ctypes.byref(sp) if sp is not None else None, 32, FAKE, wsb, FAKE,
+                                              sink_words, None)
+    sp = uq_shared_prefix(0x10000, 0x10000, 64, 32)
+    assert cgather(None) == E.UQ_ERR_INVALID_ARGUMENT
+    assert cgather(uq_shared_prefix(0x10000, 0x10000, 40, 0)) == E.UQ_ERR_INVALID_ARGUMENT
+    assert cgather(sp, head_dim=64) == E.UQ_ERR_UNSUPPORTED
+    assert cgather(sp, wsb=16) == E.UQ_ERR_WORKSPACE_TOO_SMALL
+    # 2 context partitions x 2 kv heads x 2 sequences + 2 kv heads x 1 column
+    # chunk x 2 prefix partitions = 12 blocks of 4 waves
+    assert cgather(sp, sink_words=47) == E.UQ_ERR_WORKSPACE_TOO_SMALL
+    assert cgather(sp, sink_words=48) == E.UQ_ERR_HIP
 
     def mfma(kind=0, a=FAKE, b=FAKE, sa=FAKE, sb=FAKE, n=1, d=FAKE):
         return L.uq_probe_mfma(kind, a, b, sa, sb, n, d, None)
