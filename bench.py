@@ -348,7 +348,8 @@ def achievable(uq, wl, desc, codes, scales, pt, ctx, part, alg_bytes, args, dev,
     kernel (flushed, kernel events): a plain stream of the launch's
     algorithmic bytes and of 4 GiB (uq_probe_stream_read), and the decode
     kernel's own page gather of this workload without its arithmetic
-    (uq_probe_page_gather: same grid, page walk, copies and LDS reads)."""
+    (uq_probe_page_gather, or uq_probe_page_gather_cascade for a workload
+    with a shared prefix: the kernel's own launch in its probe mode)."""
     import torch
     n = max(20, args.steps // 4)
     res = {}
