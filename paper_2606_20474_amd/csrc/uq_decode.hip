@@ -17,9 +17,11 @@
 //          token's norm; V is decoded with one fused multiply-add per
 //          element into BF16.
 //
-// decode_kernel<F, S>: one block of Fmt<F>::kWaves waves per (partition, kv
-// head, sequence), in an XCD-aware linear order (kv head fastest); S ring
-// slots per wave.
+// decode_kernel<F, S, WP, PROBE>: one block of Fmt<F>::kWaves waves per
+// (partition, kv head, sequence), in an XCD-aware linear order (kv head
+// fastest); S ring slots per wave; WP: one wave per partition (below);
+// PROBE: the same launch as the page-gather bandwidth probe (no query
+// prologue, arithmetic or epilogue).
 //   prologue  the block loads its G query heads (G <= 16), rotates them
 //             with the in-register WHT butterfly and casts them to FP8
 //             E4M3 (FP4 cache), casts them to FP8 (FP8 cache) or to BF16
