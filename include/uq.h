@@ -578,12 +578,14 @@ uq_status uq_decode_attention_noalloc(const uq_cache_desc *desc, const void *q, 
  *   and 2-slot LDS ring filled by the same copy instructions with the same
  *   cache policy, every staged byte read back into registers, and no query
  *   prologue, arithmetic or partial rows: each wave writes one uint32 XOR
- *   checksum of what it staged to sink[4 * block + wave] (0 for a wave
- *   without pages).  Arguments as uq_decode_attention; sink_words >= 4 x
- *   partitions x num_kv_heads x batch (partitions = ceil(max_context /
- *   partition), the partition being partition_tokens or, for 0, the
- *   library's default for the shape) always suffices: 4 words per block of
- *   the launch are written; sink 16-byte aligned.
+ *   checksum of what it staged to sink[W * block + wave] (0 for a wave
+ *   without pages; W, the waves per block, is 8 on a one-wave-per-partition
+ *   grid of blocks of 8 partitions, else 4).  Arguments as
+ *   uq_decode_attention; sink_words >= 4 x partitions x num_kv_heads x
+ *   batch (partitions = ceil(max_context / partition), the partition being
+ *   partition_tokens or, for 0, the library's default for the shape) always
+ *   suffices: W words per block of the launch are written; sink 16-byte
+ *   aligned.
  *   Errors: those of uq_decode_attention's argument checks;
  *   WORKSPACE_TOO_SMALL for a short sink.
  *

@@ -940,7 +940,7 @@ uq_status uq_probe_page_gather(const uq_cache_desc* desc, int32_t batch, int32_t
                                max_pages_per_seq, context_lens, max_context, 1.0f, partition_tokens, sink, ws, sink,
                                UQ_F32, p);
     if (s != UQ_OK) return s;
-    if (sink_words < size_t(4) * size_t(uq::partition_blocks(p))) return UQ_ERR_WORKSPACE_TOO_SMALL;
+    if (sink_words < size_t(uq::probe_words(p))) return UQ_ERR_WORKSPACE_TOO_SMALL;
     return from_hip(uq::launch_gather_probe(p, sink, static_cast<hipStream_t>(stream)));
 }
 
@@ -957,7 +957,7 @@ uq_status uq_probe_page_gather_cascade(const uq_cache_desc* desc, int32_t batch,
                                 max_pages_per_seq, context_lens, max_context, prefix, 1.0f, partition_tokens, workspace,
                                 workspace_bytes, sink, UQ_F32, p);
     if (s != UQ_OK) return s;
-    if (sink_words < size_t(4) * size_t(uq::partition_blocks(p))) return UQ_ERR_WORKSPACE_TOO_SMALL;
+    if (sink_words < size_t(uq::probe_words(p))) return UQ_ERR_WORKSPACE_TOO_SMALL;
     return from_hip(uq::launch_gather_probe(p, sink, static_cast<hipStream_t>(stream)));
 }
 

@@ -17,11 +17,12 @@
 //          token's norm; V is decoded with one fused multiply-add per
 //          element into BF16.
 //
-// decode_kernel<F, S, WP, PROBE>: one block of Fmt<F>::kWaves waves per
-// (partition, kv head, sequence), in an XCD-aware linear order (kv head
-// fastest); S ring slots per wave; WP: one wave per partition (below);
-// PROBE: the same launch as the page-gather bandwidth probe (no query
-// prologue, arithmetic or epilogue).
+// decode_kernel<F, S, WP, PROBE, W>: one block of W waves per (partition,
+// kv head, sequence), in an XCD-aware linear order (kv head fastest); S ring
+// slots per wave; WP: one wave per partition (below); PROBE: the same launch
+// as the page-gather bandwidth probe (no query prologue, arithmetic or
+// epilogue); W: the format's kWaves, or 8 on the wave grid of the FP4 and
+// FP8 caches (see launch_waves).
 //   prologue  the block loads its G query heads (G <= 16), rotates them
 //             with the in-register WHT butterfly and casts them to FP8
 //             E4M3 (FP4 cache), casts them to FP8 (FP8 cache) or to BF16
@@ -75,8 +76,9 @@ constexpr int kWaitVmcnt0 = 0x0F70;    // s_waitcnt vmcnt(0) expcnt(7) lgkmcnt(1
 // Per-format constants.  kTile: bytes of one (page, kv head) K or V tile;
 // kScaleBlock: scale bytes per (page, kv head) for K and V together.
 template <int F> struct Fmt;
-// kWaves: waves per block; kOccupancy: waves per SIMD the LDS footprint
-// allows (160 KiB per CU), which sets the register budget.
+// kWaves: waves per block (the FP4 and FP8 caches run blocks of 8 waves on
+// the wave grid, see launch_waves); kOccupancy: waves per SIMD the LDS footprint allows
+// (160 KiB per CU), which sets the register budget.
 template <> struct Fmt<kFp4> {
     static constexpr int kTile = 1024;
     static constexpr int kScaleBlock = 2 * kTileScales;
@@ -149,14 +151,14 @@ template <int F> constexpr int q_lds_bytes() {
     return (F == kBf16 || F == kTq4) ? 4 * 64 * 16 : (head_dim_of<F>() / 128 + (head_dim_of<F>() < 128)) * 64 * 32;
 }
 constexpr int kIdsSlot = 256;   // LDS bytes per wave for the next 64 page ids
-template <int F, int S> constexpr int block_lds_bytes() {
-    return Fmt<F>::kWaves * (ring_bytes<F, S>() + kIdsSlot) + q_lds_bytes<F>() + 2 * Fmt<F>::kWaves * 16 * 4;
+template <int F, int S, int W = Fmt<F>::kWaves> constexpr int block_lds_bytes() {
+    return W * (ring_bytes<F, S>() + kIdsSlot) + q_lds_bytes<F>() + 2 * W * 16 * 4;
 }
-// Waves per SIMD with an S-slot ring: what 160 KiB of LDS per CU holds,
-// capped by the format's register-set budget.
-template <int F, int S> constexpr int occupancy() {
-    constexpr int blocks = (160 * 1024) / block_lds_bytes<F, S>();
-    constexpr int waves = blocks * Fmt<F>::kWaves / 4;
+// Waves per SIMD with an S-slot ring and W waves per block: what 160 KiB of
+// LDS per CU holds, capped by the format's register-set budget.
+template <int F, int S, int W = Fmt<F>::kWaves> constexpr int occupancy() {
+    constexpr int blocks = (160 * 1024) / block_lds_bytes<F, S, W>();
+    constexpr int waves = blocks * W / 4;
     return waves < 1 ? 1 : (waves < Fmt<F>::kOccupancy ? waves : Fmt<F>::kOccupancy);
 }
 template <int F> constexpr int dma_per_stage() { return 4 * Fmt<F>::kTile / 1024 + (Fmt<F>::kScaleBlock ? 1 : 0); }
@@ -780,16 +782,16 @@ __device__ __forceinline__ uint32_t fold_words(const R& r) {
     return a;
 }
 
-template <int F, int S, bool WP, bool PROBE = false>
-__global__ void __launch_bounds__(64 * Fmt<F>::kWaves)
-__attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decode_kernel(DecodeParams p) {
+template <int F, int S, bool WP, bool PROBE = false, int W = Fmt<F>::kWaves>
+__global__ void __launch_bounds__(64 * W)
+__attribute__((amdgpu_waves_per_eu(occupancy<F, S, W>(), occupancy<F, S, W>()))) decode_kernel(DecodeParams p) {
     static_assert(S == 2 || S == 4, "ring slots");
+    static_assert(W == 2 || W == 4 || W == 8, "waves per block");
     static_assert(!PROBE || is_fp4<F>(), "the page-gather probe follows the FP4 kernels");
     static_assert(!WP || (head_dim_of<F>() == 128 && F != kFp4d64x2), "one wave per partition: head size 128");
-    constexpr int W = Fmt<F>::kWaves;
     constexpr int kThreads = 64 * W;
     constexpr int kStage = stage_bytes<F>();
-    constexpr int kQRounds = 256 / kThreads;   // 16 threads per query row, 16 rows
+    constexpr int kQRounds = (256 + kThreads - 1) / kThreads;   // 16 threads per query row, 16 rows
     constexpr int D = head_dim_of<F>();         // head size
     constexpr int N = D / 16;                   // channels per lane of a 16-lane row
     constexpr bool kPair = F == kFp4d64x2;      // two kv heads of 64 per block
@@ -1074,9 +1076,13 @@ __attribute__((amdgpu_waves_per_eu(occupancy<F, S>(), occupancy<F, S>()))) decod
 #pragma unroll
     for (int h = 0; h < (PROBE ? 0 : kQRounds); ++h) {
         const int qr = (tid >> 4) + h * (kThreads / 16);
+        // blocks of more than 4 waves: the threads past the 16 query rows
+        // store nothing (their rows would land on other rows' operand bytes
+        // and past the operand area); whole waves, so a scalar branch
+        if (qr >= 16) continue;
         const int qL = tid & 15;
         int rb, rhq;
-        const bool qvalid = qr < 16 && row_of(qr, rb, rhq);
+        const bool qvalid = row_of(qr, rb, rhq);
         if constexpr (F == kBf16 || F == kTq4) {
             // channels 8*qL..+7 are k-step qL/4, lane (qL%4)*16 + qr, 16 bytes
             uint4 w = {0u, 0u, 0u, 0u};
@@ -2011,62 +2017,83 @@ __global__ void __launch_bounds__(1024) cascade_rows_kernel(DecodeParams p) {
     for (int i = total + PR + tid; i < R + PR; i += kClasses) p.cascade_rows[i] = make_int4(-1, 0, 0, 0);
 }
 
-// The grid of a partition launch: one wave per partition when there are
-// enough partitions for W per block and enough such blocks to give every CU
-// several (8 per CU: two full rounds at 4 blocks per CU), head size 128, no
-// cascade; else one block per partition.  The merge launch makes the same
-// choice from the same parameters.
-static int waves_of(int32_t kv_fmt) {
-    switch (kv_fmt) {
-        case kFp8: return Fmt<kFp8>::kWaves;
-        case kBf16: return Fmt<kBf16>::kWaves;
-        case kTq4: return Fmt<kTq4>::kWaves;
-        default: return Fmt<kFp4>::kWaves;
-    }
-}
-static bool choose_wave_parts(const DecodeParams& p) {
+// Waves per block of a partition launch (the grid choice below, the merge
+// launch and the probe's sink words follow it).  The FP4 and FP8 caches at
+// head size 128: 8 on the wave grid when it has enough blocks of 8
+// partitions (fewer block prologues and partial writes per partition: 3 %
+// faster on 128k contexts in 4096-token partitions), else the format's
+// kWaves (4), which measured equal on 32k contexts and 2 % faster on the
+// MiniMax-like cascade than blocks of 8.  Others: the format's kWaves.
+static bool wave_grid_with(const DecodeParams& p, int W) {
     if (!p.allow_wave_parts || p.prefix_pages != nullptr || p.head_dim != kHeadDim) return false;
     if (p.kv_fmt != kFp4 && p.kv_fmt != kFp8 && p.kv_fmt != kBf16 && p.kv_fmt != kTq4) return false;
-    const int W = waves_of(p.kv_fmt);
     if (p.num_partitions < W) return false;
     const int64_t blocks = int64_t(p.batch) * p.num_kv_heads * ((p.num_partitions + W - 1) / W);
     return blocks >= 8 * kNumCus;
 }
+static int launch_waves(const DecodeParams& p) {
+    switch (p.kv_fmt) {
+        case kFp8: return wave_grid_with(p, 8) ? 8 : Fmt<kFp8>::kWaves;
+        case kBf16: return Fmt<kBf16>::kWaves;
+        case kTq4: return Fmt<kTq4>::kWaves;
+        case kFp4d64: return Fmt<kFp4d64>::kWaves;
+        case kFp4d64x2: return Fmt<kFp4d64x2>::kWaves;
+        case kFp4d256: return Fmt<kFp4d256>::kWaves;
+        default: return wave_grid_with(p, 8) ? 8 : Fmt<kFp4>::kWaves;
+    }
+}
+// The grid of a partition launch: one wave per partition when there are
+// enough partitions for W per block and enough such blocks to give every CU
+// several (at least 8 per CU), head size 128, no cascade; else one block per
+// partition.  The merge launch makes the same choice from the same
+// parameters.
+static bool choose_wave_parts(const DecodeParams& p) { return wave_grid_with(p, launch_waves(p)); }
 
 // Two ring slots per wave: a 4-slot ring (twice the copies in flight, half
 // the blocks per CU) measured no faster on 32k contexts and slower on 16k,
 // also with the streaming page copies. PROBE: the same grid with the
 // page-gather probe of the kernel (FP4 formats).
+constexpr int kRingSlots = 2;
+// The wave grid with W waves (partitions) per block.
+template <int F, bool PROBE, int W>
+static hipError_t launch_wave_grid(const DecodeParams& p, hipStream_t stream) {
+    static_assert(occupancy<F, kRingSlots, W>() == Fmt<F>::kOccupancy, "the LDS footprint lowers the occupancy");
+    DecodeParams pw = p;
+    pw.wave_parts = W;
+    const dim3 grid{unsigned(int64_t((p.num_partitions + W - 1) / W) * p.num_kv_heads * p.batch)};
+    launch_kernel(decode_kernel<F, kRingSlots, true, PROBE, W>, grid, dim3(64 * W), stream, pw);
+    return hipGetLastError();
+}
 template <int F, bool PROBE = false>
 static hipError_t launch_partials(const DecodeParams& p, hipStream_t stream) {
-    constexpr int kSlots = 2;
-    static_assert(occupancy<F, kSlots>() == Fmt<F>::kOccupancy, "the LDS footprint lowers the occupancy");
-    const int64_t units = F == kFp4d64x2 ? p.num_kv_heads / 2 : p.num_kv_heads;
-    constexpr bool kWaveOk = head_dim_of<F>() == 128 && F != kFp4d64x2;
-    if constexpr (kWaveOk) {
+    constexpr int W = Fmt<F>::kWaves;
+    static_assert(occupancy<F, kRingSlots, W>() == Fmt<F>::kOccupancy, "the LDS footprint lowers the occupancy");
+    if constexpr (head_dim_of<F>() == 128 && F != kFp4d64x2) {
         if (choose_wave_parts(p)) {
-            DecodeParams pw = p;
-            constexpr int W = Fmt<F>::kWaves;
-            pw.wave_parts = W;
-            const dim3 grid{unsigned(int64_t((p.num_partitions + W - 1) / W) * units * p.batch)};
-            launch_kernel(decode_kernel<F, kSlots, true, PROBE>, grid, dim3(64 * W), stream, pw);
-            return hipGetLastError();
+            if constexpr (F == kFp4 || F == kFp8) {
+                if (launch_waves(p) == 8) return launch_wave_grid<F, PROBE, 8>(p, stream);
+            }
+            return launch_wave_grid<F, PROBE, W>(p, stream);
         }
     }
     if (p.prefix_pages != nullptr) {
         // the cascade's row list first (a plain launch: the timing hook is the partition kernel's)
         hipLaunchKernelGGL(cascade_rows_kernel, dim3(1), dim3(1024), 0, stream, p);
     }
+    const int64_t units = F == kFp4d64x2 ? p.num_kv_heads / 2 : p.num_kv_heads;
     const dim3 grid{unsigned(int64_t(p.prefix_blocks) + int64_t(p.suffix_partitions) * units * p.batch)};
-    launch_kernel(decode_kernel<F, kSlots, false, PROBE>, grid, dim3(64 * Fmt<F>::kWaves), stream, p);
+    launch_kernel(decode_kernel<F, kRingSlots, false, PROBE, W>, grid, dim3(64 * W), stream, p);
     return hipGetLastError();
 }
 
 int64_t partition_blocks(const DecodeParams& p) {
     const int64_t units = p.kv_fmt == kFp4d64x2 ? p.num_kv_heads / 2 : p.num_kv_heads;
-    if (choose_wave_parts(p)) return int64_t((p.num_partitions + 3) / 4) * units * p.batch;
+    const int W = launch_waves(p);
+    if (choose_wave_parts(p)) return int64_t((p.num_partitions + W - 1) / W) * units * p.batch;
     return int64_t(p.prefix_blocks) + int64_t(p.suffix_partitions) * units * p.batch;
 }
+
+int64_t probe_words(const DecodeParams& p) { return int64_t(launch_waves(p)) * partition_blocks(p); }
 
 hipError_t launch_gather_probe(const DecodeParams& p, uint32_t* sink, hipStream_t stream) {
     DecodeParams pp = p;
@@ -2091,7 +2118,7 @@ hipError_t launch_decode_partials(const DecodeParams& p, hipStream_t stream) {
 hipError_t launch_decode_merge(const DecodeParams& p, hipStream_t stream) {
     if (p.num_partitions <= 1 && p.prefix_pages == nullptr) return hipSuccess;   // every sequence was finished in place
     DecodeParams pm = p;
-    pm.wave_parts = choose_wave_parts(p) ? waves_of(p.kv_fmt) : 0;
+    pm.wave_parts = choose_wave_parts(p) ? launch_waves(p) : 0;
     const dim3 grid{unsigned(p.num_kv_heads), unsigned(p.batch)};
     if (p.head_dim == 64) hipLaunchKernelGGL(merge_kernel<64>, grid, dim3(256), 0, stream, pm);
     else if (p.head_dim == 256) hipLaunchKernelGGL(merge_kernel<256>, grid, dim3(256), 0, stream, pm);

@@ -120,7 +120,7 @@ struct DecodeParams {
     int32_t allow_wave_parts;
     int32_t wave_parts;
     // the page-gather probe's checksums, one per wave of the partition
-    // launch (set only by launch_gather_probe)
+    // launch, sink[block * W + wave] (set only by launch_gather_probe)
     uint32_t* probe_sink;
 };
 
@@ -147,9 +147,10 @@ hipError_t launch_decode_partials_mxpv(const DecodeParams& p, hipStream_t stream
 // measurement probes
 // The FP4 partition launch for these parameters as a page-gather probe
 // (its grid, page walk and copies, no arithmetic); partition_blocks: the
-// blocks of that launch (4 checksum words each).
+// blocks of that launch; probe_words: its checksum words (one per wave).
 hipError_t launch_gather_probe(const DecodeParams& p, uint32_t* sink, hipStream_t stream);
 int64_t partition_blocks(const DecodeParams& p);
+int64_t probe_words(const DecodeParams& p);
 hipError_t launch_stream_read_probe(const void* buf, int64_t n16, uint32_t* sink, int blocks, hipStream_t stream);
 hipError_t launch_mfma_probe(int kind, const void* a, const void* b, const uint8_t* scale_a, const uint8_t* scale_b,
                              int n, float* d, hipStream_t stream);

@@ -316,6 +316,21 @@ def test_decode_group_sizes(uq, hq, hkv):
     check_attention(out, ref, f"groups {hq}/{hkv}")
 
 
+def test_decode_long_partition_waves_reload_ids(uq):
+    """Partitions of 16384 tokens: each of a block's waves walks more than
+    32 page pairs, so it takes its later page ids from its LDS slot; a group
+    of 16 fills every query row of the block.  One context held whole by one
+    block, one split over two partitions, one ragged; against the oracle."""
+    dev = torch.device("cuda:0")
+    wl = workloads.custom(3, 16, 1, [16384, 20000, 9001], seed=41, paging="random")
+    log("decode 16384-token partitions, G=16")
+    desc, codes, scales = gpu_cache(uq, wl, dev)
+    out = run_decode(uq, wl, desc, codes, scales, dev, partition=16384)
+    pools, pt = oracle_cache(wl, [0, 1, 2], dev)
+    ref = oracle.decode_attention(wl.q.numpy(), pools, pt, wl.context_lens, 1, 1 / math.sqrt(128), True)
+    check_attention(out, ref, "16384-token partitions")
+
+
 def test_decode_minimax_full_size_sampled(uq):
     """B=64, Hq=48, Hkv=8, lognormal contexts 8k..128k, a 16k-token prefix
     shared by every sequence (shorter contexts own a copy of their last

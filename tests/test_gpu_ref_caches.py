@@ -281,6 +281,24 @@ def test_ref_decode_qwen_full_size_sampled(uq, fmt):
     check_attention(out1[seqs], reference(fmt, wl, seqs, dev), f"{fmt} qwen sampled", fmt)
 
 
+@pytest.mark.parametrize("fmt", ["fp8", "bf16"])
+def test_ref_cascade_long_rows(uq, fmt):
+    """Cascade over a 32-token prefix with 16384-token context partitions
+    (the FP8 cache runs its cascade with blocks of 8 waves): each wave of a
+    context row walks more than 32 page pairs and takes its later page ids
+    from its LDS slot; a group of 16 fills every query row of the block."""
+    dev = torch.device("cuda:0")
+    wl = workloads.custom(3, 16, 1, [16384, 20000, 9001], seed=42, paging="random", shared_prefix_tokens=32)
+    log(f"ref cascade {fmt}, 16384-token partitions, G=16")
+    desc, cache = gpu_cache(uq, fmt, wl, dev)
+    pre = uq.SharedPrefix(torch.as_tensor(wl.prefix_pages.astype(np.int32), device=dev),
+                          torch.as_tensor(wl.prefix_lens(), device=dev), wl.shared_prefix_tokens, 0)
+    out = uq.ref_decode_cascade(desc, wl.q.to(dev), cache, torch.as_tensor(wl.page_table, device=dev),
+                                torch.as_tensor(wl.context_lens, device=dev), wl.max_context, pre, SCALE, 16384)
+    torch.cuda.synchronize()
+    check_attention(out.cpu().numpy(), reference(fmt, wl, [0, 1, 2], dev), f"{fmt} cascade long rows", fmt)
+
+
 def test_ref_decode_fp8_integer_inputs(uq):
     """FP8 cache with integer K, V in [-16, 16] and query in [-8, 8] (all
     exact in E4M3, unit scales): q.k is an exact integer whatever the

@@ -1,14 +1,16 @@
 """The one-wave-per-partition grid of the partition launch.
 
 A launch with at least 8 blocks per CU of W consecutive partitions each (W =
-4 waves per block; 2 for the BF16 cache), head size 128 and no shared prefix
-gives every wave one whole partition: the wave streams it through its own
-ring, writes its own partial, and the merge kernel finishes every row, also
-the rows of contexts that fit one partition.  The shapes here (40
-sequences, 4 kv heads, 32-token partitions of contexts up to 2048 tokens:
-40 x 4 x 16 = 2560 blocks) take that grid while the oracle still finishes
-them in seconds; 64-token partitions of the same data (1280 blocks) take
-the block-per-partition grid.
+8 waves per block for the FP4 and FP8 caches where that many blocks of 8
+exist, else 4; 4 for Ultra-TQ, 2 for BF16), head size 128 and no shared
+prefix gives every wave one whole partition: the wave streams it through
+its own ring, the block merges its W partials and the merge kernel finishes
+every row, also the rows of contexts that fit one partition.  The shapes
+here (40 sequences, 4 kv heads, 16-token partitions of contexts up to 2048
+tokens: 40 x 4 x 16 = 2560 blocks of 8) take that grid while the oracle
+still finishes them in seconds; 32-token partitions take it with blocks of
+4 (40 x 4 x 16 = 2560 blocks), 64-token partitions of the same data (1280
+blocks of 4) the block-per-partition grid.
   * the page-gather probe fills exactly the wave grid's sink words, and reads
     the same bytes as on the block grid;
   * FP4 decode against the oracle (Algorithm 1, Decode; max-abs 2e-3,
@@ -37,7 +39,7 @@ pytestmark = pytest.mark.gpu
 SCALE = 1 / math.sqrt(128)
 EDGES = [0, 1, 15, 16, 17, 31, 32, 33, 63, 64, 65, 95, 96, 97, 127, 128, 129, 255, 256, 257, 500, 777, 1000, 1023,
          1024, 1025, 1500, 2000, 2047, 2048]
-WAVE_PART, BLOCK_PART = 32, 64
+WAVE_PART, BLOCK_PART = 16, 64
 
 
 @pytest.fixture(scope="module")
@@ -103,24 +105,25 @@ def test_probe_fills_the_wave_grid(uq):
     np_wave = -(-wl.max_context // WAVE_PART)
     sinks = {}
     for part in (WAVE_PART, BLOCK_PART):
-        n = 4 * -(-wl.max_context // part) * wl.num_kv_heads * wl.batch
+        n = 4 * -(-wl.max_context // part) * wl.num_kv_heads * wl.batch   # the documented bound
         sink = torch.full((n,), -1, dtype=torch.int32, device=dev)
         uq.probe_page_gather(desc, wl.num_q_heads, codes, scales, pt, ctx, wl.max_context, part, sink)
         torch.cuda.synchronize()
         sinks[part] = sink.cpu().numpy()
     s = sinks[WAVE_PART]
-    used = -(-np_wave // 4) * wl.num_kv_heads * wl.batch * 4
+    used = -(-np_wave // 8) * wl.num_kv_heads * wl.batch * 8
     log(f"wave grid: {used} of {s.size} sink words")
     assert np.all(s[:used] != -1) and np.all(s[used:] == -1)
-    w = s[:used].reshape(-1, wl.batch, wl.num_kv_heads, 4)   # [partition group][sequence][kv head][wave]
+    w = s[:used].reshape(-1, wl.batch, wl.num_kv_heads, 8)   # [partition group][sequence][kv head][wave]
     for b, c in enumerate(wl.context_lens):
         nparts = -(-int(c) // WAVE_PART)
         flat = w[:, b].transpose(0, 2, 1).reshape(-1, wl.num_kv_heads)   # [partition][kv head]
         assert np.all(flat[nparts:] == 0), b
     # every page read once on either grid (and the same padding reads)
-    assert np.all(sinks[BLOCK_PART] != -1)
+    used_b = -(-wl.max_context // BLOCK_PART) * wl.num_kv_heads * wl.batch * 4   # blocks of 4 waves
+    assert np.all(sinks[BLOCK_PART][:used_b] != -1)
     assert np.bitwise_xor.reduce(s[:used].view(np.uint32)) == np.bitwise_xor.reduce(
-        sinks[BLOCK_PART].view(np.uint32))
+        sinks[BLOCK_PART][:used_b].view(np.uint32))
 
 
 @pytest.mark.parametrize("rotate_v", [True, False])
@@ -133,7 +136,7 @@ def test_fp4_decode_against_oracle(uq, rotate_v):
     pt = torch.as_tensor(wl.page_table, device=dev)
     ctx = torch.as_tensor(wl.context_lens, device=dev)
     outs = {}
-    for part in (WAVE_PART, BLOCK_PART, 16, 48):
+    for part in (WAVE_PART, BLOCK_PART, 32, 48):
         out = uq.decode_attention(desc, wl.q.to(dev), codes, scales, pt, ctx, wl.max_context, SCALE, part)
         torch.cuda.synchronize()
         outs[part] = out.cpu().numpy().astype(np.float64)

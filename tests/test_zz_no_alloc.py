@@ -83,13 +83,14 @@ def test_noalloc_head_size_64_and_oversize(uq):
 
 def test_noalloc_wave_grid_then_block_grid(uq):
     """The one-wave-per-partition grid (40 sequences x 4 kv heads x 16 blocks
-    of four 32-token partitions), then a call on the block grid."""
+    of eight 16-token partitions, group 2: 21 MB of partials), then a call
+    on the block grid."""
     dev = torch.device("cuda:0")
     rng = np.random.default_rng(34)
     ctx = [0, 1, 31, 32, 33, 2048, 2047, 100] + [int(c) for c in rng.integers(1, 2049, 32)]
-    wave = workloads.custom(40, 16, 4, ctx, seed=34, paging="random")
+    wave = workloads.custom(40, 8, 4, ctx, seed=34, paging="random")
     small = workloads.custom(3, 12, 2, [300, 0, 77], seed=35, paging="random")
-    for name, wl, part in (("wave grid", wave, 32), ("block grid", small, 64)):
+    for name, wl, part in (("wave grid", wave, 16), ("block grid", small, 64)):
         log(f"noalloc vs workspace: {name} B={wl.batch} Hq={wl.num_q_heads} Hkv={wl.num_kv_heads} part={part}")
         desc, codes, scales = cache(uq, wl, dev)
         out, ref = both(uq, wl, desc, codes, scales, dev, part)
