@@ -178,10 +178,11 @@ int32_t uq_default_partition(const uq_cache_desc *desc, int32_t batch, int32_t n
  * than one partition (max_context > partition).  The partition kernel runs
  * one block of 4 waves per (partition, kv head, sequence), the waves sharing
  * the partition's pages, or -- when the launch has at least 2048 blocks of
- * 4 partitions each (head size 128, no shared prefix) -- one wave per
- * partition, a block taking 4 consecutive partitions of one sequence and kv
- * head and reducing their partials into one before the merge.  The result
- * does not depend on the grid beyond rounding.
+ * W partitions each (head size 128, no shared prefix; W = 8 where that many
+ * blocks of 8 exist, else 4) -- one wave per partition, a block taking W
+ * consecutive partitions of one sequence and kv head and reducing their
+ * partials into one before the merge.  The result does not depend on the
+ * grid beyond rounding.
  *   q             : [batch][num_q_heads][128].  F32/BF16/F16: rotated and
  *                   cast to FP8 inside the call.  FP8_E4M3: already
  *                   prepared by uq_prepare_query.
@@ -218,7 +219,7 @@ uq_status uq_decode_attention(const uq_cache_desc *desc, const void *q, uq_dtype
  * The two launches of uq_decode_attention, for callers that time or overlap
  * them.  uq_decode_partials runs the partition kernel: each block writes
  * a partial (running max, running sum, 128 accumulators per query head) of
- * its partition (its 4 partitions on the wave grid) into the workspace, or
+ * its partition (its W partitions on the wave grid) into the workspace, or
  * the final output when it holds the whole context.  uq_decode_merge
  * merges the partials into `out` (a no-op when max_context <= partition).  Called back
  * to back on one stream with the same arguments they are exactly
