@@ -179,10 +179,10 @@ int32_t uq_default_partition(const uq_cache_desc *desc, int32_t batch, int32_t n
  * one block of 4 waves per (partition, kv head, sequence), the waves sharing
  * the partition's pages, or -- when the launch has at least 2048 blocks of
  * W partitions each (head size 128, no shared prefix; W = 8 where that many
- * blocks of 8 exist, else 4) -- one wave per partition, a block taking W
- * consecutive partitions of one sequence and kv head and reducing their
- * partials into one before the merge.  The result does not depend on the
- * grid beyond rounding.
+ * blocks of 8 exist and there are 16 partitions or more, else 4) -- one
+ * wave per partition, a block taking W consecutive partitions of one
+ * sequence and kv head and reducing their partials into one before the
+ * merge.  The result does not depend on the grid beyond rounding.
  *   q             : [batch][num_q_heads][128].  F32/BF16/F16: rotated and
  *                   cast to FP8 inside the call.  FP8_E4M3: already
  *                   prepared by uq_prepare_query.

@@ -2020,10 +2020,14 @@ __global__ void __launch_bounds__(1024) cascade_rows_kernel(DecodeParams p) {
 // Waves per block of a partition launch (the grid choice below, the merge
 // launch and the probe's sink words follow it).  The FP4 and FP8 caches at
 // head size 128: 8 on the wave grid when it has enough blocks of 8
-// partitions (fewer block prologues and partial writes per partition: 3 %
-// faster on 128k contexts in 4096-token partitions), else the format's
-// kWaves (4), which measured equal on 32k contexts and 2 % faster on the
-// MiniMax-like cascade than blocks of 8.  Others: the format's kWaves.
+// partitions and at least 16 partitions, so that a longest context spans
+// two blocks or more (fewer block prologues and partial writes per
+// partition: 3 % faster on 128k contexts in 4096-token partitions; blocks
+// of 8 holding whole contexts were 5 % slower on a ragged batch, whose
+// short contexts leave most of such a block's waves idle), else the
+// format's kWaves (4), which measured equal on 32k contexts and 2 % faster
+// on the MiniMax-like cascade than blocks of 8.  Others: the format's
+// kWaves.
 static bool wave_grid_with(const DecodeParams& p, int W) {
     if (!p.allow_wave_parts || p.prefix_pages != nullptr || p.head_dim != kHeadDim) return false;
     if (p.kv_fmt != kFp4 && p.kv_fmt != kFp8 && p.kv_fmt != kBf16 && p.kv_fmt != kTq4) return false;
@@ -2031,15 +2035,16 @@ static bool wave_grid_with(const DecodeParams& p, int W) {
     const int64_t blocks = int64_t(p.batch) * p.num_kv_heads * ((p.num_partitions + W - 1) / W);
     return blocks >= 8 * kNumCus;
 }
+static bool eight_waves(const DecodeParams& p) { return p.num_partitions >= 16 && wave_grid_with(p, 8); }
 static int launch_waves(const DecodeParams& p) {
     switch (p.kv_fmt) {
-        case kFp8: return wave_grid_with(p, 8) ? 8 : Fmt<kFp8>::kWaves;
+        case kFp8: return eight_waves(p) ? 8 : Fmt<kFp8>::kWaves;
         case kBf16: return Fmt<kBf16>::kWaves;
         case kTq4: return Fmt<kTq4>::kWaves;
         case kFp4d64: return Fmt<kFp4d64>::kWaves;
         case kFp4d64x2: return Fmt<kFp4d64x2>::kWaves;
         case kFp4d256: return Fmt<kFp4d256>::kWaves;
-        default: return wave_grid_with(p, 8) ? 8 : Fmt<kFp4>::kWaves;
+        default: return eight_waves(p) ? 8 : Fmt<kFp4>::kWaves;
     }
 }
 // The grid of a partition launch: one wave per partition when there are

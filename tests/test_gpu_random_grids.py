@@ -47,12 +47,13 @@ def params(i):
 
 def grid_of(c):
     """The launch rule of the partition kernel (head size 128, no shared
-    prefix): one wave per partition in blocks of W = 8 partitions when that
-    gives at least 8 blocks per CU (256 CUs), else blocks of 4 under the
-    same condition, else one block per partition."""
+    prefix): one wave per partition in blocks of W = 8 partitions when there
+    are at least 16 partitions and that gives at least 8 blocks per CU (256
+    CUs), else blocks of 4 under the same block count, else one block per
+    partition."""
     np_ = -(-max(c["ctx"]) // c["part"]) if max(c["ctx"]) > 0 else 1
     for w in (8, 4):
-        if np_ >= w and c["b"] * c["hkv"] * -(-np_ // w) >= 8 * 256:
+        if np_ >= max(w, 16 if w == 8 else 0) and c["b"] * c["hkv"] * -(-np_ // w) >= 8 * 256:
             return f"wave grid, {w} partitions per block"
     return "one block per partition"
 
